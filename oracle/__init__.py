@@ -1,0 +1,134 @@
+"""ctypes front end of the fp64 CPU oracle (``lr_attnres_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, by the smoke check and
+by the CPU-baseline leg of the benchmark.  The product library never imports
+it.  Arrays are numpy; bf16 data is passed as its raw ``uint16`` bits, exactly
+the bytes the GPU consumes.
+
+Every function follows Section 3 of the paper (Eqs. lr_key_norm,
+lr_attnres_weight, lr_attnres_output; sliced keys Eq. sliced_key; full-rank
+AttnRes Eqs. attnres_weight / attnres_output).  The backward is derived in the
+C file's header and pinned by finite differences in the tests.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "lr_attnres_oracle.c")
+LIB = os.path.join(HERE, "liblrattnres_oracle.so")
+
+PROJECTED, SLICED, FULL = 0, 1, 2
+_STORE = {np.dtype(np.float32): 0, np.dtype(np.uint16): 1, np.dtype(np.float64): 2}
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no fast-math: IEEE double throughout)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
+           SRC, "-o", LIB + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        build()
+    lib = ctypes.CDLL(LIB)
+    vp, ll, i, d = ctypes.c_void_p, ctypes.c_longlong, ctypes.c_int, ctypes.c_double
+    lib.orc_route_weights.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
+    lib.orc_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
+    lib.orc_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
+    for f in (lib.orc_route_weights, lib.orc_route_fwd, lib.orc_route_bwd):
+        f.restype = ctypes.c_int
+    lib.orc_num_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def num_threads() -> int:
+    return _load().orc_num_threads()
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _prep(V, K, q, mode, r):
+    V = np.ascontiguousarray(V)
+    if V.dtype not in _STORE:
+        raise TypeError(f"oracle: unsupported value storage {V.dtype}")
+    if V.ndim != 3:
+        raise ValueError("oracle: V must be [S, N, d]")
+    S, N, d = V.shape
+    if mode == PROJECTED:
+        K = np.ascontiguousarray(K)
+        if K.dtype != V.dtype or K.shape[:2] != (S, N):
+            raise ValueError("oracle: K must be [S, N, r] in V's storage")
+        r = K.shape[2]
+    else:
+        if K is not None:
+            raise ValueError("oracle: K is only used with projected keys")
+        if mode == FULL:
+            r = d
+        elif r is None:
+            raise ValueError("oracle: sliced keys need r")
+    q = np.ascontiguousarray(np.asarray(q, dtype=np.float64))
+    if q.shape != (r,):
+        raise ValueError(f"oracle: q must have shape ({r},)")
+    return V, K, q, S, N, d, r
+
+
+def route_weights(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """alpha[n, i] (Eq. lr_attnres_weight) for tokens [n0, n1)."""
+    V, K, q, S, N, d, r = _prep(V, K, q, mode, r)
+    n1 = N if n1 is None else n1
+    out = np.empty((n1 - n0, S), dtype=np.float64)
+    rc = _load().orc_route_weights(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
+                                   _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return out
+
+
+def route_fwd(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """H[n, :] = sum_i alpha_i V[i, n, :] (Eq. lr_attnres_output), fp64."""
+    V, K, q, S, N, d, r = _prep(V, K, q, mode, r)
+    n1 = N if n1 is None else n1
+    out = np.empty((n1 - n0, d), dtype=np.float64)
+    rc = _load().orc_route_fwd(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
+                               _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return out
+
+
+def route_bwd(V, K, q, dH, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """(dV, dK, dq) of L = sum(dH * H) for tokens [n0, n1), fp64.
+
+    dV is [S, n1-n0, d], dK is [S, n1-n0, r] (projected keys, else None),
+    dq is [r] summed over the token range.
+    """
+    V, K, q, S, N, d, r = _prep(V, K, q, mode, r)
+    dH = np.ascontiguousarray(dH)
+    if dH.dtype != V.dtype or dH.shape != (N, d):
+        raise ValueError("oracle: dH must be [N, d] in V's storage")
+    n1 = N if n1 is None else n1
+    nt = n1 - n0
+    dV = np.empty((S, nt, d), dtype=np.float64)
+    dK = np.empty((S, nt, r), dtype=np.float64) if mode == PROJECTED else None
+    dq = np.empty((r,), dtype=np.float64)
+    rc = _load().orc_route_bwd(_ptr(V), _ptr(K), _ptr(q), _ptr(dH), _ptr(dV), _ptr(dK),
+                               _ptr(dq), S, N, d, r, mode, _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return dV, dK, dq

@@ -1,0 +1,336 @@
+/*
+ * fp64 CPU oracle for the depth-wise residual routing of Low-Rank Attention
+ * Residuals (LR-AttnRes), arXiv 2607.09694.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * statement of what the routing computes.  It is linked only by the test
+ * suite, by the smoke check and by the CPU-baseline leg of the benchmark.
+ * The GPU library never includes, links or calls it, and it shares no code,
+ * header, table or constant with the GPU library.
+ *
+ * What it follows (Section 3 of the paper, "Method"):
+ *   - Eq. (lr_source_pair): source i is a pair (o_i in R^d, k_i in R^r).
+ *   - Eq. (lr_key_norm): kbar_i = RMSNorm(k_i); parameter-free RMSNorm
+ *     (Appendix A, "Parameters": the paper's RMSNorm convention has no gain),
+ *     rho_i = sqrt(mean_j k_ij^2 + eps), kbar_i = k_i / rho_i.
+ *   - Eq. (lr_attnres_weight): alpha_i = softmax over sources of q^T kbar_i.
+ *   - Eq. (lr_attnres_output): h = sum_i alpha_i o_i.
+ *   - Projected keys (Sec. 3.3, Eq. fused_projection): k_i is a separate
+ *     input tensor K[S][N][r].
+ *   - Sliced keys (Sec. 3.4, Eq. sliced_key): k_i = tail_r(o_i), the last r
+ *     coordinates of the value (1-based d-r+1..d, 0-based [d-r, d)).
+ *   - Full-rank AttnRes (Sec. 3.1, Eqs. attnres_weight / attnres_output):
+ *     the key is the whole value, r = d; Sec. 3.4 states that sliced keys
+ *     with r = d reduce to it.
+ *
+ * Readings where the paper is silent (each also listed in the design notes):
+ *   - eps: never stated; it is an explicit argument added to the mean of
+ *     squares inside the square root.
+ *   - The softmax subtracts the per-token maximum score first; this is an
+ *     identity of the softmax, not an approximation.
+ *   - Source order is the stack order i = 0 (embedding) .. S-1.
+ *   - The backward pass is not stated by the paper; it is derived here by
+ *     hand for the scalar loss L = sum_n dH[n] . h[n]:
+ *         g_i   = dH . o_i
+ *         ds_i  = alpha_i (g_i - sum_l alpha_l g_l)        (softmax)
+ *         dV_i  = alpha_i dH                               (value path)
+ *         dk_i  = (ds_i / rho_i) (q - kbar_i s_i / r)      (RMSNorm, s_i = q.kbar_i)
+ *         dq    = sum_n sum_i ds_i kbar_i
+ *     With sliced keys dk_i is added into the last r coordinates of dV_i,
+ *     with full-rank keys into all d coordinates (the key is the value).
+ *     The forward is pinned by closed-form cases and invariants, the
+ *     backward by central finite differences of this same forward.
+ *
+ * Arithmetic: every input is widened exactly to double (bf16 by placing its
+ * 16 bits in the high half of an IEEE single, fp32 by conversion), and every
+ * operation is done in double.  Outputs are double and unrounded.
+ *
+ * Storage codes for V, K and dH: 0 = fp32, 1 = bf16 (raw uint16 bits),
+ * 2 = fp64.  Key modes: 0 = projected, 1 = sliced, 2 = full-rank.
+ * q and eps are passed as double (callers widen the fp32 values exactly).
+ *
+ * Token ranges: each call computes tokens n in [n0, n1) of a problem whose
+ * inputs are the complete [S][N][.] stacks; outputs hold only that range.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORC_STORE_F32 = 0, ORC_STORE_BF16 = 1, ORC_STORE_F64 = 2 };
+enum { ORC_KEYS_PROJECTED = 0, ORC_KEYS_SLICED = 1, ORC_KEYS_FULL = 2 };
+
+struct orc_problem {
+    const void *V;   /* [S][N][d] values o_i            */
+    const void *K;   /* [S][N][r] projected keys or NULL */
+    const double *q; /* [r] pseudo-query                 */
+    long long S, N, d, r;
+    int mode, store;
+    double eps;
+};
+
+/* Exact widening of one stored element to double. */
+static double widen(const void *base, int store, long long idx)
+{
+    if (store == ORC_STORE_F32)
+        return (double)((const float *)base)[idx];
+    if (store == ORC_STORE_F64)
+        return ((const double *)base)[idx];
+    {
+        uint32_t bits = (uint32_t)((const uint16_t *)base)[idx] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+}
+
+/* o_i[j] for token n: V[i][n][j]. */
+static double value_elem(const struct orc_problem *p, long long i, long long n, long long j)
+{
+    return widen(p->V, p->store, (i * p->N + n) * p->d + j);
+}
+
+/* k_i[j] for token n, per the key mode (Eq. fused_projection / sliced_key /
+ * attnres_weight). */
+static double key_elem(const struct orc_problem *p, long long i, long long n, long long j)
+{
+    if (p->mode == ORC_KEYS_PROJECTED)
+        return widen(p->K, p->store, (i * p->N + n) * p->r + j);
+    if (p->mode == ORC_KEYS_SLICED)
+        return value_elem(p, i, n, p->d - p->r + j);
+    return value_elem(p, i, n, j);
+}
+
+/* Eq. lr_key_norm: rho_i = sqrt(mean_j k_ij^2 + eps), kbar_i = k_i / rho_i.
+ * Then the score s_i = q^T kbar_i (Eq. lr_attnres_weight).
+ * kbar is [S][r]; rho and s are [S]. */
+static void normalised_keys_and_scores(const struct orc_problem *p, long long n,
+                                       double *kbar, double *rho, double *s)
+{
+    for (long long i = 0; i < p->S; ++i) {
+        double sumsq = 0.0;
+        for (long long j = 0; j < p->r; ++j) {
+            double k = key_elem(p, i, n, j);
+            sumsq += k * k;
+        }
+        rho[i] = sqrt(sumsq / (double)p->r + p->eps);
+        s[i] = 0.0;
+        for (long long j = 0; j < p->r; ++j) {
+            kbar[i * p->r + j] = key_elem(p, i, n, j) / rho[i];
+            s[i] += p->q[j] * kbar[i * p->r + j];
+        }
+    }
+}
+
+/* Eq. lr_attnres_weight: alpha = softmax over the sources of the scores. */
+static void depth_softmax(long long S, const double *s, double *alpha)
+{
+    double m = s[0];
+    for (long long i = 1; i < S; ++i)
+        if (s[i] > m)
+            m = s[i];
+    double z = 0.0;
+    for (long long i = 0; i < S; ++i) {
+        alpha[i] = exp(s[i] - m);
+        z += alpha[i];
+    }
+    for (long long i = 0; i < S; ++i)
+        alpha[i] /= z;
+}
+
+static int check_problem(const struct orc_problem *p, long long n0, long long n1)
+{
+    if (p->S < 1 || p->N < 0 || p->d < 1 || p->r < 1)
+        return 1;
+    if (n0 < 0 || n1 < n0 || n1 > p->N)
+        return 1;
+    if (p->mode == ORC_KEYS_PROJECTED && p->K == NULL)
+        return 1;
+    if (p->mode == ORC_KEYS_SLICED && p->r > p->d)
+        return 1;
+    if (p->mode == ORC_KEYS_FULL && p->r != p->d)
+        return 1;
+    if (p->mode < 0 || p->mode > 2 || p->store < 0 || p->store > 2)
+        return 1;
+    return 0;
+}
+
+/* Scratch for one token: kbar[S*r], rho[S], s[S], alpha[S], g[S], ds[S]. */
+static double *token_scratch(const struct orc_problem *p)
+{
+    return (double *)malloc(sizeof(double) * (size_t)(p->S * p->r + 5 * p->S));
+}
+
+/* Softmax weights alpha[n - n0][i] for tokens in [n0, n1). */
+int orc_route_weights(const void *V, const void *K, const double *q, double *alpha,
+                      long long S, long long N, long long d, long long r,
+                      int mode, int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || alpha == NULL || q == NULL || V == NULL)
+        return 1;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *w = token_scratch(&p);
+        if (w == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(static)
+        for (long long n = n0; n < n1; ++n) {
+            if (w == NULL)
+                continue;
+            double *kbar = w, *rho = kbar + S * r, *s = rho + S;
+            normalised_keys_and_scores(&p, n, kbar, rho, s);
+            depth_softmax(S, s, alpha + (n - n0) * S);
+        }
+        free(w);
+    }
+    return failed;
+}
+
+/* Forward, Eq. lr_attnres_output: H[n - n0][:] = sum_i alpha_i o_i. */
+int orc_route_fwd(const void *V, const void *K, const double *q, double *H,
+                  long long S, long long N, long long d, long long r,
+                  int mode, int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || H == NULL || q == NULL || V == NULL)
+        return 1;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *w = token_scratch(&p);
+        if (w == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(static)
+        for (long long n = n0; n < n1; ++n) {
+            if (w == NULL)
+                continue;
+            double *kbar = w, *rho = kbar + S * r, *s = rho + S, *alpha = s + S;
+            normalised_keys_and_scores(&p, n, kbar, rho, s);
+            depth_softmax(S, s, alpha);
+            double *h = H + (n - n0) * d;
+            for (long long j = 0; j < d; ++j) {
+                double acc = 0.0;
+                for (long long i = 0; i < S; ++i)
+                    acc += alpha[i] * value_elem(&p, i, n, j);
+                h[j] = acc;
+            }
+        }
+        free(w);
+    }
+    return failed;
+}
+
+/* Backward of L = sum_n dH[n] . h[n] (derived; see the file header).
+ *   dV [S][n1-n0][d]   gradient w.r.t. the values, including the key path for
+ *                      sliced and full-rank keys (the key is part of the value)
+ *   dK [S][n1-n0][r]   gradient w.r.t. projected keys (projected mode only;
+ *                      must be NULL otherwise)
+ *   dq [r]             gradient w.r.t. q summed over tokens [n0, n1)
+ * dH is [N][d] in the same storage as V; row n is token n. */
+int orc_route_bwd(const void *V, const void *K, const double *q, const void *dH,
+                  double *dV, double *dK, double *dq,
+                  long long S, long long N, long long d, long long r,
+                  int mode, int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || q == NULL || V == NULL || dH == NULL || dV == NULL ||
+        dq == NULL)
+        return 1;
+    if ((mode == ORC_KEYS_PROJECTED) != (dK != NULL))
+        return 1;
+    const long long nt = n1 - n0;
+    /* Per-token dq contributions are summed in token order after each block,
+     * so the result does not depend on the thread count. */
+    const long long block = 256;
+    double *dq_tok = (double *)malloc(sizeof(double) * (size_t)(block * r));
+    if (dq_tok == NULL)
+        return 1;
+    for (long long j = 0; j < r; ++j)
+        dq[j] = 0.0;
+    int failed = 0;
+    for (long long b0 = n0; b0 < n1; b0 += block) {
+        long long b1 = b0 + block < n1 ? b0 + block : n1;
+#pragma omp parallel
+        {
+            double *w = token_scratch(&p);
+            if (w == NULL) {
+#pragma omp atomic write
+                failed = 1;
+            }
+#pragma omp for schedule(static)
+            for (long long n = b0; n < b1; ++n) {
+                if (w == NULL)
+                    continue;
+                double *kbar = w, *rho = kbar + S * r, *s = rho + S, *alpha = s + S;
+                double *g = alpha + S, *ds = g + S;
+                normalised_keys_and_scores(&p, n, kbar, rho, s);
+                depth_softmax(S, s, alpha);
+                /* g_i = dH . o_i and the softmax gradient. */
+                double gbar = 0.0;
+                for (long long i = 0; i < S; ++i) {
+                    g[i] = 0.0;
+                    for (long long j = 0; j < d; ++j)
+                        g[i] += widen(dH, store, n * d + j) * value_elem(&p, i, n, j);
+                    gbar += alpha[i] * g[i];
+                }
+                for (long long i = 0; i < S; ++i)
+                    ds[i] = alpha[i] * (g[i] - gbar);
+                /* Value path: dV_i = alpha_i dH. */
+                for (long long i = 0; i < S; ++i)
+                    for (long long j = 0; j < d; ++j)
+                        dV[(i * nt + (n - n0)) * d + j] = alpha[i] * widen(dH, store, n * d + j);
+                /* Key path through the score and the RMSNorm. */
+                for (long long i = 0; i < S; ++i) {
+                    for (long long j = 0; j < r; ++j) {
+                        double dk = ds[i] / rho[i] *
+                                    (q[j] - kbar[i * r + j] * s[i] / (double)r);
+                        if (mode == ORC_KEYS_PROJECTED)
+                            dK[(i * nt + (n - n0)) * r + j] = dk;
+                        else if (mode == ORC_KEYS_SLICED)
+                            dV[(i * nt + (n - n0)) * d + (d - r) + j] += dk;
+                        else
+                            dV[(i * nt + (n - n0)) * d + j] += dk;
+                    }
+                }
+                /* dq contribution of this token: sum_i ds_i kbar_i. */
+                double *dqt = dq_tok + (n - b0) * r;
+                for (long long j = 0; j < r; ++j) {
+                    dqt[j] = 0.0;
+                    for (long long i = 0; i < S; ++i)
+                        dqt[j] += ds[i] * kbar[i * r + j];
+                }
+            }
+            free(w);
+        }
+        for (long long n = b0; n < b1; ++n)
+            for (long long j = 0; j < r; ++j)
+                dq[j] += dq_tok[(n - b0) * r + j];
+    }
+    free(dq_tok);
+    return failed;
+}
+
+/* Number of OpenMP threads a parallel region of this library would use. */
+int orc_num_threads(void)
+{
+    int t = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        {
+#ifdef _OPENMP
+            t = omp_get_num_threads();
+#endif
+        }
+    }
+    return t;
+}
