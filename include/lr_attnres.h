@@ -1,0 +1,133 @@
+/*
+ * lr_attnres.h - C ABI of the MI355X (gfx950) depth-routing library of
+ * Low-Rank Attention Residuals (LR-AttnRes), arXiv 2607.09694.
+ *
+ * At one residual read site every token n mixes its S cached sources
+ * o_0..o_{S-1} (the embedding and the earlier sub-layer outputs, Sec. 3.1)
+ * with softmax weights over depth computed from r-dimensional keys
+ * (Sec. 3.2):
+ *
+ *     kbar_i  = RMSNorm(k_i),     rho_i = sqrt(mean_j k_ij^2 + eps),
+ *                                  kbar_i = k_i / rho_i          (Eq. lr_key_norm)
+ *     alpha_i = softmax_i(q^T kbar_i)                             (Eq. lr_attnres_weight)
+ *     h       = sum_i alpha_i o_i                                 (Eq. lr_attnres_output)
+ *
+ * The RMSNorm has no gain (the paper's parameter-free convention, Appendix A
+ * "Parameters"); eps is not given by the paper and is an explicit argument.
+ * There is no score temperature.
+ *
+ * Key modes:
+ *   LRAR_MODE_PROJECTED  k_i is row [i][n] of a separate key stack K[S][N][r]
+ *                        (P-LR, Sec. 3.3, Eq. fused_projection).
+ *   LRAR_MODE_SLICED     k_i = tail_r(o_i), the last r coordinates of the
+ *                        value, read in place from V (S-LR, Sec. 3.4,
+ *                        Eq. sliced_key); requires r <= d.
+ *   LRAR_MODE_FULL       full-rank AttnRes: k_i = o_i, r must equal d
+ *                        (Sec. 3.1, Eqs. attnres_weight / attnres_output).
+ *
+ * Layout: all arrays are dense and row-major.  V is [S][N][d] (source-major:
+ * the rows of one source are contiguous, so the first S' sources of a deeper
+ * stack are a valid S'-source stack), K and dK are [S][N][r], H and dH are
+ * [N][d], q and dq are [r] fp32.  Sources are indexed in stack order,
+ * i = 0 (embedding) .. S-1.  V, K, H, dH, dV, dK share one storage type,
+ * fp32 or bf16; all arithmetic is fp32, and bf16 results are rounded to
+ * nearest even.
+ *
+ * Ownership and execution: every pointer is caller-owned device memory.
+ * The library allocates nothing, keeps no pointer after a call returns and
+ * holds no state besides the per-thread error string.  Work is enqueued on
+ * `stream` (a hipStream_t; NULL means the null stream) and runs
+ * asynchronously: the caller keeps the buffers alive until the stream has
+ * reached the work.  Results are bitwise reproducible from run to run.
+ *
+ * Errors: nothing is thrown across the ABI.  All arguments are validated on
+ * the host before any HIP call, so an invalid call never touches the device:
+ *   LRAR_EINVAL       a required pointer is NULL, a size is < 1 (N may be 0),
+ *                     the mode or storage code is unknown, SLICED with r > d,
+ *                     FULL with r != d, K or dK given outside PROJECTED,
+ *                     eps negative or not finite, a tensor pointer not 16-byte
+ *                     aligned (q and dq: 4-byte), an output overlapping an
+ *                     input or another output, a size product overflowing
+ *                     int64, or a workspace that is missing or too small.
+ *   LRAR_EUNSUPPORTED a valid problem outside the kernels' limits (below).
+ *   LRAR_EHIP         a HIP launch error; its text is in lr_attnres_last_error.
+ * Limits: N <= 2^30; forward S <= 1024; backward S <= 512; backward of
+ * PROJECTED/SLICED r <= 256; FULL, and every backward, d <= 4096 (bf16) or
+ * d <= 2048 (fp32) when d is a multiple of 8 (bf16) or 4 (fp32), else
+ * d <= 1024.
+ */
+#ifndef LR_ATTNRES_H
+#define LR_ATTNRES_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LR_ATTNRES_ABI_VERSION 1
+
+enum { LRAR_MODE_PROJECTED = 0, LRAR_MODE_SLICED = 1, LRAR_MODE_FULL = 2 };
+enum { LRAR_DTYPE_F32 = 0, LRAR_DTYPE_BF16 = 1 };
+enum { LRAR_OK = 0, LRAR_EINVAL = 1, LRAR_EUNSUPPORTED = 2, LRAR_EHIP = 3 };
+
+/*
+ * Forward routing at one residual site (Sec. 3.2, Eqs. lr_key_norm,
+ * lr_attnres_weight, lr_attnres_output; modes as above).
+ *   V   [S][N][d]  values o_i, storage `dtype`, read only
+ *   K   [S][N][r]  keys, storage `dtype`; PROJECTED only, else must be NULL
+ *   q   [r]        fp32 pseudo-query of this site
+ *   H   [N][d]     output h, storage `dtype`, fully overwritten
+ * The softmax weights are not stored.  Returns LRAR_OK or an error code.
+ */
+int lr_attnres_route_fwd(const void *V, const void *K, const float *q, void *H,
+                         int64_t S, int64_t N, int64_t d, int64_t r,
+                         int mode, int dtype, float eps, void *stream);
+
+/*
+ * Bytes of device workspace lr_attnres_route_bwd needs for this problem
+ * (per-workgroup partial sums of dq).  0 for an invalid problem.
+ */
+size_t lr_attnres_route_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int64_t r,
+                                            int mode, int dtype);
+
+/*
+ * Backward of the forward above for the loss L = sum_n dH[n] . h[n].  The
+ * paper gives no backward; this is the gradient of its Eqs. lr_key_norm,
+ * lr_attnres_weight and lr_attnres_output (the weights are recomputed from
+ * the keys, not saved, as Appendix A "Activation memory" assumes):
+ *     g_i  = dH . o_i,   ds_i = alpha_i (g_i - sum_l alpha_l g_l)
+ *     dV_i = alpha_i dH  (+ the key path below for SLICED and FULL)
+ *     dk_i = (ds_i / rho_i) (q - kbar_i s_i / r),   s_i = q . kbar_i
+ *     dq   = sum_n sum_i ds_i kbar_i
+ *   V, K, q      as in the forward, read only
+ *   dH  [N][d]   upstream gradient, storage `dtype`, read only
+ *   dV  [S][N][d] storage `dtype`, fully overwritten.  SLICED adds dk_i into
+ *                the last r coordinates, FULL into all d coordinates.
+ *   dK  [S][N][r] storage `dtype`, PROJECTED only (fully overwritten), else NULL
+ *   dq  [r]      fp32, overwritten with the sum over all N tokens (0 if N = 0);
+ *                the sum is taken in a fixed order, so it is reproducible.
+ *   workspace    device scratch of at least
+ *                lr_attnres_route_bwd_workspace_bytes(...) bytes (16-byte
+ *                aligned; may be NULL when that size is 0).  Its contents on
+ *                entry are ignored; it must not overlap any other argument,
+ *                and two calls in flight must not share it.
+ */
+int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const void *dH,
+                         void *dV, void *dK, float *dq, void *workspace,
+                         size_t workspace_bytes, int64_t S, int64_t N, int64_t d, int64_t r,
+                         int mode, int dtype, float eps, void *stream);
+
+/* Text of the last error raised on the calling thread ("" if none); valid
+ * until the next call into the library on that thread. */
+const char *lr_attnres_last_error(void);
+
+/* LR_ATTNRES_ABI_VERSION of the built library. */
+int lr_attnres_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LR_ATTNRES_H */

@@ -1,0 +1,168 @@
+"""LR-AttnRes depth routing on MI355X (gfx950): Python binding.
+
+Thin ctypes layer over the C ABI of ``liblrattnres.so`` (declared in
+``include/lr_attnres.h``).  It only checks and marshals torch tensors
+(device, dtype, contiguity) and passes their device pointers and the current
+HIP stream; every step of the routing runs in the library's HIP kernels.
+There is no fallback: without the built library every call raises.
+
+Routing at one residual site (Sec. 3.2 of arXiv 2607.09694):
+    kbar_i = RMSNorm(k_i), alpha_i = softmax_i(q . kbar_i), h = sum_i alpha_i o_i
+with keys projected (separate K), sliced (last r coordinates of each value)
+or full-rank (the value itself, r = d).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PROJECTED, SLICED, FULL = 0, 1, 2
+MODES = {"projected": PROJECTED, "sliced": SLICED, "full": FULL}
+_F32, _BF16 = 0, 1
+_STATUS = {1: "EINVAL", 2: "EUNSUPPORTED", 3: "EHIP"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblrattnres.so")
+_lib = None
+
+
+class RoutingError(RuntimeError):
+    """A non-zero status from the C ABI; ``status`` holds its name."""
+
+    def __init__(self, status: int, message: str):
+        self.status = _STATUS.get(status, str(status))
+        super().__init__(f"lr_attnres {self.status}: {message}")
+
+
+def load_library(path: str | None = None) -> ctypes.CDLL:
+    """Load the HIP routing library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP routing library not built: {path} is missing "
+                           "(run paper_2607_09694_amd/build.py or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    vp, i64, i, f = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    lib.lr_attnres_route_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, i, f, vp]
+    lib.lr_attnres_route_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i, i]
+    lib.lr_attnres_route_bwd_workspace_bytes.restype = ctypes.c_size_t
+    lib.lr_attnres_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
+                                         i64, i64, i64, i64, i, i, f, vp]
+    lib.lr_attnres_route_bwd.restype = ctypes.c_int
+    lib.lr_attnres_last_error.argtypes = []
+    lib.lr_attnres_last_error.restype = ctypes.c_char_p
+    lib.lr_attnres_abi_version.argtypes = []
+    lib.lr_attnres_abi_version.restype = ctypes.c_int
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def _check(lib, rc):
+    if rc != 0:
+        raise RoutingError(rc, lib.lr_attnres_last_error().decode())
+
+
+def _mode(mode) -> int:
+    return MODES[mode] if isinstance(mode, str) else int(mode)
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return _BF16
+    if t.dtype == torch.float32:
+        return _F32
+    raise TypeError(f"values must be bfloat16 or float32, got {t.dtype}")
+
+
+def _dev(t, name, dtype=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(t):
+    import torch
+
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _shape(V, K, q, mode):
+    if V.dim() != 3:
+        raise ValueError("V must be [S, N, d]")
+    S, N, d = V.shape
+    r = K.shape[2] if mode == PROJECTED else q.shape[0]
+    if q.dim() != 1 or q.shape[0] != r:
+        raise ValueError(f"q must have shape ({r},)")
+    if mode == PROJECTED and (K is None or K.dim() != 3 or tuple(K.shape[:2]) != (S, N)):
+        raise ValueError("K must be [S, N, r] for projected keys")
+    return S, N, d, r
+
+
+def route_fwd(V, K, q, mode, eps: float = 1e-6, out=None):
+    """h[n] = sum_i alpha_i V[i, n] (Eq. lr_attnres_output) on V's device.
+
+    V [S,N,d] bf16/fp32; K [S,N,r] (projected) or None; q [r] fp32 (full-rank:
+    r = d); returns H [N,d] in V's dtype (written into ``out`` if given).
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    H = out if out is not None else torch.empty((N, d), dtype=V.dtype, device=V.device)
+    rc = lib.lr_attnres_route_fwd(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                  _dev(q, "q", torch.float32), _dev(H, "H", V.dtype),
+                                  S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return H
+
+
+def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:
+    import torch
+
+    code = _BF16 if dtype == torch.bfloat16 else _F32
+    return load_library().lr_attnres_route_bwd_workspace_bytes(S, N, d, r, _mode(mode), code)
+
+
+def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None):
+    """Gradients (dV, dK, dq) of L = sum(dH * H) for the forward above.
+
+    dV [S,N,d] includes the key path for sliced / full-rank keys; dK [S,N,r]
+    for projected keys (else None); dq [r] fp32 summed over all tokens.
+    ``out`` may supply (dV, dK, dq) buffers, ``workspace`` a uint8 device
+    buffer of at least route_bwd_workspace_bytes(...) bytes.
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    if out is not None:
+        dV, dK, dq = out
+    else:
+        dV = torch.empty_like(V)
+        dK = torch.empty_like(K) if mode == PROJECTED else None
+        dq = torch.empty((r,), dtype=torch.float32, device=V.device)
+    code = _dtype_code(V)
+    need = lib.lr_attnres_route_bwd_workspace_bytes(S, N, d, r, mode, code)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=V.device)
+    rc = lib.lr_attnres_route_bwd(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                  _dev(q, "q", torch.float32), _dev(dH, "dH", V.dtype),
+                                  _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
+                                  _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"),
+                                  workspace.numel(), S, N, d, r, mode, code, float(eps),
+                                  _stream(V))
+    _check(lib, rc)
+    return dV, dK, dq

@@ -1,0 +1,186 @@
+// C ABI entry points of the routing library: argument validation (entirely
+// on the host, before any HIP call) and dispatch to the kernel launchers.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "lr_attnres.h"
+#include "route_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string &msg)
+{
+    g_last_error = msg;
+    return code;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t *out) { return !__builtin_mul_overflow(a, b, out); }
+
+struct Span {
+    const char *name;
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Span span(const char *name, const void *p, int64_t bytes)
+{
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Span{name, lo, p ? lo + (uintptr_t)bytes : lo};
+}
+
+bool overlaps(const Span &a, const Span &b)
+{
+    return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
+}
+
+// Shapes, mode, storage, eps.  Fills the element counts on success.
+int check_shape(int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype, float eps,
+                int64_t *v_elems, int64_t *k_elems, int64_t *h_elems)
+{
+    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED && mode != LRAR_MODE_FULL)
+        return fail(LRAR_EINVAL, "unknown key mode " + std::to_string(mode));
+    if (dtype != LRAR_DTYPE_F32 && dtype != LRAR_DTYPE_BF16)
+        return fail(LRAR_EINVAL, "unknown storage type " + std::to_string(dtype));
+    if (S < 1 || d < 1 || r < 1 || N < 0)
+        return fail(LRAR_EINVAL, "sizes must satisfy S >= 1, N >= 0, d >= 1, r >= 1");
+    if (mode == LRAR_MODE_SLICED && r > d)
+        return fail(LRAR_EINVAL, "sliced keys need r <= d");
+    if (mode == LRAR_MODE_FULL && r != d)
+        return fail(LRAR_EINVAL, "full-rank keys need r == d");
+    if (!isfinite(eps) || eps < 0.0f)
+        return fail(LRAR_EINVAL, "eps must be finite and >= 0");
+    const int64_t esize = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t sn, vb, kb, hb;
+    if (!mul_ok(S, N, &sn) || !mul_ok(sn, d, v_elems) || !mul_ok(*v_elems, esize, &vb) ||
+        !mul_ok(sn, r, k_elems) || !mul_ok(*k_elems, esize, &kb) || !mul_ok(N, d, h_elems) ||
+        !mul_ok(*h_elems, esize, &hb))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    return LRAR_OK;
+}
+
+int check_ptr(const void *p, const char *name, size_t align, bool required)
+{
+    if (!p) {
+        if (required)
+            return fail(LRAR_EINVAL, std::string(name) + " is NULL");
+        return LRAR_OK;
+    }
+    if (reinterpret_cast<uintptr_t>(p) % align != 0)
+        return fail(LRAR_EINVAL, std::string(name) + " is not " + std::to_string(align) +
+                                     "-byte aligned");
+    return LRAR_OK;
+}
+
+// No output may overlap an input or another output.
+int check_aliasing(const Span *outs, int nout, const Span *ins, int nin)
+{
+    for (int a = 0; a < nout; ++a) {
+        for (int b = 0; b < nin; ++b)
+            if (overlaps(outs[a], ins[b]))
+                return fail(LRAR_EINVAL, std::string("output ") + outs[a].name +
+                                             " overlaps input " + ins[b].name);
+        for (int b = a + 1; b < nout; ++b)
+            if (overlaps(outs[a], outs[b]))
+                return fail(LRAR_EINVAL, std::string("outputs ") + outs[a].name + " and " +
+                                             outs[b].name + " overlap");
+    }
+    return LRAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lr_attnres_route_fwd(const void *V, const void *K, const float *q, void *H, int64_t S,
+                         int64_t N, int64_t d, int64_t r, int mode, int dtype, float eps,
+                         void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(H, "H", 16, data)) ||
+        (rc = check_ptr(K, "K", 16, data && mode == LRAR_MODE_PROJECTED)))
+        return rc;
+    if (mode != LRAR_MODE_PROJECTED && K)
+        return fail(LRAR_EINVAL, "K must be NULL unless keys are projected");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    const Span outs[] = {span("H", H, he * es)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4)};
+    if ((rc = check_aliasing(outs, 1, ins, 3)))
+        return rc;
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_supported(p, false, &why)))
+        return fail(rc, why);
+    if ((rc = lrar::launch_fwd(p, H, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+size_t lr_attnres_route_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int64_t r,
+                                            int mode, int dtype)
+{
+    int64_t ve, ke, he;
+    const std::string saved = g_last_error;
+    const int rc = check_shape(S, N, d, r, mode, dtype, 0.0f, &ve, &ke, &he);
+    g_last_error = saved;
+    if (rc)
+        return 0;
+    lrar::Problem p{nullptr, nullptr, nullptr, S, N, d, r, mode, dtype, 0.0f};
+    return lrar::bwd_workspace_bytes(p);
+}
+
+int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const void *dH, void *dV,
+                         void *dK, float *dq, void *workspace, size_t workspace_bytes,
+                         int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                         float eps, void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(dH, "dH", 16, data)) || (rc = check_ptr(dV, "dV", 16, data)) ||
+        (rc = check_ptr(dq, "dq", 4, true)) || (rc = check_ptr(K, "K", 16, data && proj)) ||
+        (rc = check_ptr(dK, "dK", 16, data && proj)) ||
+        (rc = check_ptr(workspace, "workspace", 16, false)))
+        return rc;
+    if (!proj && (K || dK))
+        return fail(LRAR_EINVAL, "K and dK must be NULL unless keys are projected");
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_supported(p, true, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::bwd_workspace_bytes(p);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    const Span outs[] = {span("dV", dV, ve * es), span("dK", dK, ke * es),
+                         span("dq", dq, r * 4), span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4),
+                        span("dH", dH, he * es)};
+    if ((rc = check_aliasing(outs, 4, ins, 4)))
+        return rc;
+    if ((rc = lrar::launch_bwd(p, dH, dV, dK, dq, workspace, static_cast<hipStream_t>(stream),
+                               &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }
+
+int lr_attnres_abi_version(void) { return LR_ATTNRES_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,172 @@
+// Device-side building blocks of the gfx950 routing kernels: 16-byte vector
+// loads and stores with fp32 widening / bf16 narrowing, and wave64
+// reductions.  Storage types: float, or uint16_t holding bf16 bits.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lrar {
+
+constexpr int kWaveSize = 64;
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Raw<T, VEC>::type is what one lane moves per access: 16 bytes for the
+// vector paths (4 fp32 or 8 bf16), one element for the scalar paths.
+template <typename T, int VEC> struct Raw;
+template <> struct Raw<float, 4> { typedef f32x4_t type; };
+template <> struct Raw<float, 1> { typedef float type; };
+template <> struct Raw<uint16_t, 8> { typedef u32x4_t type; };
+template <> struct Raw<uint16_t, 1> { typedef uint16_t type; };
+
+template <typename T> struct VecOf;
+template <> struct VecOf<float> { static constexpr int value = 4; };
+template <> struct VecOf<uint16_t> { static constexpr int value = 8; };
+
+__device__ __forceinline__ float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Round two fp32 to bf16 (nearest even; gfx950 v_cvt_pk_bf16_f32) and pack.
+__device__ __forceinline__ unsigned pack_bf16x2(float a, float b)
+{
+    f32x2_t v = {a, b};
+    return __builtin_bit_cast(unsigned, __builtin_convertvector(v, bf16x2_t));
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float a)
+{
+    return (uint16_t)(pack_bf16x2(a, 0.0f) & 0xffffu);
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ typename Raw<T, VEC>::type load_raw(const T *p)
+{
+    return *reinterpret_cast<const typename Raw<T, VEC>::type *>(p);
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void store_raw(T *p, typename Raw<T, VEC>::type v)
+{
+    *reinterpret_cast<typename Raw<T, VEC>::type *>(p) = v;
+}
+
+// Widen one raw access to VEC fp32 values (exact).
+__device__ __forceinline__ void widen(const f32x4_t &r, float (&x)[4])
+{
+    x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
+}
+__device__ __forceinline__ void widen(const float &r, float (&x)[1]) { x[0] = r; }
+__device__ __forceinline__ void widen(const u32x4_t &r, float (&x)[8])
+{
+    x[0] = bf16_lo(r.x); x[1] = bf16_hi(r.x);
+    x[2] = bf16_lo(r.y); x[3] = bf16_hi(r.y);
+    x[4] = bf16_lo(r.z); x[5] = bf16_hi(r.z);
+    x[6] = bf16_lo(r.w); x[7] = bf16_hi(r.w);
+}
+__device__ __forceinline__ void widen(const uint16_t &r, float (&x)[1])
+{
+    x[0] = __uint_as_float((unsigned)r << 16);
+}
+
+// Narrow VEC fp32 values to one raw access (bf16: round to nearest even).
+template <typename T, int VEC> struct Narrow;
+template <> struct Narrow<float, 4> {
+    __device__ static f32x4_t run(const float (&x)[4]) { return f32x4_t{x[0], x[1], x[2], x[3]}; }
+};
+template <> struct Narrow<float, 1> {
+    __device__ static float run(const float (&x)[1]) { return x[0]; }
+};
+template <> struct Narrow<uint16_t, 8> {
+    __device__ static u32x4_t run(const float (&x)[8])
+    {
+        return u32x4_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                       pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7])};
+    }
+};
+template <> struct Narrow<uint16_t, 1> {
+    __device__ static uint16_t run(const float (&x)[1]) { return to_bf16(x[0]); }
+};
+
+__device__ __forceinline__ float load_elem(const float *p) { return *p; }
+__device__ __forceinline__ float load_elem(const uint16_t *p)
+{
+    return __uint_as_float((unsigned)*p << 16);
+}
+__device__ __forceinline__ void store_elem(float *p, float v) { *p = v; }
+__device__ __forceinline__ void store_elem(uint16_t *p, float v) { *p = to_bf16(v); }
+
+// Butterfly reductions over the 64 lanes of a wave; every lane gets the result.
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+        v += __shfl_xor(v, m, kWaveSize);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+        v = fmaxf(v, __shfl_xor(v, m, kWaveSize));
+    return v;
+}
+
+// Sum M per-lane values (M a power of two, M <= 64) over the wave with
+// log2(M) halving exchanges followed by plain butterflies: at each halving
+// step a lane keeps the half of its values selected by one lane bit and
+// receives its partner's copy of that half.  On return lane l holds the
+// wave-wide sum of value index multi_sum_index<M>(l).
+template <int M>
+__device__ __forceinline__ float multi_sum(float (&v)[M], int lane)
+{
+    int bit = kWaveSize / 2;
+#pragma unroll
+    for (int half = M / 2; half >= 1; half >>= 1, bit >>= 1) {
+        const bool upper = (lane & bit) != 0;
+#pragma unroll
+        for (int k = 0; k < half; ++k) {
+            float keep = upper ? v[k + half] : v[k];
+            float give = upper ? v[k] : v[k + half];
+            v[k] = keep + __shfl_xor(give, bit, kWaveSize);
+        }
+    }
+    float s = v[0];
+    for (; bit >= 1; bit >>= 1)
+        s += __shfl_xor(s, bit, kWaveSize);
+    return s;
+}
+
+// Value index whose sum multi_sum<M> leaves in lane `lane`: the lane bits
+// 32, 16, ... consumed by the halving steps, most significant first.
+template <int M>
+__device__ __forceinline__ int multi_sum_index(int lane)
+{
+    int idx = 0, bit = kWaveSize / 2;
+#pragma unroll
+    for (int half = M / 2; half >= 1; half >>= 1, bit >>= 1)
+        idx += (lane & bit) ? half : 0;
+    return idx;
+}
+
+// True on exactly one lane per value index after multi_sum<M>.
+template <int M>
+__device__ __forceinline__ bool multi_sum_writer(int lane)
+{
+    constexpr int low_bits = kWaveSize / M;  // lanes sharing one value index
+    return (lane & (low_bits - 1)) == 0;
+}
+
+// Make this wave's LDS writes visible to its other lanes.
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+}  // namespace lrar

@@ -1,0 +1,35 @@
+// Host-side interface between the C ABI layer (argument validation) and the
+// kernel launchers.  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "lr_attnres.h"
+
+namespace lrar {
+
+struct Problem {
+    const void *V;   // [S][N][d]
+    const void *K;   // [S][N][r] (projected keys) or NULL
+    const float *q;  // [r]
+    int64_t S, N, d, r;
+    int mode, dtype;
+    float eps;
+};
+
+// LRAR_OK if a kernel covers the (already validated) problem, else
+// LRAR_EUNSUPPORTED with the reason in *why.  No HIP call.
+int check_supported(const Problem &p, bool bwd, std::string *why);
+
+// Workspace of the backward (per-workgroup dq partials).  No HIP call.
+size_t bwd_workspace_bytes(const Problem &p);
+
+int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err);
+int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
+               hipStream_t st, std::string *err);
+
+}  // namespace lrar

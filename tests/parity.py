@@ -1,0 +1,51 @@
+"""Parity bars between the HIP path and the fp64 oracle.
+
+fp32 storage: normwise relative error <= 1e-5, both max|err| / max|ref| and
+||err||_2 / ||ref||_2.
+bf16 storage (outputs rounded to bf16): values and value gradients
+max|err| <= 2e-2 and ||err||_2 / ||ref||_2 <= 5e-3.  Key gradients grow past
+|dK| = 8, where the bf16 half-ulp alone exceeds 2e-2, so they take
+|err| <= 2e-2 * max(1, |ref|) element by element, with the same relative L2.
+dq is fp32 accumulated over N*S terms: normwise 1e-4 (the fp32 bar scaled
+for the length of the sum), and rel-L2 <= 5e-3.
+"""
+import numpy as np
+
+
+def rel_errors(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.isfinite(got).all(), "non-finite values in the HIP result"
+    d = got - ref
+    ref_max = max(np.abs(ref).max(initial=0.0), 1e-30)
+    ref_l2 = max(np.linalg.norm(ref.ravel()), 1e-30)
+    return np.abs(d).max(initial=0.0), np.abs(d).max(initial=0.0) / ref_max, \
+        np.linalg.norm(d.ravel()) / ref_l2
+
+
+def check_f32(name, got, ref, tol=1e-5):
+    amax, nmax, nl2 = rel_errors(got, ref)
+    assert nmax <= tol and nl2 <= tol, \
+        f"{name}: normwise max {nmax:.3e}, rel-L2 {nl2:.3e} (bar {tol:g})"
+
+
+def check_bf16_value(name, got, ref):
+    amax, nmax, nl2 = rel_errors(got, ref)
+    assert amax <= 2e-2 and nl2 <= 5e-3, \
+        f"{name}: max-abs {amax:.3e} (bar 2e-2), rel-L2 {nl2:.3e} (bar 5e-3)"
+
+
+def check_bf16_key_grad(name, got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    _, _, nl2 = rel_errors(got, ref)
+    worst = (np.abs(got - ref) / np.maximum(1.0, np.abs(ref))).max(initial=0.0)
+    assert worst <= 2e-2 and nl2 <= 5e-3, \
+        f"{name}: scaled max {worst:.3e} (bar 2e-2), rel-L2 {nl2:.3e} (bar 5e-3)"
+
+
+def check_dq(name, got, ref, tol=1e-4):
+    _, nmax, nl2 = rel_errors(got, ref)
+    assert nmax <= tol and nl2 <= min(tol, 5e-3), \
+        f"{name}: normwise max {nmax:.3e}, rel-L2 {nl2:.3e} (bar {tol:g})"

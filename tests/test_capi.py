@@ -1,0 +1,157 @@
+"""The C ABI on the CPU: the library loads, exports what include/lr_attnres.h
+declares, and rejects every invalid call during host-side validation, which
+runs before any HIP call (so no device is touched; no pointer is
+dereferenced on the host)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2607_09694_amd as lr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lr_attnres.h")
+EINVAL, EUNSUPPORTED = 1, 2
+P, SL, F = lr.PROJECTED, lr.SLICED, lr.FULL
+BF16, F32 = 1, 0
+
+# Distinct fake device addresses, far apart and 256-byte aligned.  Validation
+# only compares them; nothing reads through them.
+A, B, C, D, E, G, W = (0x10_0000_0000 * k for k in range(1, 8))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(lr.LIB_PATH):
+        from paper_2607_09694_amd.build import build
+
+        build()
+    return lr.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lr_attnres_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
+                            "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
+                            "lr_attnres_abi_version"])
+    out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s+(\w+)", out))
+    for name in names:
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_abi_version(lib):
+    assert lib.lr_attnres_abi_version() == 1
+
+
+def fwd(lib, V=A, K=None, q=B, H=C, S=4, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_fwd(V, K, q, H, S, N, d, r, mode, dtype, eps, None)
+
+
+def bwd(lib, V=A, K=None, q=B, dH=C, dV=D, dK=None, dq=E, ws=W, wsb=1 << 30, S=4, N=8, d=64,
+        r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_bwd(V, K, q, dH, dV, dK, dq, ws, wsb, S, N, d, r, mode, dtype,
+                                    eps, None)
+
+
+def err(lib):
+    return lib.lr_attnres_last_error().decode()
+
+
+FWD_INVALID = [
+    ("V NULL", dict(V=None), "V is NULL"),
+    ("q NULL", dict(q=None), "q is NULL"),
+    ("H NULL", dict(H=None), "H is NULL"),
+    ("S zero", dict(S=0), "sizes"),
+    ("d zero", dict(d=0), "sizes"),
+    ("r zero", dict(r=0), "sizes"),
+    ("N negative", dict(N=-1), "sizes"),
+    ("sliced r > d", dict(r=65), "r <= d"),
+    ("full r != d", dict(mode=F, r=8), "r == d"),
+    ("K outside projected", dict(K=G), "K must be NULL"),
+    ("projected without K", dict(mode=P, K=None), "K is NULL"),
+    ("unknown mode", dict(mode=7), "mode"),
+    ("unknown dtype", dict(dtype=5), "storage"),
+    ("eps negative", dict(eps=-1.0), "eps"),
+    ("eps nan", dict(eps=float("nan")), "eps"),
+    ("eps inf", dict(eps=float("inf")), "eps"),
+    ("V misaligned", dict(V=A + 2), "aligned"),
+    ("H misaligned", dict(H=C + 8), "aligned"),
+    ("q misaligned", dict(q=B + 2), "aligned"),
+    ("H overlaps V", dict(H=A + 256), "overlaps"),
+    ("H overlaps q", dict(H=B - 16), "overlaps"),
+    ("overflow", dict(S=1 << 40, N=1 << 20, d=1 << 10), "overflow"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", FWD_INVALID, ids=[c[0] for c in FWD_INVALID])
+def test_forward_rejects(lib, name, kw, msg):
+    assert fwd(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+BWD_INVALID = [
+    ("dH NULL", dict(dH=None), "dH is NULL"),
+    ("dV NULL", dict(dV=None), "dV is NULL"),
+    ("dq NULL", dict(dq=None), "dq is NULL"),
+    ("dK outside projected", dict(dK=G), "must be NULL"),
+    ("projected without dK", dict(mode=P, K=G, dK=None), "dK is NULL"),
+    ("workspace too small", dict(mode=P, K=G, dK=G + 0x1_0000_0000, wsb=4), "workspace"),
+    ("workspace NULL", dict(ws=None), "workspace"),
+    ("dV overlaps V", dict(dV=A + 64), "overlaps"),
+    ("dV overlaps dH", dict(dV=C), "overlaps"),
+    ("dq overlaps dV", dict(dq=D + 16), "overlap"),
+    ("workspace overlaps dV", dict(ws=D + 64), "overlap"),
+    ("dV misaligned", dict(dV=D + 4), "aligned"),
+    ("eps nan", dict(eps=float("nan")), "eps"),
+    ("full r != d", dict(mode=F, r=8), "r == d"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", BWD_INVALID, ids=[c[0] for c in BWD_INVALID])
+def test_backward_rejects(lib, name, kw, msg):
+    assert bwd(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_unsupported_shapes(lib):
+    assert fwd(lib, S=1025) == EUNSUPPORTED
+    assert "1024" in err(lib)
+    assert bwd(lib, S=513) == EUNSUPPORTED
+    assert bwd(lib, mode=P, K=G, dK=G + 0x1_0000_0000, r=257, d=1024) == EUNSUPPORTED
+    assert bwd(lib, mode=F, r=8192, d=8192) == EUNSUPPORTED
+    assert fwd(lib, mode=F, r=8192, d=8192) == EUNSUPPORTED
+    assert fwd(lib, N=(1 << 30) + 1, S=1, d=8, r=8) == EUNSUPPORTED
+
+
+def test_workspace_query(lib):
+    q = lib.lr_attnres_route_bwd_workspace_bytes
+    # per-workgroup dq partials: ceil(N / tokens per workgroup) x r fp32
+    assert q(64, 16384, 2048, 32, P, BF16) > 0
+    assert q(64, 16384, 2048, 32, P, BF16) % 4 == 0
+    assert q(49, 16384, 1024, 1024, F, BF16) >= 1024 * 4
+    assert q(4, 0, 64, 8, SL, BF16) == 0
+    assert q(0, 8, 64, 8, SL, BF16) == 0          # invalid -> 0
+    assert q(4, 8, 64, 8, 9, BF16) == 0           # unknown mode -> 0
+
+
+def test_error_text_is_per_call(lib):
+    assert fwd(lib, S=0) == EINVAL
+    assert err(lib) != ""
+    assert fwd(lib, V=None) == EINVAL
+    assert "V is NULL" in err(lib)
+
+
+def test_python_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError, match="not built"):
+        lr.load_library(str(tmp_path / "missing.so"))

@@ -1,0 +1,306 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Small cases span several workgroup tiles, a ragged token tail, every code
+path (vector and scalar loads, masked column chunks, column-split forward,
+S above one wave, unaligned sliced tails) and the degenerate cases.  The
+full-size cases run at the benchmark's launch configuration and compare
+sampled tokens against the oracle computed token by token (dq over all N).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import (FULL, PROJECTED, SLICED, bf16_tensor_to_bits,
+                                         f32_from_bf16_bits, make_device_problem,
+                                         make_host_problem)
+from parity import check_bf16_key_grad, check_bf16_value, check_dq, check_f32
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+NAMES = {PROJECTED: "P", SLICED: "S", FULL: "F"}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(x).to(dev)
+
+
+def to_host(t):
+    """Device tensor -> numpy fp32 (bf16 widened exactly)."""
+    if t.dtype == torch.bfloat16:
+        return f32_from_bf16_bits(bf16_tensor_to_bits(t))
+    return t.detach().cpu().numpy()
+
+
+def host_bits(t):
+    """Device tensor -> the exact bytes the oracle reads (uint16 for bf16)."""
+    if t.dtype == torch.bfloat16:
+        return bf16_tensor_to_bits(t)
+    return t.detach().contiguous().cpu().numpy()
+
+
+def check_values(name, dtype, got, ref):
+    (check_f32 if dtype == "f32" else check_bf16_value)(name, got, ref)
+
+
+def check_key_grad(name, dtype, got, ref):
+    (check_f32 if dtype == "f32" else check_bf16_key_grad)(name, got, ref)
+
+
+# (mode, storage, S, N, d, r): every forward / backward code path.
+CASES = [
+    (SLICED, "f32", 8, 256, 64, 8),          # the small fp32 sliced workload
+    (PROJECTED, "bf16", 49, 130, 1024, 16),  # model shape, ragged token tail
+    (PROJECTED, "bf16", 64, 67, 2048, 32),   # fwd+bwd workload shape
+    (PROJECTED, "bf16", 5, 9, 1000, 8),      # masked column chunk
+    (PROJECTED, "bf16", 3, 5, 100, 4),       # scalar (unvectorised) path
+    (PROJECTED, "f32", 65, 33, 256, 16),     # S above one wave
+    (PROJECTED, "f32", 73, 17, 1032, 7),     # scalar key loads, S = 73
+    (PROJECTED, "bf16", 1, 40, 512, 16),     # single source
+    (PROJECTED, "bf16", 9, 11, 512, 1),      # rank-1 keys
+    (SLICED, "bf16", 49, 130, 1024, 8),
+    (SLICED, "bf16", 49, 130, 1024, 64),
+    (SLICED, "bf16", 7, 21, 1000, 12),       # tail not vector aligned
+    (SLICED, "f32", 64, 19, 2048, 64),
+    (SLICED, "f32", 2, 11, 36, 36),          # r = d
+    (SLICED, "bf16", 5, 6, 4096, 256),       # widest bf16 backward row, max rank
+    (FULL, "bf16", 49, 66, 1024, 1024),
+    (FULL, "f32", 9, 13, 200, 200),
+    (FULL, "bf16", 5, 7, 72, 72),
+    (FULL, "bf16", 3, 5, 4096, 4096),
+]
+
+
+def _id(c):
+    return f"{NAMES[c[0]]}-{c[1]}-S{c[2]}-N{c[3]}-d{c[4]}-r{c[5]}"
+
+
+@pytest.mark.parametrize("case", CASES, ids=_id)
+def test_forward_matches_oracle(dev, case):
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S * 1000 + N, with_dH=True)
+    H = lr.route_fwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    torch.cuda.synchronize()
+    ref = oracle.route_fwd(p.V, p.K, p.q, mode, r=p.r)
+    check_values("H", dtype, to_host(H), ref)
+
+
+@pytest.mark.parametrize("case", CASES, ids=_id)
+def test_backward_matches_oracle(dev, case):
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S * 1000 + N + 1, with_dH=True)
+    dV, dK, dq = lr.route_bwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev),
+                              to_dev(p.dH, dev), mode)
+    torch.cuda.synchronize()
+    dV_ref, dK_ref, dq_ref = oracle.route_bwd(p.V, p.K, p.q, p.dH, mode, r=p.r)
+    check_values("dV", dtype, to_host(dV), dV_ref)
+    if mode == PROJECTED:
+        check_key_grad("dK", dtype, to_host(dK), dK_ref)
+    else:
+        assert dK is None
+    check_dq("dq", to_host(dq), dq_ref, tol=1e-5 if dtype == "f32" else 1e-4)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_column_split_forward(dev, mode, dtype):
+    """Rows wider than one wave's registers split into column blocks; each
+    block recomputes the r-dimensional scores."""
+    d = 4100 if dtype == "f32" else 8200
+    p = make_host_problem(mode, 3, 5, d, 16, dtype=dtype, seed=5)
+    H = lr.route_fwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    torch.cuda.synchronize()
+    check_values("H", dtype, to_host(H), oracle.route_fwd(p.V, p.K, p.q, mode, r=p.r))
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED, FULL])
+def test_empty_token_set(dev, mode):
+    """N = 0: the forward writes nothing, the backward's dq is exactly zero."""
+    S, d, r = 4, 64, 64 if mode == FULL else 8
+    V = torch.empty((S, 0, d), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((S, 0, r), dtype=torch.bfloat16, device=dev) if mode == PROJECTED else None
+    q = torch.ones((r,), dtype=torch.float32, device=dev)
+    H = lr.route_fwd(V, K, q, mode)
+    assert H.shape == (0, d)
+    dq = torch.full((r,), float("nan"), dtype=torch.float32, device=dev)
+    _, _, dq = lr.route_bwd(V, K, q, torch.empty((0, d), dtype=torch.bfloat16, device=dev),
+                            mode, out=(torch.empty_like(V),
+                                       torch.empty_like(K) if K is not None else None, dq))
+    torch.cuda.synchronize()
+    assert (dq.cpu() == 0).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED, FULL])
+def test_single_source_is_bitwise_copy(dev, mode, dtype):
+    """S = 1: alpha = 1 exactly, so h = o_0 bit for bit (and dV = dH for
+    projected keys)."""
+    d = 1024
+    p = make_host_problem(mode, 1, 77, d, 16, dtype=dtype, seed=11, with_dH=True)
+    V = to_dev(p.V, dev)
+    H = lr.route_fwd(V, to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    torch.cuda.synchronize()
+    assert torch.equal(H.view(torch.int16 if dtype == "bf16" else torch.int32),
+                       V[0].view(torch.int16 if dtype == "bf16" else torch.int32))
+    if mode == PROJECTED:
+        dH = to_dev(p.dH, dev)
+        dV, _, _ = lr.route_bwd(V, to_dev(p.K, dev), to_dev(p.q, dev), dH, mode)
+        torch.cuda.synchronize()
+        assert torch.equal(dV[0], dH)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED, FULL])
+def test_zero_query_is_uniform_mean(dev, mode):
+    """q = 0 (the paper's initialisation) gives the plain mean of the sources."""
+    p = make_host_problem(mode, 12, 50, 512, 16, dtype="f32", seed=12)
+    q = np.zeros_like(p.q)
+    H = lr.route_fwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(q, dev), mode)
+    torch.cuda.synchronize()
+    check_f32("H", to_host(H), p.V.astype(np.float64).mean(axis=0))
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED, FULL])
+def test_peaked_weights_and_outlier_channels(dev, mode):
+    """Numerics stress: queries x8 (near one-hot weights) and a few value
+    channels x30 (activation outliers)."""
+    S, N, d, r = 49, 70, 1024, 16
+    p = make_host_problem(mode, S, N, d, r, dtype="f32", seed=13, q_scale=8.0, with_dH=True)
+    V = p.V.copy()
+    V[:, :, [3, 500, 1000]] *= 30.0
+    if mode != PROJECTED:
+        V[:, :, -2] *= 30.0  # an outlier inside the sliced key
+    H = lr.route_fwd(to_dev(V, dev), to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    dV, dK, dq = lr.route_bwd(to_dev(V, dev), to_dev(p.K, dev), to_dev(p.q, dev),
+                              to_dev(p.dH, dev), mode)
+    torch.cuda.synchronize()
+    check_f32("H", to_host(H), oracle.route_fwd(V, p.K, p.q, mode, r=p.r))
+    dV_ref, dK_ref, dq_ref = oracle.route_bwd(V, p.K, p.q, p.dH, mode, r=p.r)
+    check_f32("dV", to_host(dV), dV_ref)
+    if mode == PROJECTED:
+        check_f32("dK", to_host(dK), dK_ref)
+    check_dq("dq", to_host(dq), dq_ref, tol=1e-5)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED, FULL])
+def test_bitwise_reproducible_and_fully_written(dev, mode):
+    """Two runs give identical bits (dq is reduced in a fixed order), and
+    NaN-poisoned output buffers are completely overwritten."""
+    S, N, d, r = 33, 300, 1024, 32
+    p = make_host_problem(mode, S, N, d, r, dtype="bf16", seed=14, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    outs = []
+    for _ in range(2):
+        H = torch.full((N, d), float("nan"), dtype=torch.bfloat16, device=dev)
+        dV = torch.full_like(V, float("nan"))
+        dK = torch.full_like(K, float("nan")) if K is not None else None
+        dq = torch.full((p.r,), float("nan"), dtype=torch.float32, device=dev)
+        lr.route_fwd(V, K, q, mode, out=H)
+        lr.route_bwd(V, K, q, dH, mode, out=(dV, dK, dq))
+        torch.cuda.synchronize()
+        for t in (H, dV, dK, dq):
+            if t is not None:
+                assert not torch.isnan(t).any()
+        outs.append((H, dV, dK, dq))
+    for a, b in zip(outs[0], outs[1]):
+        if a is not None:
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, at the launch configuration the benchmark times.
+# ---------------------------------------------------------------------------
+
+def sample_tokens(N, k=64, seed=0):
+    rng = np.random.default_rng(seed)
+    edge = list(range(4)) + list(range(N - 4, N))
+    mid = rng.choice(np.arange(4, N - 4), size=k - len(edge), replace=False)
+    return np.sort(np.concatenate([edge, mid])).astype(np.int64)
+
+
+def sampled(t, idx, axis):
+    return host_bits(t.index_select(axis, torch.from_numpy(idx).to(t.device)))
+
+
+@pytest.fixture(scope="module")
+def model_stack(dev):
+    """Value stack of the ~0.5B model (d = 1024, 49 sources, N = 8 x 2048)
+    with projected keys (r = 16) and one query per site."""
+    g = make_device_problem(PROJECTED, 49, 16384, 1024, 16, dev, seed=0, n_queries=49)
+    yield g
+    del g
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("S", [1, 2, 25, 49])
+def test_model_pass_projected_sites(dev, model_stack, S):
+    V, K, q = model_stack["V"][:S], model_stack["K"][:S], model_stack["q"][S - 1].contiguous()
+    H = lr.route_fwd(V, K, q, PROJECTED)
+    torch.cuda.synchronize()
+    idx = sample_tokens(V.shape[1], seed=S)
+    ref = oracle.route_fwd(sampled(V, idx, 1), sampled(K, idx, 1), q.cpu().numpy(),
+                           oracle.PROJECTED)
+    check_bf16_value("H", to_host(H.index_select(0, torch.from_numpy(idx).to(dev))), ref)
+
+
+@pytest.mark.parametrize("r", [8, 16, 32, 64])
+def test_model_pass_sliced_site49(dev, model_stack, r):
+    V = model_stack["V"]
+    q = (torch.randn((r,), generator=torch.Generator(device=dev).manual_seed(r), device=dev)
+         / r ** 0.5)
+    H = lr.route_fwd(V, None, q, SLICED)
+    torch.cuda.synchronize()
+    idx = sample_tokens(V.shape[1], seed=100 + r)
+    ref = oracle.route_fwd(sampled(V, idx, 1), None, q.cpu().numpy(), oracle.SLICED, r=r)
+    check_bf16_value("H", to_host(H.index_select(0, torch.from_numpy(idx).to(dev))), ref)
+
+
+def test_full_rank_site49(dev, model_stack):
+    V = model_stack["V"]
+    q = torch.randn((1024,), generator=torch.Generator(device=dev).manual_seed(7),
+                    device=dev) / 32.0
+    H = lr.route_fwd(V, None, q, FULL)
+    torch.cuda.synchronize()
+    idx = sample_tokens(V.shape[1], seed=7)
+    ref = oracle.route_fwd(sampled(V, idx, 1), None, q.cpu().numpy(), oracle.FULL)
+    check_bf16_value("H", to_host(H.index_select(0, torch.from_numpy(idx).to(dev))), ref)
+
+
+def test_projected_fwd_bwd_d2048_full_size(dev, model_stack):
+    """d = 2048, r = 32, N = 4 x 4096, S = 64 (V is exactly 2^32 bytes): H, dV
+    and dK on sampled tokens, dq over all N tokens."""
+    g = make_device_problem(PROJECTED, 64, 16384, 2048, 32, dev, seed=0, with_dH=True)
+    V, K, q, dH = g["V"], g["K"], g["q"][0].contiguous(), g["dH"]
+    H = lr.route_fwd(V, K, q, PROJECTED)
+    dV, dK, dq = lr.route_bwd(V, K, q, dH, PROJECTED)
+    torch.cuda.synchronize()
+    idx = sample_tokens(V.shape[1], seed=5)
+    ti = torch.from_numpy(idx).to(dev)
+    Vs, Ks, dHs = sampled(V, idx, 1), sampled(K, idx, 1), sampled(dH, idx, 0)
+    qn = q.cpu().numpy()
+    check_bf16_value("H", to_host(H.index_select(0, ti)),
+                     oracle.route_fwd(Vs, Ks, qn, oracle.PROJECTED))
+    dV_ref, dK_ref, _ = oracle.route_bwd(Vs, Ks, qn, dHs, oracle.PROJECTED)
+    check_bf16_value("dV", to_host(dV.index_select(1, ti)), dV_ref)
+    check_bf16_key_grad("dK", to_host(dK.index_select(1, ti)), dK_ref)
+    # dq sums over every token: the oracle walks all N in chunks.
+    Vh, Kh, dHh = host_bits(V), host_bits(K), host_bits(dH)
+    del H, dV, dK, g
+    torch.cuda.empty_cache()
+    dq_ref = np.zeros(32)
+    for n0 in range(0, 16384, 1024):
+        _, _, part = oracle.route_bwd(Vh, Kh, qn, dHh, oracle.PROJECTED, n0=n0, n1=n0 + 1024)
+        dq_ref += part
+    check_dq("dq", to_host(dq), dq_ref)
