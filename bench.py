@@ -1,0 +1,343 @@
+"""Benchmark of the LR-AttnRes depth-routing path on one MI355X.
+
+One step = one pass of the whole routing hot path (scores, depth softmax,
+value mix; then the backward's recomputation, value-gradient dots, dV, dK and
+dq) over one batch: projected low-rank keys, d = 2048, r = 32, N = 4 x 4096
+tokens, S = 64 sources, bf16 values and keys, fp32 arithmetic, fp32 q / dq.
+Inputs are synthetic Gaussians resident in HBM before the timed region.
+
+Prints ONE JSON line: tokens/s of the step, the HBM roofline of the dominant
+kernel (the backward) from HIP events on its stream, the fp64 CPU oracle
+timed on a bounded token sample, and the other measured workloads (the
+49-site model pass with projected and sliced keys, the full-rank baseline at
+S = 49, the forward alone) under "extra".
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+METRIC = "depth-routing tokens/s and achieved HBM TB/s (% of peak), fwd and fwd+bwd"
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_09694_amd", "csrc", "route_kernels.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "route_bwd_lr_d2048_counters.txt")
+
+# Main workload: projected keys, forward + backward.
+S5, N5, D5, R5 = 64, 16384, 2048, 32
+
+
+def fwd_bytes(S, N, d, r, mode):
+    """Algorithmic HBM bytes of one forward call (bf16): every value row once,
+    projected keys once (sliced keys are a view of the values), H written."""
+    key = r if mode == 0 else 0
+    return S * N * (d + key) * 2 + N * d * 2
+
+
+def bwd_bytes(S, N, d, r):
+    """Projected-key backward (bf16): V and K read, dV and dK written, dH read."""
+    return 2 * S * N * (d + r) * 2 + N * d * 2
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(os.path.dirname(KERNEL_SRC))):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(algo_bytes):
+    """HBM bytes per launch of the backward kernel from committed rocprofv3
+    counter summaries, if they were taken on the current kernel sources."""
+    try:
+        with open(COUNTERS) as f:
+            c = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if c.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def load_probe():
+    """Streaming copy / read kernels of known traffic (benchmark helper)."""
+    import ctypes
+
+    path = os.path.join(ROOT, "paper_2607_09694_amd", "libhbmprobe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build the package first")
+    lib = ctypes.CDLL(path)
+    for f in (lib.hbm_probe_copy, lib.hbm_probe_read):
+        f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_longlong, ctypes.c_int,
+                      ctypes.c_void_p]
+        f.restype = ctypes.c_int
+    return lib
+
+
+def probe_ceilings(torch, dev, reps, warmup):
+    """HBM ceilings measured on this GPU with 4 GiB streams: read only, and
+    read + write (copy), each the best over a few grid sizes."""
+    probe = load_probe()
+    nbytes = 4 << 30
+    src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream().cuda_stream
+    best = {"read_GBps": 0.0, "copy_GBps": 0.0}
+    for blocks in (1024, 2048, 8192, 65536):
+        for key, fn, mult in (
+                ("read_GBps", lambda: probe.hbm_probe_read(src.data_ptr(), sink.data_ptr(),
+                                                            nbytes, blocks, st), 1),
+                ("copy_GBps", lambda: probe.hbm_probe_copy(src.data_ptr(), dst.data_ptr(),
+                                                            nbytes, blocks, st), 2)):
+            ts = time_calls(torch, lambda: check_probe(fn()), reps, warmup)
+            best[key] = max(best[key], round(mult * nbytes / (np.median(ts) * 1e-3) / 1e9, 1))
+    del src, dst
+    return best
+
+
+def check_probe(rc):
+    if rc != 0:
+        raise RuntimeError(f"hbm probe launch failed ({rc})")
+
+
+class Flusher:
+    """Untimed write of a 1 GiB buffer between timed calls, so that the 256 MB
+    memory-side cache (MALL) does not serve data a previous call left in it."""
+
+    def __init__(self, torch, dev):
+        self.buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        self.k = 0.0
+
+    def __call__(self):
+        self.k += 1.0
+        self.buf.fill_(self.k)
+
+
+def time_calls(torch, fn, reps, warmup, flush=None):
+    """Per-call device time (ms) from HIP events on the current stream."""
+    st = torch.cuda.current_stream()
+    for _ in range(warmup):
+        fn()
+    ts = []
+    for _ in range(reps):
+        if flush:
+            flush()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        fn()
+        b.record(st)
+        ts.append((a, b))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ts]
+
+
+def cpu_baseline(g, q, target_s=10.0, chunk=1024):
+    """fp64 oracle (as it stands) on the host: fwd + bwd of the main workload
+    in 1024-token chunks, in order, repeated over the whole token set until
+    about target_s seconds have passed.  Host copies of the inputs are made
+    before timing."""
+    import oracle
+    from paper_2607_09694_amd.inputs import bf16_tensor_to_bits
+
+    V, K, dH = (bf16_tensor_to_bits(g[k]) for k in ("V", "K", "dH"))
+    done, spent = 0, 0.0
+    while spent < target_s:
+        n0 = done % N5
+        n1 = min(N5, n0 + chunk)
+        t0 = time.perf_counter()
+        oracle.route_fwd(V, K, q, oracle.PROJECTED, n0=n0, n1=n1)
+        oracle.route_bwd(V, K, q, dH, oracle.PROJECTED, n0=n0, n1=n1)
+        spent += time.perf_counter() - t0
+        done += n1 - n0
+    return {"value": round(done / spent, 1), "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{done} tokens ({done / N5:.2f} passes over all {N5} tokens) of the main "
+                      f"workload, fwd+bwd in fp64, {spent:.1f} s"}
+
+
+def extras(torch, lr, dev, reps, warmup):
+    """The other workloads: the 49-site forward model pass (projected r=16 and
+    sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
+    kernel ceiling.  Cold: the MALL is flushed before every timed call."""
+    from paper_2607_09694_amd.inputs import FULL, PROJECTED, SLICED, make_device_problem
+
+    out = {}
+    flush = Flusher(torch, dev)
+    N, d = 16384, 1024
+    g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=49)
+    V, K, Q = g["V"], g["K"], g["q"]
+    H = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+
+    def model_pass(mode, r, queries):
+        per_site, nbytes = [], 0
+        for t in range(1, 50):
+            Kt = K[:t] if mode == PROJECTED else None
+            qt = queries[t - 1]
+            ts = time_calls(torch, lambda: lr.route_fwd(V[:t], Kt, qt, mode, out=H),
+                            reps, warmup, flush)
+            per_site.append(float(np.median(ts)))
+            nbytes += fwd_bytes(t, N, d, r, mode)
+        total_ms = sum(per_site)
+        return {"total_ms": total_ms, "tokens_per_s": N / (total_ms * 1e-3),
+                "algo_GBps": nbytes / (total_ms * 1e-3) / 1e9,
+                "frac_of_peak": nbytes / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "site49_ms": per_site[-1]}
+
+    out["model_pass_projected_r16"] = model_pass(PROJECTED, 16, Q)
+    gen = torch.Generator(device=dev)
+    for r in (8, 16, 32, 64):
+        gen.manual_seed(r)
+        qs = torch.randn((49, r), generator=gen, device=dev) / r ** 0.5
+        out[f"model_pass_sliced_r{r}"] = model_pass(SLICED, r, qs)
+
+    # Head to head at S = 49: full-rank (two passes over V) vs low-rank.
+    gen.manual_seed(1024)
+    qf = torch.randn((d,), generator=gen, device=dev) / d ** 0.5
+    head = {}
+    for name, fn, nbytes in (
+            ("full_rank", lambda: lr.route_fwd(V, None, qf, FULL, out=H),
+             fwd_bytes(49, N, d, d, FULL)),
+            ("projected_r16", lambda: lr.route_fwd(V, K, Q[48], PROJECTED, out=H),
+             fwd_bytes(49, N, d, 16, PROJECTED)),
+            ("sliced_r16", lambda: lr.route_fwd(V, None, Q[48], SLICED, out=H),
+             fwd_bytes(49, N, d, 16, SLICED))):
+        ts = time_calls(torch, fn, reps, warmup, flush)
+        head[name] = {"median_ms": float(np.median(ts)), "min_ms": float(np.min(ts)),
+                      "max_ms": float(np.max(ts)),
+                      "algo_GBps": nbytes / (np.median(ts) * 1e-3) / 1e9}
+    out["site49_head_to_head"] = head
+
+    out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
+    del g, V, K, H, flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--counters-pass", action="store_true",
+                    help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
+                         "backward calls of the main workload (for rocprofv3 --pmc runs)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only; --gpus must be 1 "
+              "(tokens are independent, see the sharding notes in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_09694_amd as lr
+    from paper_2607_09694_amd.inputs import PROJECTED, make_device_problem
+
+    lr.load_library()
+    dev = torch.device("cuda:0")
+    print(f"bench: generating inputs S={S5} N={N5} d={D5} r={R5}", file=sys.stderr, flush=True)
+    g = make_device_problem(PROJECTED, S5, N5, D5, R5, dev, seed=0, with_dH=True)
+    V, K, q, dH = g["V"], g["K"], g["q"][0].contiguous(), g["dH"]
+    H = torch.empty((N5, D5), dtype=torch.bfloat16, device=dev)
+    dV, dK = torch.empty_like(V), torch.empty_like(K)
+    dq = torch.empty((R5,), dtype=torch.float32, device=dev)
+    ws = torch.empty((lr.route_bwd_workspace_bytes(S5, N5, D5, R5, PROJECTED, V.dtype),),
+                     dtype=torch.uint8, device=dev)
+    st = torch.cuda.current_stream()
+
+    def step(ev=None):
+        lr.route_fwd(V, K, q, PROJECTED, out=H)
+        if ev is not None:
+            ev[0].record(st)
+        lr.route_bwd(V, K, q, dH, PROJECTED, out=(dV, dK, dq), workspace=ws)
+        if ev is not None:
+            ev[1].record(st)
+
+    if args.counters_pass:
+        probe = load_probe()
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            check_probe(probe.hbm_probe_copy(src.data_ptr(), dst.data_ptr(), 1 << 30, 8192,
+                                             st.cuda_stream))
+        torch.cuda.synchronize()
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        print("bench: counters pass done", file=sys.stderr, flush=True)
+        return
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    print(f"bench: timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    bwd_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    # Forward alone (same inputs), for the record.
+    fwd_ts = time_calls(torch, lambda: lr.route_fwd(V, K, q, PROJECTED, out=H), args.steps, 2)
+    fwd_ms = float(np.mean(fwd_ts))
+
+    b_bwd = bwd_bytes(S5, N5, D5, R5)
+    achieved = b_bwd / (bwd_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": "route_bwd_lr (+ dq_reduce)",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(b_bwd),
+                "algo_bytes_per_launch": b_bwd, "avg_launch_ms": round(bwd_ms, 4)}
+
+    result = {
+        "metric": METRIC,
+        "value": round(N5 / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "projected-key LR-AttnRes routing fwd+bwd, d=2048, r=32, "
+                               "N=4x4096 tokens, S=64 sources",
+                   "global_batch": N5, "seq_len": 4096, "sources": S5, "d": D5, "r": R5,
+                   "storage": "bf16", "parallelism": "single GPU"},
+        "roofline": roofline,
+        "fwd": {"avg_ms": round(fwd_ms, 4),
+                "tokens_per_s": round(N5 / (fwd_ms * 1e-3), 1),
+                "algo_GBps": round(fwd_bytes(S5, N5, D5, R5, 0) / (fwd_ms * 1e-3) / 1e9, 1)},
+    }
+    if not args.no_cpu:
+        print("bench: CPU oracle baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(g, q.cpu().numpy())
+    del g, V, K, dH, dV, dK, H, ws
+    torch.cuda.empty_cache()
+    if not args.no_extra:
+        print("bench: other workloads", file=sys.stderr, flush=True)
+        result["extra"] = extras(torch, lr, dev, reps=20, warmup=3)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

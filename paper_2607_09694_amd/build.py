@@ -12,6 +12,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblrattnres.so")
 SOURCES = ["route_kernels.hip", "capi.cpp"]
+# Benchmark-only helper: streaming copy / read kernels of known traffic.
+PROBE_LIB = os.path.join(PKG, "libhbmprobe.so")
+PROBE_SOURCES = ["hbm_probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # gfx950 only.  Packed fp32 VALU ops are disabled for every HIP translation
@@ -22,7 +25,14 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link liblrattnres.so next to this file."""
+    """Compile every source and link liblrattnres.so (and the benchmark's
+    libhbmprobe.so) next to this file."""
+    _build_lib(SOURCES, LIB, verbose)
+    _build_lib(PROBE_SOURCES, PROBE_LIB, verbose)
+    return LIB
+
+
+def _build_lib(sources, lib, verbose):
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
 
@@ -36,15 +46,14 @@ def build(verbose: bool = False) -> str:
             print(res.stderr, file=sys.stderr)
         return obj
 
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + ".tmp"
+    with ThreadPoolExecutor(max_workers=len(sources)) as ex:
+        objs = list(ex.map(compile_one, sources))
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":

@@ -54,6 +54,28 @@ __device__ __forceinline__ void store_raw(T *p, typename Raw<T, VEC>::type v)
     *reinterpret_cast<typename Raw<T, VEC>::type *>(p) = v;
 }
 
+// Streaming variants: data touched exactly once, marked non-temporal so it
+// does not displace reusable lines (keys, the token's dH row) in the caches.
+template <typename T, int VEC, bool NT>
+__device__ __forceinline__ typename Raw<T, VEC>::type load_stream(const T *p)
+{
+    typedef typename Raw<T, VEC>::type raw_t;
+    if constexpr (NT)
+        return __builtin_nontemporal_load(reinterpret_cast<const raw_t *>(p));
+    else
+        return *reinterpret_cast<const raw_t *>(p);
+}
+
+template <typename T, int VEC, bool NT>
+__device__ __forceinline__ void store_stream(T *p, typename Raw<T, VEC>::type v)
+{
+    typedef typename Raw<T, VEC>::type raw_t;
+    if constexpr (NT)
+        __builtin_nontemporal_store(v, reinterpret_cast<raw_t *>(p));
+    else
+        *reinterpret_cast<raw_t *>(p) = v;
+}
+
 // Widen one raw access to VEC fp32 values (exact).
 __device__ __forceinline__ void widen(const f32x4_t &r, float (&x)[4])
 {

@@ -30,6 +30,20 @@ namespace lrar {
 constexpr int kWaves = 4;                    // token waves per workgroup
 constexpr int kBlock = kWaves * kWaveSize;   // 256 threads
 
+// Streaming choices for the value rows (read once) and for H / dV (written
+// once), set by measurement on MI355X: non-temporal accesses gave +12% on
+// the forward and +9% on the backward at d = 2048, S = 64.
+constexpr bool kNtLoad = true;
+constexpr bool kNtStore = true;
+
+// Sources whose value rows one lane has in flight in the forward mix.
+template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
+// Sources loaded ahead in the backward stream (divides 8, the number of
+// sources per batched reduction of the dots dH . o_i).
+template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 4 ? 2 : 4; };
+// Tokens per wave in the backward of projected / sliced keys.
+constexpr int kBwdTokensPerWave = 2;
+
 // ---------------------------------------------------------------------------
 // Scores and softmax (Eqs. lr_key_norm and lr_attnres_weight)
 // ---------------------------------------------------------------------------
@@ -97,9 +111,6 @@ __device__ void depth_softmax(const float *s, float *alpha, int S, int lane)
 // The value stream (Eq. lr_attnres_output): h = sum_i alpha_i o_i
 // ---------------------------------------------------------------------------
 
-// Sources per load batch: about 16 outstanding 16-byte loads per lane.
-template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 16 ? 1 : 16 / NCH; };
-
 // vbase points at column (col0 + lane*VEC) of source 0's row of the token;
 // chunk c of source i is at vbase + i*plane + c*64*VEC.
 template <typename T, int VEC, int NCH, bool FULLCOLS>
@@ -122,8 +133,8 @@ __device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t pla
 #pragma unroll
             for (int c = 0; c < NCH; ++c)
                 if (FULLCOLS || ok[c])
-                    raw[u][c] = load_raw<T, VEC>(vbase + (size_t)(i + u) * plane +
-                                                 c * kWaveSize * VEC);
+                    raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + (size_t)(i + u) * plane +
+                                                             c * kWaveSize * VEC);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const float a = alpha[i + u];
@@ -145,7 +156,8 @@ __device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t pla
         for (int c = 0; c < NCH; ++c) {
             if (FULLCOLS || ok[c]) {
                 float x[VEC];
-                widen(load_raw<T, VEC>(vbase + (size_t)i * plane + c * kWaveSize * VEC), x);
+                widen(load_stream<T, VEC, kNtLoad>(vbase + (size_t)i * plane +
+                                                   c * kWaveSize * VEC), x);
 #pragma unroll
                 for (int e = 0; e < VEC; ++e)
                     acc[c][e] = fmaf(a, x[e], acc[c][e]);
@@ -161,7 +173,8 @@ __device__ __forceinline__ void store_row(T *__restrict__ base, const bool (&ok)
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
         if (FULLCOLS || ok[c])
-            store_raw<T, VEC>(base + c * kWaveSize * VEC, Narrow<T, VEC>::run(acc[c]));
+            store_stream<T, VEC, kNtStore>(base + c * kWaveSize * VEC,
+                                           Narrow<T, VEC>::run(acc[c]));
 }
 
 // ---------------------------------------------------------------------------
@@ -335,37 +348,45 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
         }
         const T *vbase = V + (size_t)n * d + col;
         T *dvbase = dV + (size_t)n * d + col;
+        constexpr int L = BwdInflight<NCH>::value;
         for (int i0 = 0; i0 < S; i0 += 8) {
             float part[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                float p = 0.0f;
-                if (i0 + u < S) {
-                    const float a = alpha[i0 + u];
-                    raw_t raw[NCH];
+            for (int h = 0; h < 8; h += L) {
+                raw_t raw[L][NCH];
 #pragma unroll
-                    for (int c = 0; c < NCH; ++c)
-                        if (FULLCOLS || ok[c])
-                            raw[c] = load_raw<T, VEC>(vbase + (size_t)(i0 + u) * plane +
-                                                      c * kWaveSize * VEC);
+                for (int u = 0; u < L; ++u)
+                    if (i0 + h + u < S)
 #pragma unroll
-                    for (int c = 0; c < NCH; ++c) {
-                        if (FULLCOLS || ok[c]) {
-                            float x[VEC], y[VEC];
-                            widen(raw[c], x);
+                        for (int c = 0; c < NCH; ++c)
+                            if (FULLCOLS || ok[c])
+                                raw[u][c] = load_stream<T, VEC, kNtLoad>(
+                                    vbase + (size_t)(i0 + h + u) * plane + c * kWaveSize * VEC);
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) {
-                                p = fmaf(dh[c][e], x[e], p);
-                                y[e] = a * dh[c][e];
+                for (int u = 0; u < L; ++u) {
+                    float p = 0.0f;
+                    const int i = i0 + h + u;
+                    if (i < S) {
+                        const float a = alpha[i];
+#pragma unroll
+                        for (int c = 0; c < NCH; ++c) {
+                            if (FULLCOLS || ok[c]) {
+                                float x[VEC], y[VEC];
+                                widen(raw[u][c], x);
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) {
+                                    p = fmaf(dh[c][e], x[e], p);
+                                    y[e] = a * dh[c][e];
+                                }
+                                if (wr[c])
+                                    store_stream<T, VEC, kNtStore>(
+                                        dvbase + (size_t)i * plane + c * kWaveSize * VEC,
+                                        Narrow<T, VEC>::run(y));
                             }
-                            if (wr[c])
-                                store_raw<T, VEC>(dvbase + (size_t)(i0 + u) * plane +
-                                                  c * kWaveSize * VEC,
-                                                  Narrow<T, VEC>::run(y));
                         }
                     }
+                    part[h + u] = p;
                 }
-                part[u] = p;
             }
             const float tot = multi_sum<8>(part, lane);
             const int idx = multi_sum_index<8>(lane);
@@ -580,22 +601,28 @@ route_bwd_full(const T *__restrict__ V, const float *__restrict__ q, const T *__
         partial[(size_t)blockIdx.x * d + j] = stage[j];
 }
 
-// dq[j] = sum_b partial[b][j] in a fixed order: 4 strided partial sums per
-// column, then combined in order.  Writes zeros when nblocks = 0.
+// dq[j] = sum_b partial[b][j] in a fixed order: one workgroup per column;
+// thread t sums rows t, t+256, ... in order, then a fixed pairwise tree over
+// the 256 thread sums.  Writes zeros when nblocks = 0.
 __global__ void __launch_bounds__(256)
 dq_reduce(const float *__restrict__ partial, float *__restrict__ dq, int nblocks, int ncols)
 {
-    __shared__ float red[4][64];
-    const int jj = threadIdx.x & 63, grp = threadIdx.x >> 6;
-    const int j = blockIdx.x * 64 + jj;
+    __shared__ float red[256];
+    const int t = threadIdx.x;
+    const int j = blockIdx.x;
     float s = 0.0f;
-    if (j < ncols)
-        for (int b = grp; b < nblocks; b += 4)
-            s += partial[(size_t)b * ncols + j];
-    red[grp][jj] = s;
+    for (int b = t; b < nblocks; b += 256)
+        s += partial[(size_t)b * ncols + j];
+    red[t] = s;
     __syncthreads();
-    if (grp == 0 && j < ncols)
-        dq[j] = ((red[0][jj] + red[1][jj]) + red[2][jj]) + red[3][jj];
+#pragma unroll
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (t < w)
+            red[t] += red[t + w];
+        __syncthreads();
+    }
+    if (t == 0)
+        dq[j] = red[0];
 }
 
 // ---------------------------------------------------------------------------
@@ -667,7 +694,7 @@ bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why)
         const int arrays = p.mode == LRAR_MODE_FULL ? 3 : 1;
         pl->lds = (size_t)kWaves * arrays * pl->s_pad * sizeof(float);
     } else {
-        pl->tpw = p.mode == LRAR_MODE_FULL ? 4 : 1;
+        pl->tpw = p.mode == LRAR_MODE_FULL ? 4 : kBwdTokensPerWave;
         const int64_t per_block = (int64_t)kWaves * pl->tpw;
         pl->nblocks = (int)((p.N + per_block - 1) / per_block);
         pl->lds = (size_t)kWaves * 4 * pl->s_pad * sizeof(float);
@@ -819,7 +846,7 @@ int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, 
     }
     const int ncols = (int)(p.mode == LRAR_MODE_FULL ? p.d : p.r);
     const int nb = p.N > 0 ? pl.nblocks : 0;
-    hipLaunchKernelGGL(dq_reduce, dim3((ncols + 63) / 64), dim3(256), 0, st, partial, dq, nb,
+    hipLaunchKernelGGL(dq_reduce, dim3(ncols), dim3(256), 0, st, partial, dq, nb,
                        ncols);
     return hip_status(hipGetLastError(), "dq_reduce launch", err);
 }
