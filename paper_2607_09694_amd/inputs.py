@@ -6,7 +6,7 @@ consume exactly the bytes produced here (bf16 data travels as its raw 16 bits).
 
 Workload shapes follow the paper's experimental model (Sec. 4.1): d = 1024,
 L = 24 blocks with two residual-writing sub-layers each plus the embedding, so
-full routing reads at most 2L + 1 = 49 sources (Sec. 4.6), context 2048.  The
+full routing reads at most 2L + 1 = 49 sources (Sec. 4.7), context 2048.  The
 paper trains on Ultra-FineWeb; that data and the trained weights are not
 available, so Gaussian tensors of the same shapes stand in for the cached
 sub-layer outputs, keys and upstream gradients.  Pseudo-queries are drawn
