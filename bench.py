@@ -201,22 +201,40 @@ def extras(torch, lr, dev, reps, warmup):
         qs = torch.randn((49, r), generator=gen, device=dev) / r ** 0.5
         out[f"model_pass_sliced_r{r}"] = model_pass(SLICED, r, qs)
 
-    # Head to head at S = 49: full-rank (two passes over V) vs low-rank.
+    # Head to head at S = 49: full rank vs low rank, forward and backward.
+    # The full-rank forward reads every row once (online softmax); its
+    # backward must read the rows twice (the key path needs o_i after every
+    # g_j is known).
     gen.manual_seed(1024)
     qf = torch.randn((d,), generator=gen, device=dev) / d ** 0.5
+    dH = torch.randn((N, d), generator=gen, device=dev).to(torch.bfloat16)
+    dV = torch.empty_like(V)
+    dK = torch.empty_like(K)
+    ws = torch.empty((lr.route_bwd_workspace_bytes(49, N, d, d, FULL, V.dtype),),
+                     dtype=torch.uint8, device=dev)
+    dqf = torch.empty((d,), dtype=torch.float32, device=dev)
+    dq16 = torch.empty((16,), dtype=torch.float32, device=dev)
     head = {}
-    for name, fn, nbytes in (
-            ("full_rank", lambda: lr.route_fwd(V, None, qf, FULL, out=H),
-             fwd_bytes(49, N, d, d, FULL)),
-            ("projected_r16", lambda: lr.route_fwd(V, K, Q[48], PROJECTED, out=H),
-             fwd_bytes(49, N, d, 16, PROJECTED)),
-            ("sliced_r16", lambda: lr.route_fwd(V, None, Q[48], SLICED, out=H),
-             fwd_bytes(49, N, d, 16, SLICED))):
-        ts = time_calls(torch, fn, reps, warmup, flush)
-        head[name] = {"median_ms": float(np.median(ts)), "min_ms": float(np.min(ts)),
-                      "max_ms": float(np.max(ts)),
-                      "algo_GBps": nbytes / (np.median(ts) * 1e-3) / 1e9}
+    cases = (
+        ("full_rank", FULL, None, qf, dqf, fwd_bytes(49, N, d, d, FULL),
+         2 * 49 * N * d * 2 + N * d * 2),
+        ("projected_r16", PROJECTED, K, Q[48], dq16, fwd_bytes(49, N, d, 16, PROJECTED),
+         bwd_bytes(49, N, d, 16)),
+        ("sliced_r16", SLICED, None, Q[48], dq16, fwd_bytes(49, N, d, 16, SLICED),
+         2 * 49 * N * d * 2 + N * d * 2))
+    for name, mode, Kc, qc, dqc, fb, bb in cases:
+        dKc = dK if mode == PROJECTED else None
+        tf = time_calls(torch, lambda: lr.route_fwd(V, Kc, qc, mode, out=H), reps, warmup, flush)
+        tb = time_calls(torch, lambda: lr.route_bwd(V, Kc, qc, dH, mode, out=(dV, dKc, dqc),
+                                                     workspace=ws), reps, warmup, flush)
+        head[name] = {"fwd_median_ms": float(np.median(tf)), "fwd_min_ms": float(np.min(tf)),
+                      "fwd_max_ms": float(np.max(tf)),
+                      "fwd_algo_GBps": fb / (np.median(tf) * 1e-3) / 1e9,
+                      "bwd_median_ms": float(np.median(tb)), "bwd_min_ms": float(np.min(tb)),
+                      "bwd_max_ms": float(np.max(tb)),
+                      "bwd_min_algo_GBps": bb / (np.median(tb) * 1e-3) / 1e9}
     out["site49_head_to_head"] = head
+    del dH, dV, dK, ws
 
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush

@@ -183,6 +183,18 @@ __device__ __forceinline__ bool multi_sum_writer(int lane)
     return (lane & (low_bits - 1)) == 0;
 }
 
+// After multi_sum<M>, the sum of value index k, read from one lane that holds
+// it (the lane whose bits 32, 16, ... spell k, most significant first).
+template <int M>
+__device__ __forceinline__ float lane_value(float tot, int k)
+{
+    int src = 0, bit = kWaveSize / 2;
+#pragma unroll
+    for (int half = M / 2; half >= 1; half >>= 1, bit >>= 1)
+        src += (k & half) ? bit : 0;
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(tot), src));
+}
+
 // Make this wave's LDS writes visible to its other lanes.
 __device__ __forceinline__ void wave_lds_sync()
 {

@@ -5,14 +5,16 @@
 // workgroup is kWaves token waves on consecutive tokens, so the projected
 // keys of neighbouring tokens, which share cache lines, are read together.
 // Per token the wave
-//   1. scores the S sources from their keys, lane = source (P-LR / S-LR), or
-//      from a wave-wide dot product per source (full-rank AttnRes),
+//   1. scores the S sources from their keys, lane = source (P-LR / S-LR),
 //   2. takes the softmax over depth with wave reductions, keeping the weights
 //      in a wave-private LDS slice (never written to HBM),
 //   3. streams the S value rows of the token through the wave: each lane
 //      owns NCH 16-byte column vectors of the row, widens bf16 to fp32 and
 //      accumulates with fp32 FMAs; the rows are independent 2-8 KB contiguous
 //      reads, several sources in flight per lane.
+// Full-rank AttnRes (the key is the whole value) scores each source with a
+// wave-wide dot product instead, folded into the same single stream of the
+// rows by an online softmax.
 // The work is a bandwidth-bound gather-reduce (about one flop per byte), so
 // it uses no MFMA: the roofline is HBM.
 #include <hip/hip_runtime.h>
@@ -40,9 +42,11 @@ constexpr bool kNtStore = true;
 template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
 // Sources loaded ahead in the backward stream (divides 8, the number of
 // sources per batched reduction of the dots dH . o_i).
-template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 4 ? 2 : 4; };
-// Tokens per wave in the backward of projected / sliced keys.
-constexpr int kBwdTokensPerWave = 2;
+template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 8 ? 1 : NCH >= 2 ? 2 : 4; };
+// Tokens per wave in the backward of projected / sliced keys, by column
+// chunks per lane: two for rows of 4+ chunks (d >= 2048 bf16), else one
+// (measured on MI355X at d = 1024 and 2048).
+constexpr int bwd_tokens_per_wave(int nch) { return nch >= 4 ? 2 : 1; }
 
 // ---------------------------------------------------------------------------
 // Scores and softmax (Eqs. lr_key_norm and lr_attnres_weight)
@@ -210,38 +214,48 @@ route_fwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
     store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)n * d + col, ok, acc);
 }
 
-// Full-rank AttnRes, two passes over the rows: pass 1 computes per source
-// sum(o^2) and q.o with one batched wave reduction per 4 sources, pass 2 is
-// the same value stream as above (the second read of the rows mostly hits
-// the caches only for small S).
+// Full-rank AttnRes in one pass over the rows: an online softmax over depth.
+// Per batch of 4 sources the rows stay in registers while one batched wave
+// reduction forms their sum(o^2) and q.o; the running maximum m, the
+// normaliser l and the accumulator are rescaled only when m grows.  Reads
+// every row once, like the low-rank kernels.
 template <typename T, int VEC, int NCH, bool FULLCOLS>
 __global__ void __launch_bounds__(kBlock)
-route_fwd_full(const T *__restrict__ V, const float *__restrict__ q, T *__restrict__ H, int S,
-               int N, int d, float eps, int s_pad)
+route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__restrict__ H,
+                  int S, int N, int d, float eps)
 {
-    extern __shared__ float lds[];
+    typedef typename Raw<T, VEC>::type raw_t;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
     const int n = blockIdx.x * kWaves + wave;
     if (n >= N)
         return;  // wave-uniform; no workgroup barrier below
-    float *ss = lds + (3 * wave + 0) * s_pad;
-    float *qd = lds + (3 * wave + 1) * s_pad;
-    float *alpha = lds + (3 * wave + 2) * s_pad;
 
     const int col = lane * VEC;
     bool ok[NCH];
-    float qv[NCH][VEC];
+    float qv[NCH][VEC], acc[NCH][VEC];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         ok[c] = col + c * kWaveSize * VEC < d;
 #pragma unroll
-        for (int e = 0; e < VEC; ++e)
+        for (int e = 0; e < VEC; ++e) {
             qv[c][e] = (FULLCOLS || ok[c]) ? q[col + c * kWaveSize * VEC + e] : 0.0f;
+            acc[c][e] = 0.0f;
+        }
     }
     const size_t plane = (size_t)N * d;
     const T *vbase = V + (size_t)n * d + col;
+    float m = -INFINITY, l = 0.0f;
     for (int i0 = 0; i0 < S; i0 += 4) {
+        raw_t raw[4][NCH];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i0 + u < S)
+#pragma unroll
+                for (int c = 0; c < NCH; ++c)
+                    if (FULLCOLS || ok[c])
+                        raw[u][c] = load_stream<T, VEC, kNtLoad>(
+                            vbase + (size_t)(i0 + u) * plane + c * kWaveSize * VEC);
         float part[8];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -251,8 +265,7 @@ route_fwd_full(const T *__restrict__ V, const float *__restrict__ q, T *__restri
                 for (int c = 0; c < NCH; ++c) {
                     if (FULLCOLS || ok[c]) {
                         float x[VEC];
-                        widen(load_raw<T, VEC>(vbase + (size_t)(i0 + u) * plane +
-                                               c * kWaveSize * VEC), x);
+                        widen(raw[u][c], x);
 #pragma unroll
                         for (int e = 0; e < VEC; ++e) {
                             a = fmaf(x[e], x[e], a);
@@ -265,18 +278,49 @@ route_fwd_full(const T *__restrict__ V, const float *__restrict__ q, T *__restri
             part[4 + u] = b;
         }
         const float tot = multi_sum<8>(part, lane);
-        const int idx = multi_sum_index<8>(lane);
-        if (multi_sum_writer<8>(lane) && i0 + (idx & 3) < S)
-            (idx < 4 ? ss : qd)[i0 + (idx & 3)] = tot;
+        float sc[4];
+        float mb = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float ssq = lane_value<8>(tot, u);
+            const float dot = lane_value<8>(tot, 4 + u);
+            sc[u] = i0 + u < S ? dot / sqrtf(ssq / (float)d + eps) : -INFINITY;
+            mb = fmaxf(mb, sc[u]);
+        }
+        if (mb > m) {  // wave-uniform
+            const float scale = expf(m - mb);
+            l *= scale;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[c][e] *= scale;
+            m = mb;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (i0 + u < S) {
+                const float w = expf(sc[u] - m);
+                l += w;
+#pragma unroll
+                for (int c = 0; c < NCH; ++c) {
+                    if (FULLCOLS || ok[c]) {
+                        float x[VEC];
+                        widen(raw[u][c], x);
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            acc[c][e] = fmaf(w, x[e], acc[c][e]);
+                    }
+                }
+            }
+        }
     }
-    wave_lds_sync();
-    for (int i = lane; i < S; i += kWaveSize) {
-        const float rho = sqrtf(ss[i] / (float)d + eps);
-        qd[i] = qd[i] / rho;
-    }
-    depth_softmax(qd, alpha, S, lane);
-    float acc[NCH][VEC];
-    mix_rows<T, VEC, NCH, FULLCOLS>(vbase, plane, S, alpha, ok, acc);
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[c][e] *= inv;
     store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)n * d + col, ok, acc);
 }
 
@@ -284,20 +328,30 @@ route_fwd_full(const T *__restrict__ V, const float *__restrict__ q, T *__restri
 // Backward kernels (gradient of L = sum_n dH[n] . h[n]; see the header)
 // ---------------------------------------------------------------------------
 
+// Key-pass geometry of the projected / sliced backward.  The key pass covers
+// `ncols` columns per source: projected keys, the r key columns; sliced keys,
+// the value columns from the vector-aligned tail start to d (the tail dV is
+// written only here, with the key gradient added).  They are `nkv` vectors of
+// KV elements.  A lane owns one vector slot v of one source of a group of
+// 64 / LPS sources (LPS = lanes per source, a power of two), so its dq
+// partial always belongs to the same columns; rows wider than 64 vectors are
+// covered in chunks of 64.
+template <int KV> struct KeyChunks { static constexpr int value = KV == 8 ? 1 : KV == 4 ? 2 : 4; };
+
 // Projected / sliced keys.  Each token wave:
 //   recomputes s, rho, alpha;  streams the S rows once, forming the partial
 //   dots g_i = dH . o_i (one batched reduction per 8 sources) and writing
 //   dV_i = alpha_i dH for every column before the key tail;
 //   forms ds_i = alpha_i (g_i - sum_l alpha_l g_l);
-//   then, lanes over key columns, writes dK (projected) or the last columns
-//   of dV including the key gradient (sliced), and accumulates dq.
+//   then, lanes over (source, key vector), writes dK (projected) or the last
+//   columns of dV including the key gradient (sliced), and accumulates dq.
 // dq is reduced per workgroup in a fixed order into partial[blockIdx.x][r].
-template <typename T, int VEC, int NCH, bool FULLCOLS>
+template <typename T, int VEC, int NCH, bool FULLCOLS, int KV>
 __global__ void __launch_bounds__(kBlock)
 route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
              const T *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
              float *__restrict__ partial, int S, int N, int d, int r, int krow, int koff,
-             int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw)
+             int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw, int lps)
 {
     extern __shared__ float lds[];
     const int lane = threadIdx.x & (kWaveSize - 1);
@@ -308,14 +362,26 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
     float *g = lds + (4 * wave + 3) * s_pad;
     float *stage = lds + 4 * kWaves * s_pad;  // [kWaves][r_pad]
 
-    constexpr int kMaxKeyChunks = 5;  // ceil((256 + 7) / 64) key columns per lane
-    float dq_acc[kMaxKeyChunks];
+    constexpr int KC = KeyChunks<KV>::value;
+    const int kbase = sliced ? tail_start : 0;   // first column of the key pass
+    const int kshift = sliced ? d - r : 0;       // column of key element 0
+    const int nkv = (sliced ? d - tail_start : r) / KV;
+    const int isub = lane / lps;                 // source within a group
+    const int spi = kWaveSize / lps;             // sources per group
+    const int vl = lane % lps;
+    const float inv_r = 1.0f / (float)r;
+
+    // Per-lane key-pass constants: q at the lane's key columns.
+    float qk[KC][KV], dq_acc[KC][KV];
 #pragma unroll
-    for (int k = 0; k < kMaxKeyChunks; ++k)
-        dq_acc[k] = 0.0f;
-    const int kcols = sliced ? d - tail_start : r;  // columns of the key pass
-    const int kbase = sliced ? tail_start : 0;
-    const int kshift = sliced ? d - r : 0;          // column of key element 0
+    for (int k = 0; k < KC; ++k)
+#pragma unroll
+        for (int e = 0; e < KV; ++e) {
+            const int v = k * kWaveSize + vl;
+            const int j = kbase + v * KV + e - kshift;
+            qk[k][e] = (v < nkv && j >= 0) ? q[j] : 0.0f;
+            dq_acc[k][e] = 0.0f;
+        }
 
     const int col = lane * VEC;
     bool ok[NCH], wr[NCH];
@@ -402,55 +468,87 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
             g[i] = alpha[i] * (g[i] - gb);  // g now holds ds
         wave_lds_sync();
 
-        // Key path, lanes over key columns.
+        // Key pass: lanes over (source, key vector).
 #pragma unroll
-        for (int k = 0; k < kMaxKeyChunks; ++k) {
-            const int jc = k * kWaveSize + lane;  // column within the key pass
-            if (jc >= kcols)
-                continue;
-            const int cabs = kbase + jc;  // projected: key index; sliced: value column
-            const int j = cabs - kshift;  // key index (sliced: < 0 before the tail)
-            const float qj = j >= 0 ? q[j] : 0.0f;
-            float acc = dq_acc[k];
-            if (!sliced) {
-                for (int i = 0; i < S; ++i) {
-                    const size_t row = (size_t)i * N + n;
-                    const float kb = load_elem(keys + row * krow + j) / rho[i];
-                    const float dsi = g[i];
-                    const float dk = dsi / rho[i] * (qj - kb * s[i] / (float)r);
-                    store_elem(dK + row * r + j, dk);
-                    acc = fmaf(dsi, kb, acc);
-                }
+        for (int k = 0; k < KC; ++k) {
+            const int v = k * kWaveSize + vl;
+            if (k * kWaveSize >= nkv)
+                break;  // wave-uniform
+            const bool vok = v < nkv;
+            const int c0 = kbase + v * KV;  // projected: key index; sliced: value column
+            float dhk[KV];
+            if (sliced && vok) {
+                widen(load_raw<T, KV>(dH + (size_t)n * d + c0), dhk);
             } else {
-                const float dhc = load_elem(dH + (size_t)n * d + cabs);
-                for (int i = 0; i < S; ++i) {
-                    const size_t row = (size_t)i * N + n;
-                    float val = alpha[i] * dhc;
-                    if (j >= 0) {
-                        const float kb = load_elem(V + row * d + cabs) / rho[i];
-                        const float dsi = g[i];
-                        val += dsi / rho[i] * (qj - kb * s[i] / (float)r);
-                        acc = fmaf(dsi, kb, acc);
+#pragma unroll
+                for (int e = 0; e < KV; ++e)
+                    dhk[e] = 0.0f;
+            }
+#pragma unroll 4
+            for (int i0 = 0; i0 < S; i0 += spi) {
+                const int i = i0 + isub;
+                if (!vok || i >= S)
+                    continue;
+                const size_t row = (size_t)i * N + n;
+                const float ri = 1.0f / rho[i];
+                const float dsi = g[i];
+                const float cq = dsi * ri;              // ds_i / rho_i
+                const float ck = cq * s[i] * inv_r;     // ds_i s_i / (rho_i r)
+                float x[KV], y[KV];
+                if (!sliced) {
+                    widen(load_raw<T, KV>(keys + row * krow + c0), x);
+#pragma unroll
+                    for (int e = 0; e < KV; ++e) {
+                        const float kb = x[e] * ri;
+                        y[e] = fmaf(cq, qk[k][e], -ck * kb);
+                        dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
                     }
-                    store_elem(dV + row * d + cabs, val);
+                    store_raw<T, KV>(dK + row * r + c0, Narrow<T, KV>::run(y));
+                } else {
+                    widen(load_raw<T, KV>(V + row * d + c0), x);
+                    const float a = alpha[i];
+#pragma unroll
+                    for (int e = 0; e < KV; ++e) {
+                        y[e] = a * dhk[e];
+                        if (c0 + e >= kshift) {
+                            const float kb = x[e] * ri;
+                            y[e] += fmaf(cq, qk[k][e], -ck * kb);
+                            dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
+                        }
+                    }
+                    store_raw<T, KV>(dV + row * d + c0, Narrow<T, KV>::run(y));
                 }
             }
-            dq_acc[k] = acc;
         }
         wave_lds_sync();  // LDS of this token is reused by the next one
     }
 
-    // Fixed-order workgroup reduction of dq.
+    // Fixed-order reduction of dq: over the source groups of the wave
+    // (butterfly over the lane bits above the vector slot), then over the
+    // waves of the workgroup in wave order.
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+#pragma unroll
+        for (int e = 0; e < KV; ++e)
+            for (int m = lps; m < kWaveSize; m <<= 1)
+                dq_acc[k][e] += __shfl_xor(dq_acc[k][e], m, kWaveSize);
     float *my = stage + wave * r_pad;
     for (int j = lane; j < r; j += kWaveSize)
         my[j] = 0.0f;
     wave_lds_sync();
+    if (isub == 0) {
 #pragma unroll
-    for (int k = 0; k < kMaxKeyChunks; ++k) {
-        const int jc = k * kWaveSize + lane;
-        const int j = kbase + jc - kshift;
-        if (jc < kcols && j >= 0)
-            my[j] = dq_acc[k];
+        for (int k = 0; k < KC; ++k) {
+            const int v = k * kWaveSize + vl;
+            if (v < nkv) {
+#pragma unroll
+                for (int e = 0; e < KV; ++e) {
+                    const int j = kbase + v * KV + e - kshift;
+                    if (j >= 0)
+                        my[j] = dq_acc[k][e];
+                }
+            }
+        }
     }
     __syncthreads();
     for (int j = threadIdx.x; j < r; j += kBlock) {
@@ -691,10 +789,11 @@ bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why)
     pl->r_pad = round_up((int)p.r, 4);
     if (!bwd) {
         pl->nblocks = (int)((p.N + kWaves - 1) / kWaves);
-        const int arrays = p.mode == LRAR_MODE_FULL ? 3 : 1;
-        pl->lds = (size_t)kWaves * arrays * pl->s_pad * sizeof(float);
+        // The low-rank forward keeps the weights in LDS; the full-rank one
+        // holds its online-softmax state in registers.
+        pl->lds = p.mode == LRAR_MODE_FULL ? 0 : (size_t)kWaves * pl->s_pad * sizeof(float);
     } else {
-        pl->tpw = p.mode == LRAR_MODE_FULL ? 4 : kBwdTokensPerWave;
+        pl->tpw = p.mode == LRAR_MODE_FULL ? 4 : bwd_tokens_per_wave(pl->nch);
         const int64_t per_block = (int64_t)kWaves * pl->tpw;
         pl->nblocks = (int)((p.N + per_block - 1) / per_block);
         pl->lds = (size_t)kWaves * 4 * pl->s_pad * sizeof(float);
@@ -741,9 +840,9 @@ hipError_t launch_fwd_t(const Problem &p, const Plan &pl, void *H, hipStream_t s
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
         if (full) {
-            hipLaunchKernelGGL((route_fwd_full<T, VEC, NCH, FC>), dim3(pl.nblocks), dim3(kBlock),
-                               pl.lds, st, V, p.q, static_cast<T *>(H), (int)p.S, (int)p.N,
-                               (int)p.d, p.eps, pl.s_pad);
+            hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC>), dim3(pl.nblocks),
+                               dim3(kBlock), 0, st, V, p.q, static_cast<T *>(H), (int)p.S,
+                               (int)p.N, (int)p.d, p.eps);
         } else {
             hipLaunchKernelGGL((route_fwd_lr<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit),
                                dim3(kBlock), pl.lds, st, V, keys, p.q, static_cast<T *>(H),
@@ -752,6 +851,25 @@ hipError_t launch_fwd_t(const Problem &p, const Plan &pl, void *H, hipStream_t s
         }
         return hipGetLastError();
     });
+}
+
+// Key-pass vector width and lanes per source of the projected / sliced
+// backward: 16-byte vectors when the key rows allow it, else scalars.
+struct KeyPass {
+    int kv, lps, nkv;
+};
+
+KeyPass key_pass(const Problem &p, const Plan &pl)
+{
+    const bool sliced = p.mode == LRAR_MODE_SLICED;
+    const int tail_start = sliced ? (int)((p.d - p.r) / pl.vec * pl.vec) : (int)p.d;
+    KeyPass k;
+    k.kv = pl.vec > 1 && (sliced || p.r % pl.vec == 0) ? pl.vec : 1;
+    k.nkv = (int)(sliced ? p.d - tail_start : p.r) / k.kv;
+    k.lps = 1;
+    while (k.lps < k.nkv && k.lps < kWaveSize)
+        k.lps <<= 1;
+    return k;
 }
 
 template <typename T, int VEC>
@@ -764,6 +882,7 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
     const T *keys = p.mode == LRAR_MODE_PROJECTED ? static_cast<const T *>(p.K) : V;
     const int krow = p.mode == LRAR_MODE_PROJECTED ? (int)p.r : (int)p.d;
     const int koff = p.mode == LRAR_MODE_SLICED ? (int)(p.d - p.r) : 0;
+    const KeyPass kp = key_pass(p, pl);
     return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
@@ -772,13 +891,24 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
                                pl.lds, st, V, p.q, static_cast<const T *>(dH),
                                static_cast<T *>(dV), partial, (int)p.S, (int)p.N, (int)p.d,
                                p.eps, pl.s_pad, pl.tpw);
+            return hipGetLastError();
+        }
+        auto launch = [&](auto kvc) {
+            constexpr int KV = decltype(kvc)::value;
+            hipLaunchKernelGGL((route_bwd_lr<T, VEC, NCH, FC, KV>), dim3(pl.nblocks),
+                               dim3(kBlock), pl.lds, st, V, keys, p.q,
+                               static_cast<const T *>(dH), static_cast<T *>(dV),
+                               static_cast<T *>(dK), partial, (int)p.S, (int)p.N, (int)p.d,
+                               (int)p.r, krow, koff, p.mode == LRAR_MODE_SLICED ? 1 : 0,
+                               tail_start, p.eps, pl.s_pad, pl.r_pad, pl.tpw, kp.lps);
+        };
+        if constexpr (VEC > 1) {
+            if (kp.kv == VEC)
+                launch(std::integral_constant<int, VEC>{});
+            else
+                launch(std::integral_constant<int, 1>{});
         } else {
-            hipLaunchKernelGGL((route_bwd_lr<T, VEC, NCH, FC>), dim3(pl.nblocks), dim3(kBlock),
-                               pl.lds, st, V, keys, p.q, static_cast<const T *>(dH),
-                               static_cast<T *>(dV), static_cast<T *>(dK), partial, (int)p.S,
-                               (int)p.N, (int)p.d, (int)p.r, krow, koff,
-                               p.mode == LRAR_MODE_SLICED ? 1 : 0, tail_start, p.eps, pl.s_pad,
-                               pl.r_pad, pl.tpw);
+            launch(std::integral_constant<int, 1>{});
         }
         return hipGetLastError();
     });

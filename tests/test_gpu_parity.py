@@ -320,3 +320,34 @@ def test_projected_fwd_bwd_d2048_full_size(dev, model_stack):
         _, _, part = oracle.route_bwd(Vh, Kh, qn, dHh, oracle.PROJECTED, n0=n0, n1=n0 + 1024)
         dq_ref += part
     check_dq("dq", to_host(dq), dq_ref)
+
+
+@pytest.mark.parametrize("mode,r", [(PROJECTED, 16), (SLICED, 16), (SLICED, 64), (FULL, 1024)],
+                         ids=["P-r16", "S-r16", "S-r64", "F"])
+def test_model_shape_backward_site49(dev, model_stack, mode, r):
+    """Backward at the model's last site (S = 49, d = 1024, N = 16384): dV (and
+    dK) on sampled tokens, dq over all N tokens."""
+    V = model_stack["V"]
+    K = model_stack["K"] if mode == PROJECTED else None
+    gen = torch.Generator(device=dev).manual_seed(1000 + r)
+    q = torch.randn((r,), generator=gen, device=dev) / r ** 0.5
+    dH = torch.randn((V.shape[1], V.shape[2]), generator=gen, device=dev).to(torch.bfloat16)
+    dV, dK, dq = lr.route_bwd(V, K, q, dH, mode)
+    torch.cuda.synchronize()
+    idx = sample_tokens(V.shape[1], seed=200 + r)
+    ti = torch.from_numpy(idx).to(dev)
+    Ks = sampled(K, idx, 1) if K is not None else None
+    qn = q.cpu().numpy()
+    dV_ref, dK_ref, _ = oracle.route_bwd(sampled(V, idx, 1), Ks, qn, sampled(dH, idx, 0), mode,
+                                         r=r)
+    check_value_grad(mode, "bf16", to_host(dV.index_select(1, ti)), dV_ref, r)
+    if mode == PROJECTED:
+        check_bf16_key_grad("dK", to_host(dK.index_select(1, ti)), dK_ref)
+    del dV, dK
+    Vh, dHh = host_bits(V), host_bits(dH)
+    Kh = host_bits(K) if K is not None else None
+    dq_ref = np.zeros(r)
+    for n0 in range(0, V.shape[1], 2048):
+        _, _, part = oracle.route_bwd(Vh, Kh, qn, dHh, mode, r=r, n0=n0, n1=n0 + 2048)
+        dq_ref += part
+    check_dq("dq", to_host(dq), dq_ref)
