@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 METRIC = "depth-routing tokens/s and achieved HBM TB/s (% of peak), fwd and fwd+bwd"
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_09694_amd", "csrc", "route_kernels.hip")
+KERNEL_DIR = os.path.join(ROOT, "paper_2607_09694_amd", "csrc")
 COUNTERS = os.path.join(ROOT, "profiles", "route_bwd_lr_d2048_counters.txt")
 
 # Main workload: projected keys, forward + backward.
@@ -49,9 +49,9 @@ def bwd_bytes(S, N, d, r):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for name in sorted(os.listdir(os.path.dirname(KERNEL_SRC))):
+    for name in sorted(os.listdir(KERNEL_DIR)):
         if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb") as f:
+            with open(os.path.join(KERNEL_DIR, name), "rb") as f:
                 h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
 

@@ -119,6 +119,22 @@ int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const voi
                          size_t workspace_bytes, int64_t S, int64_t N, int64_t d, int64_t r,
                          int mode, int dtype, float eps, void *stream);
 
+/*
+ * The same backward, accumulating: dV += (its gradient), dK += (projected
+ * keys), dq += (sum over tokens), instead of overwriting them.  This is the
+ * form a model pass needs: each cached source o_i receives gradient from
+ * every later residual site (Sec. 3.1: site t reads all sources written
+ * before it), so the caller keeps one dV stack and adds each site's
+ * contribution in place, saving a separate read-add-write pass over it.
+ * Arguments, validation and errors are those of lr_attnres_route_bwd; the
+ * gradient buffers must hold valid values on entry (zeros to start).
+ */
+int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q,
+                                    const void *dH, void *dV, void *dK, float *dq,
+                                    void *workspace, size_t workspace_bytes, int64_t S,
+                                    int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                    float eps, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

@@ -51,6 +51,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t,
                                          i64, i64, i64, i64, i, i, f, vp]
     lib.lr_attnres_route_bwd.restype = ctypes.c_int
+    lib.lr_attnres_route_bwd_accumulate.argtypes = lib.lr_attnres_route_bwd.argtypes
+    lib.lr_attnres_route_bwd_accumulate.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -135,13 +137,15 @@ def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:
     return load_library().lr_attnres_route_bwd_workspace_bytes(S, N, d, r, _mode(mode), code)
 
 
-def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None):
+def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None,
+              accumulate: bool = False):
     """Gradients (dV, dK, dq) of L = sum(dH * H) for the forward above.
 
     dV [S,N,d] includes the key path for sliced / full-rank keys; dK [S,N,r]
     for projected keys (else None); dq [r] fp32 summed over all tokens.
     ``out`` may supply (dV, dK, dq) buffers, ``workspace`` a uint8 device
-    buffer of at least route_bwd_workspace_bytes(...) bytes.
+    buffer of at least route_bwd_workspace_bytes(...) bytes.  With
+    ``accumulate`` the gradients are added into ``out`` (required).
     """
     import torch
 
@@ -150,6 +154,8 @@ def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None):
     S, N, d, r = _shape(V, K, q, mode)
     if out is not None:
         dV, dK, dq = out
+    elif accumulate:
+        raise ValueError("accumulate needs the out=(dV, dK, dq) buffers to add into")
     else:
         dV = torch.empty_like(V)
         dK = torch.empty_like(K) if mode == PROJECTED else None
@@ -158,11 +164,11 @@ def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None):
     need = lib.lr_attnres_route_bwd_workspace_bytes(S, N, d, r, mode, code)
     if workspace is None:
         workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=V.device)
-    rc = lib.lr_attnres_route_bwd(_dev(V, "V"), _dev(K, "K", V.dtype),
-                                  _dev(q, "q", torch.float32), _dev(dH, "dH", V.dtype),
-                                  _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
-                                  _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"),
-                                  workspace.numel(), S, N, d, r, mode, code, float(eps),
-                                  _stream(V))
+    fn = lib.lr_attnres_route_bwd_accumulate if accumulate else lib.lr_attnres_route_bwd
+    rc = fn(_dev(V, "V"), _dev(K, "K", V.dtype),
+            _dev(q, "q", torch.float32), _dev(dH, "dH", V.dtype),
+            _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
+            _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"),
+            workspace.numel(), S, N, d, r, mode, code, float(eps), _stream(V))
     _check(lib, rc)
     return dV, dK, dq

@@ -139,10 +139,13 @@ size_t lr_attnres_route_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int
     return lrar::bwd_workspace_bytes(p);
 }
 
-int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const void *dH, void *dV,
-                         void *dK, float *dq, void *workspace, size_t workspace_bytes,
-                         int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype,
-                         float eps, void *stream)
+}  // extern "C"
+
+namespace {
+
+int route_bwd(const void *V, const void *K, const float *q, const void *dH, void *dV, void *dK,
+              float *dq, void *workspace, size_t workspace_bytes, int64_t S, int64_t N, int64_t d,
+              int64_t r, int mode, int dtype, float eps, bool accumulate, void *stream)
 {
     g_last_error.clear();
     int64_t ve, ke, he;
@@ -173,10 +176,32 @@ int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const voi
                         span("dH", dH, he * es)};
     if ((rc = check_aliasing(outs, 4, ins, 4)))
         return rc;
-    if ((rc = lrar::launch_bwd(p, dH, dV, dK, dq, workspace, static_cast<hipStream_t>(stream),
-                               &why)))
+    if ((rc = lrar::launch_bwd(p, dH, dV, dK, dq, workspace, accumulate,
+                               static_cast<hipStream_t>(stream), &why)))
         return fail(rc, why);
     return LRAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const void *dH, void *dV,
+                         void *dK, float *dq, void *workspace, size_t workspace_bytes,
+                         int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                         float eps, void *stream)
+{
+    return route_bwd(V, K, q, dH, dV, dK, dq, workspace, workspace_bytes, S, N, d, r, mode, dtype,
+                     eps, false, stream);
+}
+
+int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q, const void *dH,
+                                    void *dV, void *dK, float *dq, void *workspace,
+                                    size_t workspace_bytes, int64_t S, int64_t N, int64_t d,
+                                    int64_t r, int mode, int dtype, float eps, void *stream)
+{
+    return route_bwd(V, K, q, dH, dV, dK, dq, workspace, workspace_bytes, S, N, d, r, mode, dtype,
+                     eps, true, stream);
 }
 
 const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }

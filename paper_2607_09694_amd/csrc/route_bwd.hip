@@ -1,0 +1,520 @@
+// Backward kernels of the LR-AttnRes depth routing (the gradient of Sec. 3.2
+// Eqs. lr_key_norm, lr_attnres_weight, lr_attnres_output), the fixed-order
+// dq reduction, and their launcher.
+#include "route_common.h"
+
+namespace lrar {
+
+// ---------------------------------------------------------------------------
+// Backward kernels (gradient of L = sum_n dH[n] . h[n]; see the header)
+// ---------------------------------------------------------------------------
+
+// Key-pass geometry of the projected / sliced backward.  The key pass covers
+// `ncols` columns per source: projected keys, the r key columns; sliced keys,
+// the value columns from the vector-aligned tail start to d (the tail dV is
+// written only here, with the key gradient added).  They are `nkv` vectors of
+// KV elements.  A lane owns one vector slot v of one source of a group of
+// 64 / LPS sources (LPS = lanes per source, a power of two), so its dq
+// partial always belongs to the same columns; rows wider than 64 vectors are
+// covered in chunks of 64.
+template <int KV> struct KeyChunks { static constexpr int value = KV == 8 ? 1 : KV == 4 ? 2 : 4; };
+
+// Projected / sliced keys.  Each token wave:
+//   recomputes s, rho, alpha;  streams the S rows once, forming the partial
+//   dots g_i = dH . o_i (one batched reduction per 8 sources) and writing
+//   dV_i = alpha_i dH for every column before the key tail;
+//   forms ds_i = alpha_i (g_i - sum_l alpha_l g_l);
+//   then, lanes over (source, key vector), writes dK (projected) or the last
+//   columns of dV including the key gradient (sliced), and accumulates dq.
+// dq is reduced per workgroup in a fixed order into partial[blockIdx.x][r].
+template <typename T, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC>
+__global__ void __launch_bounds__(kBlock)
+route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
+             const T *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
+             float *__restrict__ partial, int S, int N, int d, int r, int krow, int koff,
+             int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw, int lps)
+{
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    float *s = lds + (4 * wave + 0) * s_pad;
+    float *rho = lds + (4 * wave + 1) * s_pad;
+    float *alpha = lds + (4 * wave + 2) * s_pad;
+    float *g = lds + (4 * wave + 3) * s_pad;
+    float *stage = lds + 4 * kWaves * s_pad;  // [kWaves][r_pad]
+
+    constexpr int KC = KeyChunks<KV>::value;
+    const int kbase = sliced ? tail_start : 0;   // first column of the key pass
+    const int kshift = sliced ? d - r : 0;       // column of key element 0
+    const int nkv = (sliced ? d - tail_start : r) / KV;
+    const int isub = lane / lps;                 // source within a group
+    const int spi = kWaveSize / lps;             // sources per group
+    const int vl = lane % lps;
+    const float inv_r = 1.0f / (float)r;
+
+    // Per-lane key-pass constants: q at the lane's key columns.
+    float qk[KC][KV], dq_acc[KC][KV];
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+#pragma unroll
+        for (int e = 0; e < KV; ++e) {
+            const int v = k * kWaveSize + vl;
+            const int j = kbase + v * KV + e - kshift;
+            qk[k][e] = (v < nkv && j >= 0) ? q[j] : 0.0f;
+            dq_acc[k][e] = 0.0f;
+        }
+
+    const int col = lane * VEC;
+    bool ok[NCH], wr[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        ok[c] = col + c * kWaveSize * VEC < d;
+        wr[c] = col + c * kWaveSize * VEC < tail_start;
+    }
+    const size_t plane = (size_t)N * d;
+
+    for (int t = 0; t < tpw; ++t) {
+        const int n = (blockIdx.x * tpw + t) * kWaves + wave;
+        if (n >= N)
+            break;  // wave-uniform; the workgroup barrier below is outside the loop
+        lr_scores<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s, rho);
+        depth_softmax(s, alpha, S, lane);
+
+        typedef typename Raw<T, VEC>::type raw_t;
+        float dh[NCH][VEC];
+        const T *dhrow = dH + (size_t)n * d + col;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (FULLCOLS || ok[c]) {
+                widen(load_raw<T, VEC>(dhrow + c * kWaveSize * VEC), dh[c]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    dh[c][e] = 0.0f;
+            }
+        }
+        const T *vbase = V + (size_t)n * d + col;
+        T *dvbase = dV + (size_t)n * d + col;
+        constexpr int L = BwdInflight<NCH>::value;
+        for (int i0 = 0; i0 < S; i0 += 8) {
+            float part[8];
+#pragma unroll
+            for (int h = 0; h < 8; h += L) {
+                raw_t raw[L][NCH], old[ACC ? L : 1][NCH];
+#pragma unroll
+                for (int u = 0; u < L; ++u)
+                    if (i0 + h + u < S)
+#pragma unroll
+                        for (int c = 0; c < NCH; ++c)
+                            if (FULLCOLS || ok[c]) {
+                                const size_t off = (size_t)(i0 + h + u) * plane + c * kWaveSize * VEC;
+                                raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + off);
+                                if constexpr (ACC)
+                                    if (wr[c])
+                                        old[u][c] = load_stream<T, VEC, kNtLoad>(dvbase + off);
+                            }
+#pragma unroll
+                for (int u = 0; u < L; ++u) {
+                    float p = 0.0f;
+                    const int i = i0 + h + u;
+                    if (i < S) {
+                        const float a = alpha[i];
+#pragma unroll
+                        for (int c = 0; c < NCH; ++c) {
+                            if (FULLCOLS || ok[c]) {
+                                float x[VEC], y[VEC];
+                                widen(raw[u][c], x);
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) {
+                                    p = fmaf(dh[c][e], x[e], p);
+                                    y[e] = a * dh[c][e];
+                                }
+                                if constexpr (ACC)
+                                    if (wr[c])
+                                        add_stored(y, old[u][c]);
+                                if (wr[c])
+                                    store_stream<T, VEC, kNtStore>(
+                                        dvbase + (size_t)i * plane + c * kWaveSize * VEC,
+                                        Narrow<T, VEC>::run(y));
+                            }
+                        }
+                    }
+                    part[h + u] = p;
+                }
+            }
+            const float tot = multi_sum<8>(part, lane);
+            const int idx = multi_sum_index<8>(lane);
+            if (multi_sum_writer<8>(lane) && i0 + idx < S)
+                g[i0 + idx] = tot;
+        }
+        wave_lds_sync();
+        float gb = 0.0f;
+        for (int i = lane; i < S; i += kWaveSize)
+            gb = fmaf(alpha[i], g[i], gb);
+        gb = wave_sum(gb);
+        for (int i = lane; i < S; i += kWaveSize)
+            g[i] = alpha[i] * (g[i] - gb);  // g now holds ds
+        wave_lds_sync();
+
+        // Key pass: lanes over (source, key vector).
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+            const int v = k * kWaveSize + vl;
+            if (k * kWaveSize >= nkv)
+                break;  // wave-uniform
+            const bool vok = v < nkv;
+            const int c0 = kbase + v * KV;  // projected: key index; sliced: value column
+            float dhk[KV];
+            if (sliced && vok) {
+                widen(load_raw<T, KV>(dH + (size_t)n * d + c0), dhk);
+            } else {
+#pragma unroll
+                for (int e = 0; e < KV; ++e)
+                    dhk[e] = 0.0f;
+            }
+#pragma unroll 4
+            for (int i0 = 0; i0 < S; i0 += spi) {
+                const int i = i0 + isub;
+                if (!vok || i >= S)
+                    continue;
+                const size_t row = (size_t)i * N + n;
+                const float ri = 1.0f / rho[i];
+                const float dsi = g[i];
+                const float cq = dsi * ri;              // ds_i / rho_i
+                const float ck = cq * s[i] * inv_r;     // ds_i s_i / (rho_i r)
+                float x[KV], y[KV];
+                if (!sliced) {
+                    widen(load_raw<T, KV>(keys + row * krow + c0), x);
+#pragma unroll
+                    for (int e = 0; e < KV; ++e) {
+                        const float kb = x[e] * ri;
+                        y[e] = fmaf(cq, qk[k][e], -ck * kb);
+                        dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
+                    }
+                    if constexpr (ACC)
+                        add_stored(y, load_raw<T, KV>(dK + row * r + c0));
+                    store_raw<T, KV>(dK + row * r + c0, Narrow<T, KV>::run(y));
+                } else {
+                    widen(load_raw<T, KV>(V + row * d + c0), x);
+                    const float a = alpha[i];
+#pragma unroll
+                    for (int e = 0; e < KV; ++e) {
+                        y[e] = a * dhk[e];
+                        if (c0 + e >= kshift) {
+                            const float kb = x[e] * ri;
+                            y[e] += fmaf(cq, qk[k][e], -ck * kb);
+                            dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
+                        }
+                    }
+                    if constexpr (ACC)
+                        add_stored(y, load_raw<T, KV>(dV + row * d + c0));
+                    store_raw<T, KV>(dV + row * d + c0, Narrow<T, KV>::run(y));
+                }
+            }
+        }
+        wave_lds_sync();  // LDS of this token is reused by the next one
+    }
+
+    // Fixed-order reduction of dq: over the source groups of the wave
+    // (butterfly over the lane bits above the vector slot), then over the
+    // waves of the workgroup in wave order.
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+#pragma unroll
+        for (int e = 0; e < KV; ++e)
+            for (int m = lps; m < kWaveSize; m <<= 1)
+                dq_acc[k][e] += __shfl_xor(dq_acc[k][e], m, kWaveSize);
+    float *my = stage + wave * r_pad;
+    for (int j = lane; j < r; j += kWaveSize)
+        my[j] = 0.0f;
+    wave_lds_sync();
+    if (isub == 0) {
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+            const int v = k * kWaveSize + vl;
+            if (v < nkv) {
+#pragma unroll
+                for (int e = 0; e < KV; ++e) {
+                    const int j = kbase + v * KV + e - kshift;
+                    if (j >= 0)
+                        my[j] = dq_acc[k][e];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < r; j += kBlock) {
+        float sum = 0.0f;
+        for (int w = 0; w < kWaves; ++w)
+            sum += stage[w * r_pad + j];
+        partial[(size_t)blockIdx.x * r + j] = sum;
+    }
+}
+
+// Full-rank AttnRes backward: pass 1 reads the rows once for sum(o^2), q.o
+// and dH.o (one batched reduction per 4 sources); pass 2 re-reads them to
+// write dV_i = alpha_i dH + (ds_i/rho_i)(q - o_i s_i/(rho_i d)) and to
+// accumulate dq = sum ds_i o_i / rho_i per lane column.
+template <typename T, int VEC, int NCH, bool FULLCOLS, bool ACC>
+__global__ void __launch_bounds__(kBlock)
+route_bwd_full(const T *__restrict__ V, const float *__restrict__ q, const T *__restrict__ dH,
+               T *__restrict__ dV, float *__restrict__ partial, int S, int N, int d, float eps,
+               int s_pad, int tpw)
+{
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    float *ss = lds + (4 * wave + 0) * s_pad;     // sum o^2, then rho
+    float *sc = lds + (4 * wave + 1) * s_pad;     // q.o, then the score
+    float *g = lds + (4 * wave + 2) * s_pad;      // dH.o, then ds
+    float *alpha = lds + (4 * wave + 3) * s_pad;
+    float *stage = lds + 4 * kWaves * s_pad;      // [d]
+
+    const int col = lane * VEC;
+    bool ok[NCH];
+    float qv[NCH][VEC], dqa[NCH][VEC];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        ok[c] = col + c * kWaveSize * VEC < d;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            qv[c][e] = (FULLCOLS || ok[c]) ? q[col + c * kWaveSize * VEC + e] : 0.0f;
+            dqa[c][e] = 0.0f;
+        }
+    }
+    const size_t plane = (size_t)N * d;
+    const float inv_d = 1.0f / (float)d;
+
+    for (int t = 0; t < tpw; ++t) {
+        const int n = (blockIdx.x * tpw + t) * kWaves + wave;
+        if (n >= N)
+            break;  // wave-uniform; the workgroup barriers are after the loop
+        float dh[NCH][VEC];
+        const T *vbase = V + (size_t)n * d + col;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (FULLCOLS || ok[c]) {
+                widen(load_raw<T, VEC>(dH + (size_t)n * d + col + c * kWaveSize * VEC), dh[c]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    dh[c][e] = 0.0f;
+            }
+        }
+        for (int i0 = 0; i0 < S; i0 += 4) {
+            float part[16];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                float a = 0.0f, b = 0.0f, p = 0.0f;
+                if (i0 + u < S) {
+#pragma unroll
+                    for (int c = 0; c < NCH; ++c) {
+                        if (FULLCOLS || ok[c]) {
+                            float x[VEC];
+                            widen(load_raw<T, VEC>(vbase + (size_t)(i0 + u) * plane +
+                                                   c * kWaveSize * VEC), x);
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                a = fmaf(x[e], x[e], a);
+                                b = fmaf(qv[c][e], x[e], b);
+                                p = fmaf(dh[c][e], x[e], p);
+                            }
+                        }
+                    }
+                }
+                part[u] = a;
+                part[4 + u] = b;
+                part[8 + u] = p;
+                part[12 + u] = 0.0f;
+            }
+            const float tot = multi_sum<16>(part, lane);
+            const int idx = multi_sum_index<16>(lane);
+            const int i = i0 + (idx & 3);
+            if (multi_sum_writer<16>(lane) && idx < 12 && i < S)
+                (idx < 4 ? ss : idx < 8 ? sc : g)[i] = tot;
+        }
+        wave_lds_sync();
+        for (int i = lane; i < S; i += kWaveSize) {
+            const float rho = sqrtf(ss[i] / (float)d + eps);
+            ss[i] = rho;
+            sc[i] = sc[i] / rho;
+        }
+        depth_softmax(sc, alpha, S, lane);
+        float gb = 0.0f;
+        for (int i = lane; i < S; i += kWaveSize)
+            gb = fmaf(alpha[i], g[i], gb);
+        gb = wave_sum(gb);
+        for (int i = lane; i < S; i += kWaveSize)
+            g[i] = alpha[i] * (g[i] - gb);
+        wave_lds_sync();
+
+        T *dvbase = dV + (size_t)n * d + col;
+        for (int i = 0; i < S; ++i) {
+            const float a = alpha[i];
+            const float c1 = g[i] / ss[i];                  // ds_i / rho_i
+            const float c2 = c1 * sc[i] / ss[i] * inv_d;    // ds_i s_i / (rho_i^2 d)
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULLCOLS || ok[c]) {
+                    float x[VEC], y[VEC];
+                    widen(load_raw<T, VEC>(vbase + (size_t)i * plane + c * kWaveSize * VEC), x);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        y[e] = fmaf(a, dh[c][e], fmaf(c1, qv[c][e], -c2 * x[e]));
+                        dqa[c][e] = fmaf(c1, x[e], dqa[c][e]);
+                    }
+                    if constexpr (ACC)
+                        add_stored(y, load_raw<T, VEC>(dvbase + (size_t)i * plane +
+                                                       c * kWaveSize * VEC));
+                    store_raw<T, VEC>(dvbase + (size_t)i * plane + c * kWaveSize * VEC,
+                                      Narrow<T, VEC>::run(y));
+                }
+            }
+        }
+        wave_lds_sync();
+    }
+
+    // Fixed-order workgroup reduction of dq: waves add their columns in turn.
+    for (int w = 0; w < kWaves; ++w) {
+        if (wave == w) {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULLCOLS || ok[c]) {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        float *p = stage + col + c * kWaveSize * VEC + e;
+                        *p = (w == 0 ? 0.0f : *p) + dqa[c][e];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+    for (int j = threadIdx.x; j < d; j += kBlock)
+        partial[(size_t)blockIdx.x * d + j] = stage[j];
+}
+
+// dq[j] = sum_b partial[b][j] in a fixed order: one workgroup per column;
+// thread t sums rows t, t+256, ... in order, then a fixed pairwise tree over
+// the 256 thread sums.  Writes zeros when nblocks = 0.
+template <bool ACC>
+__global__ void __launch_bounds__(256)
+dq_reduce(const float *__restrict__ partial, float *__restrict__ dq, int nblocks, int ncols)
+{
+    __shared__ float red[256];
+    const int t = threadIdx.x;
+    const int j = blockIdx.x;
+    float s = 0.0f;
+    for (int b = t; b < nblocks; b += 256)
+        s += partial[(size_t)b * ncols + j];
+    red[t] = s;
+    __syncthreads();
+#pragma unroll
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (t < w)
+            red[t] += red[t + w];
+        __syncthreads();
+    }
+    if (t == 0)
+        dq[j] = ACC ? dq[j] + red[0] : red[0];
+}
+
+namespace {
+
+// Key-pass vector width and lanes per source of the projected / sliced
+// backward: 16-byte vectors when the key rows allow it, else scalars.
+struct KeyPass {
+    int kv, lps, nkv;
+};
+
+KeyPass key_pass(const Problem &p, const Plan &pl)
+{
+    const bool sliced = p.mode == LRAR_MODE_SLICED;
+    const int tail_start = sliced ? (int)((p.d - p.r) / pl.vec * pl.vec) : (int)p.d;
+    KeyPass k;
+    k.kv = pl.vec > 1 && (sliced || p.r % pl.vec == 0) ? pl.vec : 1;
+    k.nkv = (int)(sliced ? p.d - tail_start : p.r) / k.kv;
+    k.lps = 1;
+    while (k.lps < k.nkv && k.lps < kWaveSize)
+        k.lps <<= 1;
+    return k;
+}
+
+template <typename T, int VEC, bool ACC>
+hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
+                        float *partial, hipStream_t st)
+{
+    const T *V = static_cast<const T *>(p.V);
+    const int tail_start = p.mode == LRAR_MODE_SLICED ? (int)((p.d - p.r) / pl.vec * pl.vec)
+                                                      : (int)p.d;
+    const T *keys = p.mode == LRAR_MODE_PROJECTED ? static_cast<const T *>(p.K) : V;
+    const int krow = p.mode == LRAR_MODE_PROJECTED ? (int)p.r : (int)p.d;
+    const int koff = p.mode == LRAR_MODE_SLICED ? (int)(p.d - p.r) : 0;
+    const KeyPass kp = key_pass(p, pl);
+    return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
+        constexpr int NCH = decltype(nch)::value;
+        constexpr bool FC = decltype(fc)::value;
+        if (p.mode == LRAR_MODE_FULL) {
+            hipLaunchKernelGGL((route_bwd_full<T, VEC, NCH, FC, ACC>), dim3(pl.nblocks), dim3(kBlock),
+                               pl.lds, st, V, p.q, static_cast<const T *>(dH),
+                               static_cast<T *>(dV), partial, (int)p.S, (int)p.N, (int)p.d,
+                               p.eps, pl.s_pad, pl.tpw);
+            return hipGetLastError();
+        }
+        auto launch = [&](auto kvc) {
+            constexpr int KV = decltype(kvc)::value;
+            hipLaunchKernelGGL((route_bwd_lr<T, VEC, NCH, FC, KV, ACC>), dim3(pl.nblocks),
+                               dim3(kBlock), pl.lds, st, V, keys, p.q,
+                               static_cast<const T *>(dH), static_cast<T *>(dV),
+                               static_cast<T *>(dK), partial, (int)p.S, (int)p.N, (int)p.d,
+                               (int)p.r, krow, koff, p.mode == LRAR_MODE_SLICED ? 1 : 0,
+                               tail_start, p.eps, pl.s_pad, pl.r_pad, pl.tpw, kp.lps);
+        };
+        if constexpr (VEC > 1) {
+            if (kp.kv == VEC)
+                launch(std::integral_constant<int, VEC>{});
+            else
+                launch(std::integral_constant<int, 1>{});
+        } else {
+            launch(std::integral_constant<int, 1>{});
+        }
+        return hipGetLastError();
+    });
+}
+
+template <bool ACC>
+hipError_t launch_bwd_acc(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
+                          float *dq, float *partial, hipStream_t st)
+{
+    hipError_t e = hipSuccess;
+    if (p.N > 0) {
+        if (p.dtype == LRAR_DTYPE_BF16)
+            e = pl.vec > 1 ? launch_bwd_t<uint16_t, 8, ACC>(p, pl, dH, dV, dK, partial, st)
+                           : launch_bwd_t<uint16_t, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+        else
+            e = pl.vec > 1 ? launch_bwd_t<float, 4, ACC>(p, pl, dH, dV, dK, partial, st)
+                           : launch_bwd_t<float, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+        if (e != hipSuccess)
+            return e;
+    }
+    const int ncols = (int)(p.mode == LRAR_MODE_FULL ? p.d : p.r);
+    const int nb = p.N > 0 ? pl.nblocks : 0;
+    hipLaunchKernelGGL(dq_reduce<ACC>, dim3(ncols), dim3(256), 0, st, partial, dq, nb, ncols);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
+               bool accumulate, hipStream_t st, std::string *err)
+{
+    Plan pl;
+    if (!make_plan(p, true, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    float *partial = static_cast<float *>(ws);
+    const hipError_t e = accumulate ? launch_bwd_acc<true>(p, pl, dH, dV, dK, dq, partial, st)
+                                    : launch_bwd_acc<false>(p, pl, dH, dV, dK, dq, partial, st);
+    return hip_status(e, "route_bwd launch", err);
+}
+
+}  // namespace lrar

@@ -1,0 +1,233 @@
+#pragma once
+// Shared pieces of the gfx950 LR-AttnRes depth-routing kernels (arXiv
+// 2607.09694, Sec. 3): tiling constants, the score / softmax / value-stream
+// device building blocks, and the launch plan shared by the host launchers.
+//
+// Work decomposition: one wave64 owns one token n ("token wave"); a
+// workgroup is kWaves token waves on consecutive tokens, so the projected
+// keys of neighbouring tokens, which share cache lines, are read together.
+// Per token the wave
+//   1. scores the S sources from their keys, lane = source (P-LR / S-LR),
+//   2. takes the softmax over depth with wave reductions, keeping the weights
+//      in a wave-private LDS slice (never written to HBM),
+//   3. streams the S value rows of the token through the wave: each lane
+//      owns NCH 16-byte column vectors of the row, widens bf16 to fp32 and
+//      accumulates with fp32 FMAs; the rows are independent 2-8 KB contiguous
+//      reads, several sources in flight per lane.
+// Full-rank AttnRes (the key is the whole value) scores each source with a
+// wave-wide dot product instead, folded into the same single stream of the
+// rows by an online softmax.
+// The work is a bandwidth-bound gather-reduce (about one flop per byte), so
+// it uses no MFMA: the roofline is HBM.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string>
+#include <type_traits>
+
+#include "route_device.h"
+#include "route_launch.h"
+
+namespace lrar {
+
+constexpr int kWaves = 4;                    // token waves per workgroup
+constexpr int kBlock = kWaves * kWaveSize;   // 256 threads
+
+// Streaming choices for the value rows (read once) and for H / dV (written
+// once), set by measurement on MI355X: non-temporal accesses gave +12% on
+// the forward and +9% on the backward at d = 2048, S = 64.
+constexpr bool kNtLoad = true;
+constexpr bool kNtStore = true;
+
+// Sources whose value rows one lane has in flight in the forward mix.
+template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
+// Sources loaded ahead in the backward stream (divides 8, the number of
+// sources per batched reduction of the dots dH . o_i).
+template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 8 ? 1 : NCH >= 2 ? 2 : 4; };
+// Tokens per wave in the backward of projected / sliced keys, by column
+// chunks per lane: two for rows of 4+ chunks (d >= 2048 bf16), else one
+// (measured on MI355X at d = 1024 and 2048).
+constexpr int bwd_tokens_per_wave(int nch) { return nch >= 4 ? 2 : 1; }
+
+// ---------------------------------------------------------------------------
+// Scores and softmax (Eqs. lr_key_norm and lr_attnres_weight)
+// ---------------------------------------------------------------------------
+
+// Lane-per-source scores of token n: rho_i = sqrt(mean_j k_ij^2 + eps),
+// s_i = q . k_i / rho_i.  Key element j of source i is
+// keys[(i*N + n)*krow + koff + j]  (projected: keys = K, krow = r, koff = 0;
+// sliced: keys = V, krow = d, koff = d - r).  Each lane writes only the
+// entries of its own sources.
+template <typename T, int VEC>
+__device__ inline void lr_scores(const T *__restrict__ keys, const float *__restrict__ q, int S,
+                          int N, int r, int krow, int koff, float eps, int n, int lane,
+                          float *s_out, float *rho_out)
+{
+    const bool kvec = VEC > 1 && r % VEC == 0 && krow % VEC == 0 && koff % VEC == 0;
+    for (int i = lane; i < S; i += kWaveSize) {
+        const T *kp = keys + ((size_t)i * N + n) * krow + koff;
+        float ss = 0.0f, dot = 0.0f;
+        if (kvec) {
+            for (int j = 0; j < r; j += VEC) {
+                float x[VEC];
+                widen(load_raw<T, VEC>(kp + j), x);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    ss = fmaf(x[e], x[e], ss);
+                    dot = fmaf(q[j + e], x[e], dot);
+                }
+            }
+        } else {
+            for (int j = 0; j < r; ++j) {
+                const float x = load_elem(kp + j);
+                ss = fmaf(x, x, ss);
+                dot = fmaf(q[j], x, dot);
+            }
+        }
+        const float rho = sqrtf(ss / (float)r + eps);
+        s_out[i] = dot / rho;
+        if (rho_out)
+            rho_out[i] = rho;
+    }
+}
+
+// alpha_i = exp(s_i - max) / sum_l exp(s_l - max) over the S sources.
+// s and alpha may alias.  Ends with the wave's LDS writes visible.
+__device__ inline void depth_softmax(const float *s, float *alpha, int S, int lane)
+{
+    float m = -INFINITY;
+    for (int i = lane; i < S; i += kWaveSize)
+        m = fmaxf(m, s[i]);
+    m = wave_max(m);
+    float z = 0.0f;
+    for (int i = lane; i < S; i += kWaveSize) {
+        const float e = expf(s[i] - m);
+        alpha[i] = e;
+        z += e;
+    }
+    z = wave_sum(z);
+    const float inv = 1.0f / z;
+    for (int i = lane; i < S; i += kWaveSize)
+        alpha[i] *= inv;
+    wave_lds_sync();
+}
+
+// ---------------------------------------------------------------------------
+// The value stream (Eq. lr_attnres_output): h = sum_i alpha_i o_i
+// ---------------------------------------------------------------------------
+
+// vbase points at column (col0 + lane*VEC) of source 0's row of the token;
+// chunk c of source i is at vbase + i*plane + c*64*VEC.
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t plane, int S,
+                                         const float *alpha, const bool (&ok)[NCH],
+                                         float (&acc)[NCH][VEC])
+{
+    typedef typename Raw<T, VEC>::type raw_t;
+    constexpr int U = MixUnroll<NCH>::value;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[c][e] = 0.0f;
+    int i = 0;
+    for (; i + U <= S; i += U) {
+        raw_t raw[U][NCH];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+                if (FULLCOLS || ok[c])
+                    raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + (size_t)(i + u) * plane +
+                                                             c * kWaveSize * VEC);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float a = alpha[i + u];
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULLCOLS || ok[c]) {
+                    float x[VEC];
+                    widen(raw[u][c], x);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        acc[c][e] = fmaf(a, x[e], acc[c][e]);
+                }
+            }
+        }
+    }
+    for (; i < S; ++i) {
+        const float a = alpha[i];
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            if (FULLCOLS || ok[c]) {
+                float x[VEC];
+                widen(load_stream<T, VEC, kNtLoad>(vbase + (size_t)i * plane +
+                                                   c * kWaveSize * VEC), x);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[c][e] = fmaf(a, x[e], acc[c][e]);
+            }
+        }
+    }
+}
+
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__device__ __forceinline__ void store_row(T *__restrict__ base, const bool (&ok)[NCH],
+                                          const float (&acc)[NCH][VEC])
+{
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        if (FULLCOLS || ok[c])
+            store_stream<T, VEC, kNtStore>(base + c * kWaveSize * VEC,
+                                           Narrow<T, VEC>::run(acc[c]));
+}
+
+// ---------------------------------------------------------------------------
+// Launch plan (host)
+// ---------------------------------------------------------------------------
+
+struct Plan {
+    int vec = 1;          // elements per lane access
+    int nch = 1;          // column chunks per lane
+    bool fullcols = false;
+    int ysplit = 1;       // column blocks (forward, projected/sliced only)
+    int tpw = 1;          // tokens per wave (backward)
+    int nblocks = 0;      // workgroups along x
+    int s_pad = 4;
+    int r_pad = 4;
+    size_t lds = 0;
+};
+
+// Fills *pl for a validated problem, or returns false with the reason.
+bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why);
+
+// LRAR_OK, or LRAR_EHIP with the HIP error text in *err.
+int hip_status(hipError_t e, const char *what, std::string *err);
+
+// Calls f(std::integral_constant<int, NCH>, std::integral_constant<bool, FULLCOLS>).
+template <int VEC, typename F>
+hipError_t dispatch_chunks(const Plan &pl, F &&f)
+{
+    typedef std::true_type Y;
+    typedef std::false_type Nf;
+    if constexpr (VEC > 1) {
+        switch (pl.nch) {
+        case 1: return pl.fullcols ? f(std::integral_constant<int, 1>{}, Y{}) : f(std::integral_constant<int, 1>{}, Nf{});
+        case 2: return pl.fullcols ? f(std::integral_constant<int, 2>{}, Y{}) : f(std::integral_constant<int, 2>{}, Nf{});
+        case 4: return pl.fullcols ? f(std::integral_constant<int, 4>{}, Y{}) : f(std::integral_constant<int, 4>{}, Nf{});
+        case 8: return pl.fullcols ? f(std::integral_constant<int, 8>{}, Y{}) : f(std::integral_constant<int, 8>{}, Nf{});
+        }
+    } else {
+        switch (pl.nch) {
+        case 1: return f(std::integral_constant<int, 1>{}, Nf{});
+        case 2: return f(std::integral_constant<int, 2>{}, Nf{});
+        case 4: return f(std::integral_constant<int, 4>{}, Nf{});
+        case 8: return f(std::integral_constant<int, 8>{}, Nf{});
+        case 16: return f(std::integral_constant<int, 16>{}, Nf{});
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace lrar

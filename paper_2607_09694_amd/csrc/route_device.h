@@ -113,6 +113,17 @@ template <> struct Narrow<uint16_t, 1> {
     __device__ static uint16_t run(const float (&x)[1]) { return to_bf16(x[0]); }
 };
 
+// y += the VEC values of one stored raw access (accumulating outputs).
+template <int VEC, typename R>
+__device__ __forceinline__ void add_stored(float (&y)[VEC], const R &stored)
+{
+    float x[VEC];
+    widen(stored, x);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e)
+        y[e] += x[e];
+}
+
 __device__ __forceinline__ float load_elem(const float *p) { return *p; }
 __device__ __forceinline__ float load_elem(const uint16_t *p)
 {

@@ -29,7 +29,8 @@ int check_supported(const Problem &p, bool bwd, std::string *why);
 size_t bwd_workspace_bytes(const Problem &p);
 
 int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err);
+// accumulate: add the gradients into dV, dK and dq instead of overwriting.
 int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
-               hipStream_t st, std::string *err);
+               bool accumulate, hipStream_t st, std::string *err);
 
 }  // namespace lrar

@@ -40,6 +40,7 @@ def _declared_functions():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
+                            "lr_attnres_route_bwd_accumulate",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -59,9 +60,9 @@ def fwd(lib, V=A, K=None, q=B, H=C, S=4, N=8, d=64, r=8, mode=SL, dtype=BF16, ep
 
 
 def bwd(lib, V=A, K=None, q=B, dH=C, dV=D, dK=None, dq=E, ws=W, wsb=1 << 30, S=4, N=8, d=64,
-        r=8, mode=SL, dtype=BF16, eps=1e-6):
-    return lib.lr_attnres_route_bwd(V, K, q, dH, dV, dK, dq, ws, wsb, S, N, d, r, mode, dtype,
-                                    eps, None)
+        r=8, mode=SL, dtype=BF16, eps=1e-6, accumulate=False):
+    fn = lib.lr_attnres_route_bwd_accumulate if accumulate else lib.lr_attnres_route_bwd
+    return fn(V, K, q, dH, dV, dK, dq, ws, wsb, S, N, d, r, mode, dtype, eps, None)
 
 
 def err(lib):
@@ -121,6 +122,12 @@ BWD_INVALID = [
 @pytest.mark.parametrize("name,kw,msg", BWD_INVALID, ids=[c[0] for c in BWD_INVALID])
 def test_backward_rejects(lib, name, kw, msg):
     assert bwd(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+@pytest.mark.parametrize("name,kw,msg", BWD_INVALID, ids=[c[0] for c in BWD_INVALID])
+def test_accumulating_backward_rejects(lib, name, kw, msg):
+    assert bwd(lib, accumulate=True, **kw) == EINVAL
     assert msg in err(lib)
 
 

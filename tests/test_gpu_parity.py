@@ -130,6 +130,40 @@ def test_backward_matches_oracle(dev, case):
     check_dq("dq", to_host(dq), dq_ref, tol=1e-5 if dtype == "f32" else 1e-4)
 
 
+ACC_CASES = [
+    (PROJECTED, "bf16", 49, 130, 1024, 16),
+    (PROJECTED, "f32", 64, 67, 2048, 32),
+    (PROJECTED, "bf16", 3, 5, 100, 4),
+    (SLICED, "bf16", 7, 21, 1000, 12),
+    (SLICED, "f32", 49, 33, 1024, 64),
+    (FULL, "bf16", 9, 13, 200, 200),
+    (FULL, "f32", 5, 7, 72, 72),
+]
+
+
+@pytest.mark.parametrize("case", ACC_CASES, ids=_id)
+def test_accumulating_backward(dev, case):
+    """lr_attnres_route_bwd_accumulate adds the gradient into existing dV, dK
+    and dq: compare with their initial values plus the oracle's gradient."""
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S * 1000 + N + 2, with_dH=True)
+    init = make_host_problem(PROJECTED, S, N, d, p.r, dtype=dtype, seed=S * 1000 + N + 3,
+                             with_dH=True)  # Gaussian initial gradients, same storage
+    dV0, dK0 = init.V, init.K
+    dq0 = init.q
+    dV, dK, dq = to_dev(dV0.copy(), dev), to_dev(dK0.copy(), dev), to_dev(dq0.copy(), dev)
+    lr.route_bwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev), to_dev(p.dH, dev), mode,
+                 out=(dV, dK if mode == PROJECTED else None, dq), accumulate=True)
+    torch.cuda.synchronize()
+    gV, gK, gq = oracle.route_bwd(p.V, p.K, p.q, p.dH, mode, r=p.r)
+    widen = (lambda x: f32_from_bf16_bits(x)) if dtype == "bf16" else (lambda x: x)
+    check_value_grad(mode, dtype, to_host(dV), widen(dV0).astype(np.float64) + gV, p.r)
+    if mode == PROJECTED:
+        check_key_grad("dK", dtype, to_host(dK), widen(dK0).astype(np.float64) + gK)
+    check_dq("dq", to_host(dq), dq0.astype(np.float64) + gq,
+             tol=1e-5 if dtype == "f32" else 1e-4)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [PROJECTED, SLICED])
 def test_column_split_forward(dev, mode, dtype):
