@@ -135,6 +135,41 @@ int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q
                                     int64_t N, int64_t d, int64_t r, int mode, int dtype,
                                     float eps, void *stream);
 
+/*
+ * Block-source routing forward at one residual site: Block AttnRes (Sec. 3.1,
+ * Eqs. block_attnres_sum and block_attnres_partial_sum) with the low-rank
+ * keys of Sec. 3.2.  The 2L sub-layer outputs are grouped into consecutive
+ * blocks; site t reads the embedding, every completed block summary and the
+ * partial summary of the block in progress.  The summaries are kept by the
+ * caller in fp32 slots, updated here one member at a time:
+ *   B   [n_src][N][d] fp32  slot 0 = embedding, slot j >= 1 = sum of block j's
+ *                           outputs so far.  Slot n_src-1 is updated in place:
+ *                           B[n_src-1] = (start ? 0 : B[n_src-1]) + o_new.
+ *   KB  [n_src][N][r] fp32  projected keys only (else NULL): the key of a
+ *                           summary is the sum of its members' keys, updated
+ *                           like B with k_new.  Sliced keys are the last r
+ *                           columns of each slot (the tail of the summed row).
+ *   o_new [N][d], k_new [N][r]  the newest sub-layer output and its projected
+ *                           key (k_new NULL for sliced keys), storage `dtype`.
+ *   q [r] fp32; H [N][d] storage `dtype`, fully overwritten.
+ * The routing over slots 0..n_src-1 (after the update) is that of
+ * lr_attnres_route_fwd.  A model pass calls this once per site: at site 1
+ * with o_new = the embedding, n_src = 1, start = 1; at site t >= 2 with
+ * o_new = o_{t-1}, which belongs to block j = floor((t-2)/c) + 1 for blocks
+ * of c outputs, so n_src = j + 1 and start = ((t-2) mod c == 0).
+ * The reading that a summary's key is the sum of its members' keys is this
+ * library's (the paper does not define block keys for projected keys).
+ * Errors as for lr_attnres_route_fwd, plus EINVAL for start not 0/1 and for
+ * an unknown mode; full-rank keys, d not a multiple of 4, d > 2048 and
+ * n_src > 1024 are EUNSUPPORTED.  k_new needs only element alignment (it is
+ * read element by element), the other tensors 16 bytes.  H must not overlap
+ * any other argument; B and KB are rewritten and must not overlap the inputs.
+ */
+int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const void *k_new,
+                               const float *q, void *H, int64_t n_src, int start, int64_t N,
+                               int64_t d, int64_t r, int mode, int dtype, float eps,
+                               void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

@@ -51,6 +51,10 @@ def _load():
     for f in (lib.orc_route_weights, lib.orc_route_fwd, lib.orc_route_bwd):
         f.restype = ctypes.c_int
     lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_block_num_sources.argtypes = [ll, ll]
+    lib.orc_block_num_sources.restype = ll
+    lib.orc_block_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll]
+    lib.orc_block_route_fwd.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -132,3 +136,36 @@ def route_bwd(V, K, q, dH, mode, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid problem")
     return dV, dK, dq
+
+
+def block_num_sources(t: int, c: int) -> int:
+    """Sources read at site t with blocks of c outputs (Sec. 3.1 Block AttnRes)."""
+    return _load().orc_block_num_sources(t, c)
+
+
+def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """Block-source forward at site t (Sec. 3.1 Eqs. block_attnres_sum /
+    block_attnres_partial_sum with the routing of Sec. 3.2).
+
+    O [t, N, d] holds o_0 .. o_{t-1}; KO [t, N, r] their projected keys (or
+    None for sliced keys).  Returns H [n1-n0, d] in fp64.
+    """
+    O = np.ascontiguousarray(O)
+    if O.dtype not in _STORE or O.ndim != 3 or O.shape[0] < t:
+        raise ValueError("oracle: O must be [>=t, N, d] in a supported storage")
+    O = np.ascontiguousarray(O[:t])
+    _, N, d = O.shape
+    if mode == PROJECTED:
+        KO = np.ascontiguousarray(np.ascontiguousarray(KO)[:t])
+        r = KO.shape[2]
+    elif r is None:
+        raise ValueError("oracle: sliced keys need r")
+    q = np.ascontiguousarray(np.asarray(q, dtype=np.float64))
+    n1 = N if n1 is None else n1
+    out = np.empty((n1 - n0, d), dtype=np.float64)
+    rc = _load().orc_block_route_fwd(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
+                                     _ptr(out), t, c, N, d, r, mode, _STORE[O.dtype], float(eps),
+                                     n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid block problem")
+    return out

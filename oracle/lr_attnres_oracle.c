@@ -319,6 +319,71 @@ int orc_route_bwd(const void *V, const void *K, const double *q, const void *dH,
     return failed;
 }
 
+/* ---------------------------------------------------------------------------
+ * Block sources (Sec. 3.1 "Block AttnRes", Eqs. block_attnres_sum and
+ * block_attnres_partial_sum, with the low-rank keys of Sec. 3.2).
+ *
+ * The 2L residual-writing sub-layers are grouped into consecutive blocks of
+ * c outputs: block j (1-based) holds outputs (j-1)c+1 .. jc.  Site t reads
+ * the embedding o_0, every completed block summary b_j = sum of its members,
+ * and the partial summary of the block in progress if it has members.
+ * Reading where the paper is silent: a summary's key is the sum of its
+ * members' keys.  For sliced keys that is exactly the tail of the summed
+ * value; for projected keys it is the key part of the summed [o_i; k_i].
+ * ------------------------------------------------------------------------- */
+
+/* Number of sources at site t >= 1 with blocks of c outputs:
+ * 1 + floor((t-1)/c) completed-or-current blocks, counting a non-empty
+ * partial block. */
+long long orc_block_num_sources(long long t, long long c)
+{
+    if (t < 1 || c < 1)
+        return -1;
+    return 1 + (t - 1) / c + ((t - 1) % c != 0);
+}
+
+/* Forward at site t: O is [t][N][d] (o_0 .. o_{t-1}), KO is [t][N][r]
+ * (projected keys) or NULL.  H[n - n0][:] as in orc_route_fwd, with the
+ * block summaries of the outputs as sources, for tokens [n0, n1).  The
+ * summaries are formed in double; then the routing of Sec. 3.2 applies to
+ * them unchanged (sliced keys: the tail of each summary). */
+int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *H,
+                        long long t, long long c, long long N, long long d, long long r,
+                        int mode, int store, double eps, long long n0, long long n1)
+{
+    const long long S = orc_block_num_sources(t, c);
+    if (S < 1 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
+        q == NULL || H == NULL || (mode != ORC_KEYS_PROJECTED && mode != ORC_KEYS_SLICED) ||
+        (mode == ORC_KEYS_PROJECTED) != (KO != NULL) || (mode == ORC_KEYS_SLICED && r > d) ||
+        store < 0 || store > 2)
+        return 1;
+    const long long nt = n1 - n0;
+    /* Summaries of the token range, double: B [S][nt][d], KB [S][nt][r]. */
+    double *B = (double *)calloc((size_t)(S * nt * d), sizeof(double));
+    double *KB = mode == ORC_KEYS_PROJECTED ? (double *)calloc((size_t)(S * nt * r), sizeof(double))
+                                            : NULL;
+    if (B == NULL || (mode == ORC_KEYS_PROJECTED && KB == NULL)) {
+        free(B);
+        free(KB);
+        return 1;
+    }
+    for (long long i = 0; i < t; ++i) {
+        /* output i belongs to slot 0 (embedding) or block ceil(i / c) */
+        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
+        for (long long n = n0; n < n1; ++n) {
+            for (long long j = 0; j < d; ++j)
+                B[(slot * nt + (n - n0)) * d + j] += widen(O, store, (i * N + n) * d + j);
+            if (KB)
+                for (long long j = 0; j < r; ++j)
+                    KB[(slot * nt + (n - n0)) * r + j] += widen(KO, store, (i * N + n) * r + j);
+        }
+    }
+    const int rc = orc_route_fwd(B, KB, q, H, S, nt, d, r, mode, ORC_STORE_F64, eps, 0, nt);
+    free(B);
+    free(KB);
+    return rc;
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {

@@ -53,6 +53,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_bwd.restype = ctypes.c_int
     lib.lr_attnres_route_bwd_accumulate.argtypes = lib.lr_attnres_route_bwd.argtypes
     lib.lr_attnres_route_bwd_accumulate.restype = ctypes.c_int
+    lib.lr_attnres_block_route_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i, i64, i64, i64,
+                                               i, i, f, vp]
+    lib.lr_attnres_block_route_fwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -172,3 +175,35 @@ def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None,
             workspace.numel(), S, N, d, r, mode, code, float(eps), _stream(V))
     _check(lib, rc)
     return dV, dK, dq
+
+
+def block_route_fwd(B, KB, o_new, k_new, q, n_src: int, start: bool, mode, eps: float = 1e-6,
+                    out=None):
+    """One residual site of block-source routing (Sec. 3.1 Block AttnRes
+    summaries with the low-rank keys of Sec. 3.2).
+
+    B [>=n_src, N, d] fp32 summary slots (slot 0 = embedding); slot n_src-1
+    becomes (0 if start else itself) + o_new.  KB [>=n_src, N, r] fp32 key
+    summaries for projected keys (else None), updated with k_new.  o_new
+    [N, d] and k_new [N, r] in the model dtype (bf16 / fp32); q [r] fp32.
+    Returns H [N, d] in o_new's dtype.
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    if B.dtype != torch.float32 or (KB is not None and KB.dtype != torch.float32):
+        raise TypeError("summary slots must be float32")
+    if B.dim() != 3 or B.shape[0] < n_src:
+        raise ValueError("B must be [>= n_src, N, d]")
+    _, N, d = B.shape
+    r = KB.shape[2] if mode == PROJECTED else q.shape[0]
+    if tuple(o_new.shape) != (N, d):
+        raise ValueError("o_new must be [N, d]")
+    H = out if out is not None else torch.empty((N, d), dtype=o_new.dtype, device=B.device)
+    rc = lib.lr_attnres_block_route_fwd(
+        _dev(B, "B"), _dev(KB, "KB"), _dev(o_new, "o_new"), _dev(k_new, "k_new", o_new.dtype),
+        _dev(q, "q", torch.float32), _dev(H, "H", o_new.dtype), int(n_src), int(bool(start)),
+        N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
+    _check(lib, rc)
+    return H

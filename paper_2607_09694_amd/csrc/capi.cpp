@@ -204,6 +204,50 @@ int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q
                      eps, true, stream);
 }
 
+int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const void *k_new,
+                               const float *q, void *H, int64_t n_src, int start, int64_t N,
+                               int64_t d, int64_t r, int mode, int dtype, float eps,
+                               void *stream)
+{
+    g_last_error.clear();
+    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
+        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
+                    "block routing takes projected or sliced keys");
+    if (start != 0 && start != 1)
+        return fail(LRAR_EINVAL, "start must be 0 or 1");
+    int64_t ve, ke, he;
+    int rc = check_shape(n_src, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(o_new, "o_new", 16, data)) ||
+        (rc = check_ptr(q, "q", 4, true)) || (rc = check_ptr(H, "H", 16, data)) ||
+        (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(k_new, "k_new", (size_t)(dtype == LRAR_DTYPE_BF16 ? 2 : 4),
+                        data && proj)))
+        return rc;
+    if (!proj && (KB || k_new))
+        return fail(LRAR_EINVAL, "KB and k_new must be NULL unless keys are projected");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t nr;
+    if (!mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    // B and KB are read and rewritten: checked as outputs.
+    const Span outs[] = {span("H", H, he * es), span("B", B, ve * 4), span("KB", KB, ke * 4)};
+    const Span ins[] = {span("o_new", o_new, he * es), span("k_new", k_new, nr * es),
+                        span("q", q, r * 4)};
+    if ((rc = check_aliasing(outs, 3, ins, 3)))
+        return rc;
+    lrar::BlockProblem p{B, KB, o_new, k_new, q, H, n_src, N, d, r, start, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_block_supported(p, &why)))
+        return fail(rc, why);
+    if ((rc = lrar::launch_block_fwd(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }
 
 int lr_attnres_abi_version(void) { return LR_ATTNRES_ABI_VERSION; }

@@ -13,6 +13,7 @@ constexpr int kWaveSize = 64;
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 // Raw<T, VEC>::type is what one lane moves per access: 16 bytes for the
@@ -21,6 +22,7 @@ template <typename T, int VEC> struct Raw;
 template <> struct Raw<float, 4> { typedef f32x4_t type; };
 template <> struct Raw<float, 1> { typedef float type; };
 template <> struct Raw<uint16_t, 8> { typedef u32x4_t type; };
+template <> struct Raw<uint16_t, 4> { typedef u32x2_t type; };  // 4 bf16 in 8 bytes
 template <> struct Raw<uint16_t, 1> { typedef uint16_t type; };
 
 template <typename T> struct VecOf;
@@ -89,6 +91,11 @@ __device__ __forceinline__ void widen(const u32x4_t &r, float (&x)[8])
     x[4] = bf16_lo(r.z); x[5] = bf16_hi(r.z);
     x[6] = bf16_lo(r.w); x[7] = bf16_hi(r.w);
 }
+__device__ __forceinline__ void widen(const u32x2_t &r, float (&x)[4])
+{
+    x[0] = bf16_lo(r.x); x[1] = bf16_hi(r.x);
+    x[2] = bf16_lo(r.y); x[3] = bf16_hi(r.y);
+}
 __device__ __forceinline__ void widen(const uint16_t &r, float (&x)[1])
 {
     x[0] = __uint_as_float((unsigned)r << 16);
@@ -107,6 +114,12 @@ template <> struct Narrow<uint16_t, 8> {
     {
         return u32x4_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
                        pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7])};
+    }
+};
+template <> struct Narrow<uint16_t, 4> {
+    __device__ static u32x2_t run(const float (&x)[4])
+    {
+        return u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
     }
 };
 template <> struct Narrow<uint16_t, 1> {

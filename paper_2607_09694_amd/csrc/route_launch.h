@@ -33,4 +33,20 @@ int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err);
 int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
                bool accumulate, hipStream_t st, std::string *err);
 
+// One residual site of block-source routing (see lr_attnres_block_route_fwd).
+struct BlockProblem {
+    float *B;           // [nsrc][N][d] fp32 summary slots; slot nsrc-1 updated
+    float *KB;          // [nsrc][N][r] fp32 key summaries (projected) or NULL
+    const void *o_new;  // [N][d] newest sub-layer output, storage dtype
+    const void *k_new;  // [N][r] its projected key, storage dtype, or NULL
+    const float *q;     // [r]
+    void *H;            // [N][d] storage dtype
+    int64_t nsrc, N, d, r;
+    int start, mode, dtype;
+    float eps;
+};
+
+int check_block_supported(const BlockProblem &p, std::string *why);
+int launch_block_fwd(const BlockProblem &p, hipStream_t st, std::string *err);
+
 }  // namespace lrar

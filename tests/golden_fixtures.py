@@ -46,4 +46,41 @@ def load(path):
 
 
 def all_fixtures():
-    return [load(p) for p in sorted(glob.glob(os.path.join(GOLDEN_DIR, "*.txt")))]
+    """The single-site routing examples (files named after a key mode)."""
+    names = sorted(glob.glob(os.path.join(GOLDEN_DIR, "*.txt")))
+    return [load(p) for p in names
+            if os.path.basename(p).split("_")[0] in ("sliced", "projected", "full")]
+
+
+def load_block(name):
+    """A block-source worked example: outputs O[i], block size c, site t."""
+    spec, O, res = {}, {}, {}
+    with open(os.path.join(GOLDEN_DIR, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            lhs, rhs = (x.strip() for x in line.split("=", 1))
+            key = lhs.split()
+            nums = [float(x) for x in rhs.split()]
+            if key[0] == "O":
+                O[int(key[1])] = nums
+            elif key[0] in ("alpha", "H", "q"):
+                res[key[0]] = np.array(nums)
+            else:
+                spec[key[0]] = nums[0]
+    t = int(spec["t"])
+    return dict(t=t, c=int(spec["c"]), d=int(spec["d"]), r=int(spec["r"]), eps=spec["eps"],
+                O=np.array([O[i] for i in range(t)])[:, None, :], **res)
+
+
+def load_table1():
+    """Rows (kind, blocks, rank, printed value) of the Table 1 fixture."""
+    rows = []
+    with open(os.path.join(GOLDEN_DIR, "table1_added_flops.txt")) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                kind, nb, r, v = line.split()
+                rows.append((kind, int(nb), int(r), float(v)))
+    return rows

@@ -3,8 +3,9 @@
 fp32 storage: normwise relative error <= 1e-5, both max|err| / max|ref| and
 ||err||_2 / ||ref||_2.
 bf16 storage (outputs rounded to bf16): values and value gradients
-max|err| <= 2e-2 and ||err||_2 / ||ref||_2 <= 5e-3.  Key gradients grow past
-|dK| = 8, where the bf16 half-ulp alone exceeds 2e-2, so they take
+max|err| <= 2e-2 and ||err||_2 / ||ref||_2 <= 5e-3.  Results that grow past
+|x| = 8 (key gradients; h over block summaries, which are sums of several
+outputs), where the bf16 half-ulp alone exceeds 2e-2, take
 |err| <= 2e-2 * max(1, |ref|) element by element, with the same relative L2.
 dq is fp32 accumulated over N*S terms: normwise 1e-4 (the fp32 bar scaled
 for the length of the sum), and rel-L2 <= 5e-3.

@@ -40,7 +40,7 @@ def _declared_functions():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
-                            "lr_attnres_route_bwd_accumulate",
+                            "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -162,3 +162,40 @@ def test_error_text_is_per_call(lib):
 def test_python_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError, match="not built"):
         lr.load_library(str(tmp_path / "missing.so"))
+
+
+def blk(lib, B=A, KB=None, o_new=C, k_new=None, q=E, H=D, n_src=3, start=0, N=8, d=64, r=8,
+        mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_block_route_fwd(B, KB, o_new, k_new, q, H, n_src, start, N, d, r,
+                                          mode, dtype, eps, None)
+
+
+BLOCK_INVALID = [
+    ("B NULL", dict(B=None), "B is NULL"),
+    ("o_new NULL", dict(o_new=None), "o_new is NULL"),
+    ("H NULL", dict(H=None), "H is NULL"),
+    ("start not 0/1", dict(start=2), "start"),
+    ("unknown mode", dict(mode=9), "projected or sliced"),
+    ("projected without KB", dict(mode=P, k_new=G), "KB is NULL"),
+    ("projected without k_new", dict(mode=P, KB=G), "k_new is NULL"),
+    ("KB outside projected", dict(KB=G), "must be NULL"),
+    ("n_src zero", dict(n_src=0), "sizes"),
+    ("sliced r > d", dict(r=65), "r <= d"),
+    ("H overlaps B", dict(H=A + 64), "overlap"),
+    ("B overlaps o_new", dict(o_new=A + 4096), "overlaps"),
+    ("B misaligned", dict(B=A + 4), "aligned"),
+    ("eps negative", dict(eps=-1.0), "eps"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", BLOCK_INVALID, ids=[c[0] for c in BLOCK_INVALID])
+def test_block_forward_rejects(lib, name, kw, msg):
+    assert blk(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_block_forward_unsupported(lib):
+    assert blk(lib, mode=F, r=64) == EUNSUPPORTED
+    assert blk(lib, d=66) == EUNSUPPORTED
+    assert blk(lib, d=4096) == EUNSUPPORTED
+    assert blk(lib, n_src=1025) == EUNSUPPORTED

@@ -1,0 +1,119 @@
+"""GPU parity of the fused block-source forward (Sec. 3.1 Block AttnRes with
+the low-rank keys of Sec. 3.2): a whole model pass is driven site by site,
+exactly as a model calls it, and every site's h is checked against the fp64
+oracle, which forms the block summaries from the raw outputs."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
+                                         f32_from_bf16_bits, make_host_problem)
+from parity import check_bf16_key_grad, check_f32
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(x).to(dev)
+
+
+def to_host(t):
+    if t.dtype == torch.bfloat16:
+        return f32_from_bf16_bits(bf16_tensor_to_bits(t))
+    return t.detach().cpu().numpy()
+
+
+def site_args(t, c):
+    """Slot count and start flag of site t (1-based) with blocks of c."""
+    if t == 1:
+        return 1, True
+    return (t - 2) // c + 2, (t - 2) % c == 0
+
+
+def drive_model_pass(dev, O, KO, Q, c, mode, sites):
+    """Call the fused op at sites 1..max(sites); return {t: H_t}."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    KB = (torch.zeros((nslots, N, KO.shape[2]), dtype=torch.float32, device=dev)
+          if mode == PROJECTED else None)
+    out = {}
+    for t in range(1, max(sites) + 1):
+        n_src, start = site_args(t, c)
+        knew = KO[t - 1] if mode == PROJECTED else None
+        H = lr.block_route_fwd(B, KB, O[t - 1], knew, Q[t - 1], n_src, start, mode)
+        if t in sites:
+            out[t] = H
+    torch.cuda.synchronize()
+    return out, B, KB
+
+
+CASES = [
+    (PROJECTED, "bf16", 13, 70, 256, 16, 3),
+    (SLICED, "bf16", 13, 70, 256, 16, 3),
+    (PROJECTED, "f32", 10, 33, 1024, 32, 4),
+    (SLICED, "f32", 10, 33, 1000, 64, 2),
+    (SLICED, "bf16", 9, 21, 2048, 8, 1),     # blocks of one: full routing
+    (PROJECTED, "bf16", 9, 24, 100, 7, 20),  # one partial block; masked columns
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"{'P' if c[0] == 0 else 'S'}-{c[1]}-T{c[2]}-N{c[3]}-d{c[4]}-r{c[5]}-c{c[6]}")
+def test_block_model_pass_matches_oracle(dev, case):
+    mode, dtype, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype=dtype, seed=T * 100 + N)
+    rng = np.random.default_rng(T)
+    Qh = (rng.standard_normal((T, r)) / np.sqrt(r)).astype(np.float32)
+    O, KO, Q = to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev)
+    sites = list(range(1, T + 1))
+    out, B, KB = drive_model_pass(dev, O, KO, Q, c, mode, sites)
+    # Block summaries are sums of up to c outputs, so h reaches |h| >= 8 where
+    # the bf16 half-ulp alone exceeds an absolute 2e-2: the scaled bar applies.
+    check = check_f32 if dtype == "f32" else check_bf16_key_grad
+    for t in sites:
+        ref = oracle.block_route_fwd(p.V, p.K, Qh[t - 1], t, c, mode, r=r)
+        check(f"H at site {t}", to_host(out[t]), ref)
+    # the slots end as the exact block sums (fp32 accumulation of the outputs)
+    Ow = p.V.astype(np.float64) if dtype == "f32" else f32_from_bf16_bits(p.V).astype(np.float64)
+    last = (T - 2) // c + 1
+    for j in range(0, last + 1):
+        members = [0] if j == 0 else list(range((j - 1) * c + 1, min(j * c, T - 1) + 1))
+        check_f32(f"slot {j}", B[j].cpu().numpy(), Ow[members].sum(axis=0), tol=1e-6)
+
+
+@pytest.mark.parametrize("mode,r", [(SLICED, 64), (PROJECTED, 32)], ids=["S-r64", "P-r32"])
+def test_block_model_pass_full_size(dev, mode, r):
+    """The paper's best block settings (8 blocks, Table 1): d = 1024, 48
+    sub-layers plus the embedding, N = 8 x 2048 tokens; sampled tokens at
+    sites around block boundaries."""
+    T, N, d, c = 49, 16384, 1024, 6
+    g = torch.Generator(device=dev).manual_seed(0)
+    O = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+    for i in range(T):
+        O[i].copy_(torch.randn((N, d), generator=g, device=dev))
+    KO = (torch.randn((T, N, r), generator=g, device=dev).to(torch.bfloat16)
+          if mode == PROJECTED else None)
+    Q = torch.randn((T, r), generator=g, device=dev) / r ** 0.5
+    sites = [1, 2, 7, 8, 25, 49]
+    out, _, _ = drive_model_pass(dev, O, KO, Q, c, mode, sites)
+    idx = np.sort(np.concatenate([[0, 1, N - 1], np.random.default_rng(1).choice(N, 29, replace=False)]))
+    ti = torch.from_numpy(idx).to(dev)
+    Os = bf16_tensor_to_bits(O.index_select(1, ti))
+    Ks = bf16_tensor_to_bits(KO.index_select(1, ti)) if KO is not None else None
+    for t in sites:
+        ref = oracle.block_route_fwd(Os, Ks, Q[t - 1].cpu().numpy(), t, c, mode, r=r)
+        check_bf16_key_grad(f"H at site {t}", to_host(out[t].index_select(0, ti)), ref)

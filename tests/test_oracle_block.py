@@ -1,0 +1,86 @@
+"""Pins of the oracle's block-source forward (Sec. 3.1 Block AttnRes, Eqs.
+block_attnres_sum / block_attnres_partial_sum, routed as in Sec. 3.2)."""
+import numpy as np
+import pytest
+
+import golden_fixtures
+from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_host_problem
+
+L, D, M = 24, 1024, 2816            # Sec. 4.1
+C_BASE = L * (4 * D * D + 3 * D * M)  # Appendix A, numerical example
+
+
+def s_src(orc, blocks):
+    """Source reads summed over sites t = 2 .. 2L+1 (site 1 reads only the
+    embedding); full routing is blocks of one output."""
+    c = 1 if blocks == 0 else 2 * L // blocks
+    return sum(orc.block_num_sources(t, c) for t in range(2, 2 * L + 2))
+
+
+def test_source_counts_reproduce_table1(orc):
+    """The block source count reproduces every kernel-cost entry of Table 1's
+    added-FLOPs column to the printed 4 decimals."""
+    assert s_src(orc, 0) == 1224
+    assert [s_src(orc, n) for n in (4, 8, 16)] == [168, 264, 456]
+    for kind, blocks, r, printed in golden_fixtures.load_table1():
+        S = s_src(orc, blocks)
+        if kind == "attnres":
+            cost = 2 * D * S
+        elif kind == "sliced":
+            cost = (D + r) * S
+        else:
+            cost = (D + r) * S + r * (L * (D + M) + D)
+        assert abs(100.0 * cost / C_BASE - printed) < 5e-5, (kind, blocks, r)
+
+
+@pytest.mark.parametrize("c", [1, 2, 3, 6, 12, 48])
+def test_slot_of_the_newest_output(orc, c):
+    """At site t >= 2 the newest output o_{t-1} lands in block
+    floor((t-2)/c) + 1, which is the last source read at t."""
+    for t in range(2, 50):
+        assert orc.block_num_sources(t, c) == (t - 2) // c + 2
+    assert orc.block_num_sources(1, c) == 1
+
+
+def _stack(mode, t, N, d, r, seed, dtype="f32"):
+    p = make_host_problem(mode, t, N, d, r, dtype=dtype, seed=seed, q_scale=2.0)
+    return p.V, p.K, p.q
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_blocks_of_one_equal_full_routing(orc, mode):
+    """c = 1: every output is its own block, so block routing is full routing."""
+    O, KO, q = _stack(mode, 9, 7, 12, 4, seed=1)
+    H = orc.block_route_fwd(O, KO, q, t=9, c=1, mode=mode, r=4)
+    np.testing.assert_allclose(H, orc.route_fwd(O, KO, q, mode, r=4), rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_one_partial_block_is_the_plain_sum(orc, mode):
+    """c >= t - 1: the sources are o_0 and the sum of every later output."""
+    t = 6
+    O, KO, q = _stack(mode, t, 5, 10, 3, seed=2)
+    H = orc.block_route_fwd(O, KO, q, t=t, c=8, mode=mode, r=3)
+    O64 = O.astype(np.float64)
+    V = np.stack([O64[0], O64[1:].sum(axis=0)])
+    K = None if KO is None else np.stack([KO[0].astype(np.float64),
+                                          KO[1:].astype(np.float64).sum(axis=0)])
+    np.testing.assert_allclose(H, orc.route_fwd(V, K, q, mode, r=3), rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("mode", [SLICED, PROJECTED])
+def test_hand_derived_block_example(orc, mode):
+    fx = golden_fixtures.load_block("block_sliced_two_blocks.txt")
+    O = fx["O"]
+    KO = np.ascontiguousarray(O[:, :, -fx["r"]:]) if mode == PROJECTED else None
+    for q, tol in ((fx["q"], 1e-12), (fx["q"].astype(np.float32), 1e-6)):
+        H = orc.block_route_fwd(O, KO, q, t=fx["t"], c=fx["c"], mode=mode, r=fx["r"],
+                                eps=fx["eps"])
+        np.testing.assert_allclose(H[0], fx["H"], rtol=0, atol=tol * 8)
+
+
+def test_block_token_ranges_compose(orc):
+    O, KO, q = _stack(PROJECTED, 11, 20, 8, 4, seed=3)
+    H = orc.block_route_fwd(O, KO, q, t=11, c=3, mode=PROJECTED)
+    part = orc.block_route_fwd(O, KO, q, t=11, c=3, mode=PROJECTED, n0=6, n1=15)
+    assert np.array_equal(H[6:15], part)
