@@ -47,12 +47,16 @@ def bwd_bytes(S, N, d, r):
     return 2 * S * N * (d + r) * 2 + N * d * 2
 
 
+# The sources that define the measured backward and forward kernels; the
+# committed counter summary is valid only while these are unchanged.
+KERNEL_FILES = ("route_bwd.hip", "route_fwd.hip", "route_common.h", "route_device.h")
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
-    for name in sorted(os.listdir(KERNEL_DIR)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(KERNEL_DIR, name), "rb") as f:
-                h.update(name.encode() + f.read())
+    for name in KERNEL_FILES:
+        with open(os.path.join(KERNEL_DIR, name), "rb") as f:
+            h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
 
 
@@ -166,6 +170,71 @@ def cpu_baseline(g, q, target_s=10.0, chunk=1024):
                       f"workload, fwd+bwd in fp64, {spent:.1f} s"}
 
 
+def block_pass_bytes(t, c, N, d, r, mode, es=2):
+    """Algorithmic HBM bytes of the fused block call at site t: the earlier
+    fp32 slots (with their fp32 key slots for projected keys) read once, the
+    updated slot read (unless it starts) and written, o_{t-1} read, h written."""
+    if t == 1:
+        j, start = 0, True
+    else:
+        j, start = (t - 2) // c + 1, (t - 2) % c == 0
+    row = d + (r if mode == 0 else 0)
+    b = j * N * row * 4 + (0 if start else N * row * 4) + N * row * 4
+    return b + N * row * es + N * d * es
+
+
+def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush):
+    """49-site block-source forward pass over the output stack O [49, N, d].
+    Each site's real call (with its own start flag) is timed `reps` times;
+    before each, untimed, the updated slot is restored and the MALL flushed."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev) if mode == 0 else None
+    gen = torch.Generator(device=dev).manual_seed(100 + r)
+    KO = (torch.randn((T, N, r), generator=gen, device=dev).to(torch.bfloat16)
+          if mode == 0 else None)
+    Q = torch.randn((T, r), generator=gen, device=dev) / r ** 0.5
+    H = torch.empty((N, d), dtype=O.dtype, device=dev)
+    st = torch.cuda.current_stream()
+    total, nbytes = 0.0, 0
+    for t in range(1, T + 1):
+        n_src, start = (1, True) if t == 1 else ((t - 2) // c + 2, (t - 2) % c == 0)
+        j = n_src - 1
+        kn = KO[t - 1] if KO is not None else None
+        saved = B[j].clone()
+        ksaved = KB[j].clone() if KB is not None else None
+
+        def restore():
+            B[j].copy_(saved)
+            if KB is not None:
+                KB[j].copy_(ksaved)
+
+        def call():
+            lr.block_route_fwd(B, KB, O[t - 1], kn, Q[t - 1], n_src, start, mode, out=H)
+
+        for _ in range(warmup):
+            restore()
+            call()
+        ev = []
+        for _ in range(reps):
+            restore()
+            flush()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            call()
+            b.record(st)
+            ev.append((a, b))
+        torch.cuda.synchronize()
+        total += float(np.median([a.elapsed_time(b) for a, b in ev]))
+        nbytes += block_pass_bytes(t, c, N, d, r, mode)
+        del saved, ksaved
+    del B, KB, KO
+    return {"total_ms": total, "tokens_per_s": N / (total * 1e-3),
+            "algo_GBps": nbytes / (total * 1e-3) / 1e9,
+            "frac_of_peak": nbytes / (total * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
 def extras(torch, lr, dev, reps, warmup):
     """The other workloads: the 49-site forward model pass (projected r=16 and
     sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
@@ -236,6 +305,13 @@ def extras(torch, lr, dev, reps, warmup):
     out["site49_head_to_head"] = head
     del dH, dV, dK, ws
 
+    # Block sources (8 blocks of 6 sub-layer outputs), the paper's best
+    # settings: one fused call per site adds o_{t-1} into its fp32 summary
+    # slot and routes over the embedding and the block summaries.
+    out["block_model_pass_sliced_r64_8blocks"] = block_pass(torch, lr, dev, V, SLICED, 64,
+                                                            6, reps, warmup, flush)
+    out["block_model_pass_projected_r32_8blocks"] = block_pass(torch, lr, dev, V, PROJECTED,
+                                                               32, 6, reps, warmup, flush)
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush
     torch.cuda.empty_cache()
