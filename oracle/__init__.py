@@ -55,6 +55,9 @@ def _load():
     lib.orc_block_num_sources.restype = ll
     lib.orc_block_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll]
     lib.orc_block_route_fwd.restype = ctypes.c_int
+    lib.orc_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d,
+                                        ll, ll]
+    lib.orc_block_route_bwd.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -169,3 +172,32 @@ def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid block problem")
     return out
+
+
+def block_route_bwd(O, KO, q, dH, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """Gradients (dO, dKO, dq) of L = sum(dH * h_t) for the block-source
+    forward at site t: every member of a block receives its summary's
+    gradient.  dO [t, n1-n0, d], dKO [t, n1-n0, r] (projected, else None),
+    dq [r] summed over the token range; all fp64."""
+    O = np.ascontiguousarray(np.ascontiguousarray(O)[:t])
+    _, N, d = O.shape
+    if mode == PROJECTED:
+        KO = np.ascontiguousarray(np.ascontiguousarray(KO)[:t])
+        r = KO.shape[2]
+    elif r is None:
+        raise ValueError("oracle: sliced keys need r")
+    dH = np.ascontiguousarray(dH)
+    if dH.dtype != O.dtype or dH.shape != (N, d):
+        raise ValueError("oracle: dH must be [N, d] in O's storage")
+    q = np.ascontiguousarray(np.asarray(q, dtype=np.float64))
+    n1 = N if n1 is None else n1
+    nt = n1 - n0
+    dO = np.empty((t, nt, d), dtype=np.float64)
+    dKO = np.empty((t, nt, r), dtype=np.float64) if mode == PROJECTED else None
+    dq = np.empty((r,), dtype=np.float64)
+    rc = _load().orc_block_route_bwd(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
+                                     _ptr(dH), _ptr(dO), _ptr(dKO), _ptr(dq), t, c, N, d, r,
+                                     mode, _STORE[O.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid block problem")
+    return dO, dKO, dq

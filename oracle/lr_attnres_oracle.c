@@ -384,6 +384,66 @@ int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *
     return rc;
 }
 
+/* Backward of the block-source forward at site t for L = sum_n dH[n] . h[n]:
+ * the routing backward (orc_route_bwd) applied to the block summaries gives
+ * each summary's gradient; since a summary is the plain sum of its members,
+ * every member's output (and projected key) receives its summary's gradient
+ * unchanged.  dO is [t][n1-n0][d], dKO [t][n1-n0][r] (projected only, else
+ * NULL), dq [r] summed over tokens [n0, n1); dH is [N][d] in O's storage. */
+int orc_block_route_bwd(const void *O, const void *KO, const double *q, const void *dH,
+                        double *dO, double *dKO, double *dq, long long t, long long c,
+                        long long N, long long d, long long r, int mode, int store, double eps,
+                        long long n0, long long n1)
+{
+    const long long S = orc_block_num_sources(t, c);
+    if (S < 1 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
+        q == NULL || dH == NULL || dO == NULL || dq == NULL ||
+        (mode != ORC_KEYS_PROJECTED && mode != ORC_KEYS_SLICED) ||
+        (mode == ORC_KEYS_PROJECTED) != (KO != NULL) ||
+        (mode == ORC_KEYS_PROJECTED) != (dKO != NULL) || (mode == ORC_KEYS_SLICED && r > d) ||
+        store < 0 || store > 2)
+        return 1;
+    const long long nt = n1 - n0;
+    const int proj = mode == ORC_KEYS_PROJECTED;
+    double *B = (double *)calloc((size_t)(S * nt * d), sizeof(double));
+    double *KB = proj ? (double *)calloc((size_t)(S * nt * r), sizeof(double)) : NULL;
+    double *dHr = (double *)malloc(sizeof(double) * (size_t)(nt * d));
+    double *dB = (double *)malloc(sizeof(double) * (size_t)(S * nt * d));
+    double *dKB = proj ? (double *)malloc(sizeof(double) * (size_t)(S * nt * r)) : NULL;
+    int rc = 1;
+    if (B == NULL || dHr == NULL || dB == NULL || (proj && (KB == NULL || dKB == NULL)))
+        goto done;
+    for (long long i = 0; i < t; ++i) {
+        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
+        for (long long n = n0; n < n1; ++n) {
+            for (long long j = 0; j < d; ++j)
+                B[(slot * nt + (n - n0)) * d + j] += widen(O, store, (i * N + n) * d + j);
+            if (proj)
+                for (long long j = 0; j < r; ++j)
+                    KB[(slot * nt + (n - n0)) * r + j] += widen(KO, store, (i * N + n) * r + j);
+        }
+    }
+    for (long long n = n0; n < n1; ++n)
+        for (long long j = 0; j < d; ++j)
+            dHr[(n - n0) * d + j] = widen(dH, store, n * d + j);
+    rc = orc_route_bwd(B, KB, q, dHr, dB, dKB, dq, S, nt, d, r, mode, ORC_STORE_F64, eps, 0, nt);
+    if (rc)
+        goto done;
+    for (long long i = 0; i < t; ++i) {
+        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
+        memcpy(dO + i * nt * d, dB + slot * nt * d, sizeof(double) * (size_t)(nt * d));
+        if (proj)
+            memcpy(dKO + i * nt * r, dKB + slot * nt * r, sizeof(double) * (size_t)(nt * r));
+    }
+done:
+    free(B);
+    free(KB);
+    free(dHr);
+    free(dB);
+    free(dKB);
+    return rc;
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {

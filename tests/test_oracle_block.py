@@ -84,3 +84,51 @@ def test_block_token_ranges_compose(orc):
     H = orc.block_route_fwd(O, KO, q, t=11, c=3, mode=PROJECTED)
     part = orc.block_route_fwd(O, KO, q, t=11, c=3, mode=PROJECTED, n0=6, n1=15)
     assert np.array_equal(H[6:15], part)
+
+
+STEP = 1e-6
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+@pytest.mark.parametrize("t,c", [(1, 2), (4, 2), (7, 3), (6, 1), (5, 9)])
+def test_block_backward_matches_central_differences(orc, mode, t, c):
+    """The block backward (summary gradients handed to every member) against
+    fp64 central differences of the block forward."""
+    rng = np.random.default_rng(10 * t + c)
+    N, d, r, eps = 2, 6, 3, 0.2
+    O = rng.standard_normal((t, N, d))
+    KO = rng.standard_normal((t, N, r)) if mode == PROJECTED else None
+    q = rng.standard_normal(r) * 1.5
+    dH = rng.standard_normal((N, d))
+    dO, dKO, dq = orc.block_route_bwd(O, KO, q, dH, t, c, mode, r=r, eps=eps)
+
+    def loss():
+        return float((orc.block_route_fwd(O, KO, q, t, c, mode, r=r, eps=eps) * dH).sum())
+
+    def fd(x):
+        g = np.empty_like(x)
+        for idx in np.ndindex(x.shape):
+            v = x[idx]
+            x[idx] = v + STEP
+            lp = loss()
+            x[idx] = v - STEP
+            lm = loss()
+            x[idx] = v
+            g[idx] = (lp - lm) / (2 * STEP)
+        return g
+
+    np.testing.assert_allclose(dO, fd(O), rtol=1e-6, atol=1e-7)
+    if mode == PROJECTED:
+        np.testing.assert_allclose(dKO, fd(KO), rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(dq, fd(q), rtol=1e-6, atol=1e-7)
+
+
+def test_block_backward_of_blocks_of_one_is_the_routing_backward(orc):
+    O, KO, q = _stack(PROJECTED, 8, 5, 10, 4, seed=4)
+    rng = np.random.default_rng(5)
+    dH = rng.standard_normal((5, 10)).astype(np.float32)
+    dO, dKO, dq = orc.block_route_bwd(O, KO, q, dH, 8, 1, PROJECTED)
+    dV, dK, dq2 = orc.route_bwd(O, KO, q, dH, PROJECTED)
+    np.testing.assert_allclose(dO, dV, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(dKO, dK, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(dq, dq2, rtol=0, atol=1e-13)
