@@ -235,6 +235,66 @@ def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush):
             "frac_of_peak": nbytes / (total * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
 
+def block_training_pass(torch, lr, dev, O, mode, r, c, reps, warmup):
+    """A whole block-source training pass: the forward at all 49 sites, then
+    the reverse pass (slot gradients zeroed first, then one fused backward
+    call per site, last site first).  Timed end to end with HIP events; the
+    MALL is not flushed between sites (a real step runs them back to back)."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    dB = torch.zeros_like(B)
+    KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev) if mode == 0 else None
+    dKB = torch.zeros_like(KB) if KB is not None else None
+    gen = torch.Generator(device=dev).manual_seed(200 + r)
+    KO = (torch.randn((T, N, r), generator=gen, device=dev).to(torch.bfloat16)
+          if mode == 0 else None)
+    Q = torch.randn((T, r), generator=gen, device=dev) / r ** 0.5
+    dHs = torch.randn((T, N, d), generator=gen, device=dev).to(torch.bfloat16)
+    H = torch.empty((N, d), dtype=O.dtype, device=dev)
+    dO = torch.empty((N, d), dtype=O.dtype, device=dev)
+    dK = torch.empty((N, r), dtype=O.dtype, device=dev) if mode == 0 else None
+    dq = torch.empty((r,), dtype=torch.float32, device=dev)
+    ws = torch.empty((lr.route_bwd_workspace_bytes(nslots, N, d, r, mode, torch.float32),),
+                     dtype=torch.uint8, device=dev)
+    sites = [(1, True)] + [((t - 2) // c + 2, (t - 2) % c == 0) for t in range(2, T + 1)]
+
+    def fwd():
+        for t in range(1, T + 1):
+            n_src, start = sites[t - 1]
+            lr.block_route_fwd(B, KB, O[t - 1], KO[t - 1] if KO is not None else None,
+                               Q[t - 1], n_src, start, mode, out=H)
+
+    def bwd():
+        dB.zero_()
+        if dKB is not None:
+            dKB.zero_()
+        for t in range(T, 0, -1):
+            lr.block_route_bwd(B, KB, dB, dKB, O[t - 1], KO[t - 1] if KO is not None else None,
+                               Q[t - 1], dHs[t - 1], sites[t - 1][0], mode,
+                               out=(dO, dK, dq), workspace=ws)
+
+    st = torch.cuda.current_stream()
+    for _ in range(warmup):
+        fwd()
+        bwd()
+    tf, tb = [], []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(st)
+        fwd()
+        e[1].record(st)
+        bwd()
+        e[2].record(st)
+        torch.cuda.synchronize()
+        tf.append(e[0].elapsed_time(e[1]))
+        tb.append(e[1].elapsed_time(e[2]))
+    f, b = float(np.median(tf)), float(np.median(tb))
+    del B, dB, KB, dKB, KO, dHs, ws
+    return {"fwd_pass_ms": f, "bwd_pass_ms": b, "step_ms": f + b,
+            "tokens_per_s": N / ((f + b) * 1e-3)}
+
+
 def extras(torch, lr, dev, reps, warmup):
     """The other workloads: the 49-site forward model pass (projected r=16 and
     sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
@@ -312,6 +372,10 @@ def extras(torch, lr, dev, reps, warmup):
                                                             6, reps, warmup, flush)
     out["block_model_pass_projected_r32_8blocks"] = block_pass(torch, lr, dev, V, PROJECTED,
                                                                32, 6, reps, warmup, flush)
+    out["block_training_pass_sliced_r64_8blocks"] = block_training_pass(
+        torch, lr, dev, V, SLICED, 64, 6, 5, 1)
+    out["block_training_pass_projected_r32_8blocks"] = block_training_pass(
+        torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush
     torch.cuda.empty_cache()

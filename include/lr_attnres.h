@@ -170,6 +170,36 @@ int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const voi
                                int64_t d, int64_t r, int mode, int dtype, float eps,
                                void *stream);
 
+/*
+ * Block-source backward at one residual site, for the reverse pass of a
+ * model that ran lr_attnres_block_route_fwd at every site (Sec. 3.1 "Block
+ * AttnRes" with Sec. 3.2; the gradient of L = sum_n dH[n] . h[n]).  Sites are
+ * visited in reverse order.  On entry the slots hold what the forward of this
+ * site saw (slot n_src-1 includes o_new); on return:
+ *   dB  [n_src][N][d] fp32 += the gradient of each slot (value path and, for
+ *                       sliced keys, the key path in the last r columns);
+ *   dKB [n_src][N][r] fp32 += the gradient of each key summary (projected;
+ *                       else NULL);
+ *   dO  [N][d], dK [N][r] (storage `dtype`) = dB[n_src-1], dKB[n_src-1]: a
+ *                       summary is the plain sum of its members, so the member
+ *                       o_new receives its slot's gradient, which at this
+ *                       point holds the contributions of every later site;
+ *   B[n_src-1] -= o_new, KB[n_src-1] -= k_new: the member leaves its slot, so
+ *                       the previous site sees its own partial summary;
+ *   dq [r] fp32 = this site's query gradient (summed over tokens).
+ *   dH [N][d] is in storage `dtype`; workspace as for lr_attnres_route_bwd
+ *   with S = n_src and LRAR_DTYPE_F32.
+ * Limits: those of lr_attnres_block_route_fwd and of the backward.  Outputs
+ * (B, KB, dB, dKB, dO, dK, dq, workspace) must not overlap each other or the
+ * inputs (o_new, k_new, q, dH).  Removing o_new from the fp32 slot by
+ * subtraction differs from the forward's partial sum by fp32 rounding only.
+ */
+int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const void *o_new,
+                               const void *k_new, const float *q, const void *dH, void *dO,
+                               void *dK, float *dq, void *workspace, size_t workspace_bytes,
+                               int64_t n_src, int64_t N, int64_t d, int64_t r, int mode,
+                               int dtype, float eps, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

@@ -56,6 +56,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_block_route_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i, i64, i64, i64,
                                                i, i, f, vp]
     lib.lr_attnres_block_route_fwd.restype = ctypes.c_int
+    lib.lr_attnres_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                               ctypes.c_size_t, i64, i64, i64, i64, i, i, f, vp]
+    lib.lr_attnres_block_route_bwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -207,3 +210,39 @@ def block_route_fwd(B, KB, o_new, k_new, q, n_src: int, start: bool, mode, eps: 
         N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
     _check(lib, rc)
     return H
+
+
+def block_route_bwd(B, KB, dB, dKB, o_new, k_new, q, dH, n_src: int, mode, eps: float = 1e-6,
+                    out=None, workspace=None):
+    """One site of the block-source reverse pass (see lr_attnres_block_route_bwd).
+
+    Adds the site's slot gradients into dB / dKB (fp32), removes o_new (and
+    k_new) from slot n_src-1 of B / KB, and returns (dO, dK, dq): the
+    gradient of o_new (= dB[n_src-1]), of k_new (projected keys, else None)
+    and of this site's query.
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    _, N, d = B.shape
+    r = KB.shape[2] if mode == PROJECTED else q.shape[0]
+    if out is not None:
+        dO, dK, dq = out
+    else:
+        dO = torch.empty((N, d), dtype=o_new.dtype, device=B.device)
+        dK = (torch.empty((N, r), dtype=o_new.dtype, device=B.device)
+              if mode == PROJECTED else None)
+        dq = torch.empty((r,), dtype=torch.float32, device=B.device)
+    need = lib.lr_attnres_route_bwd_workspace_bytes(n_src, N, d, r, mode, _F32)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=B.device)
+    rc = lib.lr_attnres_block_route_bwd(
+        _dev(B, "B", torch.float32), _dev(KB, "KB", torch.float32),
+        _dev(dB, "dB", torch.float32), _dev(dKB, "dKB", torch.float32),
+        _dev(o_new, "o_new"), _dev(k_new, "k_new", o_new.dtype), _dev(q, "q", torch.float32),
+        _dev(dH, "dH", o_new.dtype), _dev(dO, "dO", o_new.dtype), _dev(dK, "dK", o_new.dtype),
+        _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"), workspace.numel(),
+        int(n_src), N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
+    _check(lib, rc)
+    return dO, dK, dq

@@ -117,7 +117,7 @@ int lr_attnres_route_fwd(const void *V, const void *K, const float *q, void *H, 
     const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4)};
     if ((rc = check_aliasing(outs, 1, ins, 3)))
         return rc;
-    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps};
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps, dtype};
     std::string why;
     if ((rc = lrar::check_supported(p, false, &why)))
         return fail(rc, why);
@@ -135,7 +135,7 @@ size_t lr_attnres_route_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int
     g_last_error = saved;
     if (rc)
         return 0;
-    lrar::Problem p{nullptr, nullptr, nullptr, S, N, d, r, mode, dtype, 0.0f};
+    lrar::Problem p{nullptr, nullptr, nullptr, S, N, d, r, mode, dtype, 0.0f, dtype};
     return lrar::bwd_workspace_bytes(p);
 }
 
@@ -162,7 +162,7 @@ int route_bwd(const void *V, const void *K, const float *q, const void *dH, void
         return rc;
     if (!proj && (K || dK))
         return fail(LRAR_EINVAL, "K and dK must be NULL unless keys are projected");
-    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps};
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps, dtype};
     std::string why;
     if ((rc = lrar::check_supported(p, true, &why)))
         return fail(rc, why);
@@ -244,6 +244,66 @@ int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const voi
     if ((rc = lrar::check_block_supported(p, &why)))
         return fail(rc, why);
     if ((rc = lrar::launch_block_fwd(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const void *o_new,
+                               const void *k_new, const float *q, const void *dH, void *dO,
+                               void *dK, float *dq, void *workspace, size_t workspace_bytes,
+                               int64_t n_src, int64_t N, int64_t d, int64_t r, int mode,
+                               int dtype, float eps, void *stream)
+{
+    g_last_error.clear();
+    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
+        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
+                    "block routing takes projected or sliced keys");
+    int64_t ve, ke, he;
+    int rc = check_shape(n_src, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const size_t ek = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(dB, "dB", 16, data)) ||
+        (rc = check_ptr(o_new, "o_new", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(dH, "dH", 16, data)) || (rc = check_ptr(dO, "dO", 16, data)) ||
+        (rc = check_ptr(dq, "dq", 4, true)) || (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(dKB, "dKB", 16, data && proj)) ||
+        (rc = check_ptr(k_new, "k_new", ek, data && proj)) ||
+        (rc = check_ptr(dK, "dK", ek, data && proj)) ||
+        (rc = check_ptr(workspace, "workspace", 16, false)))
+        return rc;
+    if (!proj && (KB || dKB || k_new || dK))
+        return fail(LRAR_EINVAL, "KB, dKB, k_new and dK must be NULL unless keys are projected");
+    const lrar::BlockProblem bp{B, KB, o_new, k_new, q, nullptr, n_src, N, d, r, 0, mode,
+                                dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_block_supported(bp, &why)))
+        return fail(rc, why);
+    // The routing backward runs over the fp32 slots with the model-dtype dH.
+    lrar::Problem p{B, KB, q, n_src, N, d, r, mode, LRAR_DTYPE_F32, eps, dtype};
+    if ((rc = lrar::check_supported(p, true, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::bwd_workspace_bytes(p);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t nr;
+    if (!mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("B", B, ve * 4),         span("KB", KB, ke * 4),
+                         span("dB", dB, ve * 4),       span("dKB", dKB, ke * 4),
+                         span("dO", dO, he * es),      span("dK", dK, nr * es),
+                         span("dq", dq, r * 4),        span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("o_new", o_new, he * es), span("k_new", k_new, nr * es),
+                        span("q", q, r * 4), span("dH", dH, he * es)};
+    if ((rc = check_aliasing(outs, 8, ins, 4)))
+        return rc;
+    const lrar::BlockRetire br{B, KB, dB, dKB, o_new, k_new, dO, dK, n_src - 1, N, d, r, mode,
+                               dtype};
+    if ((rc = lrar::launch_block_bwd(p, br, dH, dB, dKB, dq, workspace,
+                                     static_cast<hipStream_t>(stream), &why)))
         return fail(rc, why);
     return LRAR_OK;
 }

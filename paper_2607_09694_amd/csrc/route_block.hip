@@ -11,6 +11,8 @@
 // slot j comes from the registers.  A summary's key is the sum of its
 // members' keys: for sliced keys the tail of the summed row, for projected
 // keys a second fp32 slot stack [slot][N][r] updated the same way.
+#include <algorithm>
+
 #include "route_common.h"
 
 namespace lrar {
@@ -117,6 +119,61 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
                                             Narrow<TO, VEC>::run(acc[c]));
 }
 
+// Retire the member o_new from slot j and hand it its gradient (see
+// BlockRetire): 4 consecutive row elements per thread, grid-stride.
+template <typename TO>
+__global__ void __launch_bounds__(256)
+block_retire(float *__restrict__ Bj, const float *__restrict__ dBj, const TO *__restrict__ o_new,
+             TO *__restrict__ dO, long long nvec)
+{
+    const long long stride = (long long)gridDim.x * 256;
+    for (long long v = (long long)blockIdx.x * 256 + threadIdx.x; v < nvec; v += stride) {
+        const long long e0 = v * 4;
+        float b[4], o[4], g[4];
+        widen(load_raw<float, 4>(Bj + e0), b);
+        widen(load_raw<TO, 4>(o_new + e0), o);
+        widen(load_raw<float, 4>(dBj + e0), g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            b[e] -= o[e];
+        store_raw<float, 4>(Bj + e0, Narrow<float, 4>::run(b));
+        store_raw<TO, 4>(dO + e0, Narrow<TO, 4>::run(g));
+    }
+}
+
+// The same for the projected key rows (any r): one element per thread.
+template <typename TO>
+__global__ void __launch_bounds__(256)
+block_retire_keys(float *__restrict__ KBj, const float *__restrict__ dKBj,
+                  const TO *__restrict__ k_new, TO *__restrict__ dK, long long n)
+{
+    const long long stride = (long long)gridDim.x * 256;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) {
+        KBj[i] -= load_elem(k_new + i);
+        store_elem(dK + i, dKBj[i]);
+    }
+}
+
+template <typename TO>
+hipError_t launch_retire_t(const BlockRetire &br, hipStream_t st)
+{
+    const size_t plane = (size_t)br.N * br.d;
+    const long long nvec = (long long)(plane / 4);
+    const int grid = (int)std::min<long long>((nvec + 255) / 256, 8192);
+    hipLaunchKernelGGL(block_retire<TO>, dim3(grid), dim3(256), 0, st, br.B + br.j * plane,
+                       br.dB + br.j * plane, static_cast<const TO *>(br.o_new),
+                       static_cast<TO *>(br.dO), nvec);
+    if (br.mode == LRAR_MODE_PROJECTED) {
+        const size_t kplane = (size_t)br.N * br.r;
+        const int kgrid = (int)std::min<long long>(((long long)kplane + 255) / 256, 8192);
+        hipLaunchKernelGGL(block_retire_keys<TO>, dim3(kgrid), dim3(256), 0, st,
+                           br.KB + br.j * kplane, br.dKB + br.j * kplane,
+                           static_cast<const TO *>(br.k_new), static_cast<TO *>(br.dK),
+                           (long long)kplane);
+    }
+    return hipGetLastError();
+}
+
 namespace {
 
 template <typename TO>
@@ -147,6 +204,12 @@ hipError_t launch_block_t(const BlockProblem &p, int nch, bool fullcols, size_t 
 }
 
 }  // namespace
+
+hipError_t launch_block_retire(const BlockRetire &br, hipStream_t st)
+{
+    return br.dtype == LRAR_DTYPE_BF16 ? launch_retire_t<uint16_t>(br, st)
+                                       : launch_retire_t<float>(br, st);
+}
 
 int check_block_supported(const BlockProblem &p, std::string *why)
 {

@@ -27,10 +27,12 @@ template <int KV> struct KeyChunks { static constexpr int value = KV == 8 ? 1 : 
 //   then, lanes over (source, key vector), writes dK (projected) or the last
 //   columns of dV including the key gradient (sliced), and accumulates dq.
 // dq is reduced per workgroup in a fixed order into partial[blockIdx.x][r].
-template <typename T, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC>
+// T is the storage of V, K, dV and dK; TH that of dH (the same except for
+// block sources, whose fp32 summary slots meet the model's bf16 gradient).
+template <typename T, typename TH, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC>
 __global__ void __launch_bounds__(kBlock)
 route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
-             const T *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
+             const TH *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
              float *__restrict__ partial, int S, int N, int d, int r, int krow, int koff,
              int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw, int lps)
 {
@@ -82,11 +84,11 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
 
         typedef typename Raw<T, VEC>::type raw_t;
         float dh[NCH][VEC];
-        const T *dhrow = dH + (size_t)n * d + col;
+        const TH *dhrow = dH + (size_t)n * d + col;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             if (FULLCOLS || ok[c]) {
-                widen(load_raw<T, VEC>(dhrow + c * kWaveSize * VEC), dh[c]);
+                widen(load_raw<TH, VEC>(dhrow + c * kWaveSize * VEC), dh[c]);
             } else {
 #pragma unroll
                 for (int e = 0; e < VEC; ++e)
@@ -166,7 +168,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
             const int c0 = kbase + v * KV;  // projected: key index; sliced: value column
             float dhk[KV];
             if (sliced && vok) {
-                widen(load_raw<T, KV>(dH + (size_t)n * d + c0), dhk);
+                widen(load_raw<TH, KV>(dH + (size_t)n * d + c0), dhk);
             } else {
 #pragma unroll
                 for (int e = 0; e < KV; ++e)
@@ -440,7 +442,7 @@ KeyPass key_pass(const Problem &p, const Plan &pl)
     return k;
 }
 
-template <typename T, int VEC, bool ACC>
+template <typename T, typename TH, int VEC, bool ACC>
 hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
                         float *partial, hipStream_t st)
 {
@@ -454,18 +456,20 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
     return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
-        if (p.mode == LRAR_MODE_FULL) {
-            hipLaunchKernelGGL((route_bwd_full<T, VEC, NCH, FC, ACC>), dim3(pl.nblocks), dim3(kBlock),
-                               pl.lds, st, V, p.q, static_cast<const T *>(dH),
-                               static_cast<T *>(dV), partial, (int)p.S, (int)p.N, (int)p.d,
-                               p.eps, pl.s_pad, pl.tpw);
-            return hipGetLastError();
+        if constexpr (std::is_same<T, TH>::value) {
+            if (p.mode == LRAR_MODE_FULL) {
+                hipLaunchKernelGGL((route_bwd_full<T, VEC, NCH, FC, ACC>), dim3(pl.nblocks),
+                                   dim3(kBlock), pl.lds, st, V, p.q, static_cast<const T *>(dH),
+                                   static_cast<T *>(dV), partial, (int)p.S, (int)p.N, (int)p.d,
+                                   p.eps, pl.s_pad, pl.tpw);
+                return hipGetLastError();
+            }
         }
         auto launch = [&](auto kvc) {
             constexpr int KV = decltype(kvc)::value;
-            hipLaunchKernelGGL((route_bwd_lr<T, VEC, NCH, FC, KV, ACC>), dim3(pl.nblocks),
+            hipLaunchKernelGGL((route_bwd_lr<T, TH, VEC, NCH, FC, KV, ACC>), dim3(pl.nblocks),
                                dim3(kBlock), pl.lds, st, V, keys, p.q,
-                               static_cast<const T *>(dH), static_cast<T *>(dV),
+                               static_cast<const TH *>(dH), static_cast<T *>(dV),
                                static_cast<T *>(dK), partial, (int)p.S, (int)p.N, (int)p.d,
                                (int)p.r, krow, koff, p.mode == LRAR_MODE_SLICED ? 1 : 0,
                                tail_start, p.eps, pl.s_pad, pl.r_pad, pl.tpw, kp.lps);
@@ -482,24 +486,33 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
     });
 }
 
-template <bool ACC>
+// The routing backward (accumulating dV / dK when ACC) and the dq reduction
+// (accumulating when ACCQ).  Mixed storage (fp32 values, bf16 dH) exists only
+// for the accumulating form used by block sources.
+template <bool ACC, bool ACCQ>
 hipError_t launch_bwd_acc(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
                           float *dq, float *partial, hipStream_t st)
 {
     hipError_t e = hipSuccess;
     if (p.N > 0) {
+        const bool mixed = p.dtype == LRAR_DTYPE_F32 && p.dh_dtype == LRAR_DTYPE_BF16;
         if (p.dtype == LRAR_DTYPE_BF16)
-            e = pl.vec > 1 ? launch_bwd_t<uint16_t, 8, ACC>(p, pl, dH, dV, dK, partial, st)
-                           : launch_bwd_t<uint16_t, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+            e = pl.vec > 1 ? launch_bwd_t<uint16_t, uint16_t, 8, ACC>(p, pl, dH, dV, dK, partial, st)
+                           : launch_bwd_t<uint16_t, uint16_t, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+        else if (!mixed)
+            e = pl.vec > 1 ? launch_bwd_t<float, float, 4, ACC>(p, pl, dH, dV, dK, partial, st)
+                           : launch_bwd_t<float, float, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+        else if constexpr (ACC)
+            e = pl.vec > 1 ? launch_bwd_t<float, uint16_t, 4, ACC>(p, pl, dH, dV, dK, partial, st)
+                           : launch_bwd_t<float, uint16_t, 1, ACC>(p, pl, dH, dV, dK, partial, st);
         else
-            e = pl.vec > 1 ? launch_bwd_t<float, 4, ACC>(p, pl, dH, dV, dK, partial, st)
-                           : launch_bwd_t<float, 1, ACC>(p, pl, dH, dV, dK, partial, st);
+            e = hipErrorInvalidValue;
         if (e != hipSuccess)
             return e;
     }
     const int ncols = (int)(p.mode == LRAR_MODE_FULL ? p.d : p.r);
     const int nb = p.N > 0 ? pl.nblocks : 0;
-    hipLaunchKernelGGL(dq_reduce<ACC>, dim3(ncols), dim3(256), 0, st, partial, dq, nb, ncols);
+    hipLaunchKernelGGL(dq_reduce<ACCQ>, dim3(ncols), dim3(256), 0, st, partial, dq, nb, ncols);
     return hipGetLastError();
 }
 
@@ -512,9 +525,27 @@ int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, 
     if (!make_plan(p, true, &pl, err))
         return LRAR_EUNSUPPORTED;
     float *partial = static_cast<float *>(ws);
-    const hipError_t e = accumulate ? launch_bwd_acc<true>(p, pl, dH, dV, dK, dq, partial, st)
-                                    : launch_bwd_acc<false>(p, pl, dH, dV, dK, dq, partial, st);
+    const hipError_t e =
+        accumulate ? launch_bwd_acc<true, true>(p, pl, dH, dV, dK, dq, partial, st)
+                   : launch_bwd_acc<false, false>(p, pl, dH, dV, dK, dq, partial, st);
     return hip_status(e, "route_bwd launch", err);
+}
+
+// Block sources, one site of the reverse pass: accumulate the slot gradients
+// (fp32) from the model-dtype dH, write dq, then retire the site (the
+// member's gradient is its slot's gradient so far; the member leaves its
+// slot).
+int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,
+                     void *dKB, float *dq, void *ws, hipStream_t st, std::string *err)
+{
+    Plan pl;
+    if (!make_plan(p, true, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    hipError_t e = launch_bwd_acc<true, false>(p, pl, dH, dB, dKB, dq, static_cast<float *>(ws),
+                                               st);
+    if (e == hipSuccess && p.N > 0)
+        e = launch_block_retire(br, st);
+    return hip_status(e, "block_route_bwd launch", err);
 }
 
 }  // namespace lrar

@@ -19,6 +19,7 @@ struct Problem {
     int64_t S, N, d, r;
     int mode, dtype;
     float eps;
+    int dh_dtype;    // storage of dH; differs from dtype only for block sources
 };
 
 // LRAR_OK if a kernel covers the (already validated) problem, else
@@ -48,5 +49,26 @@ struct BlockProblem {
 
 int check_block_supported(const BlockProblem &p, std::string *why);
 int launch_block_fwd(const BlockProblem &p, hipStream_t st, std::string *err);
+
+// The end of one site of the block reverse pass: the member o_new (and its
+// projected key) leaves slot j (B[j] -= o_new, KB[j] -= k_new), and its
+// gradient is the slot's gradient accumulated so far (dO = dB[j],
+// dK = dKB[j], in the model dtype).
+struct BlockRetire {
+    float *B, *KB;
+    const float *dB, *dKB;
+    const void *o_new, *k_new;
+    void *dO, *dK;
+    int64_t j, N, d, r;
+    int mode, dtype;
+};
+
+hipError_t launch_block_retire(const BlockRetire &br, hipStream_t st);
+
+// One site of the block reverse pass: the routing backward over the fp32
+// slots (p.dtype = F32, p.dh_dtype = the model dtype) accumulating into dB
+// and dKB, dq written, then the retire step above.
+int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,
+                     void *dKB, float *dq, void *ws, hipStream_t st, std::string *err);
 
 }  // namespace lrar

@@ -41,6 +41,7 @@ def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
+                            "lr_attnres_block_route_bwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -199,3 +200,37 @@ def test_block_forward_unsupported(lib):
     assert blk(lib, d=66) == EUNSUPPORTED
     assert blk(lib, d=4096) == EUNSUPPORTED
     assert blk(lib, n_src=1025) == EUNSUPPORTED
+
+
+B_, X, Y, Z = (0x10_0000_0000 * k for k in range(8, 12))
+
+
+def bblk(lib, B=A, KB=None, dB=B_, dKB=None, o_new=C, k_new=None, q=E, dH=D, dO=G, dK=None,
+         dq=X, ws=W, wsb=1 << 30, n_src=3, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_block_route_bwd(B, KB, dB, dKB, o_new, k_new, q, dH, dO, dK, dq, ws,
+                                          wsb, n_src, N, d, r, mode, dtype, eps, None)
+
+
+BLOCK_BWD_INVALID = [
+    ("dB NULL", dict(dB=None), "dB is NULL"),
+    ("dO NULL", dict(dO=None), "dO is NULL"),
+    ("dH NULL", dict(dH=None), "dH is NULL"),
+    ("projected without dKB", dict(mode=P, KB=Y, k_new=Z, dK=Z + 0x1000_0000), "dKB is NULL"),
+    ("dK outside projected", dict(dK=Y), "must be NULL"),
+    ("dB overlaps B", dict(dB=A + 64), "overlap"),
+    ("dO overlaps dH", dict(dO=D), "overlaps"),
+    ("workspace too small", dict(wsb=4), "workspace"),
+    ("unknown mode", dict(mode=9), "projected or sliced"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", BLOCK_BWD_INVALID, ids=[c[0] for c in BLOCK_BWD_INVALID])
+def test_block_backward_rejects(lib, name, kw, msg):
+    assert bblk(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_block_backward_unsupported(lib):
+    assert bblk(lib, mode=F, r=64) == EUNSUPPORTED
+    assert bblk(lib, d=66) == EUNSUPPORTED
+    assert bblk(lib, n_src=513) == EUNSUPPORTED

@@ -9,7 +9,7 @@ import oracle
 import paper_2607_09694_amd as lr
 from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
                                          f32_from_bf16_bits, make_host_problem)
-from parity import check_bf16_key_grad, check_f32
+from parity import check_bf16_key_grad, check_dq, check_f32
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -117,3 +117,53 @@ def test_block_model_pass_full_size(dev, mode, r):
     for t in sites:
         ref = oracle.block_route_fwd(Os, Ks, Q[t - 1].cpu().numpy(), t, c, mode, r=r)
         check_bf16_key_grad(f"H at site {t}", to_host(out[t].index_select(0, ti)), ref)
+
+
+TRAIN_CASES = [
+    (PROJECTED, "bf16", 13, 70, 256, 16, 3),
+    (SLICED, "bf16", 13, 70, 256, 16, 3),
+    (PROJECTED, "f32", 10, 33, 1024, 32, 4),
+    (SLICED, "f32", 10, 33, 1000, 64, 2),
+    (SLICED, "bf16", 7, 21, 512, 8, 1),
+]
+
+
+@pytest.mark.parametrize("case", TRAIN_CASES, ids=lambda c: f"{'P' if c[0] == 0 else 'S'}-{c[1]}-T{c[2]}-N{c[3]}-d{c[4]}-r{c[5]}-c{c[6]}")
+def test_block_training_pass_matches_oracle(dev, case):
+    """Forward at every site, then the reverse pass site by site: each
+    member's gradient (summed over every later site) and each site's dq
+    against the oracle's per-site block backward, summed over sites."""
+    mode, dtype, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype=dtype, seed=T * 10 + N)
+    rng = np.random.default_rng(N)
+    Qh = (rng.standard_normal((T, r)) / np.sqrt(r)).astype(np.float32)
+    dHh = make_host_problem(PROJECTED, T, N, d, 1, dtype=dtype, seed=T * 10 + N + 1).V
+    O, KO, Q, dHs = to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev), to_dev(dHh, dev)
+    _, B, KB = drive_model_pass(dev, O, KO, Q, c, mode, [T])
+    dB = torch.zeros_like(B)
+    dKB = torch.zeros_like(KB) if KB is not None else None
+    dO = torch.empty_like(O)
+    dK = torch.empty_like(KO) if KO is not None else None
+    dq = torch.empty((T, r), dtype=torch.float32, device=dev)
+    for t in range(T, 0, -1):
+        n_src, _ = site_args(t, c)
+        lr.block_route_bwd(B, KB, dB, dKB, O[t - 1], KO[t - 1] if KO is not None else None,
+                           Q[t - 1], dHs[t - 1], n_src, mode,
+                           out=(dO[t - 1], dK[t - 1] if dK is not None else None, dq[t - 1]))
+    torch.cuda.synchronize()
+    ref_dO = np.zeros((T, N, d))
+    ref_dK = np.zeros((T, N, r)) if mode == PROJECTED else None
+    for t in range(1, T + 1):
+        gO, gK, gq = oracle.block_route_bwd(p.V, p.K, Qh[t - 1], dHh[t - 1], t, c, mode, r=r)
+        ref_dO[:t] += gO
+        if mode == PROJECTED:
+            ref_dK[:t] += gK
+        check_dq(f"dq at site {t}", dq[t - 1].cpu().numpy(), gq,
+                 tol=1e-5 if dtype == "f32" else 1e-4)
+    check = check_f32 if dtype == "f32" else check_bf16_key_grad
+    check("dO", to_host(dO), ref_dO)
+    if mode == PROJECTED:
+        check("dK", to_host(dK), ref_dK)
+    # every member has left its slot again
+    assert float(B.abs().max()) < 1e-3 * max(1.0, float(torch.from_numpy(
+        np.abs(to_host(O)).sum(axis=0)).max()))
