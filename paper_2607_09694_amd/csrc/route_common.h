@@ -54,42 +54,65 @@ constexpr int bwd_tokens_per_wave(int nch) { return nch >= 4 ? 2 : 1; }
 // Scores and softmax (Eqs. lr_key_norm and lr_attnres_weight)
 // ---------------------------------------------------------------------------
 
-// Lane-per-source scores of token n: rho_i = sqrt(mean_j k_ij^2 + eps),
-// s_i = q . k_i / rho_i.  Key element j of source i is
-// keys[(i*N + n)*krow + koff + j]  (projected: keys = K, krow = r, koff = 0;
-// sliced: keys = V, krow = d, koff = d - r).  Each lane writes only the
-// entries of its own sources.
-template <typename T, int VEC>
-__device__ inline void lr_scores(const T *__restrict__ keys, const float *__restrict__ q, int S,
-                          int N, int r, int krow, int koff, float eps, int n, int lane,
-                          float *s_out, float *rho_out)
+// Scores of token n: rho_i = sqrt(mean_j k_ij^2 + eps), s_i = q . k_i / rho_i.
+// Key element j of source i is keys[(i*N + n)*krow + koff + j] (projected:
+// keys = K, krow = r, koff = 0; sliced: keys = V, krow = d, koff = d - r).
+// The key of one source is nkv vectors of KV elements; a group of lps lanes
+// (the power of two >= nkv, at most 64) reads one source's key, each lane its
+// vectors, and the group sums its partial dot products with lps-lane
+// butterflies, so 64 / lps sources are scored per step.  The group's first
+// lane writes s_out[i] (and rho_out[i]).
+template <typename T, int KV>
+__device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__restrict__ q,
+                                    int S, int N, int r, int krow, int koff, float eps, int n,
+                                    int lane, float *s_out, float *rho_out)
 {
-    const bool kvec = VEC > 1 && r % VEC == 0 && krow % VEC == 0 && koff % VEC == 0;
-    for (int i = lane; i < S; i += kWaveSize) {
-        const T *kp = keys + ((size_t)i * N + n) * krow + koff;
+    const int nkv = r / KV;
+    int lps = 1;
+    while (lps < nkv && lps < kWaveSize)
+        lps <<= 1;
+    const int spi = kWaveSize / lps;
+    const int isub = lane / lps, v = lane % lps;
+    for (int i0 = 0; i0 < S; i0 += spi) {
+        const int i = i0 + isub;
         float ss = 0.0f, dot = 0.0f;
-        if (kvec) {
-            for (int j = 0; j < r; j += VEC) {
-                float x[VEC];
-                widen(load_raw<T, VEC>(kp + j), x);
+        if (i < S) {
+            const T *kp = keys + ((size_t)i * N + n) * krow + koff;
+            for (int vv = v; vv < nkv; vv += lps) {
+                float x[KV];
+                widen(load_raw<T, KV>(kp + vv * KV), x);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
+                for (int e = 0; e < KV; ++e) {
                     ss = fmaf(x[e], x[e], ss);
-                    dot = fmaf(q[j + e], x[e], dot);
+                    dot = fmaf(q[vv * KV + e], x[e], dot);
                 }
             }
-        } else {
-            for (int j = 0; j < r; ++j) {
-                const float x = load_elem(kp + j);
-                ss = fmaf(x, x, ss);
-                dot = fmaf(q[j], x, dot);
-            }
         }
-        const float rho = sqrtf(ss / (float)r + eps);
-        s_out[i] = dot / rho;
-        if (rho_out)
-            rho_out[i] = rho;
+        for (int m = 1; m < lps; m <<= 1) {
+            ss += __shfl_xor(ss, m, kWaveSize);
+            dot += __shfl_xor(dot, m, kWaveSize);
+        }
+        if (v == 0 && i < S) {
+            const float rho = sqrtf(ss / (float)r + eps);
+            s_out[i] = dot / rho;
+            if (rho_out)
+                rho_out[i] = rho;
+        }
     }
+}
+
+// The scores with 16-byte key vectors when the key rows allow them, else
+// element by element.  Ends with the wave's LDS writes visible.
+template <typename T, int VEC>
+__device__ inline void lr_scores(const T *__restrict__ keys, const float *__restrict__ q, int S,
+                                 int N, int r, int krow, int koff, float eps, int n, int lane,
+                                 float *s_out, float *rho_out)
+{
+    if (VEC > 1 && r % VEC == 0 && krow % VEC == 0 && koff % VEC == 0)
+        lr_scores_kv<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
+    else
+        lr_scores_kv<T, 1>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
+    wave_lds_sync();
 }
 
 // alpha_i = exp(s_i - max) / sum_l exp(s_l - max) over the S sources.
