@@ -295,6 +295,64 @@ def block_training_pass(torch, lr, dev, O, mode, r, c, reps, warmup):
             "tokens_per_s": N / ((f + b) * 1e-3)}
 
 
+def block_inference_passes(torch, lr, dev, O, mode, r, c, reps, warmup):
+    """Warm, back-to-back 49-site block-source inference: one fused call per
+    site, against the two-phase form of Sec. 3.5 (phase 1 once per block over
+    the completed slots for all of its sites' queries, then one merge call per
+    site).  Both produce the same h."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev) if mode == 0 else None
+    gen = torch.Generator(device=dev).manual_seed(300 + r)
+    KO = (torch.randn((T, N, r), generator=gen, device=dev).to(torch.bfloat16)
+          if mode == 0 else None)
+    Q = torch.randn((T, r), generator=gen, device=dev) / r ** 0.5
+    H = torch.empty((N, d), dtype=O.dtype, device=dev)
+    M = torch.empty((c, N), dtype=torch.float32, device=dev)
+    L = torch.empty((c, N), dtype=torch.float32, device=dev)
+    ACC = torch.empty((c, N, d), dtype=torch.float32, device=dev)
+    kn = (lambda t: KO[t - 1]) if KO is not None else (lambda t: None)
+
+    def per_site():
+        lr.block_route_fwd(B, KB, O[0], kn(1), Q[0], 1, True, mode, out=H)
+        for t in range(2, T + 1):
+            lr.block_route_fwd(B, KB, O[t - 1], kn(t), Q[t - 1], (t - 2) // c + 2,
+                               (t - 2) % c == 0, mode, out=H)
+
+    def two_phase():
+        lr.block_merge_fwd(B, KB, O[0], kn(1), Q[0], None, 0, True, mode, out=H)
+        t = 2
+        while t <= T:
+            j = (t - 2) // c + 1
+            span = list(range(t, min(t + c, T + 1)))
+            nq = len(span)
+            lr.block_inter_fwd(B, KB, Q[span[0] - 1:span[-1]], j, mode,
+                               out=(M[:nq], L[:nq], ACC[:nq]))
+            for k, s_ in enumerate(span):
+                lr.block_merge_fwd(B, KB, O[s_ - 1], kn(s_), Q[s_ - 1], (M[k], L[k], ACC[k]), j,
+                                   k == 0, mode, out=H)
+            t = span[-1] + 1
+
+    st = torch.cuda.current_stream()
+    res = {}
+    for name, fn in (("per_site_ms", per_site), ("two_phase_ms", two_phase)):
+        for _ in range(warmup):
+            fn()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            fn()
+            b.record(st)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        res[name] = float(np.median(ts))
+    res["tokens_per_s_two_phase"] = N / (res["two_phase_ms"] * 1e-3)
+    del B, KB, KO, ACC
+    return res
+
+
 def extras(torch, lr, dev, reps, warmup):
     """The other workloads: the 49-site forward model pass (projected r=16 and
     sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
@@ -375,6 +433,10 @@ def extras(torch, lr, dev, reps, warmup):
     out["block_training_pass_sliced_r64_8blocks"] = block_training_pass(
         torch, lr, dev, V, SLICED, 64, 6, 5, 1)
     out["block_training_pass_projected_r32_8blocks"] = block_training_pass(
+        torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
+    out["block_inference_sliced_r64_8blocks"] = block_inference_passes(
+        torch, lr, dev, V, SLICED, 64, 6, 5, 1)
+    out["block_inference_projected_r32_8blocks"] = block_inference_passes(
         torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush

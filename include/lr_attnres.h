@@ -200,6 +200,41 @@ int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const
                                int64_t n_src, int64_t N, int64_t d, int64_t r, int mode,
                                int dtype, float eps, void *stream);
 
+/*
+ * Two-phase block inference (Sec. 3.5): the site queries do not depend on
+ * the input, and routing over the completed slots merges with routing over
+ * the partial block by an online-softmax update.  The c sites whose newest
+ * output falls in one block all read the same completed slots 0..n_prev-1,
+ * so phase 1 reads those slot rows once for all of their queries:
+ *   B [n_prev][N][d] fp32, KB [n_prev][N][r] fp32 (projected, else NULL):
+ *     the completed slots, as in lr_attnres_block_route_fwd;
+ *   Q [n_queries][r] fp32: the queries of those sites;
+ *   M, L [n_queries][N] fp32, ACC [n_queries][N][d] fp32, overwritten with
+ *     each query's state: M = max score, L = sum exp(s - M),
+ *     ACC = sum exp(s - M) b_i  (so ACC / L is the routing over those slots).
+ * EUNSUPPORTED beyond 1024 completed slots or 64 queries, or d not a
+ * multiple of 4.
+ */
+int lr_attnres_block_inter_fwd(const float *B, const float *KB, const float *Q, float *M,
+                               float *L, float *ACC, int64_t n_prev, int64_t n_queries,
+                               int64_t N, int64_t d, int64_t r, int mode, float eps,
+                               void *stream);
+
+/*
+ * Phase 2 at one site: slot `slot` (the block in progress, = n_prev) gains
+ * o_new exactly as in lr_attnres_block_route_fwd with n_src = slot + 1, and
+ * its score merges into the site's phase-1 state (M, L: [N], ACC: [N][d], the
+ * rows of this site's query; all NULL when slot = 0, where there are no
+ * completed slots):
+ *   m' = max(M, s), h = (e^(M-m') ACC + e^(s-m') b_slot) / (e^(M-m') L + e^(s-m')).
+ * H [N][d] in storage `dtype` equals lr_attnres_block_route_fwd's h up to
+ * rounding.  Errors and limits as for lr_attnres_block_route_fwd.
+ */
+int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const void *k_new,
+                               const float *q, const float *M, const float *L, const float *ACC,
+                               void *H, int64_t slot, int start, int64_t N, int64_t d, int64_t r,
+                               int mode, int dtype, float eps, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

@@ -58,6 +58,8 @@ def _load():
     lib.orc_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d,
                                         ll, ll]
     lib.orc_block_route_bwd.restype = ctypes.c_int
+    lib.orc_route_state.argtypes = [vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
+    lib.orc_route_state.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -201,3 +203,19 @@ def block_route_bwd(O, KO, q, dH, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid block problem")
     return dO, dKO, dq
+
+
+def route_state(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """Online-softmax state (M, Lsum, ACC) of the routing over the sources of
+    V (Sec. 3.5): M = max score, Lsum = sum exp(s - M), ACC = sum exp(s - M) o.
+    Returns fp64 arrays [n1-n0], [n1-n0], [n1-n0, d]."""
+    V, K, q, S, N, d, r = _prep(V, K, q, mode, r)
+    n1 = N if n1 is None else n1
+    M = np.empty((n1 - n0,), dtype=np.float64)
+    L = np.empty((n1 - n0,), dtype=np.float64)
+    A = np.empty((n1 - n0, d), dtype=np.float64)
+    rc = _load().orc_route_state(_ptr(V), _ptr(K), _ptr(q), _ptr(M), _ptr(L), _ptr(A), S, N, d,
+                                 r, mode, _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return M, L, A

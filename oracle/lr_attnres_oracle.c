@@ -444,6 +444,58 @@ done:
     return rc;
 }
 
+/* Online-softmax state of the routing over a set of sources (Sec. 3.5: the
+ * two-phase inference merges inter-block and intra-block results with an
+ * online-softmax update).  For each token in [n0, n1), over the S sources
+ * given (same layout and key modes as orc_route_fwd):
+ *   M[n]      = max_i s_i
+ *   Lsum[n]   = sum_i exp(s_i - M[n])
+ *   ACC[n][:] = sum_i exp(s_i - M[n]) o_i
+ * so that ACC / Lsum is orc_route_fwd over the same sources. */
+int orc_route_state(const void *V, const void *K, const double *q, double *Mx, double *Lsum,
+                    double *ACC, long long S, long long N, long long d, long long r, int mode,
+                    int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || Mx == NULL || Lsum == NULL || ACC == NULL || q == NULL ||
+        V == NULL)
+        return 1;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *w = token_scratch(&p);
+        if (w == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(static)
+        for (long long n = n0; n < n1; ++n) {
+            if (w == NULL)
+                continue;
+            double *kbar = w, *rho = kbar + S * r, *s = rho + S;
+            normalised_keys_and_scores(&p, n, kbar, rho, s);
+            double m = s[0];
+            for (long long i = 1; i < S; ++i)
+                if (s[i] > m)
+                    m = s[i];
+            double l = 0.0;
+            double *acc = ACC + (n - n0) * d;
+            for (long long j = 0; j < d; ++j)
+                acc[j] = 0.0;
+            for (long long i = 0; i < S; ++i) {
+                const double e = exp(s[i] - m);
+                l += e;
+                for (long long j = 0; j < d; ++j)
+                    acc[j] += e * value_elem(&p, i, n, j);
+            }
+            Mx[n - n0] = m;
+            Lsum[n - n0] = l;
+        }
+        free(w);
+    }
+    return failed;
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {

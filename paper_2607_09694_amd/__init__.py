@@ -59,6 +59,12 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                ctypes.c_size_t, i64, i64, i64, i64, i, i, f, vp]
     lib.lr_attnres_block_route_bwd.restype = ctypes.c_int
+    lib.lr_attnres_block_inter_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64,
+                                               i, f, vp]
+    lib.lr_attnres_block_inter_fwd.restype = ctypes.c_int
+    lib.lr_attnres_block_merge_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i, i64,
+                                               i64, i64, i, i, f, vp]
+    lib.lr_attnres_block_merge_fwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -246,3 +252,51 @@ def block_route_bwd(B, KB, dB, dKB, o_new, k_new, q, dH, n_src: int, mode, eps: 
         int(n_src), N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
     _check(lib, rc)
     return dO, dK, dq
+
+
+def block_inter_fwd(B, KB, Q, n_prev: int, mode, eps: float = 1e-6, out=None):
+    """Phase 1 of the two-phase block inference (Sec. 3.5): for each query of
+    Q [nq, r], the online-softmax state over the completed fp32 slots
+    B[:n_prev] (KB[:n_prev] for projected keys).  Returns (M [nq, N],
+    L [nq, N], ACC [nq, N, d]), fp32."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    _, N, d = B.shape
+    nq, r = Q.shape
+    if out is not None:
+        M, L, ACC = out
+    else:
+        M = torch.empty((nq, N), dtype=torch.float32, device=B.device)
+        L = torch.empty((nq, N), dtype=torch.float32, device=B.device)
+        ACC = torch.empty((nq, N, d), dtype=torch.float32, device=B.device)
+    rc = lib.lr_attnres_block_inter_fwd(
+        _dev(B, "B", torch.float32), _dev(KB, "KB", torch.float32), _dev(Q, "Q", torch.float32),
+        _dev(M, "M", torch.float32), _dev(L, "L", torch.float32), _dev(ACC, "ACC", torch.float32),
+        int(n_prev), nq, N, d, r, mode, float(eps), _stream(B))
+    _check(lib, rc)
+    return M, L, ACC
+
+
+def block_merge_fwd(B, KB, o_new, k_new, q, state, slot: int, start: bool, mode,
+                    eps: float = 1e-6, out=None):
+    """Phase 2 at one site: add o_new into slot `slot` (as block_route_fwd with
+    n_src = slot + 1) and merge its score into the site's phase-1 state
+    (M [N], L [N], ACC [N, d]; None when slot = 0).  Returns H [N, d]."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    _, N, d = B.shape
+    r = KB.shape[2] if mode == PROJECTED else q.shape[0]
+    M, L, ACC = state if state is not None else (None, None, None)
+    H = out if out is not None else torch.empty((N, d), dtype=o_new.dtype, device=B.device)
+    rc = lib.lr_attnres_block_merge_fwd(
+        _dev(B, "B", torch.float32), _dev(KB, "KB", torch.float32), _dev(o_new, "o_new"),
+        _dev(k_new, "k_new", o_new.dtype), _dev(q, "q", torch.float32),
+        _dev(M, "M", torch.float32), _dev(L, "L", torch.float32),
+        _dev(ACC, "ACC", torch.float32), _dev(H, "H", o_new.dtype), int(slot), int(bool(start)),
+        N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
+    _check(lib, rc)
+    return H

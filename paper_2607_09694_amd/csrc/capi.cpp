@@ -308,6 +308,94 @@ int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const
     return LRAR_OK;
 }
 
+int lr_attnres_block_inter_fwd(const float *B, const float *KB, const float *Q, float *M,
+                               float *L, float *ACC, int64_t n_prev, int64_t n_queries,
+                               int64_t N, int64_t d, int64_t r, int mode, float eps,
+                               void *stream)
+{
+    g_last_error.clear();
+    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
+        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
+                    "block routing takes projected or sliced keys");
+    if (n_queries < 1)
+        return fail(LRAR_EINVAL, "n_queries must be >= 1");
+    int64_t ve, ke, he;
+    int rc = check_shape(n_prev, N, d, r, mode, LRAR_DTYPE_F32, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(Q, "Q", 4, true)) ||
+        (rc = check_ptr(M, "M", 4, data)) || (rc = check_ptr(L, "L", 4, data)) ||
+        (rc = check_ptr(ACC, "ACC", 16, data)) || (rc = check_ptr(KB, "KB", 16, data && proj)))
+        return rc;
+    if (!proj && KB)
+        return fail(LRAR_EINVAL, "KB must be NULL unless keys are projected");
+    int64_t qn, qnd, qr;
+    if (!mul_ok(n_queries, N, &qn) || !mul_ok(qn, d, &qnd) || !mul_ok(n_queries, r, &qr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("M", M, qn * 4), span("L", L, qn * 4), span("ACC", ACC, qnd * 4)};
+    const Span ins[] = {span("B", B, ve * 4), span("KB", KB, ke * 4), span("Q", Q, qr * 4)};
+    if ((rc = check_aliasing(outs, 3, ins, 3)))
+        return rc;
+    const lrar::BlockInterProblem p{B, KB, Q, M, L, ACC, n_prev, n_queries, N, d, r, mode, eps};
+    std::string why;
+    if ((rc = lrar::launch_block_inter(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const void *k_new,
+                               const float *q, const float *M, const float *L, const float *ACC,
+                               void *H, int64_t slot, int start, int64_t N, int64_t d, int64_t r,
+                               int mode, int dtype, float eps, void *stream)
+{
+    g_last_error.clear();
+    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
+        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
+                    "block routing takes projected or sliced keys");
+    if (start != 0 && start != 1)
+        return fail(LRAR_EINVAL, "start must be 0 or 1");
+    if (slot < 0)
+        return fail(LRAR_EINVAL, "slot must be >= 0");
+    int64_t ve, ke, he;
+    int rc = check_shape(slot + 1, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const bool state = slot > 0;
+    const size_t ek = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(o_new, "o_new", 16, data)) ||
+        (rc = check_ptr(q, "q", 4, true)) || (rc = check_ptr(H, "H", 16, data)) ||
+        (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(k_new, "k_new", ek, data && proj)) ||
+        (rc = check_ptr(M, "M", 4, data && state)) || (rc = check_ptr(L, "L", 4, data && state)) ||
+        (rc = check_ptr(ACC, "ACC", 16, data && state)))
+        return rc;
+    if (!proj && (KB || k_new))
+        return fail(LRAR_EINVAL, "KB and k_new must be NULL unless keys are projected");
+    if (!state && (M || L || ACC))
+        return fail(LRAR_EINVAL, "slot 0 has no completed slots: M, L and ACC must be NULL");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t nr;
+    if (!mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("H", H, he * es), span("B", B, ve * 4), span("KB", KB, ke * 4)};
+    const Span ins[] = {span("o_new", o_new, he * es), span("k_new", k_new, nr * es),
+                        span("q", q, r * 4), span("M", M, N * 4), span("L", L, N * 4),
+                        span("ACC", ACC, he * 4)};
+    if ((rc = check_aliasing(outs, 3, ins, 6)))
+        return rc;
+    lrar::BlockProblem p{B, KB, o_new, k_new, q, H, slot + 1, N, d, r, start, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::launch_block_merge(p, state ? M : nullptr, state ? L : nullptr,
+                                       state ? ACC : nullptr, static_cast<hipStream_t>(stream),
+                                       &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }
 
 int lr_attnres_abi_version(void) { return LR_ATTNRES_ABI_VERSION; }

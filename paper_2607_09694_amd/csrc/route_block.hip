@@ -119,6 +119,234 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
                                             Narrow<TO, VEC>::run(acc[c]));
 }
 
+// ---------------------------------------------------------------------------
+// Two-phase block inference (Sec. 3.5): the site queries do not depend on
+// the input, so the c sites of one block can route over the completed slots
+// together (phase 1); each site then adds the partial block it reads and
+// merges it into that state with an online-softmax update (phase 2).
+// ---------------------------------------------------------------------------
+
+// Unnormalised softmax of one query over S scores in place:
+// s_i <- exp(s_i - m), returns m = max_i s_i and *l = sum_i exp(s_i - m).
+__device__ inline float partial_softmax(float *s, int S, int lane, float *l)
+{
+    float m = -INFINITY;
+    for (int i = lane; i < S; i += kWaveSize)
+        m = fmaxf(m, s[i]);
+    m = wave_max(m);
+    float z = 0.0f;
+    for (int i = lane; i < S; i += kWaveSize) {
+        const float e = expf(s[i] - m);
+        s[i] = e;
+        z += e;
+    }
+    *l = wave_sum(z);
+    return m;
+}
+
+// Phase 1: for nq queries, the online-softmax state over the nprev completed
+// slots: M[q][n] = max score, L[q][n] = sum exp(s - M), ACC[q][n][:] =
+// sum exp(s - M) b_i.  Queries go in groups of QG; each slot row is read once
+// per group.  Grid: x = token groups, y = column blocks of NCH*256 (each
+// recomputes the cheap r-dimensional scores).
+template <int NCH, int QG, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock)
+route_block_inter(const float *__restrict__ B, const float *__restrict__ KB,
+                  const float *__restrict__ Qs, float *__restrict__ M, float *__restrict__ L,
+                  float *__restrict__ ACC, int nprev, int nq, int N, int d, int r, int sliced,
+                  float eps, int s_pad)
+{
+    constexpr int VEC = 4;
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= N)
+        return;  // wave-uniform; no workgroup barrier below
+    float *sc = lds + (size_t)wave * QG * s_pad;  // [QG][s_pad]
+    const int col = blockIdx.y * (NCH * kWaveSize * VEC) + lane * VEC;
+    bool ok[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        ok[c] = col + c * kWaveSize * VEC < d;
+    const size_t plane = (size_t)N * d;
+    const float *keys = sliced ? B : KB;
+    const int krow = sliced ? d : r, koff = sliced ? d - r : 0;
+
+    for (int q0 = 0; q0 < nq; q0 += QG) {
+        const int qg = nq - q0 < QG ? nq - q0 : QG;
+        float mq[QG], lq[QG];
+#pragma unroll
+        for (int u = 0; u < QG; ++u) {
+            mq[u] = -INFINITY;
+            lq[u] = 0.0f;
+            if (u < qg) {
+                lr_scores<float, VEC>(keys, Qs + (size_t)(q0 + u) * r, nprev, N, r, krow, koff,
+                                      eps, n, lane, sc + u * s_pad, nullptr);
+                mq[u] = partial_softmax(sc + u * s_pad, nprev, lane, &lq[u]);
+            }
+        }
+        wave_lds_sync();
+        float acc[QG][NCH][VEC];
+#pragma unroll
+        for (int u = 0; u < QG; ++u)
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[u][c][e] = 0.0f;
+        const float *vbase = B + (size_t)n * d + col;
+        for (int i = 0; i < nprev; ++i) {
+            float x[NCH][VEC];
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULLCOLS || ok[c]) {
+                    widen(load_stream<float, VEC, kNtLoad>(vbase + (size_t)i * plane +
+                                                           c * kWaveSize * VEC), x[c]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        x[c][e] = 0.0f;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < QG; ++u) {
+                if (u < qg) {
+                    const float w = sc[u * s_pad + i];
+#pragma unroll
+                    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            acc[u][c][e] = fmaf(w, x[c][e], acc[u][c][e]);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < QG; ++u) {
+            if (u < qg) {
+                float *arow = ACC + (size_t)(q0 + u) * plane + (size_t)n * d + col;
+#pragma unroll
+                for (int c = 0; c < NCH; ++c)
+                    if (FULLCOLS || ok[c])
+                        store_raw<float, VEC>(arow + c * kWaveSize * VEC,
+                                              Narrow<float, VEC>::run(acc[u][c]));
+                if (blockIdx.y == 0 && lane == 0) {
+                    M[(size_t)(q0 + u) * N + n] = mq[u];
+                    L[(size_t)(q0 + u) * N + n] = lq[u];
+                }
+            }
+        }
+        wave_lds_sync();  // the next group reuses sc
+    }
+}
+
+// Phase 2 at one site: slot j = `slot` (the partial block) gains o_new as in
+// route_fwd_block; its score merges into the site's phase-1 state:
+//   m' = max(M, s_j),  h = (e^{M-m'} ACC + e^{s_j-m'} b_j) / (e^{M-m'} L + e^{s_j-m'}).
+// Without completed slots (has_state = 0) the state is empty and h = b_j.
+template <typename TO, int NCH, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock)
+route_block_merge(float *__restrict__ B, float *__restrict__ KB, const TO *__restrict__ o_new,
+                  const TO *__restrict__ k_new, const float *__restrict__ q,
+                  const float *__restrict__ Ms, const float *__restrict__ Ls,
+                  const float *__restrict__ ACC, TO *__restrict__ H, int slot, int start,
+                  int has_state, int N, int d, int r, int sliced, float eps)
+{
+    constexpr int VEC = 4;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= N)
+        return;  // wave-uniform
+    const int j = slot;
+    const size_t plane = (size_t)N * d;
+    const int col = lane * VEC;
+    bool ok[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        ok[c] = col + c * kWaveSize * VEC < d;
+
+    float nw[NCH][VEC], st[NCH][VEC];
+    float *brow = B + (size_t)j * plane + (size_t)n * d + col;
+    const TO *orow = o_new + (size_t)n * d + col;
+    const float *arow = has_state ? ACC + (size_t)n * d + col : nullptr;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (FULLCOLS || ok[c]) {
+            float x[VEC];
+            widen(load_raw<TO, VEC>(orow + c * kWaveSize * VEC), x);
+            if (has_state)
+                widen(load_stream<float, VEC, kNtLoad>(arow + c * kWaveSize * VEC), st[c]);
+            if (!start) {
+                float b[VEC];
+                widen(load_raw<float, VEC>(brow + c * kWaveSize * VEC), b);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    x[e] += b[e];
+            }
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                nw[c][e] = x[e];
+            store_raw<float, VEC>(brow + c * kWaveSize * VEC, Narrow<float, VEC>::run(nw[c]));
+        }
+        if (!has_state || !(FULLCOLS || ok[c])) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                st[c][e] = 0.0f;
+        }
+        if (!(FULLCOLS || ok[c])) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                nw[c][e] = 0.0f;
+        }
+    }
+
+    // Score of the updated partial slot (as in route_fwd_block).
+    float ss = 0.0f, dot = 0.0f;
+    if (sliced) {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const int cc = col + c * kWaveSize * VEC + e;
+                if ((FULLCOLS || ok[c]) && cc >= d - r) {
+                    ss = fmaf(nw[c][e], nw[c][e], ss);
+                    dot = fmaf(q[cc - (d - r)], nw[c][e], dot);
+                }
+            }
+    } else {
+        float *krow = KB + ((size_t)j * N + n) * r;
+        const TO *knew = k_new + (size_t)n * r;
+        for (int jj = lane; jj < r; jj += kWaveSize) {
+            const float k = (start ? 0.0f : krow[jj]) + load_elem(knew + jj);
+            krow[jj] = k;
+            ss = fmaf(k, k, ss);
+            dot = fmaf(q[jj], k, dot);
+        }
+    }
+    ss = wave_sum(ss);
+    dot = wave_sum(dot);
+    const float sj = dot / sqrtf(ss / (float)r + eps);
+
+    const float m = has_state ? Ms[n] : -INFINITY;
+    const float l = has_state ? Ls[n] : 0.0f;
+    const float mm = fmaxf(m, sj);
+    const float e1 = has_state ? expf(m - mm) : 0.0f;
+    const float e2 = expf(sj - mm);
+    const float inv = 1.0f / (e1 * l + e2);
+    TO *hrow = H + (size_t)n * d + col;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (FULLCOLS || ok[c]) {
+            float y[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                y[e] = fmaf(e1, st[c][e], e2 * nw[c][e]) * inv;
+            store_stream<TO, VEC, kNtStore>(hrow + c * kWaveSize * VEC, Narrow<TO, VEC>::run(y));
+        }
+    }
+}
+
 // Retire the member o_new from slot j and hand it its gradient (see
 // BlockRetire): 4 consecutive row elements per thread, grid-stride.
 template <typename TO>
@@ -209,6 +437,100 @@ hipError_t launch_block_retire(const BlockRetire &br, hipStream_t st)
 {
     return br.dtype == LRAR_DTYPE_BF16 ? launch_retire_t<uint16_t>(br, st)
                                        : launch_retire_t<float>(br, st);
+}
+
+int launch_block_inter(const BlockInterProblem &p, hipStream_t st, std::string *err)
+{
+    if (p.d % 4 != 0) {
+        *err = "block routing needs d to be a multiple of 4";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.nprev > 1024 || p.nq > 64) {
+        *err = "two-phase block routing supports at most 1024 completed slots and 64 queries";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N > (1 << 30)) {
+        *err = "N exceeds 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N == 0)
+        return LRAR_OK;
+    const int need = (int)((p.d + 255) / 256);
+    int nch = 1;
+    while (nch < need && nch < 4)
+        nch <<= 1;
+    const int ysplit = (need + nch - 1) / nch;
+    const bool fullcols = p.d % (256 * nch) == 0;
+    const int s_pad = (int)((p.nprev + 3) / 4 * 4);
+    const int nblocks = (int)((p.N + kWaves - 1) / kWaves);
+    const int sliced = p.mode == LRAR_MODE_SLICED ? 1 : 0;
+    auto go = [&](auto nchc, auto fc) {
+        constexpr int NCH = decltype(nchc)::value;
+        constexpr bool FC = decltype(fc)::value;
+        constexpr int QG = NCH >= 4 ? 4 : 8;
+        const size_t lds = (size_t)kWaves * QG * s_pad * sizeof(float);
+        hipLaunchKernelGGL((route_block_inter<NCH, QG, FC>), dim3(nblocks, ysplit), dim3(kBlock),
+                           lds, st, p.B, p.KB, p.Q, p.M, p.L, p.ACC, (int)p.nprev, (int)p.nq,
+                           (int)p.N, (int)p.d, (int)p.r, sliced, p.eps, s_pad);
+        return hipGetLastError();
+    };
+    typedef std::true_type Y;
+    typedef std::false_type F;
+    hipError_t e;
+    switch (nch) {
+    case 1: e = fullcols ? go(std::integral_constant<int, 1>{}, Y{}) : go(std::integral_constant<int, 1>{}, F{}); break;
+    case 2: e = fullcols ? go(std::integral_constant<int, 2>{}, Y{}) : go(std::integral_constant<int, 2>{}, F{}); break;
+    default: e = fullcols ? go(std::integral_constant<int, 4>{}, Y{}) : go(std::integral_constant<int, 4>{}, F{}); break;
+    }
+    return hip_status(e, "block_inter_fwd launch", err);
+}
+
+template <typename TO>
+hipError_t launch_merge_t(const BlockProblem &p, const float *Ms, const float *Ls,
+                          const float *ACC, int nch, bool fullcols, int nblocks, hipStream_t st)
+{
+    const int sliced = p.mode == LRAR_MODE_SLICED ? 1 : 0;
+    const int has_state = Ms != nullptr;
+    auto go = [&](auto nchc, auto fc) {
+        constexpr int NCH = decltype(nchc)::value;
+        constexpr bool FC = decltype(fc)::value;
+        hipLaunchKernelGGL((route_block_merge<TO, NCH, FC>), dim3(nblocks), dim3(kBlock), 0, st,
+                           p.B, p.KB, static_cast<const TO *>(p.o_new),
+                           static_cast<const TO *>(p.k_new), p.q, Ms, Ls, ACC,
+                           static_cast<TO *>(p.H), (int)(p.nsrc - 1), p.start, has_state,
+                           (int)p.N, (int)p.d, (int)p.r, sliced, p.eps);
+        return hipGetLastError();
+    };
+    typedef std::true_type Y;
+    typedef std::false_type F;
+    switch (nch) {
+    case 1: return fullcols ? go(std::integral_constant<int, 1>{}, Y{}) : go(std::integral_constant<int, 1>{}, F{});
+    case 2: return fullcols ? go(std::integral_constant<int, 2>{}, Y{}) : go(std::integral_constant<int, 2>{}, F{});
+    case 4: return fullcols ? go(std::integral_constant<int, 4>{}, Y{}) : go(std::integral_constant<int, 4>{}, F{});
+    case 8: return fullcols ? go(std::integral_constant<int, 8>{}, Y{}) : go(std::integral_constant<int, 8>{}, F{});
+    }
+    return hipErrorInvalidValue;
+}
+
+int launch_block_merge(const BlockProblem &p, const float *Ms, const float *Ls, const float *ACC,
+                       hipStream_t st, std::string *err)
+{
+    int rc = check_block_supported(p, err);
+    if (rc)
+        return rc;
+    if (p.N == 0)
+        return LRAR_OK;
+    const int need = (int)((p.d + 255) / 256);
+    int nch = 1;
+    while (nch < need)
+        nch <<= 1;
+    const bool fullcols = p.d % (256 * nch) == 0;
+    const int nblocks = (int)((p.N + kWaves - 1) / kWaves);
+    const hipError_t e =
+        p.dtype == LRAR_DTYPE_BF16
+            ? launch_merge_t<uint16_t>(p, Ms, Ls, ACC, nch, fullcols, nblocks, st)
+            : launch_merge_t<float>(p, Ms, Ls, ACC, nch, fullcols, nblocks, st);
+    return hip_status(e, "block_merge_fwd launch", err);
 }
 
 int check_block_supported(const BlockProblem &p, std::string *why)

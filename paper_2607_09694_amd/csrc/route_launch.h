@@ -65,6 +65,23 @@ struct BlockRetire {
 
 hipError_t launch_block_retire(const BlockRetire &br, hipStream_t st);
 
+// Phase 1 of the two-phase block inference (see lr_attnres_block_inter_fwd).
+struct BlockInterProblem {
+    const float *B, *KB;  // [nprev][N][d], [nprev][N][r] (projected) or NULL
+    const float *Q;       // [nq][r]
+    float *M, *L, *ACC;   // [nq][N], [nq][N], [nq][N][d]
+    int64_t nprev, nq, N, d, r;
+    int mode;
+    float eps;
+};
+
+int launch_block_inter(const BlockInterProblem &p, hipStream_t st, std::string *err);
+
+// Phase 2 at one site: p as for launch_block_fwd (p.nsrc - 1 = the partial
+// slot); Ms, Ls, ACC this site's phase-1 state, or all NULL without one.
+int launch_block_merge(const BlockProblem &p, const float *Ms, const float *Ls, const float *ACC,
+                       hipStream_t st, std::string *err);
+
 // One site of the block reverse pass: the routing backward over the fp32
 // slots (p.dtype = F32, p.dh_dtype = the model dtype) accumulating into dB
 // and dKB, dq written, then the retire step above.

@@ -41,7 +41,8 @@ def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
-                            "lr_attnres_block_route_bwd",
+                            "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
+                            "lr_attnres_block_merge_fwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -234,3 +235,40 @@ def test_block_backward_unsupported(lib):
     assert bblk(lib, mode=F, r=64) == EUNSUPPORTED
     assert bblk(lib, d=66) == EUNSUPPORTED
     assert bblk(lib, n_src=513) == EUNSUPPORTED
+
+
+def inter(lib, B=A, KB=None, Q=E, M=G, L=X, ACC=Y, n_prev=3, nq=6, N=8, d=64, r=8, mode=SL,
+          eps=1e-6):
+    return lib.lr_attnres_block_inter_fwd(B, KB, Q, M, L, ACC, n_prev, nq, N, d, r, mode, eps,
+                                          None)
+
+
+def merge(lib, B=A, KB=None, o_new=C, k_new=None, q=E, M=G, L=X, ACC=Y, H=D, slot=2, start=0,
+          N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_block_merge_fwd(B, KB, o_new, k_new, q, M, L, ACC, H, slot, start, N,
+                                          d, r, mode, dtype, eps, None)
+
+
+TWO_PHASE_INVALID = [
+    (inter, "no queries", dict(nq=0), "n_queries"),
+    (inter, "ACC NULL", dict(ACC=None), "ACC is NULL"),
+    (inter, "ACC overlaps B", dict(ACC=A + 16), "overlaps"),
+    (inter, "KB outside projected", dict(KB=Z), "must be NULL"),
+    (merge, "state at slot 0", dict(slot=0), "must be NULL"),
+    (merge, "no state at slot 2", dict(M=None), "M is NULL"),
+    (merge, "negative slot", dict(slot=-1), "slot"),
+    (merge, "H overlaps ACC", dict(H=Y + 64), "overlaps"),
+    (merge, "start not 0/1", dict(start=3), "start"),
+]
+
+
+@pytest.mark.parametrize("fn,name,kw,msg", TWO_PHASE_INVALID, ids=[c[1] for c in TWO_PHASE_INVALID])
+def test_two_phase_rejects(lib, fn, name, kw, msg):
+    assert fn(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_two_phase_unsupported(lib):
+    assert inter(lib, mode=F, r=64) == EUNSUPPORTED
+    assert inter(lib, nq=65) == EUNSUPPORTED
+    assert merge(lib, d=4096) == EUNSUPPORTED

@@ -167,3 +167,60 @@ def test_block_training_pass_matches_oracle(dev, case):
     # every member has left its slot again
     assert float(B.abs().max()) < 1e-3 * max(1.0, float(torch.from_numpy(
         np.abs(to_host(O)).sum(axis=0)).max()))
+
+
+@pytest.mark.parametrize("mode,nprev,nq,d,r", [(PROJECTED, 5, 6, 1024, 32), (SLICED, 9, 12, 2048, 64),
+                                               (SLICED, 1, 3, 100, 4), (PROJECTED, 70, 9, 256, 7)],
+                         ids=["P-5x6-d1024", "S-9x12-d2048", "S-1x3-d100", "P-70x9-d256"])
+def test_inter_state_matches_oracle(dev, mode, nprev, nq, d, r):
+    """Phase 1 (Sec. 3.5): each query's online-softmax state over the
+    completed fp32 slots equals the oracle's state over the same sources."""
+    N = 37
+    p = make_host_problem(mode, nprev, N, d, r, dtype="f32", seed=nprev * 7 + nq, q_scale=2.0)
+    Qh = (np.random.default_rng(nq).standard_normal((nq, r)) * 2.0 / np.sqrt(r)).astype(np.float32)
+    M, L, ACC = lr.block_inter_fwd(to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev),
+                                   nprev, mode)
+    torch.cuda.synchronize()
+    for u in range(nq):
+        Mr, Lr, Ar = oracle.route_state(p.V, p.K, Qh[u], mode, r=r)
+        check_f32(f"M[{u}]", M[u].cpu().numpy(), Mr)
+        check_f32(f"L[{u}]", L[u].cpu().numpy(), Lr)
+        check_f32(f"ACC[{u}]", ACC[u].cpu().numpy(), Ar)
+
+
+def drive_two_phase(dev, O, KO, Q, c, mode):
+    """Two-phase inference over a whole model pass; returns {t: H_t}."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    KB = (torch.zeros((nslots, N, KO.shape[2]), dtype=torch.float32, device=dev)
+          if mode == PROJECTED else None)
+    out = {}
+    out[1] = lr.block_merge_fwd(B, KB, O[0], KO[0] if KO is not None else None, Q[0], None, 0,
+                                True, mode)
+    t = 2
+    while t <= T:
+        j = (t - 2) // c + 1                      # block of o_{t-1}: the partial slot
+        span = list(range(t, min(t + c, T + 1)))  # the sites of this block
+        M, L, ACC = lr.block_inter_fwd(B, KB, Q[span[0] - 1:span[-1]].contiguous(), j, mode)
+        for k, s in enumerate(span):
+            out[s] = lr.block_merge_fwd(B, KB, O[s - 1], KO[s - 1] if KO is not None else None,
+                                        Q[s - 1], (M[k], L[k], ACC[k]), j, k == 0, mode)
+        t = span[-1] + 1
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("case", CASES[:5], ids=lambda c: f"{'P' if c[0] == 0 else 'S'}-{c[1]}-T{c[2]}-N{c[3]}-d{c[4]}-r{c[5]}-c{c[6]}")
+def test_two_phase_model_pass_matches_oracle(dev, case):
+    """Phase 1 once per block, phase 2 at every site: every site's h equals
+    the block-source routing of the oracle."""
+    mode, dtype, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype=dtype, seed=T * 100 + N + 5)
+    Qh = (np.random.default_rng(T + 1).standard_normal((T, r)) / np.sqrt(r)).astype(np.float32)
+    out = drive_two_phase(dev, to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev),
+                          c, mode)
+    check = check_f32 if dtype == "f32" else check_bf16_key_grad
+    for t in range(1, T + 1):
+        ref = oracle.block_route_fwd(p.V, p.K, Qh[t - 1], t, c, mode, r=r)
+        check(f"H at site {t}", to_host(out[t]), ref)
