@@ -159,9 +159,11 @@ int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q
  * of c outputs, so n_src = j + 1 and start = ((t-2) mod c == 0).
  * The reading that a summary's key is the sum of its members' keys is this
  * library's (the paper does not define block keys for projected keys).
+ * Full-rank keys (block AttnRes itself, r = d) run as sliced keys over the
+ * whole row, which Sec. 3.4 states is the same routing.
  * Errors as for lr_attnres_route_fwd, plus EINVAL for start not 0/1 and for
- * an unknown mode; full-rank keys, d not a multiple of 4, d > 2048 and
- * n_src > 1024 are EUNSUPPORTED.  k_new needs only element alignment (it is
+ * an unknown mode; d not a multiple of 4, d > 2048 and n_src > 1024 are
+ * EUNSUPPORTED.  k_new needs only element alignment (it is
  * read element by element), the other tensors 16 bytes.  H must not overlap
  * any other argument; B and KB are rewritten and must not overlap the inputs.
  */
@@ -188,8 +190,9 @@ int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const voi
  *                       the previous site sees its own partial summary;
  *   dq [r] fp32 = this site's query gradient (summed over tokens).
  *   dH [N][d] is in storage `dtype`; workspace as for lr_attnres_route_bwd
- *   with S = n_src and LRAR_DTYPE_F32.
- * Limits: those of lr_attnres_block_route_fwd and of the backward.  Outputs
+ *   with S = n_src, LRAR_DTYPE_F32 and, for full-rank keys, LRAR_MODE_SLICED.
+ * Limits: those of lr_attnres_block_route_fwd and of the backward (so
+ * full-rank keys, which run as sliced keys with r = d, need d <= 256).  Outputs
  * (B, KB, dB, dKB, dO, dK, dq, workspace) must not overlap each other or the
  * inputs (o_new, k_new, q, dH).  Removing o_new from the fp32 slot by
  * subtraction differs from the forward's partial sum by fp32 rounding only.

@@ -240,7 +240,9 @@ def block_route_bwd(B, KB, dB, dKB, o_new, k_new, q, dH, n_src: int, mode, eps: 
         dK = (torch.empty((N, r), dtype=o_new.dtype, device=B.device)
               if mode == PROJECTED else None)
         dq = torch.empty((r,), dtype=torch.float32, device=B.device)
-    need = lib.lr_attnres_route_bwd_workspace_bytes(n_src, N, d, r, mode, _F32)
+    # full-rank block keys run as sliced keys over the whole row
+    wmode = SLICED if mode == FULL else mode
+    need = lib.lr_attnres_route_bwd_workspace_bytes(n_src, N, d, r, wmode, _F32)
     if workspace is None:
         workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=B.device)
     rc = lib.lr_attnres_block_route_bwd(

@@ -92,6 +92,22 @@ int check_aliasing(const Span *outs, int nout, const Span *ins, int nin)
     return LRAR_OK;
 }
 
+// Key mode of the block entry points.  Full-rank block sources are block
+// AttnRes; by Sec. 3.4 sliced keys with r = d are exactly that, so they run
+// as sliced keys over the whole row.
+int block_keys(int *mode, int64_t d, int64_t r)
+{
+    if (*mode == LRAR_MODE_FULL) {
+        if (r != d)
+            return fail(LRAR_EINVAL, "full-rank keys need r == d");
+        *mode = LRAR_MODE_SLICED;
+        return LRAR_OK;
+    }
+    if (*mode != LRAR_MODE_PROJECTED && *mode != LRAR_MODE_SLICED)
+        return fail(LRAR_EINVAL, "block routing takes projected, sliced or full-rank keys");
+    return LRAR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -210,9 +226,8 @@ int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const voi
                                void *stream)
 {
     g_last_error.clear();
-    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
-        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
-                    "block routing takes projected or sliced keys");
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
     if (start != 0 && start != 1)
         return fail(LRAR_EINVAL, "start must be 0 or 1");
     int64_t ve, ke, he;
@@ -255,9 +270,8 @@ int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const
                                int dtype, float eps, void *stream)
 {
     g_last_error.clear();
-    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
-        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
-                    "block routing takes projected or sliced keys");
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
     int64_t ve, ke, he;
     int rc = check_shape(n_src, N, d, r, mode, dtype, eps, &ve, &ke, &he);
     if (rc)
@@ -314,9 +328,8 @@ int lr_attnres_block_inter_fwd(const float *B, const float *KB, const float *Q, 
                                void *stream)
 {
     g_last_error.clear();
-    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
-        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
-                    "block routing takes projected or sliced keys");
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
     if (n_queries < 1)
         return fail(LRAR_EINVAL, "n_queries must be >= 1");
     int64_t ve, ke, he;
@@ -351,9 +364,8 @@ int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const voi
                                int mode, int dtype, float eps, void *stream)
 {
     g_last_error.clear();
-    if (mode != LRAR_MODE_PROJECTED && mode != LRAR_MODE_SLICED)
-        return fail(mode == LRAR_MODE_FULL ? LRAR_EUNSUPPORTED : LRAR_EINVAL,
-                    "block routing takes projected or sliced keys");
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
     if (start != 0 && start != 1)
         return fail(LRAR_EINVAL, "start must be 0 or 1");
     if (slot < 0)

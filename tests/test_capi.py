@@ -177,7 +177,8 @@ BLOCK_INVALID = [
     ("o_new NULL", dict(o_new=None), "o_new is NULL"),
     ("H NULL", dict(H=None), "H is NULL"),
     ("start not 0/1", dict(start=2), "start"),
-    ("unknown mode", dict(mode=9), "projected or sliced"),
+    ("unknown mode", dict(mode=9), "projected, sliced or full-rank"),
+    ("full-rank with r != d", dict(mode=F, r=8), "r == d"),
     ("projected without KB", dict(mode=P, k_new=G), "KB is NULL"),
     ("projected without k_new", dict(mode=P, KB=G), "k_new is NULL"),
     ("KB outside projected", dict(KB=G), "must be NULL"),
@@ -197,7 +198,6 @@ def test_block_forward_rejects(lib, name, kw, msg):
 
 
 def test_block_forward_unsupported(lib):
-    assert blk(lib, mode=F, r=64) == EUNSUPPORTED
     assert blk(lib, d=66) == EUNSUPPORTED
     assert blk(lib, d=4096) == EUNSUPPORTED
     assert blk(lib, n_src=1025) == EUNSUPPORTED
@@ -221,7 +221,7 @@ BLOCK_BWD_INVALID = [
     ("dB overlaps B", dict(dB=A + 64), "overlap"),
     ("dO overlaps dH", dict(dO=D), "overlaps"),
     ("workspace too small", dict(wsb=4), "workspace"),
-    ("unknown mode", dict(mode=9), "projected or sliced"),
+    ("unknown mode", dict(mode=9), "projected, sliced or full-rank"),
 ]
 
 
@@ -232,7 +232,7 @@ def test_block_backward_rejects(lib, name, kw, msg):
 
 
 def test_block_backward_unsupported(lib):
-    assert bblk(lib, mode=F, r=64) == EUNSUPPORTED
+    assert bblk(lib, mode=F, r=1024, d=1024) == EUNSUPPORTED  # runs as sliced r = 1024 > 256
     assert bblk(lib, d=66) == EUNSUPPORTED
     assert bblk(lib, n_src=513) == EUNSUPPORTED
 
@@ -269,6 +269,6 @@ def test_two_phase_rejects(lib, fn, name, kw, msg):
 
 
 def test_two_phase_unsupported(lib):
-    assert inter(lib, mode=F, r=64) == EUNSUPPORTED
+    assert inter(lib, mode=F, r=8) == EINVAL  # full rank needs r == d
     assert inter(lib, nq=65) == EUNSUPPORTED
     assert merge(lib, d=4096) == EUNSUPPORTED

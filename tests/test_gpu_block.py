@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 import paper_2607_09694_amd as lr
-from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
+from paper_2607_09694_amd.inputs import (FULL, PROJECTED, SLICED, bf16_tensor_to_bits,
                                          f32_from_bf16_bits, make_host_problem)
 from parity import check_bf16_key_grad, check_dq, check_f32
 
@@ -224,3 +224,45 @@ def test_two_phase_model_pass_matches_oracle(dev, case):
     for t in range(1, T + 1):
         ref = oracle.block_route_fwd(p.V, p.K, Qh[t - 1], t, c, mode, r=r)
         check(f"H at site {t}", to_host(out[t]), ref)
+
+
+# Block AttnRes with full-rank keys: the sliced routing with r = d (Sec. 3.4).
+FULL_CASES = [(FULL, "bf16", 9, 40, 256, 256, 3), (FULL, "f32", 7, 17, 1024, 1024, 2)]
+
+
+@pytest.mark.parametrize("case", FULL_CASES, ids=lambda c: f"F-{c[1]}-T{c[2]}-N{c[3]}-d{c[4]}-c{c[6]}")
+def test_full_rank_block_forward_and_two_phase(dev, case):
+    mode, dtype, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype=dtype, seed=T + N)
+    Qh = (np.random.default_rng(T).standard_normal((T, d)) / np.sqrt(d)).astype(np.float32)
+    O, Q = to_dev(p.V, dev), torch.from_numpy(Qh).to(dev)
+    out, _, _ = drive_model_pass(dev, O, None, Q, c, mode, list(range(1, T + 1)))
+    out2 = drive_two_phase(dev, O, None, Q, c, mode)
+    check = check_f32 if dtype == "f32" else check_bf16_key_grad
+    for t in range(1, T + 1):
+        ref = oracle.block_route_fwd(p.V, None, Qh[t - 1], t, c, SLICED, r=d)
+        check(f"H at site {t}", to_host(out[t]), ref)
+        check(f"two-phase H at site {t}", to_host(out2[t]), ref)
+
+
+def test_full_rank_block_training_pass(dev):
+    mode, dtype, T, N, d, c = FULL, "bf16", 9, 40, 256, 3
+    p = make_host_problem(mode, T, N, d, d, dtype=dtype, seed=3)
+    Qh = (np.random.default_rng(4).standard_normal((T, d)) / np.sqrt(d)).astype(np.float32)
+    dHh = make_host_problem(PROJECTED, T, N, d, 1, dtype=dtype, seed=5).V
+    O, Q, dHs = to_dev(p.V, dev), torch.from_numpy(Qh).to(dev), to_dev(dHh, dev)
+    _, B, _ = drive_model_pass(dev, O, None, Q, c, mode, [T])
+    dB = torch.zeros_like(B)
+    dO = torch.empty_like(O)
+    dq = torch.empty((T, d), dtype=torch.float32, device=dev)
+    for t in range(T, 0, -1):
+        n_src, _ = site_args(t, c)
+        lr.block_route_bwd(B, None, dB, None, O[t - 1], None, Q[t - 1], dHs[t - 1], n_src, mode,
+                           out=(dO[t - 1], None, dq[t - 1]))
+    torch.cuda.synchronize()
+    ref_dO = np.zeros((T, N, d))
+    for t in range(1, T + 1):
+        gO, _, gq = oracle.block_route_bwd(p.V, None, Qh[t - 1], dHh[t - 1], t, c, SLICED, r=d)
+        ref_dO[:t] += gO
+        check_dq(f"dq at site {t}", dq[t - 1].cpu().numpy(), gq)
+    check_bf16_key_grad("dO", to_host(dO), ref_dO)

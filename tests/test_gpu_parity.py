@@ -164,6 +164,46 @@ def test_accumulating_backward(dev, case):
              tol=1e-5 if dtype == "f32" else 1e-4)
 
 
+def _random_cases(n=40, seed=2607):
+    """Seeded random problems inside the documented limits: every mode and
+    storage, S from 1 to 80, ragged N, vector and scalar row widths."""
+    rng = np.random.default_rng(seed)
+    out = []
+    widths = [4, 8, 12, 36, 64, 100, 128, 200, 256, 520, 1000, 1024, 1536, 2048]
+    for _ in range(n):
+        mode = int(rng.integers(0, 3))
+        dtype = ["f32", "bf16"][int(rng.integers(0, 2))]
+        d = int(rng.choice(widths))
+        if dtype == "f32" and d % 4 and d > 1024:
+            d = 1024
+        S = int(rng.integers(1, 81))
+        N = int(rng.integers(1, 200))
+        if mode == FULL:
+            r = d
+        elif mode == SLICED:
+            r = int(rng.integers(1, min(d, 256) + 1))
+        else:
+            r = int(rng.integers(1, 65))
+        out.append((mode, dtype, S, N, d, r))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=_id)
+def test_random_shapes_forward_and_backward(dev, case):
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S * 7 + N, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    H = lr.route_fwd(V, K, q, mode)
+    dV, dK, dq = lr.route_bwd(V, K, q, dH, mode)
+    torch.cuda.synchronize()
+    check_values("H", dtype, to_host(H), oracle.route_fwd(p.V, p.K, p.q, mode, r=p.r))
+    dV_ref, dK_ref, dq_ref = oracle.route_bwd(p.V, p.K, p.q, p.dH, mode, r=p.r)
+    check_value_grad(mode, dtype, to_host(dV), dV_ref, p.r)
+    if mode == PROJECTED:
+        check_key_grad("dK", dtype, to_host(dK), dK_ref)
+    check_dq("dq", to_host(dq), dq_ref, tol=1e-5 if dtype == "f32" else 1e-4)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [PROJECTED, SLICED])
 def test_column_split_forward(dev, mode, dtype):
