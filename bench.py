@@ -353,6 +353,50 @@ def block_inference_passes(torch, lr, dev, O, mode, r, c, reps, warmup):
     return res
 
 
+def decode_model_pass(torch, lr, dev, reps, warmup, N=128, d=1024, r=16):
+    """A decode-sized model pass (N = 128 tokens, 49 sites, P-LR r = 16):
+    49 launches of a few microseconds each, eager and replayed from one
+    captured HIP graph."""
+    from paper_2607_09694_amd.inputs import PROJECTED, make_device_problem
+
+    g = make_device_problem(PROJECTED, 49, N, d, r, dev, seed=4, n_queries=49)
+    V, K, Q = g["V"], g["K"], g["q"]
+    Hs = torch.empty((49, N, d), dtype=torch.bfloat16, device=dev)
+
+    def pass_():
+        for t in range(1, 50):
+            lr.route_fwd(V[:t], K[:t], Q[t - 1], PROJECTED, out=Hs[t - 1])
+
+    st = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            fn()
+            b.record(st)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    eager = timed(pass_)
+    side = torch.cuda.Stream()
+    side.wait_stream(st)
+    with torch.cuda.stream(side):
+        pass_()
+    st.wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pass_()
+    replay = timed(graph.replay)
+    del g, V, K, Hs, graph
+    return {"tokens": N, "eager_ms": eager, "graph_ms": replay,
+            "graph_tokens_per_s": N / (replay * 1e-3)}
+
+
 def extras(torch, lr, dev, reps, warmup):
     """The other workloads: the 49-site forward model pass (projected r=16 and
     sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
@@ -438,6 +482,7 @@ def extras(torch, lr, dev, reps, warmup):
         torch, lr, dev, V, SLICED, 64, 6, 5, 1)
     out["block_inference_projected_r32_8blocks"] = block_inference_passes(
         torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
+    out["decode_model_pass_projected_r16_N128"] = decode_model_pass(torch, lr, dev, reps, warmup)
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush
     torch.cuda.empty_cache()

@@ -1,0 +1,103 @@
+"""The routing calls inside a captured HIP graph: the library launches only
+kernels on the caller's stream (no memset, no allocation, no host sync), so a
+captured step replays bit for bit.  Each replay is separated by eager work
+and a synchronisation, and every replay is compared with the eager result."""
+import numpy as np
+import pytest
+
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_host_problem
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(x).to(dev)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_captured_step_replays_bitwise(dev, mode):
+    S, N, d, r = 24, 300, 1024, 16
+    p = make_host_problem(mode, S, N, d, r, dtype="bf16", seed=31, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    H = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+    dV = torch.empty_like(V)
+    dK = torch.empty_like(K) if K is not None else None
+    dq = torch.empty((r,), dtype=torch.float32, device=dev)
+    ws = torch.empty((lr.route_bwd_workspace_bytes(S, N, d, r, mode, torch.bfloat16),),
+                     dtype=torch.uint8, device=dev)
+
+    def step():
+        lr.route_fwd(V, K, q, mode, out=H)
+        lr.route_bwd(V, K, q, dH, mode, out=(dV, dK, dq), workspace=ws)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (H, dV, dq) if t is not None]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for k in range(3):
+        for t in (H, dV, dq):
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(ref, (H, dV, dq)):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {k}"
+        # eager work between replays
+        V.mul_(1.0)
+        torch.cuda.synchronize()
+
+
+def test_captured_block_model_pass_replays(dev):
+    """All 13 sites of a block-source forward pass in one graph."""
+    T, N, d, r, c = 13, 70, 256, 16, 3
+    p = make_host_problem(SLICED, T, N, d, r, dtype="bf16", seed=7)
+    O = to_dev(p.V, dev)
+    Q = torch.randn((T, r), generator=torch.Generator(device=dev).manual_seed(1), device=dev)
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    Hs = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+
+    def pass_():
+        lr.block_route_fwd(B, None, O[0], None, Q[0], 1, True, SLICED, out=Hs[0])
+        for t in range(2, T + 1):
+            lr.block_route_fwd(B, None, O[t - 1], None, Q[t - 1], (t - 2) // c + 2,
+                               (t - 2) % c == 0, SLICED, out=Hs[t - 1])
+
+    pass_()
+    torch.cuda.synchronize()
+    ref = Hs.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pass_()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pass_()
+    for k in range(3):
+        Hs.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(ref.view(torch.int16), Hs.view(torch.int16)), f"replay {k}"
