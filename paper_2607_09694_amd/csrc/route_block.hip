@@ -39,19 +39,39 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
     for (int c = 0; c < NCH; ++c)
         ok[c] = col + c * kWaveSize * VEC < d;
 
-    // 1. The updated summary row of slot j (Eqs. block_attnres_sum /
-    //    block_attnres_partial_sum: one more member added), kept in registers.
-    float nw[NCH][VEC];
+    // 1. Issue the loads of the new member and of slot j's row; they stay in
+    //    flight while the earlier slots are scored.
+    typedef typename Raw<TO, VEC>::type oraw_t;
+    typedef typename Raw<float, VEC>::type braw_t;
     float *brow = B + (size_t)j * plane + (size_t)n * d + col;
     const TO *orow = o_new + (size_t)n * d + col;
+    oraw_t oraw[NCH];
+    braw_t braw[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (FULLCOLS || ok[c]) {
+            oraw[c] = load_raw<TO, VEC>(orow + c * kWaveSize * VEC);
+            if (!start)
+                braw[c] = load_raw<float, VEC>(brow + c * kWaveSize * VEC);
+        }
+    }
+
+    // 2. Scores of the earlier slots from their fp32 keys.
+    lr_scores<float, VEC>(sliced ? B : KB, q, j, N, r, sliced ? d : r, sliced ? d - r : 0, eps,
+                          n, lane, s, nullptr);
+
+    // 3. The updated summary row of slot j (Eqs. block_attnres_sum /
+    //    block_attnres_partial_sum: one more member added), kept in registers,
+    //    and its score (Eqs. lr_key_norm, lr_attnres_weight).
+    float nw[NCH][VEC];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (FULLCOLS || ok[c]) {
             float x[VEC];
-            widen(load_raw<TO, VEC>(orow + c * kWaveSize * VEC), x);
+            widen(oraw[c], x);
             if (!start) {
                 float b[VEC];
-                widen(load_raw<float, VEC>(brow + c * kWaveSize * VEC), b);
+                widen(braw[c], b);
 #pragma unroll
                 for (int e = 0; e < VEC; ++e)
                     x[e] += b[e];
@@ -66,8 +86,6 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
                 nw[c][e] = 0.0f;
         }
     }
-
-    // 2. Score of slot j from its updated key (Eqs. lr_key_norm, lr_attnres_weight).
     float ss = 0.0f, dot = 0.0f;
     if (sliced) {
 #pragma unroll
@@ -92,13 +110,8 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
     }
     ss = wave_sum(ss);
     dot = wave_sum(dot);
-    const float sj = dot / sqrtf(ss / (float)r + eps);
-
-    // 3. Scores of the earlier slots, lane per slot, from their fp32 keys.
-    lr_scores<float, VEC>(sliced ? B : KB, q, j, N, r, sliced ? d : r, sliced ? d - r : 0, eps,
-                          n, lane, s, nullptr);
     if (lane == 0)
-        s[j] = sj;
+        s[j] = dot / sqrtf(ss / (float)r + eps);
     wave_lds_sync();
     depth_softmax(s, s, nsrc, lane);
 

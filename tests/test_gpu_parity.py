@@ -204,6 +204,48 @@ def test_random_shapes_forward_and_backward(dev, case):
     check_dq("dq", to_host(dq), dq_ref, tol=1e-5 if dtype == "f32" else 1e-4)
 
 
+# The limits the header promises, each at its largest value.
+LIMIT_CASES = [
+    ("fwd", PROJECTED, "bf16", 1024, 9, 256, 16),     # forward S <= 1024
+    ("fwd", FULL, "f32", 1024, 5, 64, 64),             # full-rank forward S <= 1024
+    ("bwd", PROJECTED, "bf16", 512, 7, 256, 16),      # backward S <= 512
+    ("bwd", SLICED, "f32", 512, 5, 520, 256),         # backward S and r at their limits
+    ("bwd", PROJECTED, "bf16", 3, 9, 4096, 256),      # widest bf16 backward row, r = 256
+    ("bwd", FULL, "f32", 3, 6, 2048, 2048),           # widest fp32 full-rank row
+    ("bwd", SLICED, "bf16", 4, 7, 1020, 9),           # scalar path (d % 8 != 0), d <= 1024
+]
+
+
+@pytest.mark.parametrize("case", LIMIT_CASES,
+                         ids=lambda c: f"{c[0]}-{NAMES[c[1]]}-{c[2]}-S{c[3]}-N{c[4]}-d{c[5]}-r{c[6]}")
+def test_documented_limits(dev, case):
+    kind, mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S + d, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    if kind == "fwd":
+        H = lr.route_fwd(V, K, q, mode)
+        torch.cuda.synchronize()
+        check_values("H", dtype, to_host(H), oracle.route_fwd(p.V, p.K, p.q, mode, r=p.r))
+    else:
+        dV, dK, dq = lr.route_bwd(V, K, q, dH, mode)
+        torch.cuda.synchronize()
+        dV_ref, dK_ref, dq_ref = oracle.route_bwd(p.V, p.K, p.q, p.dH, mode, r=p.r)
+        check_value_grad(mode, dtype, to_host(dV), dV_ref, p.r)
+        if mode == PROJECTED:
+            check_key_grad("dK", dtype, to_host(dK), dK_ref)
+        check_dq("dq", to_host(dq), dq_ref, tol=1e-5 if dtype == "f32" else 1e-4)
+
+
+def test_beyond_the_limits_is_refused(dev):
+    p = make_host_problem(PROJECTED, 513, 2, 64, 8, dtype="bf16", seed=1, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    with pytest.raises(lr.RoutingError, match="EUNSUPPORTED"):
+        lr.route_bwd(V, K, q, dH, PROJECTED)
+    H = lr.route_fwd(V, K, q, PROJECTED)  # the forward takes S = 513
+    torch.cuda.synchronize()
+    check_values("H", "bf16", to_host(H), oracle.route_fwd(p.V, p.K, p.q, PROJECTED))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [PROJECTED, SLICED])
 def test_column_split_forward(dev, mode, dtype):
