@@ -60,6 +60,11 @@ def _load():
     lib.orc_block_route_bwd.restype = ctypes.c_int
     lib.orc_route_state.argtypes = [vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
     lib.orc_route_state.restype = ctypes.c_int
+    lib.orc_effective_sources.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, i, d, ll, ll]
+    lib.orc_effective_sources.restype = ctypes.c_int
+    lib.orc_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, ll, i, i, d, ll,
+                                      ll]
+    lib.orc_route_all_fwd.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -219,3 +224,38 @@ def route_state(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid problem")
     return M, L, A
+
+
+def effective_sources(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """N_eff[n] = exp(-sum_i alpha_i log alpha_i) of the routing over the
+    sources of V (Sec. 4.5, Eq. effective_sources), fp64 [n1-n0]."""
+    V, K, q, S, N, d, r = _prep(V, K, q, mode, r)
+    n1 = N if n1 is None else n1
+    out = np.empty((n1 - n0,), dtype=np.float64)
+    rc = _load().orc_effective_sources(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
+                                       _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return out
+
+
+def route_all_fwd(V, K, Q, mode, first, r=None, eps=1e-6, n0=0, n1=None):
+    """Every site of a pass over one source stack (Sec. 3.1, Eq.
+    full_attnres_source_set): site j = 0..T-1 reads the first first+j
+    sources with query Q[j].  Returns (H [T, n1-n0, d], NEFF [T, n1-n0]),
+    both fp64; NEFF per Eq. effective_sources."""
+    Q = np.ascontiguousarray(np.asarray(Q, dtype=np.float64))
+    if Q.ndim != 2:
+        raise ValueError("oracle: Q must be [T, r]")
+    T = Q.shape[0]
+    V, K, _, S, N, d, r = _prep(V, K, Q[0], mode, r)
+    if first < 1 or first + T - 1 > S:
+        raise ValueError("oracle: sites need 1 <= first and first + T - 1 <= S")
+    n1 = N if n1 is None else n1
+    H = np.empty((T, n1 - n0, d), dtype=np.float64)
+    NEFF = np.empty((T, n1 - n0), dtype=np.float64)
+    rc = _load().orc_route_all_fwd(_ptr(V), _ptr(K), _ptr(Q), _ptr(H), _ptr(NEFF), S, N, d, r,
+                                   first, T, mode, _STORE[V.dtype], float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return H, NEFF

@@ -496,6 +496,104 @@ int orc_route_state(const void *V, const void *K, const double *q, double *Mx, d
     return failed;
 }
 
+/* Eq. effective_sources (Sec. 4.5, "Effective number of sources"): the
+ * perplexity of the routing distribution, exp(-sum_i alpha_i log alpha_i).
+ * Terms with alpha_i = 0 (possible only after underflow) contribute their
+ * limit 0. */
+static double effective_sources(long long S, const double *alpha)
+{
+    double ent = 0.0;
+    for (long long i = 0; i < S; ++i)
+        if (alpha[i] > 0.0)
+            ent -= alpha[i] * log(alpha[i]);
+    return exp(ent);
+}
+
+/* N_eff[n - n0] of the routing over the S sources (same arguments as
+ * orc_route_weights). */
+int orc_effective_sources(const void *V, const void *K, const double *q, double *NEFF,
+                          long long S, long long N, long long d, long long r, int mode,
+                          int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || NEFF == NULL || q == NULL || V == NULL)
+        return 1;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *w = token_scratch(&p);
+        if (w == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(static)
+        for (long long n = n0; n < n1; ++n) {
+            if (w == NULL)
+                continue;
+            double *kbar = w, *rho = kbar + S * r, *s = rho + S, *alpha = s + S;
+            normalised_keys_and_scores(&p, n, kbar, rho, s);
+            depth_softmax(S, s, alpha);
+            NEFF[n - n0] = effective_sources(S, alpha);
+        }
+        free(w);
+    }
+    return failed;
+}
+
+/* Every read site of a model pass from one stack of sources (Sec. 3.1, Eq.
+ * full_attnres_source_set: site t reads the sources 0 .. t-1).  Site j = 0 .. T-1 reads the first first+j sources of the
+ * [S][N][.] stacks with its own query Q[j][0..r) and gives
+ *   H[j][n - n0][:]  = its routed state (Eq. lr_attnres_output),
+ *   NEFF[j][n - n0]  = its effective number of sources (Eq. effective_sources;
+ *                      NEFF may be NULL).
+ * Requires 1 <= first and first + T - 1 <= S.  Each site is the single-site
+ * routing of that prefix: the stacks are source-major, so the first S'
+ * sources of an [S][N][.] stack are themselves an [S'][N][.] stack. */
+int orc_route_all_fwd(const void *V, const void *K, const double *Q, double *H, double *NEFF,
+                      long long S, long long N, long long d, long long r, long long first,
+                      long long T, int mode, int store, double eps, long long n0, long long n1)
+{
+    struct orc_problem p = {V, K, Q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || H == NULL || Q == NULL || V == NULL)
+        return 1;
+    if (first < 1 || T < 1 || first + T - 1 > S)
+        return 1;
+    const long long nt = n1 - n0;
+    int failed = 0;
+#pragma omp parallel
+    {
+        double *w = token_scratch(&p);
+        if (w == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for collapse(2) schedule(static)
+        for (long long j = 0; j < T; ++j) {
+            for (long long n = n0; n < n1; ++n) {
+                if (w == NULL)
+                    continue;
+                struct orc_problem site = p;
+                site.S = first + j;
+                site.q = Q + j * r;
+                double *kbar = w, *rho = kbar + S * r, *s = rho + S, *alpha = s + S;
+                normalised_keys_and_scores(&site, n, kbar, rho, s);
+                depth_softmax(site.S, s, alpha);
+                double *h = H + (j * nt + (n - n0)) * d;
+                for (long long c = 0; c < d; ++c) {
+                    double acc = 0.0;
+                    for (long long i = 0; i < site.S; ++i)
+                        acc += alpha[i] * value_elem(&site, i, n, c);
+                    h[c] = acc;
+                }
+                if (NEFF)
+                    NEFF[j * nt + (n - n0)] = effective_sources(site.S, alpha);
+            }
+        }
+        free(w);
+    }
+    return failed;
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {
