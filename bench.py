@@ -170,6 +170,13 @@ def cpu_baseline(g, q, target_s=10.0, chunk=1024):
                       f"workload, fwd+bwd in fp64, {spent:.1f} s"}
 
 
+def all_sites_bytes(S, T, N, d, r, mode, es=2):
+    """Bytes one all-sites call must move: the stack once (keys too when
+    projected), every site's state written once, N_eff in fp32."""
+    keys = S * N * r * es if mode == 0 else 0
+    return S * N * d * es + keys + T * N * d * es + T * N * 4
+
+
 def block_pass_bytes(t, c, N, d, r, mode, es=2):
     """Algorithmic HBM bytes of the fused block call at site t: the earlier
     fp32 slots (with their fp32 key slots for projected keys) read once, the
@@ -423,14 +430,36 @@ def extras(torch, lr, dev, reps, warmup):
         return {"total_ms": total_ms, "tokens_per_s": N / (total_ms * 1e-3),
                 "algo_GBps": nbytes / (total_ms * 1e-3) / 1e9,
                 "frac_of_peak": nbytes / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                "site49_ms": per_site[-1]}
+                "site49_ms": per_site[-1], "sites_2_to_49_ms": total_ms - per_site[0]}
+
+    def all_sites(mode, r, Vs, Ks, queries, per_site):
+        """Sites 2..49 (prefixes of 2..49 sources) in one call, with N_eff."""
+        T = 48
+        Ha = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+        ne = torch.empty((T, N), dtype=torch.float32, device=dev)
+        Qa = queries[1:].contiguous()
+        ts = time_calls(torch, lambda: lr.route_all_fwd(Vs, Ks, Qa, mode, 2, out=(Ha, ne)),
+                        reps, warmup, flush)
+        med = float(np.median(ts))
+        nbytes = all_sites_bytes(49, T, N, d, r, mode)
+        del Ha, ne
+        return {"median_ms": med, "min_ms": float(np.min(ts)), "max_ms": float(np.max(ts)),
+                "tokens_per_s": N / (med * 1e-3), "algo_GBps": nbytes / (med * 1e-3) / 1e9,
+                "frac_of_peak": nbytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "per_site_calls_ms": per_site["sites_2_to_49_ms"],
+                "speedup_vs_per_site_calls": per_site["sites_2_to_49_ms"] / med}
 
     out["model_pass_projected_r16"] = model_pass(PROJECTED, 16, Q)
+    out["all_sites_pass_projected_r16"] = all_sites(PROJECTED, 16, V, K, Q,
+                                                    out["model_pass_projected_r16"])
     gen = torch.Generator(device=dev)
     for r in (8, 16, 32, 64):
         gen.manual_seed(r)
         qs = torch.randn((49, r), generator=gen, device=dev) / r ** 0.5
         out[f"model_pass_sliced_r{r}"] = model_pass(SLICED, r, qs)
+        if r == 64:
+            out["all_sites_pass_sliced_r64"] = all_sites(SLICED, 64, V, None, qs,
+                                                         out["model_pass_sliced_r64"])
 
     # Head to head at S = 49: full rank vs low rank, forward and backward.
     # The full-rank forward reads every row once (online softmax); its

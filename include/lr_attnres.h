@@ -238,6 +238,35 @@ int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const voi
                                void *H, int64_t slot, int start, int64_t N, int64_t d, int64_t r,
                                int mode, int dtype, float eps, void *stream);
 
+/*
+ * Every read site of a pass over one stack of sources, in one call (Sec. 3.1,
+ * Eq. full_attnres_source_set: site t reads the sources 0 .. t-1; routing of
+ * Sec. 3.2 with projected or sliced keys, Sec. 3.3-3.4), with each site's
+ * effective number of sources (Sec. 4.5, Eq. effective_sources).  For use once
+ * all outputs of the pass exist: recomputing the routed states of a pass,
+ * probing a trained model.  Site j = 0 .. T-1 reads the first `first + j`
+ * sources:
+ *   V    [S][N][d] storage `dtype`: the sources o_0 .. o_{S-1};
+ *   K    [S][N][r] storage `dtype`: their projected keys, or NULL for sliced
+ *        keys (the last r columns of V);
+ *   Q    [T][r] fp32: the sites' queries, row j for site j;
+ *   H    [T][N][d] storage `dtype`, overwritten: row (j, n) is site j's
+ *        routed state of token n (as lr_attnres_route_fwd over the first
+ *        first + j sources with query Q[j]);
+ *   neff [T][N] fp32, overwritten, or NULL: exp(-sum_i alpha_i log alpha_i)
+ *        of site j's weights for token n.
+ * The stack is read once for all sites.  EINVAL: first < 1, T < 1,
+ * first + T - 1 > S, or the conditions of lr_attnres_route_fwd (V, H 16-byte
+ * aligned; K, Q, neff element aligned; no output may overlap an input or the
+ * other output).  EUNSUPPORTED: full-rank keys, S or T above 64, r above 64,
+ * d not a multiple of 8, N above 2^30.  Non-finite source values are not
+ * confined to the sites that read them: a source past a site's prefix enters
+ * that site's product with weight 0, and 0 * inf is NaN.
+ */
+int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void *H, float *neff,
+                             int64_t S, int64_t N, int64_t d, int64_t r, int64_t first,
+                             int64_t T, int mode, int dtype, float eps, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

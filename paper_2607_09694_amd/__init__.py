@@ -65,6 +65,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_block_merge_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i, i64,
                                                i64, i64, i, i, f, vp]
     lib.lr_attnres_block_merge_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
+                                             i, i, f, vp]
+    lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -140,6 +143,36 @@ def route_fwd(V, K, q, mode, eps: float = 1e-6, out=None):
                                   S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return H
+
+
+def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool = True,
+                  out=None):
+    """Every read site of a pass over the stack V in one call (Sec. 3.1):
+    site j = 0..T-1 reads the first first+j sources with query Q[j].
+
+    V [S,N,d] bf16/fp32; K [S,N,r] (projected) or None (sliced); Q [T,r]
+    fp32.  Returns (H [T,N,d] in V's dtype, neff [T,N] fp32 or None), neff
+    per Eq. effective_sources.  ``out`` may supply (H, neff).
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    if Q.dim() != 2:
+        raise ValueError("Q must be [T, r]")
+    S, N, d, r = _shape(V, K, Q[0], mode)
+    T = Q.shape[0]
+    if out is not None:
+        H, neff = out
+    else:
+        H = torch.empty((T, N, d), dtype=V.dtype, device=V.device)
+        neff = torch.empty((T, N), dtype=torch.float32, device=V.device) if with_neff else None
+    rc = lib.lr_attnres_route_all_fwd(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                      _dev(Q, "Q", torch.float32), _dev(H, "H", V.dtype),
+                                      _dev(neff, "neff", torch.float32), S, N, d, r, first, T,
+                                      mode, _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return H, neff
 
 
 def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:

@@ -412,4 +412,40 @@ const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }
 
 int lr_attnres_abi_version(void) { return LR_ATTNRES_ABI_VERSION; }
 
+int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void *H, float *neff,
+                             int64_t S, int64_t N, int64_t d, int64_t r, int64_t first,
+                             int64_t T, int mode, int dtype, float eps, void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    if (first < 1 || T < 1 || first > S || T > S - first + 1)
+        return fail(LRAR_EINVAL, "sites need first >= 1, T >= 1 and first + T - 1 <= S");
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(Q, "Q", 4, true)) ||
+        (rc = check_ptr(H, "H", 16, data)) || (rc = check_ptr(K, "K", es, data && proj)) ||
+        (rc = check_ptr(neff, "neff", 4, false)))
+        return rc;
+    if (!proj && K)
+        return fail(LRAR_EINVAL, "K must be NULL unless keys are projected");
+    int64_t tq, th, tn;
+    if (!mul_ok(T, r, &tq) || !mul_ok(T, he, &th) || !mul_ok(th, es, &th) || !mul_ok(T, N, &tn))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("H", H, th), span("neff", neff, tn * 4)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("Q", Q, tq * 4)};
+    if ((rc = check_aliasing(outs, 2, ins, 3)))
+        return rc;
+    lrar::AllProblem p{V, K, Q, H, neff, S, N, d, r, first, T, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_all_supported(p, &why)))
+        return fail(rc, why);
+    if ((rc = lrar::launch_all_fwd(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 }  // extern "C"

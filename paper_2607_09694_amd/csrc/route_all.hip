@@ -1,0 +1,496 @@
+// Every read site of a pass over one source stack in one launch (Sec. 3.1,
+// Eq. full_attnres_source_set: site t reads the sources 0 .. t-1), with the
+// low-rank keys of Sec. 3.2-3.4 and, optionally, each site's effective
+// number of sources (Sec. 4.5, Eq. effective_sources).
+//
+// Site j = 0 .. T-1 reads the first first+j sources.  Once every o_i of a
+// pass exists (recomputing the routed states in the backward, probing a
+// trained model), the T sites can share one read of the stack: per token the
+// routed states of all sites are one small dense product
+//     Hn[T][d] = An[T][S] * On[S][d],   An[j][i] = alpha_{j,i} (0 past the
+// site's prefix), On = the token's S source rows,
+// which this kernel evaluates on the matrix cores.  The stack is read once
+// instead of once per site (sum_j (first+j) row reads), and H is written
+// once.
+//
+// One workgroup (4 waves) per token:
+//   1. wave w scores the 16 sites of tile w against every source on the
+//      matrix cores (s_{j,i} rho_i = Q_j . k_i, Eqs. lr_key_norm and
+//      lr_attnres_weight; rho_i from the same key loads), takes each site's
+//      softmax over its prefix with lane exchanges, writes alpha to LDS
+//      (zero past the prefix) and N_eff, which follows from the same sums:
+//          -sum alpha_i log alpha_i = log z - sum alpha_i (s_i - m);
+//   2. each wave takes 128-column slabs of the row.  Lane l owns 8
+//      consecutive columns c0 = 128 slab + 8 (l mod 16) and loads them from
+//      the sources of its k-slice with 16-byte reads; an MFMA's column index
+//      l mod 16 then stands for column c0 + p in the p-th of 8 MFMAs, so the
+//      loaded vectors feed the matrix cores without an LDS transpose and
+//      the outputs come back as 8 consecutive columns per lane.
+// bf16 storage: v_mfma_f32_16x16x32_bf16 over 32 sources per step; alpha
+// enters as a pair of bf16 (hi = RNE(alpha), lo = RNE(alpha - hi), relative
+// error <= 2^-17), two MFMAs per tile, fp32 accumulation: the products with
+// the bf16 values are exact, so the state keeps fp32-level accuracy.
+// fp32 storage: v_mfma_f32_16x16x4_f32 over 4 sources per step, alpha and
+// the values as they are.
+// Sources past a site's prefix enter its product with weight exactly 0.
+#include "route_common.h"
+
+namespace lrar {
+
+constexpr int kAllMaxSources = 64;  // sources S, and sites T
+constexpr int kAllMaxRank = 64;
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+constexpr int kAllSlab = 128;                     // columns per wave pass
+constexpr int kAlphaRow = kAllMaxSources + 4;     // floats per LDS alpha row
+
+struct AllArgs {
+    const void *V;       // [S][N][d]
+    const void *keys;    // projected: K [S][N][r]; sliced: V
+    const float *Q;      // [T][r]
+    void *H;             // [T][N][d]
+    float *neff;         // [T][N] or NULL
+    int S, d, r, krow, koff, first, T;
+    int64_t N;
+    float eps;
+    bool kvec;           // bf16 keys readable as 16-byte vectors
+};
+
+// Scores, softmax and N_eff of one token.  Wave w owns the sites of tile w
+// (16 w .. 16 w + 15) and computes their scores against all sources on the
+// matrix cores: s_{j,i} rho_i = Q_j . k_i is a [16 x r] x [r x S] product per
+// tile.  The MFMA's B operand is the keys as stored (lane l: source
+// 16 nt + (l mod 16), key elements kb .. kb + 7 of its k-slice), so rho_i
+// comes from the same loads: each lane squares its elements and the four
+// k-slices of a source are summed with two exchanges.  The result tile has
+// sites on rows 4 (l / 16) + e and sources on column l mod 16, so a site's
+// softmax is a reduction over the 16 lanes of its row group.
+// Writes alpha (fp32 [64][kAlphaRow], zero past each prefix and for absent
+// sites) to LDS and N_eff to global; ends with a workgroup barrier.
+//
+// bf16 storage: v_mfma_f32_16x16x32_bf16, 32 key elements per step; the keys
+// are exact in bf16 and Q enters as hi + lo bf16 (two MFMAs), so the dot
+// product has fp32-level accuracy.  fp32 storage: v_mfma_f32_16x16x4_f32,
+// 4 key elements per step, operands as they are.
+template <typename T, int RP>
+__device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, float *alpha)
+{
+    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+    const int col = lane & 15, ks = lane >> 4;
+    const int qsite = 16 * wave + col;  // site of this lane's A-operand row
+    const T *keys = static_cast<const T *>(a.keys) + n * a.krow + a.koff;
+    const size_t kplane = (size_t)a.N * a.krow;
+
+    f32x4_t D[4];
+    float ss[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+        D[nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        ss[nt] = 0.0f;
+    }
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        constexpr int KK = RP / 32;
+        bf16x8_t Ahi[KK], Alo[KK];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            float qv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int c = 32 * kk + 8 * ks + e;
+                qv[e] = (qsite < a.T && c < a.r) ? a.Q[(size_t)qsite * a.r + c] : 0.0f;
+            }
+            u32x4_t hi, lo;
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                const unsigned hw = pack_bf16x2(qv[2 * h], qv[2 * h + 1]);
+                hi[h] = hw;
+                lo[h] = pack_bf16x2(qv[2 * h] - bf16_lo(hw), qv[2 * h + 1] - bf16_hi(hw));
+            }
+            Ahi[kk] = __builtin_bit_cast(bf16x8_t, hi);
+            Alo[kk] = __builtin_bit_cast(bf16x8_t, lo);
+        }
+        const bool kvec = a.kvec;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int i = 16 * nt + col;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int c = 32 * kk + 8 * ks;
+                u32x4_t kr = {0u, 0u, 0u, 0u};
+                if (i < a.S && c < a.r) {
+                    const uint16_t *kp = reinterpret_cast<const uint16_t *>(keys) + i * kplane + c;
+                    if (kvec) {
+                        kr = load_raw<uint16_t, 8>(kp);
+                    } else {
+#pragma unroll
+                        for (int h = 0; h < 4; ++h) {
+                            const unsigned x0 = c + 2 * h < a.r ? kp[2 * h] : 0u;
+                            const unsigned x1 = c + 2 * h + 1 < a.r ? kp[2 * h + 1] : 0u;
+                            kr[h] = x0 | (x1 << 16);
+                        }
+                    }
+                }
+                float x[8];
+                widen(kr, x);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    ss[nt] = fmaf(x[e], x[e], ss[nt]);
+                const bf16x8_t B = __builtin_bit_cast(bf16x8_t, kr);
+                D[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ahi[kk], B, D[nt], 0, 0, 0);
+                D[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Alo[kk], B, D[nt], 0, 0, 0);
+            }
+        }
+    } else {
+        constexpr int KK = RP / 4;
+        float A[KK];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const int c = 4 * kk + ks;
+            A[kk] = (qsite < a.T && c < a.r) ? a.Q[(size_t)qsite * a.r + c] : 0.0f;
+        }
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int i = 16 * nt + col;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int c = 4 * kk + ks;
+                const float x = (i < a.S && c < a.r)
+                                    ? reinterpret_cast<const float *>(keys)[i * kplane + c]
+                                    : 0.0f;
+                ss[nt] = fmaf(x, x, ss[nt]);
+                D[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[kk], x, D[nt], 0, 0, 0);
+            }
+        }
+    }
+
+    // Scores: lane l holds sites 16 w + 4 (l / 16) + e against sources
+    // 16 nt + (l mod 16).
+    float s[4][4];
+    float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+        float t = ss[nt];
+        t += __shfl_xor(t, 16, kWaveSize);
+        t += __shfl_xor(t, 32, kWaveSize);
+        const float rho = sqrtf(t / (float)a.r + a.eps);
+        const int i = 16 * nt + col;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int site = 16 * wave + 4 * ks + e;
+            const bool v = site < a.T && i < a.first + site;
+            s[nt][e] = v ? D[nt][e] / rho : -INFINITY;
+            m[e] = fmaxf(m[e], s[nt][e]);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        for (int o = 1; o < 16; o <<= 1)
+            m[e] = fmaxf(m[e], __shfl_xor(m[e], o, kWaveSize));
+    float ex[4][4], z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            ex[nt][e] = s[nt][e] > -INFINITY ? expf(s[nt][e] - m[e]) : 0.0f;
+            z[e] += ex[nt][e];
+        }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        for (int o = 1; o < 16; o <<= 1)
+            z[e] += __shfl_xor(z[e], o, kWaveSize);
+    float sa[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int site = 16 * wave + 4 * ks + e;
+        const float inv = z[e] > 0.0f ? 1.0f / z[e] : 0.0f;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const float al = ex[nt][e] * inv;
+            if (ex[nt][e] > 0.0f)
+                sa[e] = fmaf(al, s[nt][e] - m[e], sa[e]);
+            alpha[site * kAlphaRow + 16 * nt + col] = al;
+        }
+    }
+    if (a.neff) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            for (int o = 1; o < 16; o <<= 1)
+                sa[e] += __shfl_xor(sa[e], o, kWaveSize);
+            const int site = 16 * wave + 4 * ks + e;
+            if (col == 0 && site < a.T)
+                a.neff[(size_t)site * a.N + n] = expf(logf(z[e]) - sa[e]);
+        }
+    }
+    __syncthreads();
+}
+
+// Largest prefix read by a site of tile mt (sites 16 mt .. 16 mt + 15).
+__device__ __forceinline__ int tile_prefix(const AllArgs &a, int mt)
+{
+    return a.first + min(16 * mt + 15, a.T - 1);
+}
+
+__device__ __forceinline__ unsigned lo_pair(unsigned x, unsigned y)
+{
+    return (x & 0xffffu) | (y << 16);
+}
+__device__ __forceinline__ unsigned hi_pair(unsigned x, unsigned y)
+{
+    return (x >> 16) | (y & 0xffff0000u);
+}
+
+// Issue the loads of the lane's 8 sources of group kg (sources 32 kg + 8 ks
+// + e) at columns c0 .. c0 + 7.  Lanes past the columns or the sources load
+// nothing; their entries are masked to zero when the B operands are built.
+__device__ __forceinline__ void load_group(const uint16_t *__restrict__ vrow, size_t plane,
+                                           int S, int kg, int ks, bool ok, u32x4_t (&raw)[8])
+{
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int i = 32 * kg + 8 * ks + e;
+        if (ok && i < S)
+            raw[e] = load_stream<uint16_t, 8, kNtLoad>(vrow + i * plane);
+    }
+}
+
+// bf16 storage: 32 sources per MFMA step, at most 2 steps (S <= 64).  One
+// source group is in flight while the previous one is multiplied; the first
+// is issued before the weights are computed.  Every site tile multiplies
+// every group: the weights past a site's prefix are zero, and skipping the
+// few empty tile-group pairs would cost more in register traffic than the
+// matrix cores save.
+template <int MT, int RP>
+__global__ __launch_bounds__(kBlock, MT <= 3 ? 2 : 1) void route_all_fwd_bf16(AllArgs a)
+{
+    __shared__ __align__(16) float alpha[kAllMaxSources * kAlphaRow];
+    const int64_t n = blockIdx.x;
+    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+    const int col = lane & 15, ks = lane >> 4;
+    const uint16_t *V = static_cast<const uint16_t *>(a.V) + n * a.d + 8 * col;
+    uint16_t *H = static_cast<uint16_t *>(a.H) + n * a.d + 8 * col;
+    const size_t plane = (size_t)a.N * a.d;
+    const int ngroups = (a.S + 31) / 32;
+    const int nslab = (a.d + kAllSlab - 1) / kAllSlab;
+
+    u32x4_t raw[8];
+    if (wave < nslab)
+        load_group(V + wave * kAllSlab, plane, a.S, 0, ks, wave * kAllSlab + 8 * col < a.d, raw);
+    all_site_weights<uint16_t, RP>(a, n, alpha);
+
+    for (int slab = wave; slab < nslab; slab += kWaves) {
+        const int c0 = slab * kAllSlab + 8 * col;
+        const bool ok = c0 < a.d;
+        f32x4_t acc[MT][8];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int p = 0; p < 8; ++p)
+                acc[mt][p] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int kg = 0; kg < ngroups; ++kg) {
+            // B operands: column c0 + p of the lane's 8 sources, as bf16 pairs.
+            unsigned w[8][4];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const bool v = ok && 32 * kg + 8 * ks + e < a.S;
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    w[e][h] = v ? raw[e][h] : 0u;
+            }
+            u32x4_t b[8];
+#pragma unroll
+            for (int p = 0; p < 8; ++p)
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    b[p][h] = (p & 1) ? hi_pair(w[2 * h][p / 2], w[2 * h + 1][p / 2])
+                                      : lo_pair(w[2 * h][p / 2], w[2 * h + 1][p / 2]);
+            // Prefetch: the next group of this slab, else group 0 of the next.
+            int ns = slab, nk = kg + 1;
+            if (nk == ngroups) {
+                nk = 0;
+                ns += kWaves;
+            }
+            if (ns < nslab)
+                load_group(V + ns * kAllSlab, plane, a.S, nk, ks, ns * kAllSlab + 8 * col < a.d,
+                           raw);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const float *ar = alpha + (16 * mt + col) * kAlphaRow + 32 * kg + 8 * ks;
+                const f32x4_t a0 = *reinterpret_cast<const f32x4_t *>(ar);
+                const f32x4_t a1 = *reinterpret_cast<const f32x4_t *>(ar + 4);
+                const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                u32x4_t ahi, alo;
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    const unsigned hw = pack_bf16x2(av[2 * h], av[2 * h + 1]);
+                    ahi[h] = hw;
+                    alo[h] = pack_bf16x2(av[2 * h] - bf16_lo(hw), av[2 * h + 1] - bf16_hi(hw));
+                }
+                const bf16x8_t A_hi = __builtin_bit_cast(bf16x8_t, ahi);
+                const bf16x8_t A_lo = __builtin_bit_cast(bf16x8_t, alo);
+#pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    const bf16x8_t B = __builtin_bit_cast(bf16x8_t, b[p]);
+                    acc[mt][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A_hi, B, acc[mt][p], 0, 0, 0);
+                    acc[mt][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A_lo, B, acc[mt][p], 0, 0, 0);
+                }
+            }
+        }
+        // Lane l holds sites 16 mt + 4 (l / 16) + e, columns c0 .. c0 + 7.
+        if (ok) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int site = 16 * mt + 4 * ks + e;
+                    if (site < a.T) {
+                        u32x4_t o;
+#pragma unroll
+                        for (int h = 0; h < 4; ++h)
+                            o[h] = pack_bf16x2(acc[mt][2 * h][e], acc[mt][2 * h + 1][e]);
+                        store_stream<uint16_t, 8, kNtStore>(H + site * plane + slab * kAllSlab, o);
+                    }
+                }
+        }
+    }
+}
+
+// fp32 storage: 4 sources per MFMA step.
+template <int MT, int RP>
+__global__ __launch_bounds__(kBlock) void route_all_fwd_f32(AllArgs a)
+{
+    __shared__ __align__(16) float alpha[kAllMaxSources * kAlphaRow];
+    const int64_t n = blockIdx.x;
+    all_site_weights<float, RP>(a, n, alpha);
+
+    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+    const int col = lane & 15, ks = lane >> 4;
+    const float *V = static_cast<const float *>(a.V);
+    float *H = static_cast<float *>(a.H);
+    const size_t plane = (size_t)a.N * a.d;
+    const int nslab = (a.d + kAllSlab - 1) / kAllSlab;
+
+    for (int slab = wave; slab < nslab; slab += kWaves) {
+        const int c0 = slab * kAllSlab + 8 * col;
+        const bool ok = c0 < a.d;
+        f32x4_t acc[MT][8];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int p = 0; p < 8; ++p)
+                acc[mt][p] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int i0 = 0; i0 < a.S; i0 += 4) {
+            const int i = i0 + ks;
+            f32x4_t v0 = {0.0f, 0.0f, 0.0f, 0.0f}, v1 = v0;
+            if (ok && i < a.S) {
+                const float *src = V + i * plane + n * a.d + c0;
+                v0 = load_stream<float, 4, kNtLoad>(src);
+                v1 = load_stream<float, 4, kNtLoad>(src + 4);
+            }
+            const float bv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                if (i0 >= tile_prefix(a, mt))
+                    continue;
+                const float A = alpha[(16 * mt + col) * kAlphaRow + i];
+#pragma unroll
+                for (int p = 0; p < 8; ++p)
+                    acc[mt][p] = __builtin_amdgcn_mfma_f32_16x16x4f32(A, bv[p], acc[mt][p], 0, 0, 0);
+            }
+        }
+        if (ok) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int site = 16 * mt + 4 * ks + e;
+                    if (site < a.T) {
+                        float *dst = H + site * plane + n * a.d + c0;
+                        store_stream<float, 4, kNtStore>(
+                            dst, f32x4_t{acc[mt][0][e], acc[mt][1][e], acc[mt][2][e], acc[mt][3][e]});
+                        store_stream<float, 4, kNtStore>(
+                            dst + 4, f32x4_t{acc[mt][4][e], acc[mt][5][e], acc[mt][6][e], acc[mt][7][e]});
+                    }
+                }
+        }
+    }
+}
+
+template <int MT, int RP>
+hipError_t launch_all_mt_rp(const AllArgs &a, int dtype, hipStream_t st)
+{
+    if (dtype == LRAR_DTYPE_BF16)
+        hipLaunchKernelGGL((route_all_fwd_bf16<MT, RP>), dim3((unsigned)a.N), dim3(kBlock), 0, st, a);
+    else
+        hipLaunchKernelGGL((route_all_fwd_f32<MT, RP>), dim3((unsigned)a.N), dim3(kBlock), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int MT>
+hipError_t launch_all_mt(const AllArgs &a, int dtype, hipStream_t st)
+{
+    if (a.r <= 32)
+        return launch_all_mt_rp<MT, 32>(a, dtype, st);
+    return launch_all_mt_rp<MT, 64>(a, dtype, st);
+}
+
+}  // namespace
+
+int check_all_supported(const AllProblem &p, std::string *why)
+{
+    if (p.mode != LRAR_MODE_PROJECTED && p.mode != LRAR_MODE_SLICED) {
+        *why = "all-sites routing takes projected or sliced keys (full-rank keys need the whole "
+               "row per score)";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.S > kAllMaxSources || p.T > kAllMaxSources || p.r > kAllMaxRank) {
+        *why = "all-sites routing supports S <= " + std::to_string(kAllMaxSources) +
+               " sources, T <= " + std::to_string(kAllMaxSources) + " sites and r <= " +
+               std::to_string(kAllMaxRank);
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.d % 8 != 0) {
+        *why = "all-sites routing needs d % 8 == 0";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N > ((int64_t)1 << 30)) {
+        *why = "N above 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    return LRAR_OK;
+}
+
+int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err)
+{
+    if (p.N == 0)
+        return LRAR_OK;
+    AllArgs a;
+    a.V = p.V;
+    a.keys = p.mode == LRAR_MODE_PROJECTED ? p.K : p.V;
+    a.Q = p.Q;
+    a.H = p.H;
+    a.neff = p.neff;
+    a.S = (int)p.S;
+    a.d = (int)p.d;
+    a.r = (int)p.r;
+    a.krow = p.mode == LRAR_MODE_PROJECTED ? (int)p.r : (int)p.d;
+    a.koff = p.mode == LRAR_MODE_PROJECTED ? 0 : (int)(p.d - p.r);
+    a.first = (int)p.first;
+    a.T = (int)p.T;
+    a.N = p.N;
+    a.eps = p.eps;
+    a.kvec = a.r % 8 == 0 && a.koff % 8 == 0 && a.krow % 8 == 0 &&
+             reinterpret_cast<uintptr_t>(a.keys) % 16 == 0;
+    hipError_t e;
+    switch ((a.T + 15) / 16) {
+    case 1: e = launch_all_mt<1>(a, p.dtype, st); break;
+    case 2: e = launch_all_mt<2>(a, p.dtype, st); break;
+    case 3: e = launch_all_mt<3>(a, p.dtype, st); break;
+    default: e = launch_all_mt<4>(a, p.dtype, st); break;
+    }
+    return hip_status(e, "route_all_fwd", err);
+}
+
+}  // namespace lrar

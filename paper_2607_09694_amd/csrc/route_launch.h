@@ -88,4 +88,20 @@ int launch_block_merge(const BlockProblem &p, const float *Ms, const float *Ls, 
 int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,
                      void *dKB, float *dq, void *ws, hipStream_t st, std::string *err);
 
+// Every read site of a pass over one source stack (see
+// lr_attnres_route_all_fwd).
+struct AllProblem {
+    const void *V;    // [S][N][d]
+    const void *K;    // [S][N][r] (projected keys) or NULL
+    const float *Q;   // [T][r]
+    void *H;          // [T][N][d]
+    float *neff;      // [T][N] or NULL
+    int64_t S, N, d, r, first, T;
+    int mode, dtype;
+    float eps;
+};
+
+int check_all_supported(const AllProblem &p, std::string *why);
+int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err);
+
 }  // namespace lrar

@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
-                            "lr_attnres_block_merge_fwd",
+                            "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -272,3 +272,42 @@ def test_two_phase_unsupported(lib):
     assert inter(lib, mode=F, r=8) == EINVAL  # full rank needs r == d
     assert inter(lib, nq=65) == EUNSUPPORTED
     assert merge(lib, d=4096) == EUNSUPPORTED
+
+
+def allf(lib, V=A, K=None, Q=B, H=C, neff=D, S=6, N=8, d=64, r=8, first=2, T=5, mode=SL,
+         dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_all_fwd(V, K, Q, H, neff, S, N, d, r, first, T, mode, dtype, eps,
+                                        None)
+
+
+ALL_INVALID = [
+    ("first 0", dict(first=0), "first >= 1"),
+    ("no sites", dict(T=0), "T >= 1"),
+    ("sites past the stack", dict(first=2, T=6), "first + T - 1 <= S"),
+    ("V NULL", dict(V=None), "V is NULL"),
+    ("Q NULL", dict(Q=None), "Q is NULL"),
+    ("H NULL", dict(H=None), "H is NULL"),
+    ("K NULL when projected", dict(mode=P), "K is NULL"),
+    ("K outside projected", dict(K=E), "must be NULL"),
+    ("H misaligned", dict(H=C + 8), "16-byte aligned"),
+    ("neff misaligned", dict(neff=D + 2), "4-byte aligned"),
+    ("H overlaps V", dict(H=A + 64), "overlaps"),
+    ("neff overlaps H", dict(neff=C + 128), "overlap"),
+    ("sliced r > d", dict(r=65), "r <= d"),
+    ("negative eps", dict(eps=-1.0), "eps"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", ALL_INVALID, ids=[c[0] for c in ALL_INVALID])
+def test_all_sites_rejects(lib, name, kw, msg):
+    assert allf(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_all_sites_unsupported(lib):
+    assert allf(lib, mode=F, r=64) == EUNSUPPORTED
+    assert "projected or sliced" in err(lib)
+    assert allf(lib, S=65, T=3) == EUNSUPPORTED
+    assert allf(lib, S=70, first=1, T=65) == EUNSUPPORTED
+    assert allf(lib, mode=P, K=E, r=65, d=128) == EUNSUPPORTED
+    assert allf(lib, d=68) == EUNSUPPORTED

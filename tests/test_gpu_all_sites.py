@@ -1,0 +1,208 @@
+"""GPU parity of the all-sites forward (every read site of a pass over one
+source stack in one call) and of its effective number of sources, through
+the C ABI, against the fp64 oracle.
+
+Small cases cover both storages, both low-rank key modes, one and several
+16-site tiles, one and two 32-source groups, ragged column slabs, key
+lengths that need padding and the limits (64 sources, 64 sites, r = 64).
+The full-size cases run the paper's model pass (49 sources, sites reading
+2..49 of them, d = 1024, N = 16384) and compare sampled tokens.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
+                                         f32_from_bf16_bits, make_device_problem,
+                                         make_host_problem)
+from parity import check_bf16_value, check_f32
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+
+def to_host(t):
+    if t.dtype == torch.bfloat16:
+        return f32_from_bf16_bits(bf16_tensor_to_bits(t))
+    return t.detach().cpu().numpy()
+
+
+def host_bits(t):
+    if t.dtype == torch.bfloat16:
+        return bf16_tensor_to_bits(t)
+    return t.detach().contiguous().cpu().numpy()
+
+
+def check_h(name, dtype, got, ref):
+    (check_f32 if dtype == "f32" else check_bf16_value)(name, got, ref)
+
+
+def check_neff(name, got, ref):
+    check_f32(name, got, ref, tol=1e-5)
+
+
+def _queries(T, r, seed, scale=1.0):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((T, r)) * scale / np.sqrt(r)).astype(np.float32)
+
+
+# (mode, storage, S, T, first, N, d, r)
+CASES = [
+    (PROJECTED, "bf16", 49, 48, 2, 37, 256, 16),   # the paper's sites, 3 tiles, 2 groups
+    (SLICED, "bf16", 49, 48, 2, 21, 1024, 64),     # full width, r = 64
+    (PROJECTED, "f32", 8, 8, 1, 33, 64, 8),        # half a slab
+    (SLICED, "f32", 20, 17, 4, 19, 200, 12),       # ragged slab, r padded to 32
+    (PROJECTED, "bf16", 64, 64, 1, 9, 136, 64),    # every limit, 4 tiles
+    (SLICED, "bf16", 33, 30, 4, 50, 520, 32),      # group boundary, ragged slab
+    (PROJECTED, "bf16", 17, 5, 13, 12, 384, 20),   # few sites late in the stack
+    (SLICED, "f32", 64, 49, 16, 7, 128, 64),       # fp32 at the limits
+    (PROJECTED, "bf16", 1, 1, 1, 5, 8, 1),         # one source, one site
+]
+
+
+def _ids(c):
+    return "{}-{}-S{}-T{}-f{}-N{}-d{}-r{}".format("P" if c[0] == PROJECTED else "S", *c[1:])
+
+
+@pytest.mark.parametrize("case", CASES, ids=_ids)
+def test_all_sites_match_oracle(dev, case):
+    mode, dtype, S, T, first, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=11)
+    Q = _queries(T, r, seed=12, scale=2.0)
+    V, K = to_dev(p.V, dev), to_dev(p.K, dev)
+    H, ne = lr.route_all_fwd(V, K, to_dev(Q, dev), mode, first)
+    torch.cuda.synchronize()
+    Hr, NEr = oracle.route_all_fwd(p.V, p.K, Q.astype(np.float64), mode, first, r=r)
+    check_h("H", dtype, to_host(H), Hr)
+    check_neff("neff", to_host(ne), NEr)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_all_sites_single_source_site_is_a_copy(dev, dtype):
+    """first = 1: site 0 reads o_0 alone; its weight is exactly 1, so its
+    state is o_0 bit for bit, and N_eff is 1."""
+    p = make_host_problem(SLICED, 40, 23, 264, 16, dtype=dtype, seed=3)
+    Q = _queries(40, 16, seed=4, scale=3.0)
+    V = to_dev(p.V, dev)
+    H, ne = lr.route_all_fwd(V, None, to_dev(Q, dev), SLICED, 1)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_bits(H[0]), host_bits(V[0]))
+    assert np.array_equal(to_host(ne[0]), np.ones(23, dtype=np.float32))
+
+
+def test_all_sites_zero_queries_average_prefixes(dev):
+    """Q = 0: site j is the mean of its first+j rows and N_eff = first + j."""
+    S, T, first, N, d = 49, 48, 2, 13, 512
+    p = make_host_problem(PROJECTED, S, N, d, 16, dtype="bf16", seed=5)
+    V, K = to_dev(p.V, dev), to_dev(p.K, dev)
+    H, ne = lr.route_all_fwd(V, K, torch.zeros((T, 16), device=dev), PROJECTED, first)
+    torch.cuda.synchronize()
+    Vh = f32_from_bf16_bits(p.V).astype(np.float64)
+    ref = np.stack([Vh[:first + j].mean(axis=0) for j in range(T)])
+    check_bf16_value("H", to_host(H), ref)
+    want = np.repeat(np.arange(first, first + T, dtype=np.float64)[:, None], N, axis=1)
+    check_neff("neff", to_host(ne), want)
+
+
+def test_all_sites_unaligned_projected_keys(dev):
+    """K only element-aligned (r % 8 == 0 but the tensor starts 2 bytes past a
+    16-byte boundary): the scores read the keys element by element."""
+    S, T, first, N, d, r = 12, 11, 2, 17, 256, 16
+    p = make_host_problem(PROJECTED, S, N, d, r, dtype="bf16", seed=13)
+    Q = _queries(T, r, seed=14, scale=2.0)
+    flat = torch.empty((S * N * r + 1,), dtype=torch.bfloat16, device=dev)
+    K = flat[1:].view(S, N, r)
+    K.copy_(to_dev(p.K, dev))
+    assert K.data_ptr() % 16 != 0
+    H, ne = lr.route_all_fwd(to_dev(p.V, dev), K, to_dev(Q, dev), PROJECTED, first)
+    torch.cuda.synchronize()
+    Hr, NEr = oracle.route_all_fwd(p.V, p.K, Q.astype(np.float64), PROJECTED, first)
+    check_bf16_value("H", to_host(H), Hr)
+    check_neff("neff", to_host(ne), NEr)
+
+
+def test_all_sites_without_neff_and_empty(dev):
+    p = make_host_problem(SLICED, 10, 6, 64, 8, dtype="bf16", seed=6)
+    Q = _queries(9, 8, seed=7)
+    V = to_dev(p.V, dev)
+    H, ne = lr.route_all_fwd(V, None, to_dev(Q, dev), SLICED, 2, with_neff=False)
+    torch.cuda.synchronize()
+    assert ne is None
+    Hr, _ = oracle.route_all_fwd(p.V, None, Q.astype(np.float64), SLICED, 2, r=8)
+    check_bf16_value("H", to_host(H), Hr)
+    # N = 0: nothing to do, no launch.
+    E = torch.empty((10, 0, 64), dtype=torch.bfloat16, device=dev)
+    H0, ne0 = lr.route_all_fwd(E, None, to_dev(Q, dev), SLICED, 2)
+    assert H0.shape == (9, 0, 64) and ne0.shape == (9, 0)
+
+
+def test_all_sites_agree_with_per_site_routing(dev):
+    """Each site of the all-sites call against the single-site forward on its
+    prefix (both on the GPU): same routed state to the bf16 bar."""
+    S, T, first, N, d, r = 49, 48, 2, 300, 1024, 16
+    prob = make_device_problem(PROJECTED, S, N, d, r, dev, seed=8, n_queries=T)
+    H, _ = lr.route_all_fwd(prob["V"], prob["K"], prob["q"], PROJECTED, first)
+    for j in (0, 1, 15, 16, 31, 32, 47):
+        s = first + j
+        h = lr.route_fwd(prob["V"][:s], prob["K"][:s], prob["q"][j].contiguous(), PROJECTED)
+        torch.cuda.synchronize()
+        check_bf16_value(f"site {j}", to_host(H[j]), to_host(h).astype(np.float64))
+
+
+def test_all_sites_rejected_outside_limits(dev):
+    p = make_host_problem(PROJECTED, 4, 3, 64, 8, dtype="bf16", seed=9)
+    V, K = to_dev(p.V, dev), to_dev(p.K, dev)
+    with pytest.raises(lr.RoutingError):
+        lr.route_all_fwd(V, K, torch.zeros((4, 8), device=dev), PROJECTED, 2)
+    big = torch.zeros((65, 2, 64), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lr.RoutingError, match="S <= 64"):
+        lr.route_all_fwd(big, None, torch.zeros((3, 8), device=dev), SLICED, 1)
+    full = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lr.RoutingError, match="projected or sliced"):
+        lr.route_all_fwd(full, None, torch.zeros((2, 64), device=dev), 2, 1)
+
+
+FULL_SIZE = [(PROJECTED, 16), (SLICED, 64)]
+
+
+@pytest.mark.parametrize("mode,r", FULL_SIZE, ids=["P-r16", "S-r64"])
+def test_all_sites_model_pass_full_size(dev, mode, r):
+    """The paper's model pass (49 sources, sites reading 2..49, d = 1024,
+    N = 16384) in the benchmark's launch configuration; sampled tokens
+    against the oracle token by token, every site."""
+    S, T, first, N, d = 49, 48, 2, 16384, 1024
+    prob = make_device_problem(mode, S, N, d, r, dev, seed=0, n_queries=T)
+    H, ne = lr.route_all_fwd(prob["V"], prob["K"], prob["q"], mode, first)
+    torch.cuda.synchronize()
+    Vb = host_bits(prob["V"])
+    Kb = None if prob["K"] is None else host_bits(prob["K"])
+    Q = prob["q"].cpu().numpy().astype(np.float64)
+    toks = np.unique(np.concatenate([[0, 1, N - 1], np.random.default_rng(0).integers(0, N, 29)]))
+    Hh = H[:, torch.as_tensor(toks, device=dev)]
+    got = to_host(Hh.contiguous())
+    got_ne = to_host(ne[:, torch.as_tensor(toks, device=dev)].contiguous())
+    ref = np.empty(got.shape)
+    ref_ne = np.empty(got_ne.shape)
+    for k, n in enumerate(toks):
+        h, e = oracle.route_all_fwd(Vb, Kb, Q, mode, first, r=r, n0=int(n), n1=int(n) + 1)
+        ref[:, k] = h[:, 0]
+        ref_ne[:, k] = e[:, 0]
+    check_bf16_value("H", got, ref)
+    check_neff("neff", got_ne, ref_ne)
