@@ -65,6 +65,8 @@ def _load():
     lib.orc_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, ll, i, i, d, ll,
                                       ll]
     lib.orc_route_all_fwd.restype = ctypes.c_int
+    lib.orc_key_projection.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, ll, ll]
+    lib.orc_key_projection.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -259,3 +261,27 @@ def route_all_fwd(V, K, Q, mode, first, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid problem")
     return H, NEFF
+
+
+def key_projection(A, W, d, n0=0, n1=None):
+    """[o_n; k_n] = [W^O; W^K] a_n (Sec. 3.3, Eq. fused_projection) in fp64.
+
+    A [N, m] activations, W [d + r, m] (rows of W^O, then of W^K), both in
+    one storage.  Returns (O [n1-n0, d] or None when d = 0,
+    K [n1-n0, r] or None when r = 0)."""
+    A = np.ascontiguousarray(A)
+    W = np.ascontiguousarray(W)
+    if A.dtype not in _STORE or W.dtype != A.dtype or A.ndim != 2 or W.ndim != 2:
+        raise ValueError("oracle: A [N, m] and W [d + r, m] in one supported storage")
+    N, m = A.shape
+    if W.shape[1] != m or not 0 <= d <= W.shape[0]:
+        raise ValueError("oracle: W must be [d + r, m] with 0 <= d <= d + r")
+    r = W.shape[0] - d
+    n1 = N if n1 is None else n1
+    O = np.empty((n1 - n0, d), dtype=np.float64) if d > 0 else None
+    K = np.empty((n1 - n0, r), dtype=np.float64) if r > 0 else None
+    rc = _load().orc_key_projection(_ptr(A), _ptr(W), _ptr(O), _ptr(K), N, m, d, r,
+                                    _STORE[A.dtype], n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid projection")
+    return O, K

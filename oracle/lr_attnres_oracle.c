@@ -594,6 +594,43 @@ int orc_route_all_fwd(const void *V, const void *K, const double *Q, double *H, 
     return failed;
 }
 
+/* The projected-key producer (Sec. 3.3, Eq. fused_projection): the output
+ * projection of a residual-writing sub-layer and its key projection are one
+ * matrix [W^O; W^K] with d + r rows, applied to the activation a_n that
+ * enters the output projection:
+ *   [o_n; k_n] = [W^O; W^K] a_n,   o_n in R^d (the residual value),
+ *                                  k_n in R^r (its routing key).
+ * A [N][m] holds a_n row by row; W [d + r][m] holds the rows of W^O then the
+ * rows of W^K.  For tokens n in [n0, n1): O[n - n0][j] = sum_c W[j][c] A[n][c]
+ * for j < d, and Kout[n - n0][j] = sum_c W[d + j][c] A[n][c] for j < r.  O may
+ * be NULL when d = 0 (the embedding key of Eq. embedding_key_projection,
+ * k_0 = W_0^K o_0, is this with d = 0 and a_n = o_0); Kout may be NULL when
+ * r = 0 (a plain output projection). */
+int orc_key_projection(const void *A, const void *W, double *O, double *Kout, long long N,
+                       long long m, long long d, long long r, int store, long long n0,
+                       long long n1)
+{
+    if (N < 0 || m < 1 || d < 0 || r < 0 || d + r < 1 || n0 < 0 || n1 < n0 || n1 > N)
+        return 1;
+    if (A == NULL || W == NULL || (d > 0 && O == NULL) || (r > 0 && Kout == NULL))
+        return 1;
+    if (store < 0 || store > 2)
+        return 1;
+#pragma omp parallel for schedule(static)
+    for (long long n = n0; n < n1; ++n) {
+        for (long long j = 0; j < d + r; ++j) {
+            double acc = 0.0;
+            for (long long c = 0; c < m; ++c)
+                acc += widen(W, store, j * m + c) * widen(A, store, n * m + c);
+            if (j < d)
+                O[(n - n0) * d + j] = acc;
+            else
+                Kout[(n - n0) * r + (j - d)] = acc;
+        }
+    }
+    return 0;
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {
