@@ -267,6 +267,30 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
                              int64_t S, int64_t N, int64_t d, int64_t r, int64_t first,
                              int64_t T, int mode, int dtype, float eps, void *stream);
 
+/*
+ * The projected-key producer (Sec. 3.3, Eq. fused_projection): the output
+ * projection W^O [d][m] of a residual-writing sub-layer and its key
+ * projection W^K [r][m] stacked as one matrix, applied to the activations
+ * entering the output projection, so that each sub-layer emits its residual
+ * value and its routing key in one pass:
+ *   A [N][m]     storage `dtype`: row n is a_n (the attention output before
+ *                its output projection, or the gated SwiGLU hidden state);
+ *   W [d + r][m] storage `dtype`: rows 0 .. d-1 are W^O, rows d .. d+r-1 are
+ *                W^K (the [out][in] layout of a linear layer's weight);
+ *   O [N][d]     overwritten with o_n = W^O a_n, rounded to nearest even:
+ *                typically the sub-layer's plane V + i*N*d of the value stack;
+ *   K [N][r]     overwritten with k_n = W^K a_n: typically K + i*N*r.
+ * d = 0 (O NULL) gives a key projection alone, e.g. the embedding key
+ * k_0 = W_0^K o_0 of Eq. embedding_key_projection; r = 0 (K NULL) a plain
+ * output projection.  fp32 accumulation.  EINVAL: N < 0, m < 1, d or r < 0,
+ * d + r < 1, A or W NULL or not 16-byte aligned (N > 0), O (K) NULL with
+ * d > 0 (r > 0) or non-NULL with d = 0 (r = 0), O or K not element aligned,
+ * outputs overlapping each other or the inputs.  EUNSUPPORTED: fp32 storage,
+ * m % 8 != 0, m or d + r above 2^20, N above 2^30.
+ */
+int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int64_t N, int64_t m,
+                            int64_t d, int64_t r, int dtype, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

@@ -68,6 +68,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                              i, i, f, vp]
     lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
+    lib.lr_attnres_key_proj_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, vp]
+    lib.lr_attnres_key_proj_fwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -173,6 +175,34 @@ def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool 
                                       mode, _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return H, neff
+
+
+def key_proj_fwd(A, W, d: int, out=None):
+    """[o_n; k_n] = [W^O; W^K] a_n (Sec. 3.3, Eq. fused_projection).
+
+    A [N,m] bf16; W [d+r,m] bf16 (rows of W^O, then of W^K).  Returns
+    (O [N,d] or None when d = 0, K [N,r] or None when r = 0); ``out`` may
+    supply (O, K), e.g. planes of the value and key stacks.
+    """
+    import torch
+
+    lib = load_library()
+    if A.dim() != 2 or W.dim() != 2 or W.shape[1] != A.shape[1]:
+        raise ValueError("A must be [N, m] and W [d + r, m]")
+    N, m = A.shape
+    r = W.shape[0] - d
+    if d < 0 or r < 0:
+        raise ValueError("0 <= d <= W.shape[0] required")
+    if out is not None:
+        O, K = out
+    else:
+        O = torch.empty((N, d), dtype=A.dtype, device=A.device) if d > 0 else None
+        K = torch.empty((N, r), dtype=A.dtype, device=A.device) if r > 0 else None
+    rc = lib.lr_attnres_key_proj_fwd(_dev(A, "A"), _dev(W, "W", A.dtype), _dev(O, "O", A.dtype),
+                                     _dev(K, "K", A.dtype), N, m, d, r, _dtype_code(A),
+                                     _stream(A))
+    _check(lib, rc)
+    return O, K
 
 
 def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:

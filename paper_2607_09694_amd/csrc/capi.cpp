@@ -448,4 +448,40 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
     return LRAR_OK;
 }
 
+int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int64_t N,
+                            int64_t m, int64_t d, int64_t r, int dtype, void *stream)
+{
+    g_last_error.clear();
+    if (dtype != LRAR_DTYPE_F32 && dtype != LRAR_DTYPE_BF16)
+        return fail(LRAR_EINVAL, "unknown storage type " + std::to_string(dtype));
+    if (N < 0 || m < 1 || d < 0 || r < 0 || d + r < 1)
+        return fail(LRAR_EINVAL, "sizes must satisfy N >= 0, m >= 1, d >= 0, r >= 0, d + r >= 1");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t ae, we, oe, ke;
+    if (!mul_ok(N, m, &ae) || !mul_ok(d + r, m, &we) || !mul_ok(N, d, &oe) || !mul_ok(N, r, &ke) ||
+        !mul_ok(ae, es, &ae) || !mul_ok(we, es, &we) || !mul_ok(oe, es, &oe) ||
+        !mul_ok(ke, es, &ke))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const bool data = N > 0;
+    int rc;
+    if ((rc = check_ptr(A, "A", 16, data)) || (rc = check_ptr(W, "W", 16, data)) ||
+        (rc = check_ptr(O, "O", es, data && d > 0)) || (rc = check_ptr(K, "K", es, data && r > 0)))
+        return rc;
+    if (d == 0 && O)
+        return fail(LRAR_EINVAL, "O must be NULL when d = 0");
+    if (r == 0 && K)
+        return fail(LRAR_EINVAL, "K must be NULL when r = 0");
+    const Span outs[] = {span("O", O, oe), span("K", K, ke)};
+    const Span ins[] = {span("A", A, ae), span("W", W, we)};
+    if ((rc = check_aliasing(outs, 2, ins, 2)))
+        return rc;
+    lrar::KeyProjProblem p{A, W, O, K, N, m, d, r, dtype};
+    std::string why;
+    if ((rc = lrar::check_key_proj_supported(p, &why)))
+        return fail(rc, why);
+    if ((rc = lrar::launch_key_proj(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 }  // extern "C"

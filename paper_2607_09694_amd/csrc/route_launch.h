@@ -102,6 +102,19 @@ struct AllProblem {
 };
 
 int check_all_supported(const AllProblem &p, std::string *why);
+
+// The projected-key producer (see lr_attnres_key_proj_fwd).
+struct KeyProjProblem {
+    const void *A;  // [N][m]
+    const void *W;  // [d + r][m]
+    void *O;        // [N][d] or NULL
+    void *K;        // [N][r] or NULL
+    int64_t N, m, d, r;
+    int dtype;
+};
+
+int check_key_proj_supported(const KeyProjProblem &p, std::string *why);
+int launch_key_proj(const KeyProjProblem &p, hipStream_t st, std::string *err);
 int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err);
 
 }  // namespace lrar

@@ -43,6 +43,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
+                            "lr_attnres_key_proj_fwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -311,3 +312,37 @@ def test_all_sites_unsupported(lib):
     assert allf(lib, S=70, first=1, T=65) == EUNSUPPORTED
     assert allf(lib, mode=P, K=E, r=65, d=128) == EUNSUPPORTED
     assert allf(lib, d=68) == EUNSUPPORTED
+
+
+def kproj(lib, A_=A, W=B, O=C, K=D, N=8, m=64, d=32, r=16, dtype=BF16):
+    return lib.lr_attnres_key_proj_fwd(A_, W, O, K, N, m, d, r, dtype, None)
+
+
+KPROJ_INVALID = [
+    ("no outputs", dict(d=0, r=0), "d + r >= 1"),
+    ("negative N", dict(N=-1), "N >= 0"),
+    ("m zero", dict(m=0), "m >= 1"),
+    ("A NULL", dict(A_=None), "A is NULL"),
+    ("W misaligned", dict(W=B + 8), "16-byte aligned"),
+    ("O NULL with d", dict(O=None), "O is NULL"),
+    ("K NULL with r", dict(K=None), "K is NULL"),
+    ("O given with d = 0", dict(d=0), "O must be NULL"),
+    ("K given with r = 0", dict(r=0), "K must be NULL"),
+    ("O misaligned", dict(O=C + 1), "2-byte aligned"),
+    ("O overlaps A", dict(O=A + 32), "overlaps"),
+    ("K overlaps O", dict(K=C + 64), "overlap"),
+    ("unknown storage", dict(dtype=7), "storage"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", KPROJ_INVALID, ids=[c[0] for c in KPROJ_INVALID])
+def test_key_projection_rejects(lib, name, kw, msg):
+    assert kproj(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_key_projection_unsupported(lib):
+    assert kproj(lib, dtype=F32) == EUNSUPPORTED
+    assert "bf16" in err(lib)
+    assert kproj(lib, m=60) == EUNSUPPORTED
+    assert kproj(lib, N=(1 << 30) + 1, m=8, d=8, r=8) == EUNSUPPORTED
