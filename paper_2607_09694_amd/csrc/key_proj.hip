@@ -9,24 +9,28 @@
 // activation is read once for both, and the key costs r extra output
 // columns (about r / d more work) instead of a second pass over A.
 //
-// Tiling for gfx950: a workgroup of 4 waves computes 256 tokens x up to 288
-// output columns.  Column tiles are 256 wide, except the last, which also
-// takes the remaining columns up to 288: with d a multiple of 256 and
-// r <= 32 the key columns ride along with the last value tile, and N = 16384
-// tokens at d = 1024 make exactly 256 workgroups, one per CU.  Waves are
-// 2 x 2; a wave owns 128 rows and up to 10 column tiles of
-// v_mfma_f32_16x16x32_bf16 with fp32 accumulators.  Both operands are
-// k-contiguous in memory (A row-major, W in the [out][in] layout of a linear
-// layer), so 64-wide k-slices of both are staged in LDS with 16-byte reads
-// and writes, double-buffered: the next slice is loaded into registers while
-// the current one feeds the MFMAs.  LDS rows are padded to 72 elements (144
-// bytes) so that the 16 consecutive rows of one operand read fall on
-// distinct banks.  Within a k-step the B fragments are read first and each
-// A fragment one MFMA row ahead of its use.  Workgroups are ordered so that
-// the column tiles of one row tile run on one XCD and share its L2 copy of
-// the A slice.  The epilogue rounds to bf16 (nearest even), stages the tile
-// through LDS and writes 16-byte row segments, split between O and K at
-// column d.
+// Tiling for gfx950: a workgroup of 8 waves (two per SIMD) computes 256
+// tokens x up to 288 output columns.  Column tiles are 256 wide, except the
+// last, which also takes the remaining columns up to 288: with d a multiple
+// of 256 and r <= 32 the key columns ride along with the last value tile,
+// and N = 16384 tokens at d = 1024 make exactly 256 workgroups, one per CU.
+// Waves are 4 x 2; a wave owns 64 rows and half of the tile's columns, at
+// most 9 column tiles of v_mfma_f32_16x16x32_bf16 with fp32 accumulators
+// (at most 144 per lane, so two waves fit a SIMD's registers).  Both
+// operands are k-contiguous in memory (A row-major, W in the [out][in]
+// layout of a linear layer).  64-wide k-slices of both go straight from
+// memory to LDS with buffer loads (no register staging), double-buffered:
+// the next slice is in flight while the current one feeds the MFMAs.  The
+// buffer resources cover only the workgroup's rows, so rows past N or past
+// the output read as zero.  LDS rows are 128 bytes with the 16-byte chunks
+// XOR-swizzled by (row / 2) mod 8, so that the 16 consecutive rows that one
+// MFMA operand read touches fall on distinct banks.  Within a k-step the
+// MFMAs go column tile by column tile; the B fragments are read a few
+// columns ahead and the next k-step's A fragments during the first columns.
+// Workgroups are ordered so that the column tiles of one row tile run on
+// one XCD and share its L2 copy of the A slice.  The epilogue rounds to bf16
+// (nearest even), stages half of the tile at a time through LDS and writes
+// 16-byte row segments, split between O and K at column d.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -49,13 +53,14 @@ constexpr int kRow = kPK * 2;        // bytes per LDS row of a stage (unpadded)
 constexpr int kABlocks = kPM / 8;    // 1 KB blocks of 8 rows: A part of a stage
 constexpr int kBBlocks = kPNMax / 8; // ... and W part
 constexpr int kStageBytes = (kPM + kPNMax) * kRow;
-constexpr int kLoads = (kABlocks + kBBlocks) / 4;  // direct loads per wave per stage
+constexpr int kWaves8 = 8;           // waves per workgroup (2 per SIMD)
+constexpr int kLoads = (kABlocks + kBBlocks + kWaves8 - 1) / kWaves8;  // direct loads per wave
 constexpr int kCd = kPNMax + 8;      // LDS row stride of the output half-tile (elements)
-constexpr int kPThreads = 256;
+constexpr int kPThreads = kWaves8 * kWaveSize;
 // Buffer resource word 3 for raw (untyped) loads on gfx9-family parts.
 constexpr int kRawBufferFlags = 0x00020000;
 
-static_assert((kABlocks + kBBlocks) % 4 == 0 && kABlocks % 4 == 0, "stage blocks per wave");
+static_assert(kABlocks % kWaves8 == 0, "A blocks split evenly over the waves");
 static_assert(2 * kStageBytes >= kPM / 2 * kCd * 2, "output half-tile fits the stages");
 
 struct ProjArgs {
@@ -86,8 +91,8 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
                                               int j0, int width, int half)
 {
     const int tid = threadIdx.x;
-    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int lane = tid % kWaveSize, wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
+    const int wm = wave >> 1, wn = wave & 1;  // 4 row groups of 64 x 2 column halves
     const int nout = a.d + a.r;
     const int nk = (a.m + kPK - 1) / kPK;
 
@@ -99,9 +104,11 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     // rows past N, past the tile or past d + r read as zero.  A chunk past m
     // reads the next row's first elements; it is zeroed in LDS (zero_tail).
     // Each lane needs one offset; the row group and the k offset are scalar.
-    const int rr = lane >> 3, slot = lane & 7;
-    const int rl = 8 * wave + rr;                       // row within a 32-row group
-    const int voff = rl * a.m * 2 + 16 * (slot ^ ((rl >> 1) & 7));
+    // Block blk = wave + 8 u holds rows 8 blk .. 8 blk + 7 of A (blk < 32) or
+    // of W; its swizzle (row / 2) mod 8 = (4 (blk mod 2) + l / 16) mod 8 only
+    // depends on the wave's parity, so each lane needs one offset.
+    const int rl = 8 * wave + (lane >> 3);             // row within a 64-row group
+    const int voff = rl * a.m * 2 + 16 * ((lane & 7) ^ ((rl >> 1) & 7));
     const int arows = (int)min((int64_t)kPM, a.N - n0);
     const int brows = max(0, min(width, nout - j0));
     const __amdgpu_buffer_rsrc_t ares = __builtin_amdgcn_make_buffer_rsrc(
@@ -113,20 +120,20 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
         const int kbytes = kt * kPK * 2;
 #pragma unroll
         for (int u = 0; u < kLoads; ++u) {
-            const int blk = wave + 4 * u;
-            if (u < kABlocks / 4)
+            const int blk = wave + kWaves8 * u;
+            if (u < kABlocks / kWaves8)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(ares, (lds_void_t *)(sb + 1024 * blk), 16,
-                                                         voff, u * 64 * a.m + kbytes, 0, 0);
-            else
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(bres, (lds_void_t *)(sb + 1024 * blk), 16,
-                                                         voff, (u - kABlocks / 4) * 64 * a.m + kbytes,
-                                                         0, 0);
+                                                         voff, u * 128 * a.m + kbytes, 0, 0);
+            else if (blk < kABlocks + kBBlocks)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    bres, (lds_void_t *)(sb + 1024 * blk), 16, voff,
+                    (u - kABlocks / kWaves8) * 128 * a.m + kbytes, 0, 0);
         }
     };
 
-    f32x4_t acc[8][NJ];
+    f32x4_t acc[4][NJ];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
             acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -138,7 +145,7 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     auto aload = [&](int kt, int ks, int i) {
         const unsigned char *sa = lds + (kt & 1) * kStageBytes;
         return *reinterpret_cast<const bf16x8_t *>(
-            sa + chunk_at(wm * 128 + 16 * i + fr, 4 * ks + fq));
+            sa + chunk_at(wm * 64 + 16 * i + fr, 4 * ks + fq));
     };
     auto bload = [&](int kt, int ks, int j) {
         const unsigned char *sb = lds + (kt & 1) * kStageBytes + kPM * kRow;
@@ -156,13 +163,13 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
         }
     };
 
-    // One k-step, column tile by column tile: B fragment j against the 8 A
+    // One k-step, column tile by column tile: B fragment j against the 4 A
     // fragments.  The A fragments of the next k-step are read during the
-    // first columns, the B fragments RING - 1 columns ahead, so every LDS
-    // read has at least one column of MFMAs (8 x 16 cycles) to land.
+    // first columns, the B fragments RING - 1 columns ahead; the other wave
+    // on the SIMD covers what remains of the LDS latency.
     constexpr int RING = NJ % 4 == 0 ? 4 : 3;
-    bf16x8_t a0[8], a1[8], br[RING];
-    auto kstep = [&](int kt, int ks, bf16x8_t(&acur)[8], bf16x8_t(&anext)[8], bool more) {
+    bf16x8_t a0[4], a1[4], br[RING];
+    auto kstep = [&](int kt, int ks, bf16x8_t(&acur)[4], bf16x8_t(&anext)[4], bool more) {
         const int nkt = ks ? kt + 1 : kt, nks = ks ^ 1;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -170,18 +177,18 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
                 br[(j + RING - 1) % RING] = bload(kt, ks, j + RING - 1);
             else if (more)
                 br[(j + RING - 1) % RING] = bload(nkt, nks, j + RING - 1 - NJ);
-            if (more && j < 8)
+            if (more && j < 4)
                 anext[j] = aload(nkt, nks, j);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 4; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(acur[i], br[j % RING], acc[i][j],
                                                                     0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
-        if (more && NJ < 8) {
+        if (more && NJ < 4) {
 #pragma unroll
-            for (int i = NJ; i < 8; ++i)
+            for (int i = NJ; i < 4; ++i)
                 anext[i] = aload(nkt, nks, i);
         }
     };
@@ -197,7 +204,7 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     if (nk > 1)
         issue(1, 1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 4; ++i)
         a0[i] = aload(0, 0, i);
 #pragma unroll
     for (int j = 0; j < RING - 1; ++j)
@@ -228,15 +235,15 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     uint16_t *Cs = reinterpret_cast<uint16_t *>(lds);
     const int nchunk = (width + 7) / 8;
     for (int h = 0; h < 2; ++h) {
-        if (wm == h) {
+        if ((wm >> 1) == h) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < NJ; ++j)
                     if (wn == 1 || j < half) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            Cs[(16 * i + 4 * fq + e) * kCd + c0 + 16 * j + fr] =
+                            Cs[((wm & 1) * 64 + 16 * i + 4 * fq + e) * kCd + c0 + 16 * j + fr] =
                                 to_bf16(acc[i][j][e]);
                     }
         }
