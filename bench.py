@@ -27,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 METRIC = "depth-routing tokens/s and achieved HBM TB/s (% of peak), fwd and fwd+bwd"
 KERNEL_DIR = os.path.join(ROOT, "paper_2607_09694_amd", "csrc")
 COUNTERS = os.path.join(ROOT, "profiles", "route_bwd_lr_d2048_counters.txt")
@@ -404,6 +405,61 @@ def decode_model_pass(torch, lr, dev, reps, warmup, N=128, d=1024, r=16):
             "graph_tokens_per_s": N / (replay * 1e-3)}
 
 
+def key_producer(torch, lr, dev, reps, warmup, flush):
+    """The projected-key producer (Eq. fused_projection) at the paper's
+    output projections (d = 1024; attention m = 1024, SwiGLU m = 2816) for
+    N = 16384 tokens, writing planes of the value and key stacks.  The
+    library GEMM (hipBLASLt through torch) is timed beside it: one fused GEMM
+    then a split copy, and two GEMMs written straight into the planes."""
+    out = {}
+    N, d = 16384, 1024
+    for m, r in ((1024, 16), (2816, 16), (2816, 32)):
+        g = torch.Generator(device=dev)
+        g.manual_seed(m + r)
+        A = torch.randn((N, m), generator=g, device=dev).to(torch.bfloat16)
+        W = (torch.randn((d + r, m), generator=g, device=dev) / m ** 0.5).to(torch.bfloat16)
+        V = torch.empty((2, N, d), dtype=torch.bfloat16, device=dev)
+        K = torch.empty((2, N, r), dtype=torch.bfloat16, device=dev)
+        C = torch.empty((N, d + r), dtype=torch.bfloat16, device=dev)
+        Wt, Wo, Wk = W.t(), W[:d].t(), W[d:].t()
+
+        def lib_fused():
+            torch.matmul(A, Wt, out=C)
+            V[0].copy_(C[:, :d])
+            K[0].copy_(C[:, d:])
+
+        def lib_two():
+            torch.matmul(A, Wo, out=V[0])
+            torch.matmul(A, Wk, out=K[0])
+
+        flops = 2.0 * N * m * (d + r)
+        res = {}
+        for name, fn in (("fused_key_producer", lambda: lr.key_proj_fwd(A, W, d, out=(V[1], K[1]))),
+                         ("library_gemm_then_split", lib_fused),
+                         ("library_two_gemms", lib_two)):
+            ts = time_calls(torch, fn, reps, warmup, flush)
+            med = float(np.median(ts))
+            res[name] = {"median_ms": med, "min_ms": float(np.min(ts)),
+                         "TFLOPs": flops / (med * 1e-3) / 1e12,
+                         "frac_of_bf16_peak": flops / (med * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}
+        # Warm: the activation was just written by the previous kernel, as in
+        # a model, so the memory-side cache may still hold it.
+        ts = time_calls(torch, lambda: lr.key_proj_fwd(A, W, d, out=(V[1], K[1])), reps, warmup)
+        res["fused_key_producer_warm"] = {"median_ms": float(np.median(ts)),
+                                          "TFLOPs": flops / (float(np.median(ts)) * 1e-3) / 1e12}
+        ts = time_calls(torch, lib_two, reps, warmup)
+        res["library_two_gemms_warm"] = {"median_ms": float(np.median(ts)),
+                                         "TFLOPs": flops / (float(np.median(ts)) * 1e-3) / 1e12}
+        torch.matmul(A, Wt, out=C)
+        torch.cuda.synchronize()
+        res["bitwise_equal_to_library_fused_gemm"] = bool(torch.equal(V[1], C[:, :d]) and
+                                                          torch.equal(K[1], C[:, d:]))
+        out[f"m{m}_r{r}"] = res
+        del A, W, V, K, C
+        torch.cuda.empty_cache()
+    return out
+
+
 def extras(torch, lr, dev, reps, warmup):
     """The other workloads: the 49-site forward model pass (projected r=16 and
     sliced r in {8,16,32,64}), full-rank vs low-rank at S = 49, and a copy
@@ -512,9 +568,39 @@ def extras(torch, lr, dev, reps, warmup):
     out["block_inference_projected_r32_8blocks"] = block_inference_passes(
         torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
     out["decode_model_pass_projected_r16_N128"] = decode_model_pass(torch, lr, dev, reps, warmup)
+    out["key_producer_d1024_N16384"] = key_producer(torch, lr, dev, reps, warmup, flush)
     out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush
     torch.cuda.empty_cache()
+    return out
+
+
+def focused(torch, lr, dev, names, reps=20, warmup=3):
+    """Only the named workloads (for profiling one kernel at a time):
+    'key_producer' and 'all_sites' (sites 2..49 of the 49-source pass, P-LR
+    r = 16 and S-LR r = 64, cold)."""
+    from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_device_problem
+
+    flush = Flusher(torch, dev)
+    out = {}
+    if "key_producer" in names:
+        out["key_producer_d1024_N16384"] = key_producer(torch, lr, dev, reps, warmup, flush)
+    if "all_sites" in names:
+        N, d, T = 16384, 1024, 48
+        for mode, r in ((PROJECTED, 16), (SLICED, 64)):
+            g = make_device_problem(mode, 49, N, d, r, dev, seed=0, n_queries=49)
+            Ha = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+            ne = torch.empty((T, N), dtype=torch.float32, device=dev)
+            Qa = g["q"][1:].contiguous()
+            ts = time_calls(torch, lambda: lr.route_all_fwd(g["V"], g["K"], Qa, mode, 2,
+                                                            out=(Ha, ne)), reps, warmup, flush)
+            med = float(np.median(ts))
+            nbytes = all_sites_bytes(49, T, N, d, r, mode)
+            out[f"all_sites_pass_{'projected' if mode == PROJECTED else 'sliced'}_r{r}"] = {
+                "median_ms": med, "algo_GBps": nbytes / (med * 1e-3) / 1e9,
+                "frac_of_peak": nbytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS}
+            del g, Ha, ne
+            torch.cuda.empty_cache()
     return out
 
 
@@ -525,6 +611,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--extra-only", default="",
+                    help="comma-separated workloads to run alone, without the main step "
+                         "(key_producer, all_sites); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
                          "backward calls of the main workload (for rocprofv3 --pmc runs)")
@@ -542,6 +631,10 @@ def main():
 
     lr.load_library()
     dev = torch.device("cuda:0")
+    if args.extra_only:
+        names = set(args.extra_only.split(","))
+        print(json.dumps({"extra_only": focused(torch, lr, dev, names)}), flush=True)
+        return
     print(f"bench: generating inputs S={S5} N={N5} d={D5} r={R5}", file=sys.stderr, flush=True)
     g = make_device_problem(PROJECTED, S5, N5, D5, R5, dev, seed=0, with_dH=True)
     V, K, q, dH = g["V"], g["K"], g["q"][0].contiguous(), g["dH"]
