@@ -268,6 +268,18 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
                              int64_t T, int mode, int dtype, float eps, void *stream);
 
 /*
+ * Effective number of sources of one read site (Sec. 4.5, Eq.
+ * effective_sources): neff[n] = exp(-sum_i alpha_i log alpha_i) of token n's
+ * routing weights (Eq. lr_attnres_weight) over the S sources.  Reads the
+ * keys only.  Arguments and errors as for lr_attnres_route_fwd, with neff
+ * [N] fp32 (4-byte aligned) in place of H; V may be NULL with projected
+ * keys.  EUNSUPPORTED above S = 1024 or N = 2^30.
+ */
+int lr_attnres_route_neff(const void *V, const void *K, const float *q, float *neff, int64_t S,
+                          int64_t N, int64_t d, int64_t r, int mode, int dtype, float eps,
+                          void *stream);
+
+/*
  * The projected-key producer (Sec. 3.3, Eq. fused_projection): the output
  * projection W^O [d][m] of a residual-writing sub-layer and its key
  * projection W^K [r][m] stacked as one matrix, applied to the activations

@@ -68,6 +68,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                              i, i, f, vp]
     lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_neff.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, i, f, vp]
+    lib.lr_attnres_route_neff.restype = ctypes.c_int
     lib.lr_attnres_key_proj_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, vp]
     lib.lr_attnres_key_proj_fwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
@@ -145,6 +147,22 @@ def route_fwd(V, K, q, mode, eps: float = 1e-6, out=None):
                                   S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return H
+
+
+def route_neff(V, K, q, mode, eps: float = 1e-6, out=None):
+    """N_eff[n] = exp(-sum alpha log alpha) of one site's routing weights
+    (Sec. 4.5, Eq. effective_sources), from the keys alone; [N] fp32."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    ne = out if out is not None else torch.empty((N,), dtype=torch.float32, device=V.device)
+    rc = lib.lr_attnres_route_neff(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                   _dev(q, "q", torch.float32), _dev(ne, "neff", torch.float32),
+                                   S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return ne
 
 
 def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool = True,

@@ -484,4 +484,34 @@ int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int6
     return LRAR_OK;
 }
 
+int lr_attnres_route_neff(const void *V, const void *K, const float *q, float *neff, int64_t S,
+                          int64_t N, int64_t d, int64_t r, int mode, int dtype, float eps,
+                          void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(V, "V", 16, data && !proj)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(neff, "neff", 4, data)) || (rc = check_ptr(K, "K", 16, data && proj)))
+        return rc;
+    if (!proj && K)
+        return fail(LRAR_EINVAL, "K must be NULL unless keys are projected");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    const Span outs[] = {span("neff", neff, N * 4)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4)};
+    if ((rc = check_aliasing(outs, 1, ins, 3)))
+        return rc;
+    // Full rank: the key is the whole value (Sec. 3.4: sliced keys with r = d).
+    lrar::Problem p{V, K, q, S, N, d, r, mode == LRAR_MODE_FULL ? LRAR_MODE_SLICED : mode, dtype,
+                    eps, dtype};
+    std::string why;
+    if ((rc = lrar::launch_neff(p, neff, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 }  // extern "C"

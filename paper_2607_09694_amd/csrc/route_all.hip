@@ -436,6 +436,43 @@ hipError_t launch_all_mt(const AllArgs &a, int dtype, hipStream_t st)
     return launch_all_mt_rp<MT, 64>(a, dtype, st);
 }
 
+// Effective number of sources of one site (Sec. 4.5, Eq. effective_sources)
+// from the keys alone: one wave per token scores its S sources, then
+//     N_eff = exp(-sum alpha_i log alpha_i) = z exp(-t / z),
+//     z = sum_i exp(s_i - m),  t = sum_i exp(s_i - m) (s_i - m).
+// Full-rank keys run as sliced keys with r = d (Sec. 3.4).
+template <typename T, int VEC>
+__global__ __launch_bounds__(kBlock) void route_neff(const T *__restrict__ keys,
+                                                     const float *__restrict__ q,
+                                                     float *__restrict__ neff, int S, int N,
+                                                     int r, int krow, int koff, float eps,
+                                                     int s_pad)
+{
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= N)
+        return;  // wave-uniform; no workgroup barrier
+    float *s = lds + wave * s_pad;
+    lr_scores<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s, nullptr);
+    float m = -INFINITY;
+    for (int i = lane; i < S; i += kWaveSize)
+        m = fmaxf(m, s[i]);
+    m = wave_max(m);
+    float z = 0.0f, t = 0.0f;
+    for (int i = lane; i < S; i += kWaveSize) {
+        const float x = s[i] - m;
+        const float e = expf(x);
+        z += e;
+        t = fmaf(e, x, t);
+    }
+    z = wave_sum(z);
+    t = wave_sum(t);
+    if (lane == 0)
+        neff[n] = z * expf(-t / z);
+}
+
 }  // namespace
 
 int check_all_supported(const AllProblem &p, std::string *why)
@@ -491,6 +528,40 @@ int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err)
     default: e = launch_all_mt<4>(a, p.dtype, st); break;
     }
     return hip_status(e, "route_all_fwd", err);
+}
+
+}  // namespace lrar
+
+namespace lrar {
+
+int launch_neff(const Problem &p, float *neff, hipStream_t st, std::string *err)
+{
+    if (p.S > 1024) {
+        *err = "the effective number of sources supports S <= 1024";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N > ((int64_t)1 << 30)) {
+        *err = "N above 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N == 0)
+        return LRAR_OK;
+    const bool proj = p.mode == LRAR_MODE_PROJECTED;
+    const void *keys = proj ? p.K : p.V;
+    const int krow = proj ? (int)p.r : (int)p.d;
+    const int koff = proj ? 0 : (int)(p.d - p.r);
+    const int s_pad = (int)((p.S + 3) / 4 * 4);
+    const dim3 grid((unsigned)((p.N + kWaves - 1) / kWaves));
+    const size_t lds = (size_t)kWaves * s_pad * sizeof(float);
+    if (p.dtype == LRAR_DTYPE_BF16)
+        hipLaunchKernelGGL((route_neff<uint16_t, 8>), grid, dim3(kBlock), lds, st,
+                           static_cast<const uint16_t *>(keys), p.q, neff, (int)p.S, (int)p.N,
+                           (int)p.r, krow, koff, p.eps, s_pad);
+    else
+        hipLaunchKernelGGL((route_neff<float, 4>), grid, dim3(kBlock), lds, st,
+                           static_cast<const float *>(keys), p.q, neff, (int)p.S, (int)p.N,
+                           (int)p.r, krow, koff, p.eps, s_pad);
+    return hip_status(hipGetLastError(), "route_neff launch", err);
 }
 
 }  // namespace lrar

@@ -103,6 +103,10 @@ struct AllProblem {
 
 int check_all_supported(const AllProblem &p, std::string *why);
 
+// Effective number of sources of one site (see lr_attnres_route_neff); full
+// rank is passed as sliced keys with r = d.
+int launch_neff(const Problem &p, float *neff, hipStream_t st, std::string *err);
+
 // The projected-key producer (see lr_attnres_key_proj_fwd).
 struct KeyProjProblem {
     const void *A;  // [N][m]

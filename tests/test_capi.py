@@ -43,7 +43,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
-                            "lr_attnres_key_proj_fwd",
+                            "lr_attnres_key_proj_fwd", "lr_attnres_route_neff",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -346,3 +346,16 @@ def test_key_projection_unsupported(lib):
     assert "bf16" in err(lib)
     assert kproj(lib, m=60) == EUNSUPPORTED
     assert kproj(lib, N=(1 << 30) + 1, m=8, d=8, r=8) == EUNSUPPORTED
+
+
+def neff_call(lib, V=A, K=None, q=B, ne=C, S=4, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_neff(V, K, q, ne, S, N, d, r, mode, dtype, eps, None)
+
+
+def test_neff_rejects(lib):
+    assert neff_call(lib, ne=None) == EINVAL and "neff is NULL" in err(lib)
+    assert neff_call(lib, ne=A + 4) == EINVAL and "overlaps" in err(lib)
+    assert neff_call(lib, K=E) == EINVAL and "must be NULL" in err(lib)
+    assert neff_call(lib, mode=P) == EINVAL and "K is NULL" in err(lib)
+    assert neff_call(lib, mode=F, r=8) == EINVAL
+    assert neff_call(lib, S=1025, N=2) == EUNSUPPORTED

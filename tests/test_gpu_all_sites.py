@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import paper_2607_09694_amd as lr
-from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
+from paper_2607_09694_amd.inputs import (FULL, PROJECTED, SLICED, bf16_tensor_to_bits,
                                          f32_from_bf16_bits, make_device_problem,
                                          make_host_problem)
 from parity import check_bf16_value, check_f32
@@ -206,3 +206,38 @@ def test_all_sites_model_pass_full_size(dev, mode, r):
         ref_ne[:, k] = e[:, 0]
     check_bf16_value("H", got, ref)
     check_neff("neff", got_ne, ref_ne)
+
+
+# (mode, storage, S, N, d, r): the single-site N_eff from the keys alone.
+NEFF_CASES = [
+    (PROJECTED, "bf16", 49, 300, 1024, 16),
+    (SLICED, "bf16", 64, 129, 1024, 64),
+    (FULL, "bf16", 13, 77, 256, 256),
+    (PROJECTED, "f32", 7, 50, 64, 12),
+    (SLICED, "f32", 300, 33, 96, 5),
+    (FULL, "f32", 5, 20, 40, 40),
+]
+
+
+@pytest.mark.parametrize("case", NEFF_CASES,
+                         ids=lambda c: "{}-{}-S{}-N{}-d{}-r{}".format(
+                             {PROJECTED: "P", SLICED: "S", FULL: "F"}[c[0]], *c[1:]))
+def test_single_site_neff_matches_oracle(dev, case):
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=31, q_scale=3.0)
+    ne = lr.route_neff(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    torch.cuda.synchronize()
+    ref = oracle.effective_sources(p.V, p.K, p.q.astype(np.float64), mode, r=p.r)
+    check_neff("neff", to_host(ne), ref)
+
+
+def test_single_site_neff_closed_forms(dev):
+    """One source: N_eff = 1 exactly; zero query: N_eff = S."""
+    p = make_host_problem(SLICED, 1, 40, 64, 8, dtype="bf16", seed=32)
+    ne = lr.route_neff(to_dev(p.V, dev), None, to_dev(p.q, dev), SLICED)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(ne), np.ones(40, dtype=np.float32))
+    p = make_host_problem(PROJECTED, 23, 40, 64, 8, dtype="bf16", seed=33)
+    ne = lr.route_neff(to_dev(p.V, dev), to_dev(p.K, dev), torch.zeros(8, device=dev), PROJECTED)
+    torch.cuda.synchronize()
+    check_neff("neff", to_host(ne), np.full(40, 23.0))
