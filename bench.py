@@ -282,25 +282,48 @@ def block_training_pass(torch, lr, dev, O, mode, r, c, reps, warmup):
                                Q[t - 1], dHs[t - 1], sites[t - 1][0], mode,
                                out=(dO, dK, dq), workspace=ws)
 
+    # The deferred form: a completed slot's gradient is gathered once, when
+    # the reverse pass reaches its block, from the coefficients the later
+    # sites recorded; only the block in progress keeps a running gradient.
+    coef = torch.empty((T, nslots, 3, N), dtype=torch.float32, device=dev)
+    dP = dB[0]
+    dKP = dKB[0] if dKB is not None else None
+
+    def bwd_deferred():
+        cur = None
+        for t in range(T, 0, -1):
+            n_src = sites[t - 1][0]
+            p = n_src - 1
+            if p != cur:
+                first = p * c + 2 if p >= 1 else 2
+                lr.block_gather_bwd(B, KB, p, dHs, Q, coef, first - 1, mode, out=(dP, dKP))
+                cur = p
+            lr.block_route_bwd_deferred(B, KB, dP, dKP, coef[t - 1, :n_src - 1], O[t - 1],
+                                        KO[t - 1] if KO is not None else None, Q[t - 1],
+                                        dHs[t - 1], n_src, mode, out=(dO, dK, dq), workspace=ws)
+
     st = torch.cuda.current_stream()
-    for _ in range(warmup):
-        fwd()
-        bwd()
-    tf, tb = [], []
-    for _ in range(reps):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        e[0].record(st)
-        fwd()
-        e[1].record(st)
-        bwd()
-        e[2].record(st)
-        torch.cuda.synchronize()
-        tf.append(e[0].elapsed_time(e[1]))
-        tb.append(e[1].elapsed_time(e[2]))
-    f, b = float(np.median(tf)), float(np.median(tb))
-    del B, dB, KB, dKB, KO, dHs, ws
-    return {"fwd_pass_ms": f, "bwd_pass_ms": b, "step_ms": f + b,
-            "tokens_per_s": N / ((f + b) * 1e-3)}
+    res = {}
+    for name, back in (("", bwd), ("deferred_", bwd_deferred)):
+        for _ in range(warmup):
+            fwd()
+            back()
+        tf, tb = [], []
+        for _ in range(reps):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record(st)
+            fwd()
+            e[1].record(st)
+            back()
+            e[2].record(st)
+            torch.cuda.synchronize()
+            tf.append(e[0].elapsed_time(e[1]))
+            tb.append(e[1].elapsed_time(e[2]))
+        f, b = float(np.median(tf)), float(np.median(tb))
+        res.update({name + "fwd_pass_ms": f, name + "bwd_pass_ms": b, name + "step_ms": f + b,
+                    name + "tokens_per_s": N / ((f + b) * 1e-3)})
+    del B, dB, KB, dKB, KO, dHs, ws, coef
+    return res
 
 
 def block_inference_passes(torch, lr, dev, O, mode, r, c, reps, warmup):
@@ -585,6 +608,14 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
     out = {}
     if "key_producer" in names:
         out["key_producer_d1024_N16384"] = key_producer(torch, lr, dev, reps, warmup, flush)
+    if "block_training" in names:
+        N, d = 16384, 1024
+        g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=1)
+        for mode, r in ((SLICED, 64), (PROJECTED, 32)):
+            out[f"block_training_pass_{'sliced' if mode == SLICED else 'projected'}_r{r}_8blocks"] = \
+                block_training_pass(torch, lr, dev, g["V"], mode, r, 6, 5, 1)
+        del g
+        torch.cuda.empty_cache()
     if "all_sites" in names:
         N, d, T = 16384, 1024, 48
         for mode, r in ((PROJECTED, 16), (SLICED, 64)):
@@ -613,7 +644,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--extra-only", default="",
                     help="comma-separated workloads to run alone, without the main step "
-                         "(key_producer, all_sites); prints their JSON")
+                         "(key_producer, all_sites, block_training); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
                          "backward calls of the main workload (for rocprofv3 --pmc runs)")

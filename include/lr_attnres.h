@@ -204,6 +204,58 @@ int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const
                                int dtype, float eps, void *stream);
 
 /*
+ * The block reverse pass in deferred form: the same gradients as
+ * lr_attnres_block_route_bwd, with the fp32 gradient of a completed slot
+ * formed once instead of read-modified-written at every later site.  A
+ * completed slot j is read by every site after its block completes; at such
+ * a site t its gradient is alpha_{t,j} dH_t plus, on the key, the RMSNorm
+ * term (ds/rho) q_t - (ds s/(rho r)) kbar_j, so the site only records three
+ * numbers per token, and lr_attnres_block_gather_bwd later sums them.  The
+ * block in progress (slot n_src - 1) keeps a running gradient.
+ *
+ * One site (arguments as for lr_attnres_block_route_bwd, except):
+ *   dP  [N][d] fp32: the running gradient of the block in progress, += this
+ *       site's contribution (value path and, for sliced keys, the key path
+ *       in the last r columns); dKP [N][r] fp32 likewise for projected keys;
+ *   coef [n_src - 1][3][N] fp32, overwritten: for each completed slot i,
+ *       alpha_i, ds_i / rho_i and ds_i s_i / (rho_i r) per token (NULL when
+ *       n_src = 1);
+ *   dO = dP, dK = dKP (model dtype) after the addition; B[n_src - 1] -= o_new,
+ *   KB[n_src - 1] -= k_new; dq [r] = this site's query gradient.
+ * Driving a model pass in reverse: when slot j first becomes the block in
+ * progress (the last site of block j), set dP, dKP with
+ * lr_attnres_block_gather_bwd over the sites that read slot j as completed
+ * (zero sites: zeros), then call this function at each site down to the
+ * block's first.  Limits and errors as for lr_attnres_block_route_bwd.
+ */
+int lr_attnres_block_route_bwd_deferred(float *B, float *KB, float *dP, float *dKP, float *coef,
+                                        const void *o_new, const void *k_new, const float *q,
+                                        const void *dH, void *dO, void *dK, float *dq,
+                                        void *workspace, size_t workspace_bytes, int64_t n_src,
+                                        int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                        float eps, void *stream);
+
+/*
+ * The gradient of completed slot `slot` from the n_sites sites that read it
+ * as completed (see lr_attnres_block_route_bwd_deferred):
+ *   dP [N][d] = sum_u alpha_u dH_u  + (key columns) sum_u cq_u q_u - (sum_u ck_u) kbar
+ *   (sliced keys: the last r columns; projected keys: dKP [N][r] takes the
+ *   key term and dP the value term), overwritten.
+ *   B [.][N][d], KB [.][N][r] fp32: the slots; the slot's key kbar = k / rho
+ *   is recomputed from B[slot] (sliced) or KB[slot] (projected);
+ *   dHs [n_sites][N][d] model dtype: the sites' dH, in site order;
+ *   Q [n_sites][r] fp32: their queries;
+ *   coef: site u's coefficients (alpha, cq, ck) for this slot are the three
+ *   [N] rows at coef + u * coef_site_stride (floats; >= 3 N).
+ * EUNSUPPORTED: d not a multiple of 4 or above 2048, more than 1024 sites,
+ * n_sites * r above 16384.  Other errors as for lr_attnres_block_route_bwd.
+ */
+int lr_attnres_block_gather_bwd(const float *B, const float *KB, int64_t slot, const void *dHs,
+                                const float *Q, const float *coef, int64_t coef_site_stride,
+                                int64_t n_sites, float *dP, float *dKP, int64_t N, int64_t d,
+                                int64_t r, int mode, int dtype, float eps, void *stream);
+
+/*
  * Two-phase block inference (Sec. 3.5): the site queries do not depend on
  * the input, and routing over the completed slots merges with routing over
  * the partial block by an online-softmax update.  The c sites whose newest

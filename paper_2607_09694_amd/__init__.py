@@ -68,6 +68,12 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                              i, i, f, vp]
     lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
+    lib.lr_attnres_block_route_bwd_deferred.argtypes = [vp] * 13 + [ctypes.c_size_t, i64, i64,
+                                                                    i64, i64, i, i, f, vp]
+    lib.lr_attnres_block_route_bwd_deferred.restype = ctypes.c_int
+    lib.lr_attnres_block_gather_bwd.argtypes = [vp, vp, i64, vp, vp, vp, i64, i64, vp, vp, i64,
+                                                i64, i64, i, i, f, vp]
+    lib.lr_attnres_block_gather_bwd.restype = ctypes.c_int
     lib.lr_attnres_route_neff.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, i, f, vp]
     lib.lr_attnres_route_neff.restype = ctypes.c_int
     lib.lr_attnres_key_proj_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, vp]
@@ -335,6 +341,74 @@ def block_route_bwd(B, KB, dB, dKB, o_new, k_new, q, dH, n_src: int, mode, eps: 
         int(n_src), N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
     _check(lib, rc)
     return dO, dK, dq
+
+
+def block_route_bwd_deferred(B, KB, dP, dKP, coef, o_new, k_new, q, dH, n_src: int, mode,
+                             eps: float = 1e-6, out=None, workspace=None):
+    """One site of the deferred block reverse pass (see
+    lr_attnres_block_route_bwd_deferred): dP / dKP (the running gradient of
+    the block in progress) grow by this site's contribution, coef
+    [n_src-1, 3, N] receives the completed slots' coefficients, and the
+    member o_new retires with gradient dP.  Returns (dO, dK, dq)."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    _, N, d = B.shape
+    r = KB.shape[2] if mode == PROJECTED else q.shape[0]
+    if out is not None:
+        dO, dK, dq = out
+    else:
+        dO = torch.empty((N, d), dtype=o_new.dtype, device=B.device)
+        dK = (torch.empty((N, r), dtype=o_new.dtype, device=B.device)
+              if mode == PROJECTED else None)
+        dq = torch.empty((r,), dtype=torch.float32, device=B.device)
+    wmode = SLICED if mode == FULL else mode
+    need = lib.lr_attnres_route_bwd_workspace_bytes(n_src, N, d, r, wmode, _F32)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=B.device)
+    rc = lib.lr_attnres_block_route_bwd_deferred(
+        _dev(B, "B", torch.float32), _dev(KB, "KB", torch.float32),
+        _dev(dP, "dP", torch.float32), _dev(dKP, "dKP", torch.float32),
+        _dev(coef, "coef", torch.float32) if n_src > 1 else None,
+        _dev(o_new, "o_new"), _dev(k_new, "k_new", o_new.dtype), _dev(q, "q", torch.float32),
+        _dev(dH, "dH", o_new.dtype), _dev(dO, "dO", o_new.dtype), _dev(dK, "dK", o_new.dtype),
+        _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"), workspace.numel(),
+        int(n_src), N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
+    _check(lib, rc)
+    return dO, dK, dq
+
+
+def block_gather_bwd(B, KB, slot: int, dHs, Q, coef, first: int, mode, eps: float = 1e-6,
+                     out=None):
+    """The gradient of completed slot `slot` from sites first..T-1 (0-based
+    indices into dHs [T, N, d], Q [T, r] and coef [T, nslots, 3, N]), the
+    sites that read it as completed (see lr_attnres_block_gather_bwd).
+    Overwrites and returns (dP [N, d] fp32, dKP [N, r] fp32 or None)."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    _, N, d = B.shape
+    T = dHs.shape[0]
+    r = KB.shape[2] if mode == PROJECTED else Q.shape[1]
+    n_sites = max(0, T - first)
+    if out is not None:
+        dP, dKP = out
+    else:
+        dP = torch.empty((N, d), dtype=torch.float32, device=B.device)
+        dKP = (torch.empty((N, r), dtype=torch.float32, device=B.device)
+               if mode == PROJECTED else None)
+    for t, name in ((dHs, "dHs"), (Q, "Q"), (coef, "coef")):
+        _dev(t, name)
+    f0 = first if n_sites > 0 else 0
+    rc = lib.lr_attnres_block_gather_bwd(
+        _dev(B, "B", torch.float32), _dev(KB, "KB", torch.float32), int(slot),
+        dHs[f0].data_ptr(), Q[f0].data_ptr(), coef[f0, slot].data_ptr(), coef.stride(0),
+        n_sites, _dev(dP, "dP", torch.float32), _dev(dKP, "dKP", torch.float32), N, d, r, mode,
+        _dtype_code(dHs), float(eps), _stream(B))
+    _check(lib, rc)
+    return dP, dKP
 
 
 def block_inter_fwd(B, KB, Q, n_prev: int, mode, eps: float = 1e-6, out=None):

@@ -514,4 +514,111 @@ int lr_attnres_route_neff(const void *V, const void *K, const float *q, float *n
     return LRAR_OK;
 }
 
+int lr_attnres_block_route_bwd_deferred(float *B, float *KB, float *dP, float *dKP, float *coef,
+                                        const void *o_new, const void *k_new, const float *q,
+                                        const void *dH, void *dO, void *dK, float *dq,
+                                        void *workspace, size_t workspace_bytes, int64_t n_src,
+                                        int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                        float eps, void *stream)
+{
+    g_last_error.clear();
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
+    int64_t ve, ke, he;
+    int rc = check_shape(n_src, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const size_t ek = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(dP, "dP", 16, data)) ||
+        (rc = check_ptr(coef, "coef", 4, data && n_src > 1)) ||
+        (rc = check_ptr(o_new, "o_new", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(dH, "dH", 16, data)) || (rc = check_ptr(dO, "dO", 16, data)) ||
+        (rc = check_ptr(dq, "dq", 4, true)) || (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(dKP, "dKP", 16, data && proj)) ||
+        (rc = check_ptr(k_new, "k_new", ek, data && proj)) ||
+        (rc = check_ptr(dK, "dK", ek, data && proj)) ||
+        (rc = check_ptr(workspace, "workspace", 16, false)))
+        return rc;
+    if (!proj && (KB || dKP || k_new || dK))
+        return fail(LRAR_EINVAL, "KB, dKP, k_new and dK must be NULL unless keys are projected");
+    const lrar::BlockProblem bp{B, KB, o_new, k_new, q, nullptr, n_src, N, d, r, 0, mode,
+                                dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_block_supported(bp, &why)))
+        return fail(rc, why);
+    lrar::Problem p{B, KB, q, n_src, N, d, r, mode, LRAR_DTYPE_F32, eps, dtype};
+    if ((rc = lrar::check_supported(p, true, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::bwd_workspace_bytes(p);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t nr, nc;
+    if (!mul_ok(N, r, &nr) || !mul_ok(n_src - 1, 3 * N, &nc))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("B", B, ve * 4),    span("KB", KB, ke * 4),
+                         span("dP", dP, he * 4),  span("dKP", dKP, nr * 4),
+                         span("coef", coef, nc * 4), span("dO", dO, he * es),
+                         span("dK", dK, nr * es), span("dq", dq, r * 4),
+                         span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("o_new", o_new, he * es), span("k_new", k_new, nr * es),
+                        span("q", q, r * 4), span("dH", dH, he * es)};
+    if ((rc = check_aliasing(outs, 9, ins, 4)))
+        return rc;
+    lrar::BlockRetire br{B, KB, dP, dKP, o_new, k_new, dO, dK, n_src - 1, N, d, r, mode, dtype};
+    br.grad_rows = true;
+    if ((rc = lrar::launch_block_bwd_deferred(p, br, dH, dP, dKP, coef, dq, workspace,
+                                              static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+int lr_attnres_block_gather_bwd(const float *B, const float *KB, int64_t slot, const void *dHs,
+                                const float *Q, const float *coef, int64_t coef_site_stride,
+                                int64_t n_sites, float *dP, float *dKP, int64_t N, int64_t d,
+                                int64_t r, int mode, int dtype, float eps, void *stream)
+{
+    g_last_error.clear();
+    if (slot < 0 || n_sites < 0)
+        return fail(LRAR_EINVAL, "slot and n_sites must be >= 0");
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
+    int64_t ve, ke, he;
+    int rc = check_shape(slot + 1, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    if (n_sites > 0 && coef_site_stride < 3 * N)
+        return fail(LRAR_EINVAL, "coef_site_stride must be at least 3 N");
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(dP, "dP", 16, data)) ||
+        (rc = check_ptr(dHs, "dHs", 16, data && n_sites > 0)) ||
+        (rc = check_ptr(Q, "Q", 4, n_sites > 0)) ||
+        (rc = check_ptr(coef, "coef", 4, data && n_sites > 0)) ||
+        (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(dKP, "dKP", 16, data && proj)))
+        return rc;
+    if (!proj && (KB || dKP))
+        return fail(LRAR_EINVAL, "KB and dKP must be NULL unless keys are projected");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t hs, qn, cn, nr;
+    if (!mul_ok(n_sites, he, &hs) || !mul_ok(hs, es, &hs) || !mul_ok(n_sites, r, &qn) ||
+        !mul_ok(n_sites > 0 ? n_sites - 1 : 0, coef_site_stride, &cn) || !mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    cn = n_sites > 0 ? cn + 3 * N : 0;
+    const Span outs[] = {span("dP", dP, he * 4), span("dKP", dKP, nr * 4)};
+    const Span ins[] = {span("B", B, ve * 4), span("KB", KB, ke * 4), span("dHs", dHs, hs),
+                        span("Q", Q, qn * 4), span("coef", coef, cn * 4)};
+    if ((rc = check_aliasing(outs, 2, ins, 5)))
+        return rc;
+    const lrar::BlockGather g{B + slot * N * d, proj ? KB + slot * N * r : nullptr, dHs, Q, coef,
+                              coef_site_stride, n_sites, dP, dKP, N, d, r, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::launch_block_gather(g, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 }  // extern "C"

@@ -402,13 +402,13 @@ hipError_t launch_retire_t(const BlockRetire &br, hipStream_t st)
     const long long nvec = (long long)(plane / 4);
     const int grid = (int)std::min<long long>((nvec + 255) / 256, 8192);
     hipLaunchKernelGGL(block_retire<TO>, dim3(grid), dim3(256), 0, st, br.B + br.j * plane,
-                       br.dB + br.j * plane, static_cast<const TO *>(br.o_new),
-                       static_cast<TO *>(br.dO), nvec);
+                       br.dB + (br.grad_rows ? 0 : br.j * plane),
+                       static_cast<const TO *>(br.o_new), static_cast<TO *>(br.dO), nvec);
     if (br.mode == LRAR_MODE_PROJECTED) {
         const size_t kplane = (size_t)br.N * br.r;
         const int kgrid = (int)std::min<long long>(((long long)kplane + 255) / 256, 8192);
         hipLaunchKernelGGL(block_retire_keys<TO>, dim3(kgrid), dim3(256), 0, st,
-                           br.KB + br.j * kplane, br.dKB + br.j * kplane,
+                           br.KB + br.j * kplane, br.dKB + (br.grad_rows ? 0 : br.j * kplane),
                            static_cast<const TO *>(br.k_new), static_cast<TO *>(br.dK),
                            (long long)kplane);
     }
@@ -565,6 +565,171 @@ int check_block_supported(const BlockProblem &p, std::string *why)
         return LRAR_EUNSUPPORTED;
     }
     return LRAR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Deferred reverse pass: the gradient of a completed slot j from the sites
+// that read it as completed, formed once.  Each of those sites stored, per
+// token, alpha_{t,j}, cq = ds/rho and ck = ds s / (rho r) (route_bwd_lr's
+// deferred form), so that
+//     dB_j = sum_t alpha_{t,j} dH_t      (every column)
+//          + sum_t cq_t q_t - (sum_t ck_t) kbar_j   (the key columns),
+// kbar_j = k_j / rho_j recomputed from the summary's key.  One wave per
+// token streams the sites' dH rows like the forward's value stream.
+// ---------------------------------------------------------------------------
+
+struct GatherArgs {
+    const float *Bj, *KBj;
+    const void *dHs;
+    const float *Q, *coef;
+    long long site_stride;
+    float *dP, *dKP;
+    int n_sites, N, d, r, sliced, s_pad;
+    float eps;
+};
+
+template <typename TH, int NCH, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
+{
+    extern __shared__ float lds[];
+    float *Qs = lds + kWaves * 3 * a.s_pad;  // [n_sites][r], shared by the waves
+    for (int i = threadIdx.x; i < a.n_sites * a.r; i += kBlock)
+        Qs[i] = a.Q[i];
+    __syncthreads();
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= a.N)
+        return;  // wave-uniform; no workgroup barrier below
+    float *al = lds + wave * 3 * a.s_pad, *cq = al + a.s_pad, *ck = cq + a.s_pad;
+    const size_t N = (size_t)a.N;
+    float ck_sum = 0.0f;
+    for (int u = lane; u < a.n_sites; u += kWaveSize) {
+        const float *cu = a.coef + u * a.site_stride;
+        al[u] = cu[n];
+        cq[u] = cu[N + n];
+        ck[u] = cu[2 * N + n];
+        ck_sum += ck[u];
+    }
+    ck_sum = wave_sum(ck_sum);
+    wave_lds_sync();
+
+    // rho of the slot's key: the last r columns of the summary (sliced) or
+    // its projected key summary.
+    const float *key = a.sliced ? a.Bj + (size_t)n * a.d + (a.d - a.r) : a.KBj + (size_t)n * a.r;
+    float ss = 0.0f;
+    for (int e = lane; e < a.r; e += kWaveSize)
+        ss = fmaf(key[e], key[e], ss);
+    const float rho = sqrtf(wave_sum(ss) / (float)a.r + a.eps);
+    const float kscale = a.n_sites > 0 ? ck_sum / rho : 0.0f;
+    // The key-column term of key element e: sum_t cq_t q_t[e] - kscale * k[e].
+    auto key_term = [&](int e) {
+        float v = 0.0f;
+        for (int u = 0; u < a.n_sites; ++u)
+            v = fmaf(cq[u], Qs[u * a.r + e], v);
+        return v - kscale * key[e];
+    };
+
+    const int col = lane * 4;
+    bool ok[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        ok[c] = col + c * kWaveSize * 4 < a.d;
+    float acc[NCH][4];
+    mix_rows<TH, 4, NCH, FULLCOLS>(static_cast<const TH *>(a.dHs) + (size_t)n * a.d + col,
+                                   N * a.d, a.n_sites, al, ok, acc);
+    float *prow = a.dP + (size_t)n * a.d + col;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!(FULLCOLS || ok[c]))
+            continue;
+        if (a.sliced) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int kc = col + c * kWaveSize * 4 + e - (a.d - a.r);
+                if (kc >= 0)
+                    acc[c][e] += key_term(kc);
+            }
+        }
+        store_raw<float, 4>(prow + c * kWaveSize * 4, Narrow<float, 4>::run(acc[c]));
+    }
+    if (!a.sliced && a.dKP) {
+        for (int e = lane; e < a.r; e += kWaveSize)
+            a.dKP[(size_t)n * a.r + e] = key_term(e);
+    }
+}
+
+int check_gather_supported(const BlockGather &g, std::string *why)
+{
+    if (g.d % 4 != 0 || g.d > 2048) {
+        *why = "the block gather needs d % 4 == 0 and d <= 2048";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (g.n_sites > 1024 || g.n_sites * g.r > 16384) {
+        *why = "the block gather supports up to 1024 sites and n_sites * r <= 16384";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (g.N > (1 << 30)) {
+        *why = "N exceeds 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    return LRAR_OK;
+}
+
+int launch_block_gather(const BlockGather &g, hipStream_t st, std::string *err)
+{
+    int rc = check_gather_supported(g, err);
+    if (rc)
+        return rc;
+    if (g.N == 0)
+        return LRAR_OK;
+    GatherArgs a;
+    a.Bj = g.Bj;
+    a.KBj = g.KBj;
+    a.dHs = g.dHs;
+    a.Q = g.Q;
+    a.coef = g.coef;
+    a.site_stride = g.site_stride;
+    a.dP = g.dP;
+    a.dKP = g.dKP;
+    a.n_sites = (int)g.n_sites;
+    a.N = (int)g.N;
+    a.d = (int)g.d;
+    a.r = (int)g.r;
+    a.sliced = g.mode == LRAR_MODE_SLICED ? 1 : 0;
+    a.s_pad = (int)((g.n_sites + 3) / 4 * 4);
+    a.eps = g.eps;
+    const int need = (int)((g.d + 255) / 256);
+    int nch = 1;
+    while (nch < need)
+        nch <<= 1;
+    const bool fullcols = g.d % (256 * nch) == 0;
+    const size_t lds = ((size_t)kWaves * 3 * a.s_pad + (size_t)a.n_sites * a.r) * sizeof(float);
+    const dim3 grid((unsigned)((g.N + kWaves - 1) / kWaves));
+    auto go = [&](auto th) {
+        typedef decltype(th) TH;
+        auto launch = [&](auto nchc, auto fc) {
+            hipLaunchKernelGGL((block_gather<TH, decltype(nchc)::value, decltype(fc)::value>), grid,
+                               dim3(kBlock), lds, st, a);
+        };
+        auto by_fc = [&](auto nchc) {
+            if (fullcols)
+                launch(nchc, std::true_type{});
+            else
+                launch(nchc, std::false_type{});
+        };
+        switch (nch) {
+        case 1: by_fc(std::integral_constant<int, 1>{}); break;
+        case 2: by_fc(std::integral_constant<int, 2>{}); break;
+        case 4: by_fc(std::integral_constant<int, 4>{}); break;
+        default: by_fc(std::integral_constant<int, 8>{}); break;
+        }
+    };
+    if (g.dtype == LRAR_DTYPE_BF16)
+        go(uint16_t{});
+    else
+        go(float{});
+    return hip_status(hipGetLastError(), "block_gather launch", err);
 }
 
 int launch_block_fwd(const BlockProblem &p, hipStream_t st, std::string *err)

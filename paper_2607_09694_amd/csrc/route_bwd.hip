@@ -29,13 +29,34 @@ template <int KV> struct KeyChunks { static constexpr int value = KV == 8 ? 1 : 
 // dq is reduced per workgroup in a fixed order into partial[blockIdx.x][r].
 // T is the storage of V, K, dV and dK; TH that of dH (the same except for
 // block sources, whose fp32 summary slots meet the model's bf16 gradient).
-template <typename T, typename TH, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC>
+// DEFER (block sources, deferred form): only the last source (the block in
+// progress) receives gradients, added into the single rows dV [N][d] and
+// dK [N][r]; for every other source i the wave writes the three per-token
+// coefficients of its gradient instead,
+//     coef[i][0][n] = alpha_i,  coef[i][1][n] = ds_i / rho_i,
+//     coef[i][2][n] = ds_i s_i / (rho_i r),
+// from which dV_i = alpha_i dH + (key columns) coef1 q - coef2 kbar_i.  The
+// site's member then retires in the same pass (DeferOut): its gradient is
+// the new running row (dO, dK in the model dtype), and it leaves the slot
+// (Bp -= o_new, KBp -= k_new) once the slot row has been read for the last
+// time (the key columns after the key pass).
+struct DeferOut {
+    float *coef;
+    const void *o_new, *k_new;  // model dtype
+    void *dO, *dK;              // model dtype
+    float *Bp, *KBp;            // the slot of the block in progress
+};
+
+template <typename T, typename TH, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC,
+          bool DEFER = false>
 __global__ void __launch_bounds__(kBlock)
 route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
              const TH *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
              float *__restrict__ partial, int S, int N, int d, int r, int krow, int koff,
-             int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw, int lps)
+             int sliced, int tail_start, float eps, int s_pad, int r_pad, int tpw, int lps,
+             DeferOut dfo = DeferOut{})
 {
+    float *__restrict__ coef = dfo.coef;
     extern __shared__ float lds[];
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
@@ -112,8 +133,9 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                 const size_t off = (size_t)(i0 + h + u) * plane + c * kWaveSize * VEC;
                                 raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + off);
                                 if constexpr (ACC)
-                                    if (wr[c])
-                                        old[u][c] = load_stream<T, VEC, kNtLoad>(dvbase + off);
+                                    if (wr[c] && (!DEFER || i0 + h + u == S - 1))
+                                        old[u][c] = load_stream<T, VEC, kNtLoad>(
+                                            dvbase + (DEFER ? c * kWaveSize * VEC : off));
                             }
 #pragma unroll
                 for (int u = 0; u < L; ++u) {
@@ -131,13 +153,29 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                     p = fmaf(dh[c][e], x[e], p);
                                     y[e] = a * dh[c][e];
                                 }
+                                const bool wdv = wr[c] && (!DEFER || i == S - 1);
                                 if constexpr (ACC)
-                                    if (wr[c])
+                                    if (wdv)
                                         add_stored(y, old[u][c]);
-                                if (wr[c])
+                                if (wdv)
                                     store_stream<T, VEC, kNtStore>(
-                                        dvbase + (size_t)i * plane + c * kWaveSize * VEC,
+                                        dvbase + (DEFER ? 0 : (size_t)i * plane) + c * kWaveSize * VEC,
                                         Narrow<T, VEC>::run(y));
+                                if constexpr (DEFER) {
+                                    if (wdv) {
+                                        // retire: dO = the new running row;
+                                        // the member leaves the slot
+                                        const size_t ro = (size_t)n * d + col + c * kWaveSize * VEC;
+                                        store_stream<TH, VEC, kNtStore>(
+                                            static_cast<TH *>(dfo.dO) + ro, Narrow<TH, VEC>::run(y));
+                                        float o[VEC];
+                                        widen(load_raw<TH, VEC>(static_cast<const TH *>(dfo.o_new) + ro), o);
+#pragma unroll
+                                        for (int e = 0; e < VEC; ++e)
+                                            x[e] -= o[e];
+                                        store_raw<float, VEC>(dfo.Bp + ro, Narrow<float, VEC>::run(x));
+                                    }
+                                }
                             }
                         }
                     }
@@ -184,6 +222,13 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                 const float dsi = g[i];
                 const float cq = dsi * ri;              // ds_i / rho_i
                 const float ck = cq * s[i] * inv_r;     // ds_i s_i / (rho_i r)
+                const bool defer_i = DEFER && i < S - 1;
+                const size_t orow = DEFER ? (size_t)n : row;  // output row of source i
+                if (defer_i && k == 0 && vl == 0) {
+                    coef[((size_t)i * 3 + 0) * N + n] = alpha[i];
+                    coef[((size_t)i * 3 + 1) * N + n] = cq;
+                    coef[((size_t)i * 3 + 2) * N + n] = ck;
+                }
                 float x[KV], y[KV];
                 if (!sliced) {
                     widen(load_raw<T, KV>(keys + row * krow + c0), x);
@@ -193,9 +238,22 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                         y[e] = fmaf(cq, qk[k][e], -ck * kb);
                         dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
                     }
+                    if (defer_i)
+                        continue;
                     if constexpr (ACC)
-                        add_stored(y, load_raw<T, KV>(dK + row * r + c0));
-                    store_raw<T, KV>(dK + row * r + c0, Narrow<T, KV>::run(y));
+                        add_stored(y, load_raw<T, KV>(dK + orow * r + c0));
+                    store_raw<T, KV>(dK + orow * r + c0, Narrow<T, KV>::run(y));
+                    if constexpr (DEFER) {
+                        // retire the member's key: dK = the new running key
+                        // row; the key leaves the slot's key summary
+                        const size_t ro = (size_t)n * r + c0;
+#pragma unroll
+                        for (int e = 0; e < KV; ++e) {
+                            store_elem(static_cast<TH *>(dfo.dK) + ro + e, y[e]);
+                            dfo.KBp[ro + e] =
+                                x[e] - load_elem(static_cast<const TH *>(dfo.k_new) + ro + e);
+                        }
+                    }
                 } else {
                     widen(load_raw<T, KV>(V + row * d + c0), x);
                     const float a = alpha[i];
@@ -208,9 +266,23 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                             dq_acc[k][e] = fmaf(dsi, kb, dq_acc[k][e]);
                         }
                     }
+                    if (defer_i)
+                        continue;
                     if constexpr (ACC)
-                        add_stored(y, load_raw<T, KV>(dV + row * d + c0));
-                    store_raw<T, KV>(dV + row * d + c0, Narrow<T, KV>::run(y));
+                        add_stored(y, load_raw<T, KV>(dV + orow * d + c0));
+                    store_raw<T, KV>(dV + orow * d + c0, Narrow<T, KV>::run(y));
+                    if constexpr (DEFER) {
+                        // retire the member's columns of the key pass: its
+                        // gradient, and the slot without it (the slot row
+                        // was read here for the last time)
+                        const size_t ro = (size_t)n * d + c0;
+#pragma unroll
+                        for (int e = 0; e < KV; ++e) {
+                            store_elem(static_cast<TH *>(dfo.dO) + ro + e, y[e]);
+                            dfo.Bp[ro + e] =
+                                x[e] - load_elem(static_cast<const TH *>(dfo.o_new) + ro + e);
+                        }
+                    }
                 }
             }
         }
@@ -442,9 +514,9 @@ KeyPass key_pass(const Problem &p, const Plan &pl)
     return k;
 }
 
-template <typename T, typename TH, int VEC, bool ACC>
+template <typename T, typename TH, int VEC, bool ACC, bool DEFER = false>
 hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
-                        float *partial, hipStream_t st)
+                        float *partial, hipStream_t st, const DeferOut &dfo = DeferOut{})
 {
     const T *V = static_cast<const T *>(p.V);
     const int tail_start = p.mode == LRAR_MODE_SLICED ? (int)((p.d - p.r) / pl.vec * pl.vec)
@@ -456,7 +528,7 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
     return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
-        if constexpr (std::is_same<T, TH>::value) {
+        if constexpr (std::is_same<T, TH>::value && !DEFER) {
             if (p.mode == LRAR_MODE_FULL) {
                 hipLaunchKernelGGL((route_bwd_full<T, VEC, NCH, FC, ACC>), dim3(pl.nblocks),
                                    dim3(kBlock), pl.lds, st, V, p.q, static_cast<const T *>(dH),
@@ -467,12 +539,12 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
         }
         auto launch = [&](auto kvc) {
             constexpr int KV = decltype(kvc)::value;
-            hipLaunchKernelGGL((route_bwd_lr<T, TH, VEC, NCH, FC, KV, ACC>), dim3(pl.nblocks),
-                               dim3(kBlock), pl.lds, st, V, keys, p.q,
+            hipLaunchKernelGGL((route_bwd_lr<T, TH, VEC, NCH, FC, KV, ACC, DEFER>),
+                               dim3(pl.nblocks), dim3(kBlock), pl.lds, st, V, keys, p.q,
                                static_cast<const TH *>(dH), static_cast<T *>(dV),
                                static_cast<T *>(dK), partial, (int)p.S, (int)p.N, (int)p.d,
                                (int)p.r, krow, koff, p.mode == LRAR_MODE_SLICED ? 1 : 0,
-                               tail_start, p.eps, pl.s_pad, pl.r_pad, pl.tpw, kp.lps);
+                               tail_start, p.eps, pl.s_pad, pl.r_pad, pl.tpw, kp.lps, dfo);
         };
         if constexpr (VEC > 1) {
             if (kp.kv == VEC)
@@ -535,6 +607,44 @@ int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, 
 // (fp32) from the model-dtype dH, write dq, then retire the site (the
 // member's gradient is its slot's gradient so far; the member leaves its
 // slot).
+int launch_block_bwd_deferred(const Problem &p, const BlockRetire &br, const void *dH, float *dP,
+                              float *dKP, float *coef, float *dq, void *ws, hipStream_t st,
+                              std::string *err)
+{
+    Plan pl;
+    if (!make_plan(p, true, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    float *partial = static_cast<float *>(ws);
+    // The retire step runs inside the backward kernel (DeferOut).
+    const size_t plane = (size_t)p.N * p.d, kplane = (size_t)p.N * p.r;
+    DeferOut dfo;
+    dfo.coef = coef;
+    dfo.o_new = br.o_new;
+    dfo.k_new = br.k_new;
+    dfo.dO = br.dO;
+    dfo.dK = br.dK;
+    dfo.Bp = br.B + br.j * plane;
+    dfo.KBp = br.KB ? br.KB + br.j * kplane : nullptr;
+    hipError_t e = hipSuccess;
+    if (p.N > 0) {
+        if (p.dh_dtype == LRAR_DTYPE_BF16)
+            e = pl.vec > 1
+                    ? launch_bwd_t<float, uint16_t, 4, true, true>(p, pl, dH, dP, dKP, partial, st, dfo)
+                    : launch_bwd_t<float, uint16_t, 1, true, true>(p, pl, dH, dP, dKP, partial, st, dfo);
+        else
+            e = pl.vec > 1
+                    ? launch_bwd_t<float, float, 4, true, true>(p, pl, dH, dP, dKP, partial, st, dfo)
+                    : launch_bwd_t<float, float, 1, true, true>(p, pl, dH, dP, dKP, partial, st, dfo);
+    }
+    if (e == hipSuccess) {
+        const int ncols = (int)p.r;
+        hipLaunchKernelGGL(dq_reduce<false>, dim3(ncols), dim3(256), 0, st, partial, dq,
+                           p.N > 0 ? pl.nblocks : 0, ncols);
+        e = hipGetLastError();
+    }
+    return hip_status(e, "block_route_bwd_deferred launch", err);
+}
+
 int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,
                      void *dKB, float *dq, void *ws, hipStream_t st, std::string *err)
 {

@@ -61,6 +61,7 @@ struct BlockRetire {
     void *dO, *dK;
     int64_t j, N, d, r;
     int mode, dtype;
+    bool grad_rows = false;  // dB / dKB are the slot's gradient rows themselves
 };
 
 hipError_t launch_block_retire(const BlockRetire &br, hipStream_t st);
@@ -87,6 +88,31 @@ int launch_block_merge(const BlockProblem &p, const float *Ms, const float *Ls, 
 // and dKB, dq written, then the retire step above.
 int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,
                      void *dKB, float *dq, void *ws, hipStream_t st, std::string *err);
+
+// The deferred form of the same step (see lr_attnres_block_route_bwd_deferred):
+// only the block in progress (the last slot) accumulates into the rows dP /
+// dKP, the completed slots write their coefficients into coef
+// [n_src - 1][3][N]; then the retire step with dB = dP, dKB = dKP.
+int launch_block_bwd_deferred(const Problem &p, const BlockRetire &br, const void *dH, float *dP,
+                              float *dKP, float *coef, float *dq, void *ws, hipStream_t st,
+                              std::string *err);
+
+// A completed slot's gradient from the sites that read it as completed (see
+// lr_attnres_block_gather_bwd).
+struct BlockGather {
+    const float *Bj, *KBj;  // the slot's summary rows [N][d], key rows [N][r] or NULL
+    const void *dHs;        // [n_sites][N][d] model dtype
+    const float *Q;         // [n_sites][r]
+    const float *coef;      // site u's coefficients at coef + u * site_stride ([3][N])
+    int64_t site_stride, n_sites;
+    float *dP, *dKP;        // [N][d], [N][r] or NULL; overwritten
+    int64_t N, d, r;
+    int mode, dtype;
+    float eps;
+};
+
+int check_gather_supported(const BlockGather &g, std::string *why);
+int launch_block_gather(const BlockGather &g, hipStream_t st, std::string *err);
 
 // Every read site of a pass over one source stack (see
 // lr_attnres_route_all_fwd).

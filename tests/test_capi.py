@@ -44,6 +44,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
                             "lr_attnres_key_proj_fwd", "lr_attnres_route_neff",
+                            "lr_attnres_block_route_bwd_deferred", "lr_attnres_block_gather_bwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -359,3 +360,42 @@ def test_neff_rejects(lib):
     assert neff_call(lib, mode=P) == EINVAL and "K is NULL" in err(lib)
     assert neff_call(lib, mode=F, r=8) == EINVAL
     assert neff_call(lib, S=1025, N=2) == EUNSUPPORTED
+
+
+def dbwd(lib, B=A, KB=None, dP=B_, dKP=None, coef=X, o_new=C, k_new=None, q=E, dH=D, dO=G,
+         dK=None, dq=Y, ws=W, wsb=1 << 30, n_src=3, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_block_route_bwd_deferred(B, KB, dP, dKP, coef, o_new, k_new, q, dH, dO,
+                                                   dK, dq, ws, wsb, n_src, N, d, r, mode, dtype,
+                                                   eps, None)
+
+
+def gath(lib, B=A, KB=None, slot=1, dHs=C, Q=E, coef=X, stride=3 * 8, n_sites=4, dP=B_, dKP=None,
+         N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_block_gather_bwd(B, KB, slot, dHs, Q, coef, stride, n_sites, dP, dKP, N,
+                                           d, r, mode, dtype, eps, None)
+
+
+DEFERRED_INVALID = [
+    (dbwd, "coef NULL with completed slots", dict(coef=None), "coef is NULL"),
+    (dbwd, "dP NULL", dict(dP=None), "dP is NULL"),
+    (dbwd, "dKP outside projected", dict(dKP=Z), "must be NULL"),
+    (dbwd, "coef overlaps dH", dict(coef=D + 64), "overlaps"),
+    (dbwd, "dP overlaps coef", dict(dP=X + 16), "overlap"),
+    (gath, "negative slot", dict(slot=-1), "slot"),
+    (gath, "coef stride too small", dict(stride=8), "coef_site_stride"),
+    (gath, "dP overlaps dHs", dict(dP=C + 16), "overlaps"),
+    (gath, "dHs NULL", dict(dHs=None), "dHs is NULL"),
+    (gath, "KB outside projected", dict(KB=Z), "must be NULL"),
+]
+
+
+@pytest.mark.parametrize("fn,name,kw,msg", DEFERRED_INVALID, ids=[c[1] for c in DEFERRED_INVALID])
+def test_deferred_reverse_pass_rejects(lib, fn, name, kw, msg):
+    assert fn(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_deferred_reverse_pass_unsupported(lib):
+    assert dbwd(lib, d=66) == EUNSUPPORTED
+    assert gath(lib, n_sites=1025, stride=24) == EUNSUPPORTED
+    assert gath(lib, d=4096) == EUNSUPPORTED

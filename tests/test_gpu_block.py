@@ -169,6 +169,67 @@ def test_block_training_pass_matches_oracle(dev, case):
         np.abs(to_host(O)).sum(axis=0)).max()))
 
 
+def drive_deferred_reverse_pass(dev, B, KB, O, KO, Q, dHs, c, mode):
+    """The reverse pass in deferred form: when a slot becomes the block in
+    progress (its last site, in reverse order), its gradient from the sites
+    that read it as completed is gathered; then each site adds its own part
+    and retires its member.  Returns (dO, dK, dq)."""
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    r = Q.shape[1]
+    coef = torch.full((T, nslots, 3, N), float("nan"), dtype=torch.float32, device=dev)
+    dP = torch.empty((N, d), dtype=torch.float32, device=dev)
+    dKP = torch.empty((N, r), dtype=torch.float32, device=dev) if mode == PROJECTED else None
+    dO = torch.empty_like(O)
+    dK = torch.empty_like(KO) if KO is not None else None
+    dq = torch.empty((T, r), dtype=torch.float32, device=dev)
+    cur = None
+    for t in range(T, 0, -1):
+        n_src, _ = site_args(t, c)
+        p = n_src - 1
+        if p != cur:
+            first = p * c + 2 if p >= 1 else 2  # first site reading slot p as completed
+            lr.block_gather_bwd(B, KB, p, dHs, Q, coef, first - 1, mode, out=(dP, dKP))
+            cur = p
+        lr.block_route_bwd_deferred(B, KB, dP, dKP, coef[t - 1, :n_src - 1], O[t - 1],
+                                    KO[t - 1] if KO is not None else None, Q[t - 1], dHs[t - 1],
+                                    n_src, mode,
+                                    out=(dO[t - 1], dK[t - 1] if dK is not None else None,
+                                         dq[t - 1]))
+    torch.cuda.synchronize()
+    return dO, dK, dq
+
+
+@pytest.mark.parametrize("case", TRAIN_CASES, ids=lambda c: f"{'P' if c[0] == 0 else 'S'}-{c[1]}-T{c[2]}-N{c[3]}-d{c[4]}-r{c[5]}-c{c[6]}")
+def test_deferred_training_pass_matches_oracle(dev, case):
+    """The deferred reverse pass (completed-slot gradients gathered once per
+    block) against the oracle's per-site block backward summed over sites:
+    every member gradient and every site's dq."""
+    mode, dtype, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype=dtype, seed=T * 10 + N)
+    rng = np.random.default_rng(N)
+    Qh = (rng.standard_normal((T, r)) / np.sqrt(r)).astype(np.float32)
+    dHh = make_host_problem(PROJECTED, T, N, d, 1, dtype=dtype, seed=T * 10 + N + 1).V
+    O, KO, Q, dHs = to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev), to_dev(dHh, dev)
+    _, B, KB = drive_model_pass(dev, O, KO, Q, c, mode, [T])
+    dO, dK, dq = drive_deferred_reverse_pass(dev, B, KB, O, KO, Q, dHs, c, mode)
+    ref_dO = np.zeros((T, N, d))
+    ref_dK = np.zeros((T, N, r)) if mode == PROJECTED else None
+    for t in range(1, T + 1):
+        gO, gK, gq = oracle.block_route_bwd(p.V, p.K, Qh[t - 1], dHh[t - 1], t, c, mode, r=r)
+        ref_dO[:t] += gO
+        if mode == PROJECTED:
+            ref_dK[:t] += gK
+        check_dq(f"dq at site {t}", dq[t - 1].cpu().numpy(), gq,
+                 tol=1e-5 if dtype == "f32" else 1e-4)
+    check = check_f32 if dtype == "f32" else check_bf16_key_grad
+    check("dO", to_host(dO), ref_dO)
+    if mode == PROJECTED:
+        check("dK", to_host(dK), ref_dK)
+    assert float(B.abs().max()) < 1e-3 * max(1.0, float(torch.from_numpy(
+        np.abs(to_host(O)).sum(axis=0)).max()))
+
+
 @pytest.mark.parametrize("mode,nprev,nq,d,r", [(PROJECTED, 5, 6, 1024, 32), (SLICED, 9, 12, 2048, 64),
                                                (SLICED, 1, 3, 100, 4), (PROJECTED, 70, 9, 256, 7)],
                          ids=["P-5x6-d1024", "S-9x12-d2048", "S-1x3-d100", "P-70x9-d256"])
