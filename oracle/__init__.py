@@ -65,6 +65,9 @@ def _load():
     lib.orc_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, ll, i, i, d, ll,
                                       ll]
     lib.orc_route_all_fwd.restype = ctypes.c_int
+    lib.orc_route_all_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, ll, i, i,
+                                      d, ll, ll]
+    lib.orc_route_all_bwd.restype = ctypes.c_int
     lib.orc_key_projection.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, ll, ll]
     lib.orc_key_projection.restype = ctypes.c_int
     _lib = lib
@@ -261,6 +264,33 @@ def route_all_fwd(V, K, Q, mode, first, r=None, eps=1e-6, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid problem")
     return H, NEFF
+
+
+def route_all_bwd(V, K, Q, dH, mode, first, r=None, eps=1e-6, n0=0, n1=None):
+    """Gradient of route_all_fwd for the loss sum_j sum_n dH[j, n] . h_j[n]:
+    the sum over sites of each site's single-site backward over its prefix.
+    dH is [T, N, d] in the storage of V.  Returns (dV [S, n1-n0, d],
+    dK [S, n1-n0, r] or None, dQ [T, r]), all fp64; dQ sums the token range."""
+    Q = np.ascontiguousarray(np.asarray(Q, dtype=np.float64))
+    if Q.ndim != 2:
+        raise ValueError("oracle: Q must be [T, r]")
+    T = Q.shape[0]
+    V, K, _, S, N, d, r = _prep(V, K, Q[0], mode, r)
+    if first < 1 or first + T - 1 > S:
+        raise ValueError("oracle: sites need 1 <= first and first + T - 1 <= S")
+    dH = np.ascontiguousarray(dH)
+    if dH.dtype != V.dtype or dH.shape != (T, N, d):
+        raise ValueError("oracle: dH must be [T, N, d] in the storage of V")
+    n1 = N if n1 is None else n1
+    dV = np.empty((S, n1 - n0, d), dtype=np.float64)
+    dK = np.empty((S, n1 - n0, r), dtype=np.float64) if mode == PROJECTED else None
+    dQ = np.empty((T, r), dtype=np.float64)
+    rc = _load().orc_route_all_bwd(_ptr(V), _ptr(K), _ptr(Q), _ptr(dH), _ptr(dV), _ptr(dK),
+                                   _ptr(dQ), S, N, d, r, first, T, mode, _STORE[V.dtype],
+                                   float(eps), n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid problem")
+    return dV, dK, dQ
 
 
 def key_projection(A, W, d, n0=0, n1=None):

@@ -594,6 +594,65 @@ int orc_route_all_fwd(const void *V, const void *K, const double *Q, double *H, 
     return failed;
 }
 
+/* Backward of every read site of a pass (the gradient of orc_route_all_fwd;
+ * the paper states no backward).  For the loss
+ *   L = sum_j sum_n dH[j][n] . h_j[n],
+ * site j's routed state h_j depends on the first first+j sources and on its
+ * own query Q[j] only, so dL/dV and dL/dK are the sums over sites of each
+ * site's single-site gradient (orc_route_bwd over that prefix with dH[j]),
+ * and dL/dQ[j] is site j's dq.  Outputs, for tokens n in [n0, n1):
+ *   dV[i][n - n0][:]  for every source i < S (zero for a source no site reads),
+ *   dK[i][n - n0][:]  likewise (projected keys; NULL otherwise),
+ *   dQ[j][:]          summed over the token range.
+ * dH [T][N][d] is in the storage of V. */
+int orc_route_all_bwd(const void *V, const void *K, const double *Q, const void *dH, double *dV,
+                      double *dK, double *dQ, long long S, long long N, long long d, long long r,
+                      long long first, long long T, int mode, int store, double eps, long long n0,
+                      long long n1)
+{
+    struct orc_problem p = {V, K, Q, S, N, d, r, mode, store, eps};
+    if (check_problem(&p, n0, n1) || Q == NULL || V == NULL || dH == NULL || dV == NULL ||
+        dQ == NULL)
+        return 1;
+    if ((mode == ORC_KEYS_PROJECTED) != (dK != NULL))
+        return 1;
+    if (first < 1 || T < 1 || first + T - 1 > S)
+        return 1;
+    const long long nt = n1 - n0;
+    const size_t esize = store == ORC_STORE_F32 ? 4 : store == ORC_STORE_BF16 ? 2 : 8;
+    for (long long e = 0; e < S * nt * d; ++e)
+        dV[e] = 0.0;
+    if (dK)
+        for (long long e = 0; e < S * nt * r; ++e)
+            dK[e] = 0.0;
+    const long long smax = first + T - 1;
+    double *sdV = (double *)malloc(sizeof(double) * (size_t)(smax * nt * d));
+    double *sdK = dK ? (double *)malloc(sizeof(double) * (size_t)(smax * nt * r)) : NULL;
+    if (sdV == NULL || (dK != NULL && sdK == NULL)) {
+        free(sdV);
+        free(sdK);
+        return 1;
+    }
+    int failed = 0;
+    for (long long j = 0; j < T && !failed; ++j) {
+        const long long sj = first + j;
+        const void *dHj = (const char *)dH + (size_t)(j * N * d) * esize;
+        if (orc_route_bwd(V, K, Q + j * r, dHj, sdV, sdK, dQ + j * r, sj, N, d, r, mode, store,
+                          eps, n0, n1)) {
+            failed = 1;
+            break;
+        }
+        for (long long e = 0; e < sj * nt * d; ++e)
+            dV[e] += sdV[e];
+        if (dK)
+            for (long long e = 0; e < sj * nt * r; ++e)
+                dK[e] += sdK[e];
+    }
+    free(sdV);
+    free(sdK);
+    return failed;
+}
+
 /* The projected-key producer (Sec. 3.3, Eq. fused_projection): the output
  * projection of a residual-writing sub-layer and its key projection are one
  * matrix [W^O; W^K] with d + r rows, applied to the activation a_n that
