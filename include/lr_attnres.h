@@ -320,6 +320,35 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
                              int64_t T, int mode, int dtype, float eps, void *stream);
 
 /*
+ * Backward of every read site of a pass (the gradient of
+ * lr_attnres_route_all_fwd; the paper states no backward).  For the loss
+ * L = sum_j sum_n dH[j][n] . h_j[n], with the sites, V, K, Q and the limits
+ * of lr_attnres_route_all_fwd:
+ *   dH [T][N][d] storage `dtype`: row (j, n) is dL/dh_j[n];
+ *   dV [S][N][d] storage `dtype`: dL/dV, the sum over the sites that read
+ *        each source (zero rows for sources no site reads); with sliced keys
+ *        it includes the key path through the last r columns;
+ *   dK [S][N][r] storage `dtype`: dL/dK with projected keys, else NULL;
+ *   dQ [T][r] fp32: row j is dL/dQ[j], summed over the N tokens;
+ *   workspace: lr_attnres_route_all_bwd_workspace_bytes(...) bytes of device
+ *        memory, 4-byte aligned (per-workgroup dQ partials).
+ * accumulate = 0 overwrites dV, dK and dQ; 1 adds the gradients to them.
+ * Each source row, upstream row and dV row is moved once for all sites.
+ * dQ is reduced in a fixed order, so results are bitwise reproducible.
+ * EINVAL as for lr_attnres_route_all_fwd, plus dH, dV 16-byte aligned, dK and
+ * dQ element aligned, a too small workspace, accumulate not 0 or 1, and any
+ * output (or the workspace) overlapping an input or another output.
+ * EUNSUPPORTED: as for lr_attnres_route_all_fwd, and fp32 storage.
+ */
+size_t lr_attnres_route_all_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int64_t r,
+                                                int64_t first, int64_t T, int mode, int dtype);
+int lr_attnres_route_all_bwd(const void *V, const void *K, const float *Q, const void *dH,
+                             void *dV, void *dK, float *dQ, void *workspace,
+                             size_t workspace_bytes, int64_t S, int64_t N, int64_t d, int64_t r,
+                             int64_t first, int64_t T, int mode, int dtype, float eps,
+                             int accumulate, void *stream);
+
+/*
  * Effective number of sources of one read site (Sec. 4.5, Eq.
  * effective_sources): neff[n] = exp(-sum_i alpha_i log alpha_i) of token n's
  * routing weights (Eq. lr_attnres_weight) over the S sources.  Reads the

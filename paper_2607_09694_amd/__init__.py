@@ -68,6 +68,11 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                              i, i, f, vp]
     lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_all_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i64, i, i]
+    lib.lr_attnres_route_all_bwd_workspace_bytes.restype = ctypes.c_size_t
+    lib.lr_attnres_route_all_bwd.argtypes = [vp] * 8 + [ctypes.c_size_t, i64, i64, i64, i64, i64,
+                                                        i64, i, i, f, i, vp]
+    lib.lr_attnres_route_all_bwd.restype = ctypes.c_int
     lib.lr_attnres_block_route_bwd_deferred.argtypes = [vp] * 13 + [ctypes.c_size_t, i64, i64,
                                                                     i64, i64, i, i, f, vp]
     lib.lr_attnres_block_route_bwd_deferred.restype = ctypes.c_int
@@ -199,6 +204,58 @@ def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool 
                                       mode, _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return H, neff
+
+
+def route_all_bwd(V, K, Q, dH, mode, first: int, eps: float = 1e-6, out=None,
+                  workspace=None, accumulate: bool = False):
+    """Gradients of every read site of a pass (the backward of route_all_fwd)
+    for L = sum_j sum(dH[j] * H[j]).
+
+    dH [T,N,d] in V's dtype.  Returns (dV [S,N,d], dK [S,N,r] or None,
+    dQ [T,r] fp32 summed over the tokens); dV includes the key path for
+    sliced keys.  ``out`` may supply (dV, dK, dQ); with ``accumulate`` the
+    gradients are added into them.  ``workspace`` is a uint8 device buffer of
+    at least route_all_bwd_workspace_bytes(...) bytes.
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    if Q.dim() != 2:
+        raise ValueError("Q must be [T, r]")
+    S, N, d, r = _shape(V, K, Q[0], mode)
+    T = Q.shape[0]
+    if dH.dim() != 3 or tuple(dH.shape) != (T, N, d):
+        raise ValueError("dH must be [T, N, d]")
+    if out is not None:
+        dV, dK, dQ = out
+    elif accumulate:
+        raise ValueError("accumulate needs the out=(dV, dK, dQ) buffers to add into")
+    else:
+        dV = torch.empty_like(V)
+        dK = torch.empty_like(K) if mode == PROJECTED else None
+        dQ = torch.empty((T, r), dtype=torch.float32, device=V.device)
+    code = _dtype_code(V)
+    need = lib.lr_attnres_route_all_bwd_workspace_bytes(S, N, d, r, first, T, mode, code)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=V.device)
+    rc = lib.lr_attnres_route_all_bwd(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                      _dev(Q, "Q", torch.float32), _dev(dH, "dH", V.dtype),
+                                      _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
+                                      _dev(dQ, "dQ", torch.float32), _dev(workspace, "workspace"),
+                                      workspace.numel(), S, N, d, r, first, T, mode, code,
+                                      float(eps), int(accumulate), _stream(V))
+    _check(lib, rc)
+    return dV, dK, dQ
+
+
+def route_all_bwd_workspace_bytes(S, N, d, r, first, T, mode, dtype) -> int:
+    """Workspace bytes of route_all_bwd (per-workgroup dQ partials)."""
+    import torch
+
+    code = _BF16 if dtype == torch.bfloat16 else _F32
+    return load_library().lr_attnres_route_all_bwd_workspace_bytes(S, N, d, r, first, T,
+                                                                   _mode(mode), code)
 
 
 def key_proj_fwd(A, W, d: int, out=None):

@@ -448,6 +448,68 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
     return LRAR_OK;
 }
 
+size_t lr_attnres_route_all_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int64_t r,
+                                                int64_t first, int64_t T, int mode, int dtype)
+{
+    int64_t ve, ke, he;
+    const std::string saved = g_last_error;
+    const int rc = check_shape(S, N, d, r, mode, dtype, 0.0f, &ve, &ke, &he);
+    g_last_error = saved;
+    if (rc || first < 1 || T < 1 || first > S || T > S - first + 1)
+        return 0;
+    lrar::AllProblem p{nullptr, nullptr, nullptr, nullptr, nullptr, S, N, d, r, first, T,
+                       mode, dtype, 0.0f};
+    return lrar::all_bwd_workspace_bytes(p);
+}
+
+int lr_attnres_route_all_bwd(const void *V, const void *K, const float *Q, const void *dH,
+                             void *dV, void *dK, float *dQ, void *workspace,
+                             size_t workspace_bytes, int64_t S, int64_t N, int64_t d, int64_t r,
+                             int64_t first, int64_t T, int mode, int dtype, float eps,
+                             int accumulate, void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    if (first < 1 || T < 1 || first > S || T > S - first + 1)
+        return fail(LRAR_EINVAL, "sites need first >= 1, T >= 1 and first + T - 1 <= S");
+    if (accumulate != 0 && accumulate != 1)
+        return fail(LRAR_EINVAL, "accumulate must be 0 or 1");
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(Q, "Q", 4, true)) ||
+        (rc = check_ptr(dH, "dH", 16, data)) || (rc = check_ptr(dV, "dV", 16, data)) ||
+        (rc = check_ptr(dQ, "dQ", 4, true)) || (rc = check_ptr(K, "K", es, data && proj)) ||
+        (rc = check_ptr(dK, "dK", es, data && proj)) ||
+        (rc = check_ptr(workspace, "workspace", 4, false)))
+        return rc;
+    if (!proj && (K || dK))
+        return fail(LRAR_EINVAL, "K and dK must be NULL unless keys are projected");
+    int64_t tq, th;
+    if (!mul_ok(T, r, &tq) || !mul_ok(T, he, &th) || !mul_ok(th, es, &th))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    lrar::AllProblem p{V, K, Q, nullptr, nullptr, S, N, d, r, first, T, mode, dtype, eps};
+    std::string why;
+    if ((rc = lrar::check_all_bwd_supported(p, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::all_bwd_workspace_bytes(p);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const Span outs[] = {span("dV", dV, ve * es), span("dK", dK, ke * es),
+                         span("dQ", dQ, tq * 4), span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("Q", Q, tq * 4),
+                        span("dH", dH, th)};
+    if ((rc = check_aliasing(outs, 4, ins, 4)))
+        return rc;
+    if ((rc = lrar::launch_all_bwd(p, dH, dV, dK, dQ, workspace, accumulate == 1,
+                                   static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int64_t N,
                             int64_t m, int64_t d, int64_t r, int dtype, void *stream)
 {

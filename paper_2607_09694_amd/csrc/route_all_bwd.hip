@@ -1,0 +1,519 @@
+// Backward of every read site of a pass over one source stack (the gradient
+// of the all-sites forward; the paper states no backward).  Site j reads the
+// first first+j sources (Sec. 3.1, Eq. full_attnres_source_set) with the
+// low-rank keys of Sec. 3.2-3.4.  For the loss L = sum_j sum_n dH_j . h_j,
+// per token n, with G[j][i] = dH_j . o_i (the value dots of every site
+// against every source):
+//     ds[j][i] = alpha[j][i] (G[j][i] - sum_l alpha[j][l] G[j][l]),
+//     dV_i     = sum_j alpha[j][i] dH_j                 (+ key path, S-LR),
+//     dk_i     = (1 / rho_i) (u_i - kbar_i (kbar_i . u_i) / r),
+//                u_i = sum_j ds[j][i] Q_j,
+//     dQ_j     = sum_n sum_i ds[j][i] kbar_i.
+// (The RMSNorm term kbar_i s_{j,i} / r of each site's key gradient sums to
+// kbar_i (kbar_i . u_i) / r, because s_{j,i} = Q_j . kbar_i.)  The stack and
+// the upstream gradients are each read once and dV is written once, instead
+// of once per site: sum_j (first + j) rows each of V, dV in and dV out.
+//
+// Per token, on the matrix cores:
+//     G  = dH_n [T x d] * O_n^T [d x S]      (v_mfma_f32_16x16x32_bf16, exact
+//                                            products of bf16 operands),
+//     dV = alpha^T [S x T] * dH_n [T x d]    (alpha as hi + lo bf16, two MFMAs,
+//                                            as in the forward),
+//     u  = ds^T [S x T] * Q [T x r] and dQ += (ds / rho) [T x S] * K [S x r]
+//                                           (v_mfma_f32_16x16x4_f32).
+// Workgroups (4 waves) are persistent over a stride of tokens and keep their
+// share of dQ in registers; a fixed-order reduction adds the per-workgroup
+// partials, so dQ is bitwise reproducible.  Wave w owns sources 16 w ..
+// 16 w + 15.  The row is processed in 128-column slabs: the workgroup
+// stages the T upstream rows of a slab in LDS (16-byte chunks XOR-swizzled
+// by row, conflict-free in both read patterns below), each wave loads its 16
+// source rows of the slab into registers, then
+//   - G: A = dH rows from LDS (lane: one site, 8 columns), B = the source
+//     rows (lane: one source, the same 8 columns);
+//   - dV: A = alpha^T (lane: one source, 8 sites), B = dH read from LDS as 8
+//     site rows x 8 consecutive columns per lane and transposed in registers,
+//     so that the p-th MFMA's column index stands for column c0 + p; the
+//     result is 8 consecutive columns of 4 sources per lane, stored as
+//     16-byte rows.
+// The next slab (or the next token's first slab) is loaded while the current
+// one is multiplied.  With sliced keys the key gradient lands in the last r
+// columns of dV, which needs the whole of G first: the slabs that hold those
+// columns (at most the last two, still in the two LDS buffers when the row
+// ends) are multiplied again after the key gradient is known.
+#include "route_all_weights.h"
+
+namespace lrar {
+
+namespace {
+
+constexpr int kAllBwdGrid = 512;                       // persistent workgroups
+constexpr int kDhRowBytes = kAllSlab * 2;              // one slab row of dH, bf16
+constexpr int kDhBufBytes = kAllMaxSources * kDhRowBytes;
+
+struct AllBwdArgs {
+    AllArgs f;           // V, keys, Q, sizes (H and neff unused)
+    const uint16_t *dH;  // [T][N][d]
+    uint16_t *dV;        // [S][N][d]
+    uint16_t *dK;        // [S][N][r] (projected keys) or NULL
+    float *partial;      // [gridDim.x][T][r]
+    int s_tail;          // first slab whose dV waits for the key gradient (nslab: none)
+};
+
+// LDS byte offset of 16-byte chunk c (0..15) of slab row `row`: rows are
+// 256 bytes and the chunk index is XOR-swizzled with row mod 16, so both 16
+// rows at one logical chunk and one row's 16 chunks fall on distinct banks.
+__device__ __forceinline__ int dh_chunk(int row, int c) { return row * kDhRowBytes + 16 * (c ^ (row & 15)); }
+
+__device__ __forceinline__ float bf16_at(const uint16_t *p) { return __uint_as_float((unsigned)*p << 16); }
+
+// Keep x opaque to the optimiser for one token: the per-token control flow
+// (masks of sites, sources and columns, row offsets) is then formed inside
+// the token loop instead of being hoisted out of it and held in registers
+// for the workgroup's lifetime.
+template <typename T>
+__device__ __forceinline__ void per_token(T &x)
+{
+    asm volatile("" : "+s"(x));
+}
+
+template <int MT, int RT, bool ACC>
+__global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(AllBwdArgs b)
+{
+    constexpr int KG = (MT + 1) / 2;      // groups of 32 sites in the dV contraction
+    constexpr int RP = RT <= 2 ? 32 : 64; // key elements covered by the score MFMAs
+    __shared__ __align__(16) float alpha[kAllMaxSources * kAlphaRow];
+    __shared__ __align__(16) unsigned char dhbuf[2 * kDhBufBytes];
+    __shared__ __align__(16) uint16_t keys[kAllMaxSources * kKeyRow];
+    __shared__ float rho[kAllMaxSources];
+    __shared__ float gpart[kWaves * kAllMaxSources];
+    __shared__ float qs[kAllMaxSources * kAllMaxRank];  // Q [T][r], for the key gradient
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWaveSize, wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
+    const int lc = lane & 15, ks = lane >> 4;
+    const int src = 16 * wave + lc;  // this lane's source as a G operand
+    const int hch = tid & 15, hr0 = tid >> 4;
+
+    // Rows 16 MT .. 32 KG - 1 of the dH buffers enter the last site group's
+    // dV MFMAs with weight 0 but are never loaded: zero them once.
+    constexpr int kPadChunks = (32 * KG - 16 * MT) * 16;
+    if constexpr (kPadChunks > 0) {
+        for (int f = tid; f < 2 * kPadChunks; f += kBlock) {
+            const int g = f % kPadChunks;
+            *reinterpret_cast<u32x4_t *>(dhbuf + (f / kPadChunks) * kDhBufBytes +
+                                         dh_chunk(16 * MT + g / 16, g % 16)) =
+                u32x4_t{0u, 0u, 0u, 0u};
+        }
+    }
+    for (int f = tid; f < b.f.T * b.f.r; f += kBlock)
+        qs[f] = b.f.Q[f];
+
+    f32x4_t dq[RT];
+#pragma unroll
+    for (int ct = 0; ct < RT; ++ct)
+        dq[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int64_t n = blockIdx.x; n < b.f.N; n += gridDim.x) {
+        AllArgs a = b.f;
+        per_token(a.S);
+        per_token(a.T);
+        per_token(a.first);
+        per_token(a.r);
+        per_token(a.d);
+        per_token(a.krow);
+        per_token(a.koff);
+        per_token(a.N);
+        const size_t plane = (size_t)a.N * a.d;
+        const int nslab = (a.d + kAllSlab - 1) / kAllSlab;
+        const uint16_t *V = static_cast<const uint16_t *>(a.V);
+
+        // Slab loads: thread t brings chunk t mod 16 of dH rows t / 16 + 16 q
+        // (q < MT), and lane (lc, ks) the 4 chunks 4 u + ks of its source
+        // row.  Lanes past the rows or columns load a valid address (the
+        // token's first chunk) and keep zeros, so no load sits behind a branch.
+        u32x4_t hraw[MT], vraw[4];
+        auto load_dh = [&](int s) {
+            const int col = s * kAllSlab + 8 * hch;
+            const uint16_t *hbase = b.dH + n * a.d;
+#pragma unroll
+            for (int q = 0; q < MT; ++q) {
+                const int row = hr0 + 16 * q;
+                const bool ok = row < a.T && col < a.d;
+                const u32x4_t x =
+                    load_stream<uint16_t, 8, kNtLoad>(ok ? hbase + row * plane + col : hbase);
+                hraw[q] = ok ? x : u32x4_t{0u, 0u, 0u, 0u};
+            }
+        };
+        auto load_v = [&](int s) {
+            const uint16_t *vbase = V + n * a.d;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int c = s * kAllSlab + 32 * u + 8 * ks;
+                const bool ok = src < a.S && c < a.d;
+                const u32x4_t x =
+                    load_stream<uint16_t, 8, kNtLoad>(ok ? vbase + src * plane + c : vbase);
+                vraw[u] = ok ? x : u32x4_t{0u, 0u, 0u, 0u};
+            }
+        };
+        load_dh(0);
+        load_v(0);
+
+        __syncthreads();  // the previous token's LDS reads are done
+        all_site_weights<uint16_t, RP, true>(a, n, alpha, rho, keys);
+
+        // alpha^T operands of this wave's sources: lane (lc, ks) holds
+        // alpha[32 kg + 8 ks + e][src] as hi + lo bf16.
+        bf16x8_t Ahi[KG], Alo[KG];
+#pragma unroll
+        for (int kg = 0; kg < KG; ++kg) {
+            float av[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                av[e] = alpha[(32 * kg + 8 * ks + e) * kAlphaRow + src];
+            u32x4_t hi, lo;
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                const unsigned hw = pack_bf16x2(av[2 * h], av[2 * h + 1]);
+                hi[h] = hw;
+                lo[h] = pack_bf16x2(av[2 * h] - bf16_lo(hw), av[2 * h + 1] - bf16_hi(hw));
+            }
+            Ahi[kg] = __builtin_bit_cast(bf16x8_t, hi);
+            Alo[kg] = __builtin_bit_cast(bf16x8_t, lo);
+        }
+
+        // dV of one slab for this wave's sources (no key path): acc[p] holds
+        // sources 16 wave + 4 ks + e (e = 0..3) at column c0 + p, c0 = 128 s + 8 lc.
+        auto slab_dv = [&](const unsigned char *buf, f32x4_t(&acc)[8]) {
+#pragma unroll
+            for (int p = 0; p < 8; ++p)
+                acc[p] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kg = 0; kg < KG; ++kg) {
+                u32x4_t w[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    w[e] = *reinterpret_cast<const u32x4_t *>(buf +
+                                                              dh_chunk(32 * kg + 8 * ks + e, lc));
+#pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    u32x4_t bq;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h)
+                        bq[h] = (p & 1) ? hi_pair(w[2 * h][p / 2], w[2 * h + 1][p / 2])
+                                        : lo_pair(w[2 * h][p / 2], w[2 * h + 1][p / 2]);
+                    const bf16x8_t B = __builtin_bit_cast(bf16x8_t, bq);
+                    acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ahi[kg], B, acc[p], 0, 0, 0);
+                    acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Alo[kg], B, acc[p], 0, 0, 0);
+                }
+            }
+        };
+
+        // Round and store one slab of dV (adding the stored value when
+        // accumulating); tail[local source][c - (d - r)] is added at the
+        // columns c >= d - r.
+        auto store_dv = [&](int s, const f32x4_t(&acc)[8], const float *tail) {
+            const int c0 = s * kAllSlab + 8 * lc;
+            if (c0 >= a.d)
+                return;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                __builtin_amdgcn_sched_barrier(0);
+                const int i = 16 * wave + 4 * ks + e;
+                if (i >= a.S)
+                    continue;
+                float v[8];
+#pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    v[p] = acc[p][e];
+                    const int c = c0 + p - (a.d - a.r);
+                    if (tail && c >= 0)
+                        v[p] += tail[(4 * ks + e) * kAlphaRow + c];
+                }
+                uint16_t *dst = b.dV + i * plane + n * a.d + c0;
+                if (ACC) {
+                    float old[8];
+                    widen(load_raw<uint16_t, 8>(dst), old);
+#pragma unroll
+                    for (int p = 0; p < 8; ++p)
+                        v[p] += old[p];
+                }
+                u32x4_t o;
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    o[h] = pack_bf16x2(v[2 * h], v[2 * h + 1]);
+                store_stream<uint16_t, 8, kNtStore>(dst, o);
+            }
+        };
+
+        f32x4_t G[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            G[mt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int s = 0; s < nslab; ++s) {
+            unsigned char *buf = dhbuf + (s & 1) * kDhBufBytes;
+#pragma unroll
+            for (int q = 0; q < MT; ++q)
+                *reinterpret_cast<u32x4_t *>(buf + dh_chunk(hr0 + 16 * q, hch)) = hraw[q];
+            if (s + 1 < nslab)
+                load_dh(s + 1);
+            __syncthreads();
+            // G[16 mt + 4 ks + e][src] over this slab's columns; then the
+            // source rows of the next slab are loaded into the same registers.
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const bf16x8_t A = *reinterpret_cast<const bf16x8_t *>(
+                        buf + dh_chunk(16 * mt + lc, 4 * u + ks));
+                    G[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        A, __builtin_bit_cast(bf16x8_t, vraw[u]), G[mt], 0, 0, 0);
+                }
+            if (s + 1 < nslab)
+                load_v(s + 1);
+            if (s < b.s_tail) {
+                f32x4_t acc[8];
+                slab_dv(buf, acc);
+                store_dv(s, acc, nullptr);
+            }
+        }
+
+        // Softmax gradient.  Lane (lc, ks) holds G[site 16 mt + 4 ks + e][src].
+        float av[MT][4], ds[MT][4];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int site = 16 * mt + 4 * ks + e;
+                av[mt][e] = alpha[site * kAlphaRow + src];
+                float t = av[mt][e] * G[mt][e];
+                for (int o = 1; o < 16; o <<= 1)
+                    t += __shfl_xor(t, o, kWaveSize);
+                if (lc == 0)
+                    gpart[wave * kAllMaxSources + site] = t;
+            }
+        __syncthreads();
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int site = 16 * mt + 4 * ks + e;
+                float gbar = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kWaves; ++w)
+                    gbar += gpart[w * kAllMaxSources + site];
+                ds[mt][e] = av[mt][e] * (G[mt][e] - gbar);
+            }
+
+        // u_i = sum_j ds[j][i] Q_j: the MFMA's k index ks at step (mt, e)
+        // stands for site 16 mt + 4 ks + e, on both operands.
+        f32x4_t uk[RT];
+#pragma unroll
+        for (int ct = 0; ct < RT; ++ct) {
+            __builtin_amdgcn_sched_barrier(0);
+            uk[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+            const int c = 16 * ct + lc;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int site = 16 * mt + 4 * ks + e;
+                    const float qv = (site < a.T && c < a.r) ? qs[site * a.r + c] : 0.0f;
+                    uk[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(ds[mt][e], qv, uk[ct], 0, 0, 0);
+                }
+        }
+        // dk_i = (u_i - k_i (k_i . u_i) / (rho_i^2 r)) / rho_i; lane (lc, ks)
+        // holds sources 16 wave + 4 ks + e at key column 16 ct + lc.
+        float dk[RT][4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int i = 16 * wave + 4 * ks + e;
+            float kv[RT], dot = 0.0f;
+#pragma unroll
+            for (int ct = 0; ct < RT; ++ct) {
+                const int c = 16 * ct + lc;
+                kv[ct] = c < a.r ? bf16_at(keys + i * kKeyRow + c) : 0.0f;
+                dot = fmaf(kv[ct], uk[ct][e], dot);
+            }
+            for (int o = 1; o < 16; o <<= 1)
+                dot += __shfl_xor(dot, o, kWaveSize);
+            const float inv = i < a.S ? 1.0f / rho[i] : 0.0f;
+            const float scale = dot * inv * inv / (float)a.r;
+#pragma unroll
+            for (int ct = 0; ct < RT; ++ct)
+                dk[ct][e] = (uk[ct][e] - kv[ct] * scale) * inv;
+        }
+        if (b.dK) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int i = 16 * wave + 4 * ks + e;
+#pragma unroll
+                for (int ct = 0; ct < RT; ++ct) {
+                    const int c = 16 * ct + lc;
+                    if (i < a.S && c < a.r) {
+                        uint16_t *dst = b.dK + (i * (size_t)a.N + n) * a.r + c;
+                        float v = dk[ct][e];
+                        if (ACC)
+                            v += bf16_at(dst);
+                        *dst = (uint16_t)pack_bf16x2(v, 0.0f);
+                    }
+                }
+            }
+        }
+
+        // dQ_j += sum_i (ds[j][i] / rho_i) k_i: ds / rho replaces alpha in
+        // LDS, then wave w takes the sites of tile w.
+        __syncthreads();
+        {
+            const float inv = src < a.S ? 1.0f / rho[src] : 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    alpha[(16 * mt + 4 * ks + e) * kAlphaRow + src] = ds[mt][e] * inv;
+        }
+        __syncthreads();
+        if (wave < MT) {
+            const int nst = (a.S + 3) / 4;
+#pragma unroll
+            for (int ct = 0; ct < RT; ++ct) {
+                const int c = 16 * ct + lc;
+#pragma unroll 1
+                for (int st = 0; st < nst; ++st) {
+                    const int i = 4 * st + ks;
+                    const float A = alpha[(16 * wave + lc) * kAlphaRow + i];
+                    const float B = (i < a.S && c < a.r) ? bf16_at(keys + i * kKeyRow + c) : 0.0f;
+                    dq[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(A, B, dq[ct], 0, 0, 0);
+                }
+            }
+        }
+
+        // Sliced keys: the slabs holding the last r columns, with dk added.
+        if (b.s_tail < nslab) {
+            __syncthreads();
+            float *dkb = alpha + wave * 16 * kAlphaRow;  // [16 sources][r], this wave's
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int ct = 0; ct < RT; ++ct) {
+                    const int c = 16 * ct + lc;
+                    if (c < a.r)
+                        dkb[(4 * ks + e) * kAlphaRow + c] = dk[ct][e];
+                }
+            wave_lds_sync();
+#pragma unroll 1
+            for (int s = b.s_tail; s < nslab; ++s) {
+                f32x4_t acc[8];
+                slab_dv(dhbuf + (s & 1) * kDhBufBytes, acc);
+                store_dv(s, acc, dkb);
+            }
+        }
+    }
+
+    if (wave < MT) {
+        float *part = b.partial + (size_t)blockIdx.x * b.f.T * b.f.r;
+#pragma unroll
+        for (int ct = 0; ct < RT; ++ct)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int site = 16 * wave + 4 * ks + e, c = 16 * ct + lc;
+                if (site < b.f.T && c < b.f.r)
+                    part[site * b.f.r + c] = dq[ct][e];
+            }
+    }
+}
+
+template <int MT, int RT, bool ACC>
+void launch_all_bwd_t(const AllBwdArgs &b, unsigned grid, hipStream_t st)
+{
+    hipLaunchKernelGGL((route_all_bwd_bf16<MT, RT, ACC>), dim3(grid), dim3(kBlock), 0, st, b);
+}
+
+template <int MT, bool ACC>
+void launch_all_bwd_mt(const AllBwdArgs &b, unsigned grid, hipStream_t st)
+{
+    switch ((b.f.r + 15) / 16) {
+    case 1: launch_all_bwd_t<MT, 1, ACC>(b, grid, st); break;
+    case 2: launch_all_bwd_t<MT, 2, ACC>(b, grid, st); break;
+    case 3: launch_all_bwd_t<MT, 3, ACC>(b, grid, st); break;
+    default: launch_all_bwd_t<MT, 4, ACC>(b, grid, st); break;
+    }
+}
+
+template <bool ACC>
+void launch_all_bwd_acc(const AllBwdArgs &b, unsigned grid, hipStream_t st)
+{
+    switch ((b.f.T + 15) / 16) {
+    case 1: launch_all_bwd_mt<1, ACC>(b, grid, st); break;
+    case 2: launch_all_bwd_mt<2, ACC>(b, grid, st); break;
+    case 3: launch_all_bwd_mt<3, ACC>(b, grid, st); break;
+    default: launch_all_bwd_mt<4, ACC>(b, grid, st); break;
+    }
+}
+
+}  // namespace
+
+int64_t all_bwd_workgroups(int64_t N) { return N < kAllBwdGrid ? N : kAllBwdGrid; }
+
+size_t all_bwd_workspace_bytes(const AllProblem &p)
+{
+    return (size_t)all_bwd_workgroups(p.N) * (size_t)p.T * (size_t)p.r * sizeof(float);
+}
+
+int check_all_bwd_supported(const AllProblem &p, std::string *why)
+{
+    int rc = check_all_supported(p, why);
+    if (rc)
+        return rc;
+    if (p.dtype != LRAR_DTYPE_BF16) {
+        *why = "the all-sites backward takes bf16 storage";
+        return LRAR_EUNSUPPORTED;
+    }
+    return LRAR_OK;
+}
+
+int launch_all_bwd(const AllProblem &p, const void *dH, void *dV, void *dK, float *dQ, void *ws,
+                   bool accumulate, hipStream_t st, std::string *err)
+{
+    const unsigned grid = (unsigned)all_bwd_workgroups(p.N);
+    float *partial = static_cast<float *>(ws);
+    if (grid > 0) {
+        AllBwdArgs b;
+        b.f.V = p.V;
+        b.f.keys = p.mode == LRAR_MODE_PROJECTED ? p.K : p.V;
+        b.f.Q = p.Q;
+        b.f.H = nullptr;
+        b.f.neff = nullptr;
+        b.f.S = (int)p.S;
+        b.f.d = (int)p.d;
+        b.f.r = (int)p.r;
+        b.f.krow = p.mode == LRAR_MODE_PROJECTED ? (int)p.r : (int)p.d;
+        b.f.koff = p.mode == LRAR_MODE_PROJECTED ? 0 : (int)(p.d - p.r);
+        b.f.first = (int)p.first;
+        b.f.T = (int)p.T;
+        b.f.N = p.N;
+        b.f.eps = p.eps;
+        b.f.kvec = b.f.r % 8 == 0 && b.f.koff % 8 == 0 && b.f.krow % 8 == 0 &&
+                   reinterpret_cast<uintptr_t>(b.f.keys) % 16 == 0;
+        b.dH = static_cast<const uint16_t *>(dH);
+        b.dV = static_cast<uint16_t *>(dV);
+        b.dK = static_cast<uint16_t *>(dK);
+        b.partial = partial;
+        const int nslab = (int)((p.d + kAllSlab - 1) / kAllSlab);
+        b.s_tail = p.mode == LRAR_MODE_SLICED ? (int)((p.d - p.r) / kAllSlab) : nslab;
+        if (nslab - b.s_tail > 2) {  // r <= 64 < 128 keeps the key columns in two slabs
+            *err = "route_all_bwd: key columns span more than the two buffered slabs";
+            return LRAR_EUNSUPPORTED;
+        }
+        if (accumulate)
+            launch_all_bwd_acc<true>(b, grid, st);
+        else
+            launch_all_bwd_acc<false>(b, grid, st);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return hip_status(e, "route_all_bwd", err);
+    }
+    return hip_status(launch_dq_reduce(partial, dQ, (int)grid, (int)(p.T * p.r), accumulate, st),
+                      "route_all_bwd dq reduction", err);
+}
+
+}  // namespace lrar

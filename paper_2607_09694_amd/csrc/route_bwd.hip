@@ -493,6 +493,18 @@ dq_reduce(const float *__restrict__ partial, float *__restrict__ dq, int nblocks
         dq[j] = ACC ? dq[j] + red[0] : red[0];
 }
 
+hipError_t launch_dq_reduce(const float *partial, float *dq, int nblocks, int ncols,
+                            bool accumulate, hipStream_t st)
+{
+    if (accumulate)
+        hipLaunchKernelGGL(dq_reduce<true>, dim3(ncols), dim3(256), 0, st, partial, dq, nblocks,
+                           ncols);
+    else
+        hipLaunchKernelGGL(dq_reduce<false>, dim3(ncols), dim3(256), 0, st, partial, dq, nblocks,
+                           ncols);
+    return hipGetLastError();
+}
+
 namespace {
 
 // Key-pass vector width and lanes per source of the projected / sliced

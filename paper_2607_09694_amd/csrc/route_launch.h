@@ -129,6 +129,18 @@ struct AllProblem {
 
 int check_all_supported(const AllProblem &p, std::string *why);
 
+// Backward of every read site (see lr_attnres_route_all_bwd): dV [S][N][d],
+// dK [S][N][r] (projected keys) or NULL, dQ [T][r]; overwritten, or added
+// to when accumulating.  ws holds all_bwd_workspace_bytes(p) bytes.
+size_t all_bwd_workspace_bytes(const AllProblem &p);
+int check_all_bwd_supported(const AllProblem &p, std::string *why);
+int launch_all_bwd(const AllProblem &p, const void *dH, void *dV, void *dK, float *dQ, void *ws,
+                   bool accumulate, hipStream_t st, std::string *err);
+
+// dq[j] (+)= sum_b partial[b][j] for j < ncols, in a fixed order.
+hipError_t launch_dq_reduce(const float *partial, float *dq, int nblocks, int ncols,
+                            bool accumulate, hipStream_t st);
+
 // Effective number of sources of one site (see lr_attnres_route_neff); full
 // rank is passed as sliced keys with r = d.
 int launch_neff(const Problem &p, float *neff, hipStream_t st, std::string *err);

@@ -45,6 +45,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
                             "lr_attnres_key_proj_fwd", "lr_attnres_route_neff",
                             "lr_attnres_block_route_bwd_deferred", "lr_attnres_block_gather_bwd",
+                            "lr_attnres_route_all_bwd", "lr_attnres_route_all_bwd_workspace_bytes",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -313,6 +314,61 @@ def test_all_sites_unsupported(lib):
     assert allf(lib, S=70, first=1, T=65) == EUNSUPPORTED
     assert allf(lib, mode=P, K=E, r=65, d=128) == EUNSUPPORTED
     assert allf(lib, d=68) == EUNSUPPORTED
+
+
+def allb_ws(lib, S=6, N=8, d=64, r=8, first=2, T=5, mode=SL, dtype=BF16):
+    return lib.lr_attnres_route_all_bwd_workspace_bytes(S, N, d, r, first, T, mode, dtype)
+
+
+def allb(lib, V=A, K=None, Q=B, dH=C, dV=D, dK=None, dQ=E, ws=G, ws_bytes=1 << 20, S=6, N=8,
+         d=64, r=8, first=2, T=5, mode=SL, dtype=BF16, eps=1e-6, acc=0):
+    return lib.lr_attnres_route_all_bwd(V, K, Q, dH, dV, dK, dQ, ws, ws_bytes, S, N, d, r, first,
+                                        T, mode, dtype, eps, acc, None)
+
+
+def test_all_sites_backward_workspace(lib):
+    # one fp32 partial row of T x r per workgroup, at most 512 workgroups
+    assert allb_ws(lib) == 8 * 5 * 8 * 4
+    assert allb_ws(lib, N=100000, S=49, first=1, T=48, r=16, d=1024) == 512 * 48 * 16 * 4
+    assert allb_ws(lib, N=0) == 0
+    assert allb_ws(lib, first=0) == 0
+    assert allb_ws(lib, first=2, T=6) == 0
+
+
+ALLB_INVALID = [
+    ("first 0", dict(first=0), "first >= 1"),
+    ("sites past the stack", dict(T=6), "first + T - 1 <= S"),
+    ("accumulate 2", dict(acc=2), "accumulate"),
+    ("dH NULL", dict(dH=None), "dH is NULL"),
+    ("dV NULL", dict(dV=None), "dV is NULL"),
+    ("dQ NULL", dict(dQ=None), "dQ is NULL"),
+    ("dK NULL when projected", dict(mode=P, K=W), "dK is NULL"),
+    ("dK outside projected", dict(dK=W), "must be NULL"),
+    ("dV misaligned", dict(dV=D + 8), "16-byte aligned"),
+    ("dH misaligned", dict(dH=C + 4), "16-byte aligned"),
+    ("dQ misaligned", dict(dQ=E + 2), "4-byte aligned"),
+    ("workspace NULL", dict(ws=None), "workspace too small"),
+    ("workspace too small", dict(ws_bytes=16), "workspace too small"),
+    ("dV overlaps V", dict(dV=A + 256), "overlaps"),
+    ("dQ overlaps dH", dict(dQ=C + 64), "overlaps"),
+    ("workspace overlaps dV", dict(ws=D + 1024), "overlap"),
+    ("negative eps", dict(eps=-1.0), "eps"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", ALLB_INVALID, ids=[c[0] for c in ALLB_INVALID])
+def test_all_sites_backward_rejects(lib, name, kw, msg):
+    assert allb(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_all_sites_backward_unsupported(lib):
+    assert allb(lib, mode=F, r=64) == EUNSUPPORTED
+    assert allb(lib, dtype=F32) == EUNSUPPORTED
+    assert "bf16" in err(lib)
+    assert allb(lib, S=65, T=3) == EUNSUPPORTED
+    assert allb(lib, mode=P, K=W, dK=W + 0x1_0000_0000, r=65, d=128) == EUNSUPPORTED
+    assert allb(lib, d=68) == EUNSUPPORTED
 
 
 def kproj(lib, A_=A, W=B, O=C, K=D, N=8, m=64, d=32, r=16, dtype=BF16):

@@ -1,0 +1,213 @@
+"""GPU parity of the all-sites backward (the gradient of every read site of
+a pass over one source stack, in one call) through the C ABI, against the
+fp64 oracle.
+
+Small cases cover both low-rank key modes, one to four 16-site tiles (one
+and two 32-site groups in the dV contraction), one to four 16-column key
+tiles, ragged column slabs, a sliced-key tail that straddles two slabs, key
+lengths that are not a multiple of 8, a single site, many tokens per
+workgroup, accumulation and bitwise reruns.  The full-size cases run the
+paper's model pass (49 sources, 48 sites reading 2..49 of them, d = 1024,
+N = 16384) and compare sampled tokens; their dQ is checked against the sum
+of the single-site backward over every site.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_bits_from_f32,
+                                         bf16_tensor_to_bits, f32_from_bf16_bits,
+                                         make_host_problem)
+from parity import check_bf16_grown, check_bf16_key_grad, check_dq
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+
+def to_host(t):
+    if t.dtype == torch.bfloat16:
+        return f32_from_bf16_bits(bf16_tensor_to_bits(t)).astype(np.float64)
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def _queries(T, r, seed, scale=2.0):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((T, r)) * scale / np.sqrt(r)).astype(np.float32)
+
+
+def _upstream(T, N, d, seed):
+    rng = np.random.default_rng(seed)
+    return bf16_bits_from_f32(rng.standard_normal((T, N, d)).astype(np.float32))
+
+
+def _problem(mode, S, T, first, N, d, r, seed):
+    p = make_host_problem(mode, S, N, d, r, dtype="bf16", seed=seed)
+    return p, _queries(T, r, seed + 1), _upstream(T, N, d, seed + 2)
+
+
+def _check(name_prefix, mode, got, ref):
+    """dV is a sum over every site that reads a source, so it grows past
+    |x| = 8, where the bf16 half-ulp alone exceeds 2e-2: the bar for grown
+    sums.  With sliced keys its last r columns carry the key gradient and
+    take the key-gradient bar, as dK does."""
+    dV, dK, dQ = got
+    rV, rK, rQ = ref
+    gV = to_host(dV)
+    if mode == SLICED:
+        r = rQ.shape[1]
+        check_bf16_grown(name_prefix + "dV", gV[..., :-r], rV[..., :-r])
+        check_bf16_key_grad(name_prefix + "dV key columns", gV[..., -r:], rV[..., -r:])
+    else:
+        check_bf16_grown(name_prefix + "dV", gV, rV)
+    if mode == PROJECTED:
+        check_bf16_key_grad(name_prefix + "dK", to_host(dK), rK)
+    else:
+        assert dK is None
+    check_dq(name_prefix + "dQ", to_host(dQ), rQ)
+
+
+# (mode, S, T, first, N, d, r)
+CASES = [
+    (PROJECTED, 9, 8, 1, 37, 256, 16),      # one site tile, one key tile, two slabs
+    (SLICED, 20, 19, 2, 33, 200, 24),       # ragged slab; tail inside the last slab
+    (SLICED, 12, 10, 3, 21, 136, 16),       # tail straddles the two slabs
+    (PROJECTED, 49, 48, 1, 70, 1024, 16),   # the paper's sites: 3 tiles, 2 site groups
+    (SLICED, 49, 48, 2, 40, 1024, 64),      # S-LR r = 64: 4 key tiles
+    (PROJECTED, 64, 64, 1, 20, 64, 64),     # every limit: 4 site tiles, half a slab
+    (PROJECTED, 10, 8, 3, 17, 96, 12),      # r % 8 != 0: keys read element by element
+    (SLICED, 33, 30, 4, 26, 520, 32),       # group boundary, ragged slab, 2 key tiles
+    (PROJECTED, 5, 1, 5, 9, 128, 8),        # a single site reading every source
+    (SLICED, 12, 11, 1, 1100, 128, 16),     # several tokens per workgroup
+]
+
+
+def _ids(c):
+    return "{}-S{}-T{}-f{}-N{}-d{}-r{}".format("P" if c[0] == PROJECTED else "S", *c[1:])
+
+
+@pytest.mark.parametrize("case", CASES, ids=_ids)
+def test_all_sites_backward_matches_oracle(dev, case):
+    mode, S, T, first, N, d, r = case
+    p, Q, dH = _problem(mode, S, T, first, N, d, r, seed=S + T + N)
+    got = lr.route_all_bwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev), to_dev(dH, dev),
+                           mode, first)
+    torch.cuda.synchronize()
+    ref = oracle.route_all_bwd(p.V, p.K, Q.astype(np.float64), dH, mode, first, r=r)
+    _check("", mode, got, ref)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_all_sites_backward_accumulates(dev, mode):
+    """accumulate: the gradients are added to what dV, dK and dQ hold."""
+    S, T, first, N, d, r = 14, 12, 2, 45, 264, 16
+    p, Q, dH = _problem(mode, S, T, first, N, d, r, seed=31)
+    V, K = to_dev(p.V, dev), to_dev(p.K, dev)
+    rng = np.random.default_rng(32)
+    dV0 = bf16_bits_from_f32(rng.standard_normal((S, N, d)).astype(np.float32))
+    dK0 = bf16_bits_from_f32(rng.standard_normal((S, N, r)).astype(np.float32))
+    dQ0 = rng.standard_normal((T, r)).astype(np.float32)
+    out = (to_dev(dV0, dev), to_dev(dK0, dev) if mode == PROJECTED else None, to_dev(dQ0, dev))
+    got = lr.route_all_bwd(V, K, to_dev(Q, dev), to_dev(dH, dev), mode, first, out=out,
+                           accumulate=True)
+    torch.cuda.synchronize()
+    rV, rK, rQ = oracle.route_all_bwd(p.V, p.K, Q.astype(np.float64), dH, mode, first, r=r)
+    ref = (rV + f32_from_bf16_bits(dV0), None if rK is None else rK + f32_from_bf16_bits(dK0),
+           rQ + dQ0)
+    _check("acc ", mode, got, ref)
+
+
+def test_all_sites_backward_is_deterministic(dev):
+    S, T, first, N, d, r = 49, 48, 1, 700, 256, 32
+    p, Q, dH = _problem(PROJECTED, S, T, first, N, d, r, seed=41)
+    args = (to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev), to_dev(dH, dev), PROJECTED, first)
+    a = lr.route_all_bwd(*args)
+    b = lr.route_all_bwd(*args)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y)
+
+
+def test_sources_no_site_reads_get_zero(dev):
+    """Sources at or past first + T - 1 receive exactly zero (overwrite)."""
+    S, T, first, N, d, r = 20, 6, 3, 30, 128, 16
+    p, Q, dH = _problem(PROJECTED, S, T, first, N, d, r, seed=51)
+    dV, dK, _ = lr.route_all_bwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev),
+                                 to_dev(dH, dev), PROJECTED, first)
+    torch.cuda.synchronize()
+    assert not bool(dV[first + T - 1:].float().abs().max() > 0)
+    assert not bool(dK[first + T - 1:].float().abs().max() > 0)
+
+
+def test_empty_token_range(dev):
+    """N = 0: nothing is launched over tokens; dQ is zero (overwrite) or
+    unchanged (accumulate)."""
+    V = torch.empty((4, 0, 64), dtype=torch.bfloat16, device=dev)
+    dH = torch.empty((3, 0, 64), dtype=torch.bfloat16, device=dev)
+    Q = torch.ones((3, 8), device=dev)
+    _, _, dQ = lr.route_all_bwd(V, None, Q, dH, SLICED, 2)
+    torch.cuda.synchronize()
+    assert bool((dQ == 0).all())
+    dQ1 = torch.full((3, 8), 2.5, device=dev)
+    lr.route_all_bwd(V, None, Q, dH, SLICED, 2, out=(torch.empty_like(V), None, dQ1),
+                     accumulate=True)
+    torch.cuda.synchronize()
+    assert bool((dQ1 == 2.5).all())
+
+
+@pytest.mark.parametrize("mode,r", [(PROJECTED, 16), (SLICED, 64)], ids=["P-r16", "S-r64"])
+def test_model_pass_full_size(dev, mode, r):
+    """The paper's model (Sec. 4.1: d = 1024, 48 sub-layers plus the
+    embedding) at N = 16384 tokens: sites 1..48 read 2..49 sources.  Sampled
+    tokens against the oracle; dQ against the sum over sites of the
+    single-site backward of each prefix."""
+    S, T, first, N, d = 49, 48, 2, 16384, 1024
+    g = torch.Generator(device=dev)
+    g.manual_seed(7 + r)
+    V = torch.randn((S, N, d), generator=g, device=dev).to(torch.bfloat16)
+    K = torch.randn((S, N, r), generator=g, device=dev).to(torch.bfloat16) if mode == PROJECTED \
+        else None
+    Q = torch.randn((T, r), generator=g, device=dev) * (2.0 / r ** 0.5)
+    dH = torch.randn((T, N, d), generator=g, device=dev).to(torch.bfloat16)
+    dV, dK, dQ = lr.route_all_bwd(V, K, Q, dH, mode, first)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([[0, 511, 512, N - 1],
+                                     np.random.default_rng(r).integers(0, N, 12)]))
+    idx = torch.as_tensor(toks, device=dev)
+    Vs = bf16_tensor_to_bits(V[:, idx].contiguous())
+    Ks = bf16_tensor_to_bits(K[:, idx].contiguous()) if K is not None else None
+    dHs = bf16_tensor_to_bits(dH[:, idx].contiguous())
+    Qh = Q.cpu().numpy().astype(np.float64)
+    rV, rK, rQ = oracle.route_all_bwd(Vs, Ks, Qh, dHs, mode, first, r=r)
+    _check("", mode, (dV[:, idx].contiguous(), dK[:, idx].contiguous() if K is not None else None,
+                      torch.as_tensor(rQ, device=dev)), (rV, rK, rQ))
+    # dQ row j is site j's dq: the single-site backward over its prefix.
+    ws = torch.empty((lr.route_bwd_workspace_bytes(S, N, d, r, mode, torch.bfloat16),),
+                     dtype=torch.uint8, device=dev)
+    sdV = torch.empty_like(V)
+    sdK = torch.empty_like(K) if K is not None else None
+    want = torch.empty_like(dQ)
+    for j in range(T):
+        s = first + j
+        _, _, dq = lr.route_bwd(V[:s], K[:s] if K is not None else None, Q[j], dH[j], mode,
+                                out=(sdV[:s], sdK[:s] if sdK is not None else None, want[j]),
+                                workspace=ws)
+    torch.cuda.synchronize()
+    check_dq("dQ", to_host(dQ), to_host(want))
