@@ -178,6 +178,62 @@ def all_sites_bytes(S, T, N, d, r, mode, es=2):
     return S * N * d * es + keys + T * N * d * es + T * N * 4
 
 
+def all_sites_bwd_bytes(S, T, N, d, r, mode, es=2):
+    """Bytes one all-sites backward must move: the stack and the keys read
+    once, every site's upstream gradient read once, dV (and dK) written once."""
+    keys = 2 * S * N * r * es if mode == 0 else 0
+    return 2 * S * N * d * es + keys + T * N * d * es
+
+
+def all_sites_backward(torch, lr, dev, mode, r, V, K, queries, reps, warmup, flush,
+                       per_site=True):
+    """Backward of sites 2..49 of the 49-source pass (prefixes of 2..49
+    sources) in one call, cold; beside it, the same gradients as 48
+    accumulating single-site backward calls (warm, once)."""
+    S, N, d = V.shape
+    T = 48
+    gen = torch.Generator(device=dev).manual_seed(300 + r)
+    dH = torch.randn((T, N, d), generator=gen, device=dev).to(torch.bfloat16)
+    Qa = queries[1:].contiguous()
+    dV = torch.empty_like(V)
+    dK = torch.empty_like(K) if K is not None else None
+    dQ = torch.empty((T, r), dtype=torch.float32, device=dev)
+    ws = torch.empty((max(16, lr.route_all_bwd_workspace_bytes(S, N, d, r, 2, T, mode,
+                                                               V.dtype)),),
+                     dtype=torch.uint8, device=dev)
+    ts = time_calls(torch, lambda: lr.route_all_bwd(V, K, Qa, dH, mode, 2, out=(dV, dK, dQ),
+                                                    workspace=ws), reps, warmup, flush)
+    med = float(np.median(ts))
+    nbytes = all_sites_bwd_bytes(S, T, N, d, r, mode)
+    res = {"median_ms": med, "min_ms": float(np.min(ts)), "max_ms": float(np.max(ts)),
+           "tokens_per_s": N / (med * 1e-3), "algo_bytes": nbytes,
+           "algo_GBps": nbytes / (med * 1e-3) / 1e9,
+           "frac_of_peak": nbytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    if per_site:
+        # The same gradients from the single-site backward: site j reads the
+        # first j + 2 sources and adds into their gradient rows.
+        wsb = torch.empty((lr.route_bwd_workspace_bytes(S, N, d, r, mode, V.dtype),),
+                          dtype=torch.uint8, device=dev)
+        dq = torch.empty((T, r), dtype=torch.float32, device=dev)
+        dV.zero_()
+        if dK is not None:
+            dK.zero_()
+        dq.zero_()
+
+        def sweep():
+            for j in range(T - 1, -1, -1):
+                s = j + 2
+                lr.route_bwd(V[:s], K[:s] if K is not None else None, Qa[j], dH[j], mode,
+                             out=(dV[:s], dK[:s] if dK is not None else None, dq[j]),
+                             workspace=wsb, accumulate=True)
+        tp = time_calls(torch, sweep, 1, 0, flush)
+        res["per_site_accumulating_calls_ms"] = float(tp[0])
+        res["speedup_vs_per_site_calls"] = float(tp[0]) / med
+        del wsb, dq
+    del dH, dV, dK, dQ, ws
+    return res
+
+
 def block_pass_bytes(t, c, N, d, r, mode, es=2):
     """Algorithmic HBM bytes of the fused block call at site t: the earlier
     fp32 slots (with their fp32 key slots for projected keys) read once, the
@@ -531,6 +587,8 @@ def extras(torch, lr, dev, reps, warmup):
     out["model_pass_projected_r16"] = model_pass(PROJECTED, 16, Q)
     out["all_sites_pass_projected_r16"] = all_sites(PROJECTED, 16, V, K, Q,
                                                     out["model_pass_projected_r16"])
+    out["all_sites_backward_projected_r16"] = all_sites_backward(
+        torch, lr, dev, PROJECTED, 16, V, K, Q, reps, warmup, flush)
     gen = torch.Generator(device=dev)
     for r in (8, 16, 32, 64):
         gen.manual_seed(r)
@@ -539,6 +597,8 @@ def extras(torch, lr, dev, reps, warmup):
         if r == 64:
             out["all_sites_pass_sliced_r64"] = all_sites(SLICED, 64, V, None, qs,
                                                          out["model_pass_sliced_r64"])
+            out["all_sites_backward_sliced_r64"] = all_sites_backward(
+                torch, lr, dev, SLICED, 64, V, None, qs, reps, warmup, flush)
 
     # Head to head at S = 49: full rank vs low rank, forward and backward.
     # The full-rank forward reads every row once (online softmax); its
@@ -630,7 +690,11 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
             out[f"all_sites_pass_{'projected' if mode == PROJECTED else 'sliced'}_r{r}"] = {
                 "median_ms": med, "algo_GBps": nbytes / (med * 1e-3) / 1e9,
                 "frac_of_peak": nbytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS}
-            del g, Ha, ne
+            del Ha, ne
+            out[f"all_sites_backward_{'projected' if mode == PROJECTED else 'sliced'}_r{r}"] = \
+                all_sites_backward(torch, lr, dev, mode, r, g["V"], g["K"], g["q"], reps, warmup,
+                                   flush, per_site="per_site" in names)
+            del g
             torch.cuda.empty_cache()
     return out
 

@@ -21,13 +21,13 @@
 //                                            as in the forward),
 //     u  = ds^T [S x T] * Q [T x r] and dQ += (ds / rho) [T x S] * K [S x r]
 //                                           (v_mfma_f32_16x16x4_f32).
-// Workgroups (4 waves) are persistent over a stride of tokens and keep their
-// share of dQ in registers; a fixed-order reduction adds the per-workgroup
-// partials, so dQ is bitwise reproducible.  Wave w owns sources 16 w ..
-// 16 w + 15.  The row is processed in 128-column slabs: the workgroup
-// stages the T upstream rows of a slab in LDS (16-byte chunks XOR-swizzled
-// by row, conflict-free in both read patterns below), each wave loads its 16
-// source rows of the slab into registers, then
+// Workgroups (4 waves, two per CU) are persistent over a stride of tokens
+// and keep their share of dQ in registers; a fixed-order reduction adds the
+// per-workgroup partials, so dQ is bitwise reproducible.  Wave w owns
+// sources 16 w .. 16 w + 15.  The row is processed in 128-column slabs: the
+// workgroup stages the T upstream rows of a slab in LDS (16-byte chunks
+// XOR-swizzled by row, conflict-free in both read patterns below), each wave
+// loads its 16 source rows of the slab into registers, then
 //   - G: A = dH rows from LDS (lane: one site, 8 columns), B = the source
 //     rows (lane: one source, the same 8 columns);
 //   - dV: A = alpha^T (lane: one source, 8 sites), B = dH read from LDS as 8
@@ -35,11 +35,13 @@
 //     so that the p-th MFMA's column index stands for column c0 + p; the
 //     result is 8 consecutive columns of 4 sources per lane, stored as
 //     16-byte rows.
-// The next slab (or the next token's first slab) is loaded while the current
-// one is multiplied.  With sliced keys the key gradient lands in the last r
-// columns of dV, which needs the whole of G first: the slabs that hold those
-// columns (at most the last two, still in the two LDS buffers when the row
-// ends) are multiplied again after the key gradient is known.
+// The next slab is loaded while the current one is multiplied; the other
+// workgroup on the CU covers the per-token phases (scores, key gradients).
+// With sliced keys the key gradient lands in the last r columns of dV, which
+// needs the whole of G first: those columns' value gradients wait in LDS in
+// fp32 (where the weights were) and are rounded once the key gradient has
+// been added.  Workgroup barriers here order LDS only (lds_barrier), so
+// loads issued ahead stay in flight across them.
 #include "route_all_weights.h"
 
 namespace lrar {
@@ -49,6 +51,7 @@ namespace {
 constexpr int kAllBwdGrid = 512;                       // persistent workgroups
 constexpr int kDhRowBytes = kAllSlab * 2;              // one slab row of dH, bf16
 constexpr int kDhBufBytes = kAllMaxSources * kDhRowBytes;
+constexpr int kTailRow = 64;                           // floats per source: key-column octets
 
 struct AllBwdArgs {
     AllArgs f;           // V, keys, Q, sizes (H and neff unused)
@@ -56,7 +59,7 @@ struct AllBwdArgs {
     uint16_t *dV;        // [S][N][d]
     uint16_t *dK;        // [S][N][r] (projected keys) or NULL
     float *partial;      // [gridDim.x][T][r]
-    int s_tail;          // first slab whose dV waits for the key gradient (nslab: none)
+    bool sliced;         // the key is the last r columns of each value row
 };
 
 // LDS byte offset of 16-byte chunk c (0..15) of slab row `row`: rows are
@@ -77,34 +80,30 @@ __device__ __forceinline__ void per_token(T &x)
 }
 
 template <int MT, int RT, bool ACC>
-__global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(AllBwdArgs b)
+__global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
 {
     constexpr int KG = (MT + 1) / 2;      // groups of 32 sites in the dV contraction
     constexpr int RP = RT <= 2 ? 32 : 64; // key elements covered by the score MFMAs
+    constexpr int KK = RP / 32;
+    // alpha: the weights, then (sliced keys) the fp32 value gradient of the
+    // key columns [16 w + e][c - tail0].  dhbuf: the upstream slabs, then
+    // ds / rho [site][source] for dQ.
     __shared__ __align__(16) float alpha[kAllMaxSources * kAlphaRow];
     __shared__ __align__(16) unsigned char dhbuf[2 * kDhBufBytes];
     __shared__ __align__(16) uint16_t keys[kAllMaxSources * kKeyRow];
     __shared__ float rho[kAllMaxSources];
     __shared__ float gpart[kWaves * kAllMaxSources];
-    __shared__ float qs[kAllMaxSources * kAllMaxRank];  // Q [T][r], for the key gradient
+    __shared__ float qs[kAllMaxSources * kAllMaxRank];  // Q [T][r]
+    static_assert(2 * kDhBufBytes >= kAllMaxSources * kAlphaRow * 4, "ds / rho fits the slabs");
 
     const int tid = threadIdx.x;
     const int lane = tid % kWaveSize, wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
     const int lc = lane & 15, ks = lane >> 4;
     const int src = 16 * wave + lc;  // this lane's source as a G operand
     const int hch = tid & 15, hr0 = tid >> 4;
+    float *dsr = reinterpret_cast<float *>(dhbuf);
+    float *tailbuf = alpha + wave * 16 * kTailRow;  // this wave's 16 sources
 
-    // Rows 16 MT .. 32 KG - 1 of the dH buffers enter the last site group's
-    // dV MFMAs with weight 0 but are never loaded: zero them once.
-    constexpr int kPadChunks = (32 * KG - 16 * MT) * 16;
-    if constexpr (kPadChunks > 0) {
-        for (int f = tid; f < 2 * kPadChunks; f += kBlock) {
-            const int g = f % kPadChunks;
-            *reinterpret_cast<u32x4_t *>(dhbuf + (f / kPadChunks) * kDhBufBytes +
-                                         dh_chunk(16 * MT + g / 16, g % 16)) =
-                u32x4_t{0u, 0u, 0u, 0u};
-        }
-    }
     for (int f = tid; f < b.f.T * b.f.r; f += kBlock)
         qs[f] = b.f.Q[f];
 
@@ -125,12 +124,19 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
         per_token(a.N);
         const size_t plane = (size_t)a.N * a.d;
         const int nslab = (a.d + kAllSlab - 1) / kAllSlab;
-        const uint16_t *V = static_cast<const uint16_t *>(a.V);
+        // First column of the key octets (sliced keys; d past the row otherwise).
+        const int tail0 = b.sliced ? (a.d - a.r) / 8 * 8 : a.d;
 
         // Slab loads: thread t brings chunk t mod 16 of dH rows t / 16 + 16 q
         // (q < MT), and lane (lc, ks) the 4 chunks 4 u + ks of its source
         // row.  Lanes past the rows or columns load a valid address (the
-        // token's first chunk) and keep zeros, so no load sits behind a branch.
+        // token's first chunk), so no load sits behind a branch; the
+        // consumers (the LDS write of dH, the G operands of V) put zeros in
+        // their place, so that no load is waited for early.  The next slab is
+        // in flight while the current one is multiplied.  A source row's
+        // 128-byte lines are read by two loads (64 bytes of each of 16 rows
+        // per load), so those loads go through the caches normally; the
+        // upstream rows, read as whole lines, stream.
         u32x4_t hraw[MT], vraw[4];
         auto load_dh = [&](int s) {
             const int col = s * kAllSlab + 8 * hch;
@@ -139,51 +145,90 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
             for (int q = 0; q < MT; ++q) {
                 const int row = hr0 + 16 * q;
                 const bool ok = row < a.T && col < a.d;
-                const u32x4_t x =
-                    load_stream<uint16_t, 8, kNtLoad>(ok ? hbase + row * plane + col : hbase);
-                hraw[q] = ok ? x : u32x4_t{0u, 0u, 0u, 0u};
+                hraw[q] = load_stream<uint16_t, 8, kNtLoad>(ok ? hbase + row * plane + col : hbase);
             }
         };
         auto load_v = [&](int s) {
-            const uint16_t *vbase = V + n * a.d;
+            const uint16_t *vbase = static_cast<const uint16_t *>(a.V) + n * a.d;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int c = s * kAllSlab + 32 * u + 8 * ks;
                 const bool ok = src < a.S && c < a.d;
-                const u32x4_t x =
-                    load_stream<uint16_t, 8, kNtLoad>(ok ? vbase + src * plane + c : vbase);
-                vraw[u] = ok ? x : u32x4_t{0u, 0u, 0u, 0u};
+                vraw[u] = load_stream<uint16_t, 8, false>(ok ? vbase + src * plane + c : vbase);
             }
         };
+        // The keys first, so that waiting for them does not wait for the slab.
+        u32x4_t kown[4 * KK];
+        load_site_keys<RP>(a, n, kown);
         load_dh(0);
         load_v(0);
 
-        __syncthreads();  // the previous token's LDS reads are done
-        all_site_weights<uint16_t, RP, true>(a, n, alpha, rho, keys);
+        lds_barrier();  // the previous token's LDS reads are done
+        all_site_weights<uint16_t, RP, true>(a, n, alpha, rho, keys, kown, qs);
 
-        // alpha^T operands of this wave's sources: lane (lc, ks) holds
-        // alpha[32 kg + 8 ks + e][src] as hi + lo bf16.
+        // alpha^T operands of this wave's sources (lane (lc, ks): alpha[32 kg +
+        // 8 ks + e][src] as hi + lo bf16) and the weights at this lane's G
+        // entries; alpha's LDS then holds the key-column gradients.
         bf16x8_t Ahi[KG], Alo[KG];
+        float av[MT][4];
 #pragma unroll
         for (int kg = 0; kg < KG; ++kg) {
-            float av[8];
+            float w8[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                av[e] = alpha[(32 * kg + 8 * ks + e) * kAlphaRow + src];
+                w8[e] = alpha[(32 * kg + 8 * ks + e) * kAlphaRow + src];
             u32x4_t hi, lo;
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
-                const unsigned hw = pack_bf16x2(av[2 * h], av[2 * h + 1]);
+                const unsigned hw = pack_bf16x2(w8[2 * h], w8[2 * h + 1]);
                 hi[h] = hw;
-                lo[h] = pack_bf16x2(av[2 * h] - bf16_lo(hw), av[2 * h + 1] - bf16_hi(hw));
+                lo[h] = pack_bf16x2(w8[2 * h] - bf16_lo(hw), w8[2 * h + 1] - bf16_hi(hw));
             }
             Ahi[kg] = __builtin_bit_cast(bf16x8_t, hi);
             Alo[kg] = __builtin_bit_cast(bf16x8_t, lo);
         }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                av[mt][e] = alpha[(16 * mt + 4 * ks + e) * kAlphaRow + src];
 
-        // dV of one slab for this wave's sources (no key path): acc[p] holds
-        // sources 16 wave + 4 ks + e (e = 0..3) at column c0 + p, c0 = 128 s + 8 lc.
-        auto slab_dv = [&](const unsigned char *buf, f32x4_t(&acc)[8]) {
+        f32x4_t G[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            G[mt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int s = 0; s < nslab; ++s) {
+            unsigned char *buf = dhbuf + (s & 1) * kDhBufBytes;
+            // Rows past T, and rows 16 MT .. 32 KG - 1 that the last site
+            // group's dV MFMAs read with weight 0, are written as zeros (the
+            // buffers hold ds / rho between tokens).
+#pragma unroll
+            for (int q = 0; q < 2 * KG; ++q) {
+                const bool ok = q < MT && hr0 + 16 * q < a.T && s * kAllSlab + 8 * hch < a.d;
+                *reinterpret_cast<u32x4_t *>(buf + dh_chunk(hr0 + 16 * q, hch)) =
+                    ok ? hraw[q < MT ? q : 0] : u32x4_t{0u, 0u, 0u, 0u};
+            }
+            if (s + 1 < nslab)
+                load_dh(s + 1);
+            lds_barrier();
+            // G[16 mt + 4 ks + e][src] over this slab's columns.
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool ok = src < a.S && s * kAllSlab + 32 * u + 8 * ks < a.d;
+                const bf16x8_t B =
+                    __builtin_bit_cast(bf16x8_t, ok ? vraw[u] : u32x4_t{0u, 0u, 0u, 0u});
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const bf16x8_t A = *reinterpret_cast<const bf16x8_t *>(
+                        buf + dh_chunk(16 * mt + lc, 4 * u + ks));
+                    G[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, G[mt], 0, 0, 0);
+                }
+            }
+            if (s + 1 < nslab)
+                load_v(s + 1);
+
+            // dV: acc[p] holds sources 16 wave + 4 ks + e at column c0 + p.
+            f32x4_t acc[8];
 #pragma unroll
             for (int p = 0; p < 8; ++p)
                 acc[p] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -206,92 +251,59 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
                     acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Alo[kg], B, acc[p], 0, 0, 0);
                 }
             }
-        };
-
-        // Round and store one slab of dV (adding the stored value when
-        // accumulating); tail[local source][c - (d - r)] is added at the
-        // columns c >= d - r.
-        auto store_dv = [&](int s, const f32x4_t(&acc)[8], const float *tail) {
             const int c0 = s * kAllSlab + 8 * lc;
-            if (c0 >= a.d)
-                return;
+            if (c0 < tail0) {
+                // Rounded and stored (added to the stored value when accumulating).
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                __builtin_amdgcn_sched_barrier(0);
-                const int i = 16 * wave + 4 * ks + e;
-                if (i >= a.S)
-                    continue;
-                float v[8];
-#pragma unroll
-                for (int p = 0; p < 8; ++p) {
-                    v[p] = acc[p][e];
-                    const int c = c0 + p - (a.d - a.r);
-                    if (tail && c >= 0)
-                        v[p] += tail[(4 * ks + e) * kAlphaRow + c];
-                }
-                uint16_t *dst = b.dV + i * plane + n * a.d + c0;
-                if (ACC) {
-                    float old[8];
-                    widen(load_raw<uint16_t, 8>(dst), old);
+                for (int e = 0; e < 4; ++e) {
+                    const int i = 16 * wave + 4 * ks + e;
+                    if (i >= a.S)
+                        continue;
+                    float v[8];
 #pragma unroll
                     for (int p = 0; p < 8; ++p)
-                        v[p] += old[p];
+                        v[p] = acc[p][e];
+                    uint16_t *dst = b.dV + i * plane + n * a.d + c0;
+                    if (ACC) {
+                        float old[8];
+                        widen(load_raw<uint16_t, 8>(dst), old);
+#pragma unroll
+                        for (int p = 0; p < 8; ++p)
+                            v[p] += old[p];
+                    }
+                    u32x4_t o;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h)
+                        o[h] = pack_bf16x2(v[2 * h], v[2 * h + 1]);
+                    store_stream<uint16_t, 8, kNtStore>(dst, o);
                 }
-                u32x4_t o;
+            } else if (c0 < a.d) {
+                // Key columns: kept in fp32 until the key gradient is known.
 #pragma unroll
-                for (int h = 0; h < 4; ++h)
-                    o[h] = pack_bf16x2(v[2 * h], v[2 * h + 1]);
-                store_stream<uint16_t, 8, kNtStore>(dst, o);
-            }
-        };
-
-        f32x4_t G[MT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            G[mt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        for (int s = 0; s < nslab; ++s) {
-            unsigned char *buf = dhbuf + (s & 1) * kDhBufBytes;
-#pragma unroll
-            for (int q = 0; q < MT; ++q)
-                *reinterpret_cast<u32x4_t *>(buf + dh_chunk(hr0 + 16 * q, hch)) = hraw[q];
-            if (s + 1 < nslab)
-                load_dh(s + 1);
-            __syncthreads();
-            // G[16 mt + 4 ks + e][src] over this slab's columns; then the
-            // source rows of the next slab are loaded into the same registers.
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const bf16x8_t A = *reinterpret_cast<const bf16x8_t *>(
-                        buf + dh_chunk(16 * mt + lc, 4 * u + ks));
-                    G[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        A, __builtin_bit_cast(bf16x8_t, vraw[u]), G[mt], 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    float *t = tailbuf + (4 * ks + e) * kTailRow + (c0 - tail0);
+                    *reinterpret_cast<f32x4_t *>(t) =
+                        f32x4_t{acc[0][e], acc[1][e], acc[2][e], acc[3][e]};
+                    *reinterpret_cast<f32x4_t *>(t + 4) =
+                        f32x4_t{acc[4][e], acc[5][e], acc[6][e], acc[7][e]};
                 }
-            if (s + 1 < nslab)
-                load_v(s + 1);
-            if (s < b.s_tail) {
-                f32x4_t acc[8];
-                slab_dv(buf, acc);
-                store_dv(s, acc, nullptr);
             }
         }
 
         // Softmax gradient.  Lane (lc, ks) holds G[site 16 mt + 4 ks + e][src].
-        float av[MT][4], ds[MT][4];
+        float ds[MT][4];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int site = 16 * mt + 4 * ks + e;
-                av[mt][e] = alpha[site * kAlphaRow + src];
                 float t = av[mt][e] * G[mt][e];
                 for (int o = 1; o < 16; o <<= 1)
                     t += __shfl_xor(t, o, kWaveSize);
                 if (lc == 0)
                     gpart[wave * kAllMaxSources + site] = t;
             }
-        __syncthreads();
+        lds_barrier();  // also: every wave is past its last read of the slabs
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -303,6 +315,15 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
                     gbar += gpart[w * kAllMaxSources + site];
                 ds[mt][e] = av[mt][e] * (G[mt][e] - gbar);
             }
+        {
+            // ds / rho for dQ, in the slab buffers.
+            const float inv = src < a.S ? 1.0f / rho[src] : 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    dsr[(16 * mt + 4 * ks + e) * kAlphaRow + src] = ds[mt][e] * inv;
+        }
 
         // u_i = sum_j ds[j][i] Q_j: the MFMA's k index ks at step (mt, e)
         // stands for site 16 mt + 4 ks + e, on both operands.
@@ -322,8 +343,8 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
                 }
         }
         // dk_i = (u_i - k_i (k_i . u_i) / (rho_i^2 r)) / rho_i; lane (lc, ks)
-        // holds sources 16 wave + 4 ks + e at key column 16 ct + lc.
-        float dk[RT][4];
+        // holds sources 16 wave + 4 ks + e at key column 16 ct + lc.  Projected
+        // keys: stored into dK; sliced: added to the key columns' gradient.
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int i = 16 * wave + 4 * ks + e;
@@ -339,39 +360,25 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
             const float inv = i < a.S ? 1.0f / rho[i] : 0.0f;
             const float scale = dot * inv * inv / (float)a.r;
 #pragma unroll
-            for (int ct = 0; ct < RT; ++ct)
-                dk[ct][e] = (uk[ct][e] - kv[ct] * scale) * inv;
-        }
-        if (b.dK) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int i = 16 * wave + 4 * ks + e;
-#pragma unroll
-                for (int ct = 0; ct < RT; ++ct) {
-                    const int c = 16 * ct + lc;
-                    if (i < a.S && c < a.r) {
+            for (int ct = 0; ct < RT; ++ct) {
+                const int c = 16 * ct + lc;
+                const float dk = (uk[ct][e] - kv[ct] * scale) * inv;
+                if (i < a.S && c < a.r) {
+                    if (b.dK) {
                         uint16_t *dst = b.dK + (i * (size_t)a.N + n) * a.r + c;
-                        float v = dk[ct][e];
+                        float v = dk;
                         if (ACC)
                             v += bf16_at(dst);
                         *dst = (uint16_t)pack_bf16x2(v, 0.0f);
+                    } else {
+                        tailbuf[(4 * ks + e) * kTailRow + (a.d - a.r - tail0) + c] += dk;
                     }
                 }
             }
         }
 
-        // dQ_j += sum_i (ds[j][i] / rho_i) k_i: ds / rho replaces alpha in
-        // LDS, then wave w takes the sites of tile w.
-        __syncthreads();
-        {
-            const float inv = src < a.S ? 1.0f / rho[src] : 0.0f;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    alpha[(16 * mt + 4 * ks + e) * kAlphaRow + src] = ds[mt][e] * inv;
-        }
-        __syncthreads();
+        // dQ_j += sum_i (ds[j][i] / rho_i) k_i: wave w takes the sites of tile w.
+        lds_barrier();
         if (wave < MT) {
             const int nst = (a.S + 3) / 4;
 #pragma unroll
@@ -380,31 +387,40 @@ __global__ __launch_bounds__(kBlock, MT <= 2 ? 2 : 1) void route_all_bwd_bf16(Al
 #pragma unroll 1
                 for (int st = 0; st < nst; ++st) {
                     const int i = 4 * st + ks;
-                    const float A = alpha[(16 * wave + lc) * kAlphaRow + i];
+                    const float A = dsr[(16 * wave + lc) * kAlphaRow + i];
                     const float B = (i < a.S && c < a.r) ? bf16_at(keys + i * kKeyRow + c) : 0.0f;
                     dq[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(A, B, dq[ct], 0, 0, 0);
                 }
             }
         }
 
-        // Sliced keys: the slabs holding the last r columns, with dk added.
-        if (b.s_tail < nslab) {
-            __syncthreads();
-            float *dkb = alpha + wave * 16 * kAlphaRow;  // [16 sources][r], this wave's
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int ct = 0; ct < RT; ++ct) {
-                    const int c = 16 * ct + lc;
-                    if (c < a.r)
-                        dkb[(4 * ks + e) * kAlphaRow + c] = dk[ct][e];
-                }
+        // Sliced keys: the key columns, value and key gradients together.
+        // This wave's 16 sources x (d - tail0) / 8 octets, two per lane.
+        if (b.sliced) {
             wave_lds_sync();
-#pragma unroll 1
-            for (int s = b.s_tail; s < nslab; ++s) {
-                f32x4_t acc[8];
-                slab_dv(dhbuf + (s & 1) * kDhBufBytes, acc);
-                store_dv(s, acc, dkb);
+            const int noct = (a.d - tail0) / 8;
+            for (int f = lane; f < 16 * noct; f += kWaveSize) {
+                const int li = f / noct, oc = f % noct;
+                const int i = 16 * wave + li;
+                if (i >= a.S)
+                    continue;
+                const float *t = tailbuf + li * kTailRow + 8 * oc;
+                const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(t);
+                const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(t + 4);
+                float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+                uint16_t *dst = b.dV + i * plane + n * a.d + tail0 + 8 * oc;
+                if (ACC) {
+                    float old[8];
+                    widen(load_raw<uint16_t, 8>(dst), old);
+#pragma unroll
+                    for (int p = 0; p < 8; ++p)
+                        v[p] += old[p];
+                }
+                u32x4_t o;
+#pragma unroll
+                for (int h = 0; h < 4; ++h)
+                    o[h] = pack_bf16x2(v[2 * h], v[2 * h + 1]);
+                store_stream<uint16_t, 8, kNtStore>(dst, o);
             }
         }
     }
@@ -498,12 +514,7 @@ int launch_all_bwd(const AllProblem &p, const void *dH, void *dV, void *dK, floa
         b.dV = static_cast<uint16_t *>(dV);
         b.dK = static_cast<uint16_t *>(dK);
         b.partial = partial;
-        const int nslab = (int)((p.d + kAllSlab - 1) / kAllSlab);
-        b.s_tail = p.mode == LRAR_MODE_SLICED ? (int)((p.d - p.r) / kAllSlab) : nslab;
-        if (nslab - b.s_tail > 2) {  // r <= 64 < 128 keeps the key columns in two slabs
-            *err = "route_all_bwd: key columns span more than the two buffered slabs";
-            return LRAR_EUNSUPPORTED;
-        }
+        b.sliced = p.mode == LRAR_MODE_SLICED;
         if (accumulate)
             launch_all_bwd_acc<true>(b, grid, st);
         else

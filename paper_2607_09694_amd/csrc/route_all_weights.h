@@ -17,6 +17,20 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 constexpr int kAllSlab = 128;                     // columns per wave pass
 constexpr int kAlphaRow = kAllMaxSources + 4;     // floats per LDS alpha row
 constexpr int kKeyRow = kAllMaxRank + 8;          // bf16 per LDS key row
+// s_waitcnt immediate: lgkmcnt(0); vmcnt and expcnt left at their maxima.
+constexpr int kWaitLdsOnly = 0x000F | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
+
+// Workgroup barrier that orders LDS only: this wave's LDS accesses complete,
+// then s_barrier.  Unlike __syncthreads it does not wait for outstanding
+// global loads, so loads issued ahead stay in flight across it.  The
+// kernels that use it communicate between waves through LDS alone.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitLdsOnly);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 struct AllArgs {
     const void *V;       // [S][N][d]
@@ -40,7 +54,7 @@ struct AllArgs {
 // sites on rows 4 (l / 16) + e and sources on column l mod 16, so a site's
 // softmax is a reduction over the 16 lanes of its row group.
 // Writes alpha (fp32 [64][kAlphaRow], zero past each prefix and for absent
-// sites) to LDS and N_eff to global; ends with a workgroup barrier.
+// sites) to LDS and N_eff to global; ends with a workgroup barrier (LDS only).
 //
 // bf16 storage: v_mfma_f32_16x16x32_bf16, 32 key elements per step; the keys
 // are exact in bf16 and Q enters as hi + lo bf16 (two MFMAs), so the dot
@@ -50,10 +64,56 @@ struct AllArgs {
 // SAVE (bf16 storage only): wave 0 also leaves every source's key (bf16,
 // [64][kKeyRow], zero past r and past S) and rho_i ([64]) in LDS, for the
 // backward's key-path terms.
+//
+// bf16 storage can take the keys already loaded (kpre, from load_site_keys,
+// so that they can be issued ahead of other loads) and the queries from LDS
+// (qlds, Q [T][r]); by default both are read here from global memory.
+template <int RP>
+__device__ __forceinline__ void load_site_keys(const AllArgs &a, int64_t n, u32x4_t *kraw)
+{
+    constexpr int KK = RP / 32;
+    const int lane = threadIdx.x % kWaveSize;
+    const int col = lane & 15, ks = lane >> 4;
+    const uint16_t *keys = static_cast<const uint16_t *>(a.keys) + n * a.krow + a.koff;
+    const size_t kplane = (size_t)a.N * a.krow;
+    if (a.kvec) {
+        // Sources past S and elements past r load a valid address; they are
+        // zeroed where the keys are used.
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int i = 16 * nt + col, c = 32 * kk + 8 * ks;
+                const bool ok = i < a.S && c < a.r;
+                kraw[nt * KK + kk] = load_raw<uint16_t, 8>(ok ? keys + i * kplane + c : keys);
+            }
+    } else {
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const int i = 16 * nt + col, c = 32 * kk + 8 * ks;
+                u32x4_t kr = {0u, 0u, 0u, 0u};
+                if (i < a.S && c < a.r) {
+                    const uint16_t *kp = keys + i * kplane + c;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const unsigned x0 = c + 2 * h < a.r ? kp[2 * h] : 0u;
+                        const unsigned x1 = c + 2 * h + 1 < a.r ? kp[2 * h + 1] : 0u;
+                        kr[h] = x0 | (x1 << 16);
+                    }
+                }
+                kraw[nt * KK + kk] = kr;
+            }
+    }
+}
+
 template <typename T, int RP, bool SAVE = false>
 __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, float *alpha,
                                                  float *rho_out = nullptr,
-                                                 uint16_t *key_out = nullptr)
+                                                 uint16_t *key_out = nullptr,
+                                                 const u32x4_t *kpre = nullptr,
+                                                 const float *qlds = nullptr)
 {
     const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
     const int col = lane & 15, ks = lane >> 4;
@@ -77,7 +137,9 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int c = 32 * kk + 8 * ks + e;
-                qv[e] = (qsite < a.T && c < a.r) ? a.Q[(size_t)qsite * a.r + c] : 0.0f;
+                qv[e] = (qsite < a.T && c < a.r)
+                            ? (qlds ? qlds[qsite * a.r + c] : a.Q[(size_t)qsite * a.r + c])
+                            : 0.0f;
             }
             u32x4_t hi, lo;
 #pragma unroll
@@ -89,27 +151,18 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
             Ahi[kk] = __builtin_bit_cast(bf16x8_t, hi);
             Alo[kk] = __builtin_bit_cast(bf16x8_t, lo);
         }
-        const bool kvec = a.kvec;
+        u32x4_t kown[4 * KK];
+        if (!kpre)
+            load_site_keys<RP>(a, n, kown);
+        const u32x4_t *kraw = kpre ? kpre : kown;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
             const int i = 16 * nt + col;
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
                 const int c = 32 * kk + 8 * ks;
-                u32x4_t kr = {0u, 0u, 0u, 0u};
-                if (i < a.S && c < a.r) {
-                    const uint16_t *kp = reinterpret_cast<const uint16_t *>(keys) + i * kplane + c;
-                    if (kvec) {
-                        kr = load_raw<uint16_t, 8>(kp);
-                    } else {
-#pragma unroll
-                        for (int h = 0; h < 4; ++h) {
-                            const unsigned x0 = c + 2 * h < a.r ? kp[2 * h] : 0u;
-                            const unsigned x1 = c + 2 * h + 1 < a.r ? kp[2 * h + 1] : 0u;
-                            kr[h] = x0 | (x1 << 16);
-                        }
-                    }
-                }
+                const u32x4_t kr = (i < a.S && c < a.r) ? kraw[nt * KK + kk]
+                                                        : u32x4_t{0u, 0u, 0u, 0u};
                 if (SAVE && wave == 0)
                     *reinterpret_cast<u32x4_t *>(key_out + i * kKeyRow + c) = kr;
                 float x[8];
@@ -205,7 +258,7 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
                 a.neff[(size_t)site * a.N + n] = expf(logf(z[e]) - sa[e]);
         }
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Pairs of bf16 from two packed words: the low halves (lo_pair) or the
