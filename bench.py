@@ -708,14 +708,15 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--extra-only", default="",
                     help="comma-separated workloads to run alone, without the main step "
-                         "(key_producer, all_sites, block_training); prints their JSON")
+                         "(key_producer, all_sites, block_training; per_site adds the per-site "
+                         "backward beside the all-sites one); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
                          "backward calls of the main workload (for rocprofv3 --pmc runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build measures one GPU only; --gpus must be 1 "
-              "(tokens are independent, see the sharding notes in DESIGN.md)",
+        print("bench.py measures one GPU: --gpus must be 1 (tokens are independent, so the "
+              "routing shards over tokens with no exchange; one GPU's share is what is timed)",
               file=sys.stderr)
         sys.exit(2)
 
