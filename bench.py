@@ -234,6 +234,70 @@ def all_sites_backward(torch, lr, dev, mode, r, V, K, queries, reps, warmup, flu
     return res
 
 
+def model_training_pass(torch, lr, dev, V, K, mode, r, reps, warmup):
+    """A whole full-source training pass over the 49-source stack V [49, N, d]
+    (site t reads sources 0 .. t-1): the forward at every site, then the
+    reverse pass in two forms, each timed end to end with HIP events, warm:
+    48 + 1 accumulating single-site backward calls, and the deferred form
+    (per site its coefficients, then one gather for the source that became
+    final)."""
+    T, N, d = V.shape
+    gen = torch.Generator(device=dev).manual_seed(400 + r)
+    Q = torch.randn((T, r), generator=gen, device=dev) / r ** 0.5
+    dH = torch.randn((T, N, d), generator=gen, device=dev).to(torch.bfloat16)
+    H = torch.empty((N, d), dtype=V.dtype, device=dev)
+    dV = torch.empty_like(V)
+    dK = torch.empty_like(K) if K is not None else None
+    dq = torch.empty((T, r), dtype=torch.float32, device=dev)
+    ws = torch.empty((lr.route_bwd_workspace_bytes(T, N, d, r, mode, V.dtype),),
+                     dtype=torch.uint8, device=dev)
+    coefs = torch.empty((T, T, 3, N), dtype=torch.float32, device=dev)
+
+    def fwd():
+        for t in range(1, T + 1):
+            lr.route_fwd(V[:t], K[:t] if K is not None else None, Q[t - 1], mode, out=H)
+
+    def bwd():
+        dV.zero_()
+        if dK is not None:
+            dK.zero_()
+        for t in range(T, 0, -1):
+            lr.route_bwd(V[:t], K[:t] if K is not None else None, Q[t - 1], dH[t - 1], mode,
+                         out=(dV[:t], dK[:t] if dK is not None else None, dq[t - 1]),
+                         workspace=ws, accumulate=True)
+
+    def bwd_deferred():
+        for t in range(T, 0, -1):
+            lr.route_bwd_deferred(V[:t], K[:t] if K is not None else None, Q[t - 1], dH[t - 1],
+                                  mode, coefs[t - 1, :t], dq=dq[t - 1], workspace=ws)
+            i = t - 1
+            lr.route_gather_bwd(V, K, i, dH[i:], Q[i:], coefs[i:, i], mode,
+                                out=(dV[i], dK[i] if dK is not None else None))
+
+    st = torch.cuda.current_stream()
+    res = {}
+    for name, back in (("accumulating_", bwd), ("deferred_", bwd_deferred)):
+        for _ in range(warmup):
+            fwd()
+            back()
+        tf, tb = [], []
+        for _ in range(reps):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record(st)
+            fwd()
+            e[1].record(st)
+            back()
+            e[2].record(st)
+            torch.cuda.synchronize()
+            tf.append(e[0].elapsed_time(e[1]))
+            tb.append(e[1].elapsed_time(e[2]))
+        f, b = float(np.median(tf)), float(np.median(tb))
+        res.update({"fwd_pass_ms": f, name + "bwd_pass_ms": b, name + "step_ms": f + b,
+                    name + "tokens_per_s": N / ((f + b) * 1e-3)})
+    del dH, dV, dK, ws, coefs
+    return res
+
+
 def block_pass_bytes(t, c, N, d, r, mode, es=2):
     """Algorithmic HBM bytes of the fused block call at site t: the earlier
     fp32 slots (with their fp32 key slots for projected keys) read once, the
@@ -642,6 +706,10 @@ def extras(torch, lr, dev, reps, warmup):
                                                             6, reps, warmup, flush)
     out["block_model_pass_projected_r32_8blocks"] = block_pass(torch, lr, dev, V, PROJECTED,
                                                                32, 6, reps, warmup, flush)
+    out["model_training_pass_projected_r16"] = model_training_pass(
+        torch, lr, dev, V, K, PROJECTED, 16, 3, 1)
+    out["model_training_pass_sliced_r64"] = model_training_pass(
+        torch, lr, dev, V, None, SLICED, 64, 3, 1)
     out["block_training_pass_sliced_r64_8blocks"] = block_training_pass(
         torch, lr, dev, V, SLICED, 64, 6, 5, 1)
     out["block_training_pass_projected_r32_8blocks"] = block_training_pass(
@@ -676,6 +744,14 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
                 block_training_pass(torch, lr, dev, g["V"], mode, r, 6, 5, 1)
         del g
         torch.cuda.empty_cache()
+    if "model_training" in names:
+        N, d = 16384, 1024
+        for mode, r in ((PROJECTED, 16), (SLICED, 64)):
+            g = make_device_problem(mode, 49, N, d, r, dev, seed=0, n_queries=1)
+            out[f"model_training_pass_{'projected' if mode == PROJECTED else 'sliced'}_r{r}"] = \
+                model_training_pass(torch, lr, dev, g["V"], g["K"], mode, r, 3, 1)
+            del g
+            torch.cuda.empty_cache()
     if "all_sites" in names:
         N, d, T = 16384, 1024, 48
         for mode, r in ((PROJECTED, 16), (SLICED, 64)):
@@ -708,8 +784,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--extra-only", default="",
                     help="comma-separated workloads to run alone, without the main step "
-                         "(key_producer, all_sites, block_training; per_site adds the per-site "
-                         "backward beside the all-sites one); prints their JSON")
+                         "(key_producer, all_sites, block_training, model_training; per_site "
+                         "adds the per-site backward beside the all-sites one); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
                          "backward calls of the main workload (for rocprofv3 --pmc runs)")

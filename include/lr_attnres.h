@@ -291,6 +291,56 @@ int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const voi
                                int mode, int dtype, float eps, void *stream);
 
 /*
+ * The reverse pass of a full-source model in deferred form (gradient of
+ * Sec. 3.1 Eq. full_attnres_source_set with Sec. 3.2; the paper states no
+ * backward).  Site t reads the sources 0 .. t-1 and is the only site that
+ * has source t-1 as its newest; once site t's backward is done, every site
+ * that reads source t-1 has recorded its share, so source t-1's gradient is
+ * final.  Instead of adding into the gradient rows of all t sources at every
+ * site (lr_attnres_route_bwd_accumulate), each site records three numbers
+ * per source and token, and one gather per source then forms that source's
+ * whole gradient from the sites that read it: dV_i = sum_t alpha_{t,i} dH_t
+ * plus, on the key, sum_t (ds/rho) q_t - (sum_t ds s/(rho r)) kbar_i.
+ *
+ * lr_attnres_route_bwd_deferred: one site, arguments as for
+ * lr_attnres_route_bwd except that no gradient rows are written:
+ *   coef [S][3][N] fp32, overwritten: for every source i of the site,
+ *        alpha_i, ds_i / rho_i and ds_i s_i / (rho_i r) per token;
+ *   dq [r] fp32: the site's query gradient (summed over tokens).
+ * Projected or sliced keys (full-rank keys: EUNSUPPORTED); other limits and
+ * errors as for lr_attnres_route_bwd, with coef among the outputs.
+ *
+ * lr_attnres_route_gather_bwd: the gradient of one source from the n_sites
+ * sites that read it:
+ *   V [S][N][d], K [S][N][r] (projected, else NULL): the stacks; only plane
+ *        `source` is read (its key: the last r columns of V or K's row);
+ *   dHs [n_sites][N][d] storage `dtype`, Q [n_sites][r] fp32: those sites'
+ *        upstream gradients and queries, in the order of their coefficients;
+ *   coef: site u's coefficients for this source at coef + u * coef_site_stride
+ *        (3 rows of N floats, as written by lr_attnres_route_bwd_deferred at
+ *        that site plus 3 N * source); coef_site_stride >= 3 N;
+ *   dV [N][d], dK [N][r] (projected, else NULL) storage `dtype`, overwritten:
+ *        the source's gradient (with sliced keys the key path is in the last
+ *        r columns of dV).  n_sites = 0 writes zeros.
+ * EINVAL for source outside [0, S), negative n_sites, a short stride,
+ * misalignment (V, dV, dHs 16 bytes) or overlap of the outputs with the
+ * inputs; EUNSUPPORTED for full-rank keys, d % 4 != 0 or d > 2048,
+ * n_sites > 1024 or n_sites * r > 16384, N > 2^30.
+ * Driving the reverse pass: for t = T down to 1, lr_attnres_route_bwd_deferred
+ * at site t, then lr_attnres_route_gather_bwd for source t - 1 over sites
+ * t .. T.  The results equal the accumulating pass up to rounding order.
+ */
+int lr_attnres_route_bwd_deferred(const void *V, const void *K, const float *q, const void *dH,
+                                  float *coef, float *dq, void *workspace, size_t workspace_bytes,
+                                  int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                  float eps, void *stream);
+int lr_attnres_route_gather_bwd(const void *V, const void *K, int64_t source, const void *dHs,
+                                const float *Q, const float *coef, int64_t coef_site_stride,
+                                int64_t n_sites, void *dV, void *dK, int64_t S, int64_t N,
+                                int64_t d, int64_t r, int mode, int dtype, float eps,
+                                void *stream);
+
+/*
  * Every read site of a pass over one stack of sources, in one call (Sec. 3.1,
  * Eq. full_attnres_source_set: site t reads the sources 0 .. t-1; routing of
  * Sec. 3.2 with projected or sliced keys, Sec. 3.3-3.4), with each site's

@@ -68,6 +68,12 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_all_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64,
                                              i, i, f, vp]
     lib.lr_attnres_route_all_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_bwd_deferred.argtypes = [vp] * 7 + [ctypes.c_size_t, i64, i64, i64, i64,
+                                                             i, i, f, vp]
+    lib.lr_attnres_route_bwd_deferred.restype = ctypes.c_int
+    lib.lr_attnres_route_gather_bwd.argtypes = [vp, vp, i64, vp, vp, vp, i64, i64, vp, vp, i64, i64,
+                                                i64, i64, i, i, f, vp]
+    lib.lr_attnres_route_gather_bwd.restype = ctypes.c_int
     lib.lr_attnres_route_all_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i64, i, i]
     lib.lr_attnres_route_all_bwd_workspace_bytes.restype = ctypes.c_size_t
     lib.lr_attnres_route_all_bwd.argtypes = [vp] * 8 + [ctypes.c_size_t, i64, i64, i64, i64, i64,
@@ -204,6 +210,71 @@ def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool 
                                       mode, _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return H, neff
+
+
+def route_bwd_deferred(V, K, q, dH, mode, coef, eps: float = 1e-6, dq=None, workspace=None):
+    """One site of the full-source deferred reverse pass: writes the site's
+    coefficients for its S sources into coef [S, 3, N] fp32 (alpha, ds/rho,
+    ds s/(rho r)) and returns its dq [r] fp32.  V [S,N,d] and K (projected)
+    are the site's prefix of the stacks."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    if tuple(coef.shape) != (S, 3, N) or coef.dtype != torch.float32:
+        raise ValueError("coef must be fp32 [S, 3, N]")
+    if dq is None:
+        dq = torch.empty((r,), dtype=torch.float32, device=V.device)
+    code = _dtype_code(V)
+    need = lib.lr_attnres_route_bwd_workspace_bytes(S, N, d, r, mode, code)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=V.device)
+    rc = lib.lr_attnres_route_bwd_deferred(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                           _dev(q, "q", torch.float32), _dev(dH, "dH", V.dtype),
+                                           _dev(coef, "coef", torch.float32),
+                                           _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"),
+                                           workspace.numel(), S, N, d, r, mode, code, float(eps),
+                                           _stream(V))
+    _check(lib, rc)
+    return dq
+
+
+def route_gather_bwd(V, K, source: int, dHs, Q, coef, mode, eps: float = 1e-6, out=None):
+    """Gradient of one source from the sites that read it (deferred reverse
+    pass).  dHs [n_sites, N, d] and Q [n_sites, r] of those sites; coef a
+    view whose row u is site u's [3, N] coefficients for this source (e.g.
+    coefs[t0:, source] of a [T, S, 3, N] array).  Returns (dV [N, d],
+    dK [N, r] or None)."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    if V.dim() != 3 or Q.dim() != 2 or dHs.dim() != 3:
+        raise ValueError("V must be [S, N, d], Q [n_sites, r] and dHs [n_sites, N, d]")
+    S, N, d = V.shape
+    r = K.shape[2] if mode == PROJECTED else Q.shape[1]
+    n_sites = dHs.shape[0]
+    if Q.shape[0] != n_sites or Q.shape[1] != r or tuple(dHs.shape[1:]) != (N, d):
+        raise ValueError("Q must be [n_sites, r] and dHs [n_sites, N, d]")
+    if coef.dim() != 3 or tuple(coef.shape[1:]) != (3, N) or coef.shape[0] != n_sites:
+        raise ValueError("coef must be [n_sites, 3, N]")
+    if not coef.is_cuda or coef.dtype != torch.float32 or (
+            n_sites > 0 and (coef.stride(1) != N or coef.stride(2) != 1)):
+        raise ValueError("coef must be fp32 on the device, each site's 3 rows of N contiguous")
+    if out is not None:
+        dV, dK = out
+    else:
+        dV = torch.empty((N, d), dtype=V.dtype, device=V.device)
+        dK = torch.empty((N, r), dtype=V.dtype, device=V.device) if mode == PROJECTED else None
+    rc = lib.lr_attnres_route_gather_bwd(_dev(V, "V"), _dev(K, "K", V.dtype), source,
+                                         _dev(dHs, "dHs", V.dtype), _dev(Q, "Q", torch.float32),
+                                         coef.data_ptr(), coef.stride(0) if n_sites > 0 else 3 * N,
+                                         n_sites,
+                                         _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
+                                         S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return dV, dK
 
 
 def route_all_bwd(V, K, Q, dH, mode, first: int, eps: float = 1e-6, out=None,

@@ -637,6 +637,100 @@ int lr_attnres_block_route_bwd_deferred(float *B, float *KB, float *dP, float *d
     return LRAR_OK;
 }
 
+int lr_attnres_route_bwd_deferred(const void *V, const void *K, const float *q, const void *dH,
+                                  float *coef, float *dq, void *workspace, size_t workspace_bytes,
+                                  int64_t S, int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                  float eps, void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(dH, "dH", 16, data)) || (rc = check_ptr(coef, "coef", 4, data)) ||
+        (rc = check_ptr(dq, "dq", 4, true)) || (rc = check_ptr(K, "K", 16, data && proj)) ||
+        (rc = check_ptr(workspace, "workspace", 16, false)))
+        return rc;
+    if (!proj && K)
+        return fail(LRAR_EINVAL, "K must be NULL unless keys are projected");
+    if (mode == LRAR_MODE_FULL)
+        return fail(LRAR_EUNSUPPORTED, "the deferred backward takes projected or sliced keys");
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps, dtype};
+    std::string why;
+    if ((rc = lrar::check_supported(p, true, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::bwd_workspace_bytes(p);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t nc;
+    if (!mul_ok(S, 3 * N, &nc))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const Span outs[] = {span("coef", coef, nc * 4), span("dq", dq, r * 4),
+                         span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4),
+                        span("dH", dH, he * es)};
+    if ((rc = check_aliasing(outs, 3, ins, 4)))
+        return rc;
+    if ((rc = lrar::launch_bwd_deferred_all(p, dH, coef, dq, workspace,
+                                            static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+int lr_attnres_route_gather_bwd(const void *V, const void *K, int64_t source, const void *dHs,
+                                const float *Q, const float *coef, int64_t coef_site_stride,
+                                int64_t n_sites, void *dV, void *dK, int64_t S, int64_t N,
+                                int64_t d, int64_t r, int mode, int dtype, float eps,
+                                void *stream)
+{
+    g_last_error.clear();
+    if (source < 0 || n_sites < 0)
+        return fail(LRAR_EINVAL, "source and n_sites must be >= 0");
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    if (source >= S)
+        return fail(LRAR_EINVAL, "source must be < S");
+    if (mode == LRAR_MODE_FULL)
+        return fail(LRAR_EUNSUPPORTED, "the source gather takes projected or sliced keys");
+    if (n_sites > 0 && coef_site_stride < 3 * N)
+        return fail(LRAR_EINVAL, "coef_site_stride must be at least 3 N");
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(dV, "dV", 16, data)) ||
+        (rc = check_ptr(dHs, "dHs", 16, data && n_sites > 0)) ||
+        (rc = check_ptr(Q, "Q", 4, n_sites > 0)) ||
+        (rc = check_ptr(coef, "coef", 4, data && n_sites > 0)) ||
+        (rc = check_ptr(K, "K", es, data && proj)) || (rc = check_ptr(dK, "dK", es, data && proj)))
+        return rc;
+    if (!proj && (K || dK))
+        return fail(LRAR_EINVAL, "K and dK must be NULL unless keys are projected");
+    int64_t hs, qn, cn, nr;
+    if (!mul_ok(n_sites, he, &hs) || !mul_ok(hs, es, &hs) || !mul_ok(n_sites, r, &qn) ||
+        !mul_ok(n_sites > 0 ? n_sites - 1 : 0, coef_site_stride, &cn) || !mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    cn = n_sites > 0 ? cn + 3 * N : 0;
+    const Span outs[] = {span("dV", dV, he * es), span("dK", dK, nr * es)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("dHs", dHs, hs),
+                        span("Q", Q, qn * 4), span("coef", coef, cn * 4)};
+    if ((rc = check_aliasing(outs, 2, ins, 5)))
+        return rc;
+    lrar::BlockGather g{static_cast<const char *>(V) + source * he * es,
+                        proj ? static_cast<const char *>(K) + source * nr * es : nullptr,
+                        dHs, Q, coef, coef_site_stride, n_sites, dV, dK, N, d, r, mode, dtype, eps};
+    g.kdtype = dtype;
+    std::string why;
+    if ((rc = lrar::launch_block_gather(g, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 int lr_attnres_block_gather_bwd(const float *B, const float *KB, int64_t slot, const void *dHs,
                                 const float *Q, const float *coef, int64_t coef_site_stride,
                                 int64_t n_sites, float *dP, float *dKP, int64_t N, int64_t d,

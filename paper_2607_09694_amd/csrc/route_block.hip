@@ -579,16 +579,19 @@ int check_block_supported(const BlockProblem &p, std::string *why)
 // ---------------------------------------------------------------------------
 
 struct GatherArgs {
-    const float *Bj, *KBj;
+    const void *Bj, *KBj;  // the source's rows [N][d] and key rows [N][r], storage TK
     const void *dHs;
     const float *Q, *coef;
     long long site_stride;
-    float *dP, *dKP;
+    void *dP, *dKP;        // its gradient rows, storage TK
     int n_sites, N, d, r, sliced, s_pad;
     float eps;
 };
 
-template <typename TH, int NCH, bool FULLCOLS>
+// TK: storage of the source rows read for the key and of the gradient rows
+// written (fp32 for block summaries, the model dtype for the sources of a
+// full-source pass); TH: storage of dH.
+template <typename TK, typename TH, int NCH, bool FULLCOLS>
 __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
 {
     extern __shared__ float lds[];
@@ -616,10 +619,13 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
 
     // rho of the slot's key: the last r columns of the summary (sliced) or
     // its projected key summary.
-    const float *key = a.sliced ? a.Bj + (size_t)n * a.d + (a.d - a.r) : a.KBj + (size_t)n * a.r;
+    const TK *key = a.sliced ? static_cast<const TK *>(a.Bj) + (size_t)n * a.d + (a.d - a.r)
+                             : static_cast<const TK *>(a.KBj) + (size_t)n * a.r;
     float ss = 0.0f;
-    for (int e = lane; e < a.r; e += kWaveSize)
-        ss = fmaf(key[e], key[e], ss);
+    for (int e = lane; e < a.r; e += kWaveSize) {
+        const float x = load_elem(key + e);
+        ss = fmaf(x, x, ss);
+    }
     const float rho = sqrtf(wave_sum(ss) / (float)a.r + a.eps);
     const float kscale = a.n_sites > 0 ? ck_sum / rho : 0.0f;
     // The key-column term of key element e: sum_t cq_t q_t[e] - kscale * k[e].
@@ -627,7 +633,7 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
         float v = 0.0f;
         for (int u = 0; u < a.n_sites; ++u)
             v = fmaf(cq[u], Qs[u * a.r + e], v);
-        return v - kscale * key[e];
+        return v - kscale * load_elem(key + e);
     };
 
     const int col = lane * 4;
@@ -638,7 +644,7 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
     float acc[NCH][4];
     mix_rows<TH, 4, NCH, FULLCOLS>(static_cast<const TH *>(a.dHs) + (size_t)n * a.d + col,
                                    N * a.d, a.n_sites, al, ok, acc);
-    float *prow = a.dP + (size_t)n * a.d + col;
+    TK *prow = static_cast<TK *>(a.dP) + (size_t)n * a.d + col;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!(FULLCOLS || ok[c]))
@@ -651,11 +657,11 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
                     acc[c][e] += key_term(kc);
             }
         }
-        store_raw<float, 4>(prow + c * kWaveSize * 4, Narrow<float, 4>::run(acc[c]));
+        store_raw<TK, 4>(prow + c * kWaveSize * 4, Narrow<TK, 4>::run(acc[c]));
     }
     if (!a.sliced && a.dKP) {
         for (int e = lane; e < a.r; e += kWaveSize)
-            a.dKP[(size_t)n * a.r + e] = key_term(e);
+            store_elem(static_cast<TK *>(a.dKP) + (size_t)n * a.r + e, key_term(e));
     }
 }
 
@@ -706,11 +712,12 @@ int launch_block_gather(const BlockGather &g, hipStream_t st, std::string *err)
     const bool fullcols = g.d % (256 * nch) == 0;
     const size_t lds = ((size_t)kWaves * 3 * a.s_pad + (size_t)a.n_sites * a.r) * sizeof(float);
     const dim3 grid((unsigned)((g.N + kWaves - 1) / kWaves));
-    auto go = [&](auto th) {
+    auto go = [&](auto tk, auto th) {
+        typedef decltype(tk) TK;
         typedef decltype(th) TH;
         auto launch = [&](auto nchc, auto fc) {
-            hipLaunchKernelGGL((block_gather<TH, decltype(nchc)::value, decltype(fc)::value>), grid,
-                               dim3(kBlock), lds, st, a);
+            hipLaunchKernelGGL((block_gather<TK, TH, decltype(nchc)::value, decltype(fc)::value>),
+                               grid, dim3(kBlock), lds, st, a);
         };
         auto by_fc = [&](auto nchc) {
             if (fullcols)
@@ -725,10 +732,14 @@ int launch_block_gather(const BlockGather &g, hipStream_t st, std::string *err)
         default: by_fc(std::integral_constant<int, 8>{}); break;
         }
     };
-    if (g.dtype == LRAR_DTYPE_BF16)
-        go(uint16_t{});
-    else
-        go(float{});
+    if (g.kdtype == LRAR_DTYPE_F32) {
+        if (g.dtype == LRAR_DTYPE_BF16)
+            go(float{}, uint16_t{});
+        else
+            go(float{}, float{});
+    } else {
+        go(uint16_t{}, uint16_t{});  // bf16 sources, bf16 dH
+    }
     return hip_status(hipGetLastError(), "block_gather launch", err);
 }
 

@@ -40,6 +40,10 @@ template <int KV> struct KeyChunks { static constexpr int value = KV == 8 ? 1 : 
 // the new running row (dO, dK in the model dtype), and it leaves the slot
 // (Bp -= o_new, KBp -= k_new) once the slot row has been read for the last
 // time (the key columns after the key pass).
+// DALL (every source deferred): the coefficients of every source, the last
+// one included, are written, and no gradient row at all; each source's
+// gradient is then gathered once from the sites that read it (the
+// full-source reverse pass).
 struct DeferOut {
     float *coef;
     const void *o_new, *k_new;  // model dtype
@@ -48,7 +52,7 @@ struct DeferOut {
 };
 
 template <typename T, typename TH, int VEC, int NCH, bool FULLCOLS, int KV, bool ACC,
-          bool DEFER = false>
+          bool DEFER = false, bool DALL = false>
 __global__ void __launch_bounds__(kBlock)
 route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
              const TH *__restrict__ dH, T *__restrict__ dV, T *__restrict__ dK,
@@ -133,7 +137,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                 const size_t off = (size_t)(i0 + h + u) * plane + c * kWaveSize * VEC;
                                 raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + off);
                                 if constexpr (ACC)
-                                    if (wr[c] && (!DEFER || i0 + h + u == S - 1))
+                                    if (wr[c] && (!DEFER || (!DALL && i0 + h + u == S - 1)))
                                         old[u][c] = load_stream<T, VEC, kNtLoad>(
                                             dvbase + (DEFER ? c * kWaveSize * VEC : off));
                             }
@@ -153,7 +157,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                     p = fmaf(dh[c][e], x[e], p);
                                     y[e] = a * dh[c][e];
                                 }
-                                const bool wdv = wr[c] && (!DEFER || i == S - 1);
+                                const bool wdv = wr[c] && (!DEFER || (!DALL && i == S - 1));
                                 if constexpr (ACC)
                                     if (wdv)
                                         add_stored(y, old[u][c]);
@@ -161,7 +165,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                     store_stream<T, VEC, kNtStore>(
                                         dvbase + (DEFER ? 0 : (size_t)i * plane) + c * kWaveSize * VEC,
                                         Narrow<T, VEC>::run(y));
-                                if constexpr (DEFER) {
+                                if constexpr (DEFER && !DALL) {
                                     if (wdv) {
                                         // retire: dO = the new running row;
                                         // the member leaves the slot
@@ -222,7 +226,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                 const float dsi = g[i];
                 const float cq = dsi * ri;              // ds_i / rho_i
                 const float ck = cq * s[i] * inv_r;     // ds_i s_i / (rho_i r)
-                const bool defer_i = DEFER && i < S - 1;
+                const bool defer_i = DEFER && (DALL || i < S - 1);
                 const size_t orow = DEFER ? (size_t)n : row;  // output row of source i
                 if (defer_i && k == 0 && vl == 0) {
                     coef[((size_t)i * 3 + 0) * N + n] = alpha[i];
@@ -243,7 +247,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                     if constexpr (ACC)
                         add_stored(y, load_raw<T, KV>(dK + orow * r + c0));
                     store_raw<T, KV>(dK + orow * r + c0, Narrow<T, KV>::run(y));
-                    if constexpr (DEFER) {
+                    if constexpr (DEFER && !DALL) {
                         // retire the member's key: dK = the new running key
                         // row; the key leaves the slot's key summary
                         const size_t ro = (size_t)n * r + c0;
@@ -271,7 +275,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                     if constexpr (ACC)
                         add_stored(y, load_raw<T, KV>(dV + orow * d + c0));
                     store_raw<T, KV>(dV + orow * d + c0, Narrow<T, KV>::run(y));
-                    if constexpr (DEFER) {
+                    if constexpr (DEFER && !DALL) {
                         // retire the member's columns of the key pass: its
                         // gradient, and the slot without it (the slot row
                         // was read here for the last time)
@@ -526,7 +530,7 @@ KeyPass key_pass(const Problem &p, const Plan &pl)
     return k;
 }
 
-template <typename T, typename TH, int VEC, bool ACC, bool DEFER = false>
+template <typename T, typename TH, int VEC, bool ACC, bool DEFER = false, bool DALL = false>
 hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *dV, void *dK,
                         float *partial, hipStream_t st, const DeferOut &dfo = DeferOut{})
 {
@@ -551,7 +555,7 @@ hipError_t launch_bwd_t(const Problem &p, const Plan &pl, const void *dH, void *
         }
         auto launch = [&](auto kvc) {
             constexpr int KV = decltype(kvc)::value;
-            hipLaunchKernelGGL((route_bwd_lr<T, TH, VEC, NCH, FC, KV, ACC, DEFER>),
+            hipLaunchKernelGGL((route_bwd_lr<T, TH, VEC, NCH, FC, KV, ACC, DEFER, DALL>),
                                dim3(pl.nblocks), dim3(kBlock), pl.lds, st, V, keys, p.q,
                                static_cast<const TH *>(dH), static_cast<T *>(dV),
                                static_cast<T *>(dK), partial, (int)p.S, (int)p.N, (int)p.d,
@@ -655,6 +659,37 @@ int launch_block_bwd_deferred(const Problem &p, const BlockRetire &br, const voi
         e = hipGetLastError();
     }
     return hip_status(e, "block_route_bwd_deferred launch", err);
+}
+
+int launch_bwd_deferred_all(const Problem &p, const void *dH, float *coef, float *dq, void *ws,
+                            hipStream_t st, std::string *err)
+{
+    if (p.mode == LRAR_MODE_FULL) {
+        *err = "the deferred backward takes projected or sliced keys";
+        return LRAR_EUNSUPPORTED;
+    }
+    Plan pl;
+    if (!make_plan(p, true, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    float *partial = static_cast<float *>(ws);
+    DeferOut dfo;
+    dfo.coef = coef;
+    hipError_t e = hipSuccess;
+    if (p.N > 0) {
+        if (p.dtype == LRAR_DTYPE_BF16)
+            e = pl.vec > 1 ? launch_bwd_t<uint16_t, uint16_t, 8, false, true, true>(
+                                 p, pl, dH, nullptr, nullptr, partial, st, dfo)
+                           : launch_bwd_t<uint16_t, uint16_t, 1, false, true, true>(
+                                 p, pl, dH, nullptr, nullptr, partial, st, dfo);
+        else
+            e = pl.vec > 1 ? launch_bwd_t<float, float, 4, false, true, true>(
+                                 p, pl, dH, nullptr, nullptr, partial, st, dfo)
+                           : launch_bwd_t<float, float, 1, false, true, true>(
+                                 p, pl, dH, nullptr, nullptr, partial, st, dfo);
+    }
+    if (e == hipSuccess)
+        e = launch_dq_reduce(partial, dq, p.N > 0 ? pl.nblocks : 0, (int)p.r, false, st);
+    return hip_status(e, "route_bwd_deferred launch", err);
 }
 
 int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, void *dB,

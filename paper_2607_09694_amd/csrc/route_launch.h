@@ -97,18 +97,27 @@ int launch_block_bwd_deferred(const Problem &p, const BlockRetire &br, const voi
                               float *dKP, float *coef, float *dq, void *ws, hipStream_t st,
                               std::string *err);
 
+// One site of the full-source deferred reverse pass (see
+// lr_attnres_route_bwd_deferred): the coefficients of every source into
+// coef [S][3][N] and dq; no gradient rows.
+int launch_bwd_deferred_all(const Problem &p, const void *dH, float *coef, float *dq, void *ws,
+                            hipStream_t st, std::string *err);
+
 // A completed slot's gradient from the sites that read it as completed (see
 // lr_attnres_block_gather_bwd).
 struct BlockGather {
-    const float *Bj, *KBj;  // the slot's summary rows [N][d], key rows [N][r] or NULL
+    const void *Bj, *KBj;   // the source's rows [N][d], key rows [N][r] or NULL (storage kdtype)
     const void *dHs;        // [n_sites][N][d] model dtype
     const float *Q;         // [n_sites][r]
     const float *coef;      // site u's coefficients at coef + u * site_stride ([3][N])
     int64_t site_stride, n_sites;
-    float *dP, *dKP;        // [N][d], [N][r] or NULL; overwritten
+    void *dP, *dKP;         // [N][d], [N][r] or NULL, storage kdtype; overwritten
     int64_t N, d, r;
     int mode, dtype;
     float eps;
+    // Storage of Bj, KBj, dP and dKP: fp32 for block summaries; the model
+    // dtype for the sources of a full-source pass (lr_attnres_route_gather_bwd).
+    int kdtype = LRAR_DTYPE_F32;
 };
 
 int check_gather_supported(const BlockGather &g, std::string *why);

@@ -46,6 +46,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_key_proj_fwd", "lr_attnres_route_neff",
                             "lr_attnres_block_route_bwd_deferred", "lr_attnres_block_gather_bwd",
                             "lr_attnres_route_all_bwd", "lr_attnres_route_all_bwd_workspace_bytes",
+                            "lr_attnres_route_bwd_deferred", "lr_attnres_route_gather_bwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -369,6 +370,65 @@ def test_all_sites_backward_unsupported(lib):
     assert allb(lib, S=65, T=3) == EUNSUPPORTED
     assert allb(lib, mode=P, K=W, dK=W + 0x1_0000_0000, r=65, d=128) == EUNSUPPORTED
     assert allb(lib, d=68) == EUNSUPPORTED
+
+
+def sdef(lib, V=A, K=None, q=B, dH=C, coef=D, dq=E, ws=G, ws_bytes=1 << 20, S=6, N=8, d=64, r=8,
+         mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_bwd_deferred(V, K, q, dH, coef, dq, ws, ws_bytes, S, N, d, r, mode,
+                                             dtype, eps, None)
+
+
+def sgat(lib, V=A, K=None, source=2, dHs=C, Q=B, coef=D, stride=3 * 8 * 6, n_sites=4, dV=E,
+         dK=None, S=6, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_gather_bwd(V, K, source, dHs, Q, coef, stride, n_sites, dV, dK, S,
+                                           N, d, r, mode, dtype, eps, None)
+
+
+SDEF_INVALID = [
+    ("coef NULL", dict(coef=None), "coef is NULL"),
+    ("dq NULL", dict(dq=None), "dq is NULL"),
+    ("K outside projected", dict(K=W), "must be NULL"),
+    ("coef misaligned", dict(coef=D + 2), "4-byte aligned"),
+    ("coef overlaps V", dict(coef=A + 64), "overlaps"),
+    ("coef overlaps the workspace", dict(ws=D + 64), "overlap"),
+    ("workspace too small", dict(ws_bytes=4), "workspace too small"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", SDEF_INVALID, ids=[c[0] for c in SDEF_INVALID])
+def test_deferred_site_rejects(lib, name, kw, msg):
+    assert sdef(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_deferred_site_rejects_full_rank(lib):
+    assert sdef(lib, mode=F, r=64) == EUNSUPPORTED
+    assert "projected or sliced" in err(lib)
+
+
+SGAT_INVALID = [
+    ("negative source", dict(source=-1), "source and n_sites"),
+    ("source past the stack", dict(source=6), "source must be < S"),
+    ("negative n_sites", dict(n_sites=-1), "source and n_sites"),
+    ("short stride", dict(stride=3 * 8 - 1), "coef_site_stride"),
+    ("dV NULL", dict(dV=None), "dV is NULL"),
+    ("dHs NULL", dict(dHs=None), "dHs is NULL"),
+    ("dK NULL when projected", dict(mode=P, K=W), "dK is NULL"),
+    ("dV misaligned", dict(dV=E + 8), "16-byte aligned"),
+    ("dV overlaps dHs", dict(dV=C + 64), "overlaps"),
+    ("dV overlaps coef", dict(dV=D + 256), "overlaps"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", SGAT_INVALID, ids=[c[0] for c in SGAT_INVALID])
+def test_source_gather_rejects(lib, name, kw, msg):
+    assert sgat(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_source_gather_unsupported(lib):
+    assert sgat(lib, mode=F, r=64) == EUNSUPPORTED
+    assert sgat(lib, d=4104, r=8) == EUNSUPPORTED
 
 
 def kproj(lib, A_=A, W=B, O=C, K=D, N=8, m=64, d=32, r=16, dtype=BF16):
