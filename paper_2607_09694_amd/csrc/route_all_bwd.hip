@@ -19,8 +19,10 @@
 //                                            products of bf16 operands),
 //     dV = alpha^T [S x T] * dH_n [T x d]    (alpha as hi + lo bf16, two MFMAs,
 //                                            as in the forward),
-//     u  = ds^T [S x T] * Q [T x r] and dQ += (ds / rho) [T x S] * K [S x r]
-//                                           (v_mfma_f32_16x16x4_f32).
+//     u  = ds^T [S x T] * Q [T x r]          (ds and Q as hi + lo bf16, three
+//                                            MFMAs: hi.hi + hi.lo + lo.hi),
+//     dQ += (ds / rho) [T x S] * K [S x r]   (ds / rho as hi + lo, the keys
+//                                            exact in bf16, two MFMAs).
 // Workgroups (4 waves, two per CU) are persistent over a stride of tokens
 // and keep their share of dQ in registers; a fixed-order reduction adds the
 // per-workgroup partials, so dQ is bitwise reproducible.  Wave w owns
@@ -68,6 +70,21 @@ struct AllBwdArgs {
 __device__ __forceinline__ int dh_chunk(int row, int c) { return row * kDhRowBytes + 16 * (c ^ (row & 15)); }
 
 __device__ __forceinline__ float bf16_at(const uint16_t *p) { return __uint_as_float((unsigned)*p << 16); }
+
+// 8 fp32 values as an MFMA operand pair: hi = RNE(v), lo = RNE(v - hi), so
+// that hi + lo carries v to a relative 2^-17.
+__device__ __forceinline__ void split_hilo(const float (&v)[8], bf16x8_t &hi, bf16x8_t &lo)
+{
+    u32x4_t h, l;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const unsigned w = pack_bf16x2(v[2 * k], v[2 * k + 1]);
+        h[k] = w;
+        l[k] = pack_bf16x2(v[2 * k] - bf16_lo(w), v[2 * k + 1] - bf16_hi(w));
+    }
+    hi = __builtin_bit_cast(bf16x8_t, h);
+    lo = __builtin_bit_cast(bf16x8_t, l);
+}
 
 // Keep x opaque to the optimiser for one token: the per-token control flow
 // (masks of sites, sources and columns, row offsets) is then formed inside
@@ -325,22 +342,37 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
                     dsr[(16 * mt + 4 * ks + e) * kAlphaRow + src] = ds[mt][e] * inv;
         }
 
-        // u_i = sum_j ds[j][i] Q_j: the MFMA's k index ks at step (mt, e)
-        // stands for site 16 mt + 4 ks + e, on both operands.
+        // u_i = sum_j ds[j][i] Q_j over site groups of 32: the MFMA's k
+        // index 8 ks + e stands for site 16 (2 kg + e / 4) + 4 ks + e mod 4 on
+        // both operands, so the A operand is this lane's ds as it stands.
         f32x4_t uk[RT];
 #pragma unroll
-        for (int ct = 0; ct < RT; ++ct) {
-            __builtin_amdgcn_sched_barrier(0);
+        for (int ct = 0; ct < RT; ++ct)
             uk[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-            const int c = 16 * ct + lc;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
+        for (int kg = 0; kg < KG; ++kg) {
+            float dv[8];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int site = 16 * mt + 4 * ks + e;
-                    const float qv = (site < a.T && c < a.r) ? qs[site * a.r + c] : 0.0f;
-                    uk[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(ds[mt][e], qv, uk[ct], 0, 0, 0);
+            for (int e = 0; e < 8; ++e)
+                dv[e] = 2 * kg + e / 4 < MT ? ds[(2 * kg + e / 4) % MT][e % 4] : 0.0f;
+            bf16x8_t Dhi, Dlo;
+            split_hilo(dv, Dhi, Dlo);
+#pragma unroll
+            for (int ct = 0; ct < RT; ++ct) {
+                __builtin_amdgcn_sched_barrier(0);
+                const int c = 16 * ct + lc;
+                float qv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int site = 16 * (2 * kg + e / 4) + 4 * ks + e % 4;
+                    qv[e] = (site < a.T && c < a.r) ? qs[site * a.r + c] : 0.0f;
                 }
+                bf16x8_t Qhi, Qlo;
+                split_hilo(qv, Qhi, Qlo);
+                uk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Dhi, Qhi, uk[ct], 0, 0, 0);
+                uk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Dhi, Qlo, uk[ct], 0, 0, 0);
+                uk[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Dlo, Qhi, uk[ct], 0, 0, 0);
+            }
         }
         // dk_i = (u_i - k_i (k_i . u_i) / (rho_i^2 r)) / rho_i; lane (lc, ks)
         // holds sources 16 wave + 4 ks + e at key column 16 ct + lc.  Projected
@@ -379,17 +411,31 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
 
         // dQ_j += sum_i (ds[j][i] / rho_i) k_i: wave w takes the sites of tile w.
         lds_barrier();
+        // A: ds / rho of site 16 wave + lc at sources 32 kg + 8 ks + e (zero
+        // past S); B: the keys of those sources at column 16 ct + lc (zero
+        // past S and r in LDS).
         if (wave < MT) {
-            const int nst = (a.S + 3) / 4;
-#pragma unroll
-            for (int ct = 0; ct < RT; ++ct) {
-                const int c = 16 * ct + lc;
+            const int nkg = (a.S + 31) / 32;
 #pragma unroll 1
-                for (int st = 0; st < nst; ++st) {
-                    const int i = 4 * st + ks;
-                    const float A = dsr[(16 * wave + lc) * kAlphaRow + i];
-                    const float B = (i < a.S && c < a.r) ? bf16_at(keys + i * kKeyRow + c) : 0.0f;
-                    dq[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(A, B, dq[ct], 0, 0, 0);
+            for (int kg = 0; kg < nkg; ++kg) {
+                const float *ar = dsr + (16 * wave + lc) * kAlphaRow + 32 * kg + 8 * ks;
+                const f32x4_t a0 = *reinterpret_cast<const f32x4_t *>(ar);
+                const f32x4_t a1 = *reinterpret_cast<const f32x4_t *>(ar + 4);
+                const float av8[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                bf16x8_t Ahi, Alo;
+                split_hilo(av8, Ahi, Alo);
+#pragma unroll
+                for (int ct = 0; ct < RT; ++ct) {
+                    const int c = 16 * ct + lc;
+                    u32x4_t kb;
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        const uint16_t *k0 = keys + (32 * kg + 8 * ks + 2 * h) * kKeyRow + c;
+                        kb[h] = (unsigned)k0[0] | ((unsigned)k0[kKeyRow] << 16);
+                    }
+                    const bf16x8_t B = __builtin_bit_cast(bf16x8_t, kb);
+                    dq[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ahi, B, dq[ct], 0, 0, 0);
+                    dq[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Alo, B, dq[ct], 0, 0, 0);
                 }
             }
         }
