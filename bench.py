@@ -548,6 +548,36 @@ def decode_model_pass(torch, lr, dev, reps, warmup, N=128, d=1024, r=16):
             "graph_tokens_per_s": N / (replay * 1e-3)}
 
 
+def split_sources(torch, lr, dev, reps, warmup, flush, S=49, d=1024, r=16):
+    """The deepest site (49 sources, d = 1024, P-LR r = 16) at decode-sized
+    token counts: the one-call forward against per-chunk states + merge
+    (Sec. 3.5's merge form over the sources), cold, for several chunk sizes."""
+    from paper_2607_09694_amd.inputs import PROJECTED, make_device_problem
+
+    res = {}
+    for N in (16, 128, 1024):
+        g = make_device_problem(PROJECTED, S, N, d, r, dev, seed=6)
+        V, K, q = g["V"], g["K"], g["q"][0].contiguous()
+        H = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+        row = {"one_call_ms": float(np.median(time_calls(
+            torch, lambda: lr.route_fwd(V, K, q, PROJECTED, out=H), reps, warmup, flush)))}
+        for chunk in (1, 4, 7, 13, 25):
+            P = -(-S // chunk)
+            st = (torch.empty((P, N), dtype=torch.float32, device=dev),
+                  torch.empty((P, N), dtype=torch.float32, device=dev),
+                  torch.empty((P, N, d), dtype=torch.float32, device=dev))
+
+            def call():
+                lr.route_state_fwd(V, K, q, PROJECTED, chunk, out=st)
+                lr.route_merge_fwd(*st, out=H)
+
+            row[f"split_c{chunk}_ms"] = float(np.median(time_calls(torch, call, reps, warmup,
+                                                                    flush)))
+        res[f"N{N}"] = row
+        del g, V, K, H
+    return res
+
+
 def key_producer(torch, lr, dev, reps, warmup, flush):
     """The projected-key producer (Eq. fused_projection) at the paper's
     output projections (d = 1024; attention m = 1024, SwiGLU m = 2816) for
@@ -728,14 +758,19 @@ def extras(torch, lr, dev, reps, warmup):
 
 def focused(torch, lr, dev, names, reps=20, warmup=3):
     """Only the named workloads (for profiling one kernel at a time):
-    'key_producer' and 'all_sites' (sites 2..49 of the 49-source pass, P-LR
-    r = 16 and S-LR r = 64, cold)."""
+    'key_producer', 'split_sources' (the deepest site at decode token counts,
+    one call against states + merge), 'block_training', 'model_training' and
+    'all_sites' (sites 2..49 of the 49-source pass, P-LR r = 16 and S-LR
+    r = 64, cold; with 'per_site', also the per-site accumulating backward)."""
     from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_device_problem
 
     flush = Flusher(torch, dev)
     out = {}
     if "key_producer" in names:
         out["key_producer_d1024_N16384"] = key_producer(torch, lr, dev, reps, warmup, flush)
+    if "split_sources" in names:
+        out["split_sources_49src_d1024_projected_r16"] = split_sources(torch, lr, dev, reps,
+                                                                       warmup, flush)
     if "block_training" in names:
         N, d = 16384, 1024
         g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=1)

@@ -256,6 +256,36 @@ int lr_attnres_block_gather_bwd(const float *B, const float *KB, int64_t slot, c
                                 int64_t r, int mode, int dtype, float eps, void *stream);
 
 /*
+ * Split-sources forward (Sec. 3.5's merge of online-softmax states, applied
+ * to the sources of one site): the S sources are cut into P = ceil(S / chunk)
+ * consecutive chunks, and chunk p's state over sources p chunk ..
+ * min(S, (p + 1) chunk) - 1 is written per token:
+ *   M [P][N] = max score, L [P][N] = sum exp(s - M),
+ *   ACC [P][N][d] = sum exp(s - M) o_i      (all fp32, overwritten),
+ * with the scores of lr_attnres_route_fwd (same V, K, q, mode, dtype, eps).
+ * ACC / L is the routing over that chunk alone.  Each chunk is its own set of
+ * workgroups, so a small token count (decoding) still fills the device, and
+ * the states are what a pass whose sources are spread over several devices
+ * would exchange.  lr_attnres_route_merge_fwd turns them into h.
+ * EINVAL: chunk < 1, or as lr_attnres_route_fwd.  EUNSUPPORTED: chunk above
+ * 1024 (P any, up to 65535), or the row limits of lr_attnres_route_fwd.
+ */
+int lr_attnres_route_state_fwd(const void *V, const void *K, const float *q, float *M, float *L,
+                               float *ACC, int64_t S, int64_t N, int64_t d, int64_t r,
+                               int64_t chunk, int mode, int dtype, float eps, void *stream);
+
+/*
+ * H [N][d] (storage `dtype`) = sum_p e^(M_p - m) ACC_p / sum_p e^(M_p - m) L_p,
+ * m = max_p M_p: the routing over the union of the P chunks whose states
+ * (layout of lr_attnres_route_state_fwd) are given; with the states of all
+ * chunks of one site it equals lr_attnres_route_fwd's h up to rounding.
+ * EINVAL: P < 1, N < 0, d < 1, unknown dtype, misaligned or overlapping
+ * buffers.  EUNSUPPORTED: P above 1024.
+ */
+int lr_attnres_route_merge_fwd(const float *M, const float *L, const float *ACC, void *H,
+                               int64_t P, int64_t N, int64_t d, int dtype, void *stream);
+
+/*
  * Two-phase block inference (Sec. 3.5): the site queries do not depend on
  * the input, and routing over the completed slots merges with routing over
  * the partial block by an online-softmax update.  The c sites whose newest

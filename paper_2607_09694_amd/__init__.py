@@ -85,6 +85,11 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_block_gather_bwd.argtypes = [vp, vp, i64, vp, vp, vp, i64, i64, vp, vp, i64,
                                                 i64, i64, i, i, f, vp]
     lib.lr_attnres_block_gather_bwd.restype = ctypes.c_int
+    lib.lr_attnres_route_state_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64,
+                                               i, i, f, vp]
+    lib.lr_attnres_route_state_fwd.restype = ctypes.c_int
+    lib.lr_attnres_route_merge_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i, vp]
+    lib.lr_attnres_route_merge_fwd.restype = ctypes.c_int
     lib.lr_attnres_route_neff.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, i, f, vp]
     lib.lr_attnres_route_neff.restype = ctypes.c_int
     lib.lr_attnres_key_proj_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, vp]
@@ -162,6 +167,56 @@ def route_fwd(V, K, q, mode, eps: float = 1e-6, out=None):
     rc = lib.lr_attnres_route_fwd(_dev(V, "V"), _dev(K, "K", V.dtype),
                                   _dev(q, "q", torch.float32), _dev(H, "H", V.dtype),
                                   S, N, d, r, mode, _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return H
+
+
+def route_state_fwd(V, K, q, mode, chunk: int, eps: float = 1e-6, out=None):
+    """Online-softmax states of one site's routing over the sources cut into
+    chunks of ``chunk`` (Sec. 3.5's merge form): returns (M [P,N], L [P,N],
+    ACC [P,N,d]) fp32, P = ceil(S / chunk); ACC[p] / L[p] routes over chunk p.
+    ``out`` = (M, L, ACC) writes into given tensors of those shapes.
+    """
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    P = -(-S // int(chunk)) if chunk >= 1 else 1
+    if out is not None:
+        M, L, ACC = out
+        if tuple(M.shape) != (P, N) or tuple(L.shape) != (P, N) or tuple(ACC.shape) != (P, N, d):
+            raise ValueError(f"out must be ({P},{N}), ({P},{N}), ({P},{N},{d}) tensors")
+    else:
+        M = torch.empty((P, N), dtype=torch.float32, device=V.device)
+        L = torch.empty((P, N), dtype=torch.float32, device=V.device)
+        ACC = torch.empty((P, N, d), dtype=torch.float32, device=V.device)
+    rc = lib.lr_attnres_route_state_fwd(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                        _dev(q, "q", torch.float32),
+                                        _dev(M, "M", torch.float32), _dev(L, "L", torch.float32),
+                                        _dev(ACC, "ACC", torch.float32), S, N, d, r, int(chunk), mode,
+                                        _dtype_code(V), float(eps), _stream(V))
+    _check(lib, rc)
+    return M, L, ACC
+
+
+def route_merge_fwd(M, L, ACC, dtype=None, out=None):
+    """h from P online-softmax states (M, L [P,N], ACC [P,N,d] fp32): the
+    routing over the union of their sources, in ``dtype`` (default bf16)."""
+    import torch
+
+    lib = load_library()
+    if ACC.dim() != 3 or tuple(M.shape) != tuple(ACC.shape[:2]) or tuple(L.shape) != tuple(M.shape):
+        raise ValueError("need M, L [P, N] and ACC [P, N, d]")
+    P, N, d = ACC.shape
+    if out is not None:
+        dtype = out.dtype
+    dtype = dtype or torch.bfloat16
+    H = out if out is not None else torch.empty((N, d), dtype=dtype, device=ACC.device)
+    code = _BF16 if dtype == torch.bfloat16 else _F32
+    rc = lib.lr_attnres_route_merge_fwd(_dev(M, "M", torch.float32), _dev(L, "L", torch.float32),
+                                        _dev(ACC, "ACC", torch.float32), _dev(H, "H", dtype),
+                                        P, N, d, code, _stream(ACC))
     _check(lib, rc)
     return H
 

@@ -408,6 +408,72 @@ int lr_attnres_block_merge_fwd(float *B, float *KB, const void *o_new, const voi
     return LRAR_OK;
 }
 
+int lr_attnres_route_state_fwd(const void *V, const void *K, const float *q, float *M, float *L,
+                               float *ACC, int64_t S, int64_t N, int64_t d, int64_t r,
+                               int64_t chunk, int mode, int dtype, float eps, void *stream)
+{
+    g_last_error.clear();
+    int64_t ve, ke, he;
+    int rc = check_shape(S, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    if (chunk < 1)
+        return fail(LRAR_EINVAL, "chunk must be >= 1");
+    const int64_t P = (S + chunk - 1) / chunk;
+    const bool data = N > 0;
+    if ((rc = check_ptr(V, "V", 16, data)) || (rc = check_ptr(q, "q", 4, true)) ||
+        (rc = check_ptr(M, "M", 4, data)) || (rc = check_ptr(L, "L", 4, data)) ||
+        (rc = check_ptr(ACC, "ACC", 16, data)) ||
+        (rc = check_ptr(K, "K", 16, data && mode == LRAR_MODE_PROJECTED)))
+        return rc;
+    if (mode != LRAR_MODE_PROJECTED && K)
+        return fail(LRAR_EINVAL, "K must be NULL unless keys are projected");
+    int64_t pn, pnd;
+    if (!mul_ok(P, N, &pn) || !mul_ok(pn, d, &pnd))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    const Span outs[] = {span("M", M, pn * 4), span("L", L, pn * 4), span("ACC", ACC, pnd * 4)};
+    const Span ins[] = {span("V", V, ve * es), span("K", K, ke * es), span("q", q, r * 4)};
+    if ((rc = check_aliasing(outs, 3, ins, 3)))
+        return rc;
+    // The plan (and the source limit) is that of one chunk.
+    lrar::Problem p{V, K, q, S, N, d, r, mode, dtype, eps, dtype};
+    std::string why;
+    if ((rc = lrar::launch_state(p, chunk, M, L, ACC, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
+int lr_attnres_route_merge_fwd(const float *M, const float *L, const float *ACC, void *H,
+                               int64_t P, int64_t N, int64_t d, int dtype, void *stream)
+{
+    g_last_error.clear();
+    if (P < 1)
+        return fail(LRAR_EINVAL, "P must be >= 1");
+    if (N < 0 || d < 1)
+        return fail(LRAR_EINVAL, "need N >= 0 and d >= 1");
+    if (dtype != LRAR_DTYPE_F32 && dtype != LRAR_DTYPE_BF16)
+        return fail(LRAR_EINVAL, "dtype must be LRAR_DTYPE_F32 or LRAR_DTYPE_BF16");
+    int rc;
+    const bool data = N > 0;
+    if ((rc = check_ptr(M, "M", 4, data)) || (rc = check_ptr(L, "L", 4, data)) ||
+        (rc = check_ptr(ACC, "ACC", 16, data)) || (rc = check_ptr(H, "H", 16, data)))
+        return rc;
+    int64_t pn, pnd, nd;
+    if (!mul_ok(P, N, &pn) || !mul_ok(pn, d, &pnd) || !mul_ok(N, d, &nd))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    const Span outs[] = {span("H", H, nd * es)};
+    const Span ins[] = {span("M", M, pn * 4), span("L", L, pn * 4), span("ACC", ACC, pnd * 4)};
+    if ((rc = check_aliasing(outs, 1, ins, 3)))
+        return rc;
+    std::string why;
+    if ((rc = lrar::launch_merge(M, L, ACC, P, N, d, dtype, H, static_cast<hipStream_t>(stream),
+                                 &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 const char *lr_attnres_last_error(void) { return g_last_error.c_str(); }
 
 int lr_attnres_abi_version(void) { return LR_ATTNRES_ABI_VERSION; }

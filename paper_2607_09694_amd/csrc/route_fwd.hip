@@ -37,15 +37,155 @@ route_fwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
     store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)n * d + col, ok, acc);
 }
 
+// fp32 row segment of VEC values.
+template <int VEC>
+__device__ __forceinline__ void store_f32(float *p, const float (&x)[VEC])
+{
+    if constexpr (VEC % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < VEC; k += 4)
+            *reinterpret_cast<f32x4_t *>(p + k) = f32x4_t{x[k], x[k + 1], x[k + 2], x[k + 3]};
+    } else {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k)
+            p[k] = x[k];
+    }
+}
+
+// Online-softmax state of the routing over one chunk of the sources (Sec.
+// 3.5, the two-phase form that merges partial routings): chunk c =
+// blockIdx.z holds sources c chunk .. min(S, (c + 1) chunk) - 1, and per
+// token
+//     M = max_i s_i,  L = sum_i exp(s_i - M),  ACC = sum_i exp(s_i - M) o_i,
+// so ACC / L is the routing over that chunk, and route_merge combines the
+// chunks.  Splitting the sources gives small token counts (decoding) more
+// workgroups, and is the step a source-sharded pass exchanges.  Grid x, y
+// and layout as route_fwd_lr.
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock)
+route_state_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
+               float *__restrict__ M, float *__restrict__ L, float *__restrict__ ACC, int S, int N,
+               int d, int r, int krow, int koff, float eps, int s_pad, int chunk)
+{
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= N)
+        return;  // wave-uniform; this kernel has no workgroup barrier
+    const int c = blockIdx.z;
+    const int i0 = c * chunk;
+    const int sc = min(chunk, S - i0);
+    const size_t plane = (size_t)N * d;
+    float *w = lds + wave * s_pad;
+    lr_scores<T, VEC>(keys + (size_t)i0 * N * krow, q, sc, N, r, krow, koff, eps, n, lane, w,
+                      nullptr);
+    float m = -INFINITY;
+    for (int i = lane; i < sc; i += kWaveSize)
+        m = fmaxf(m, w[i]);
+    m = wave_max(m);
+    float l = 0.0f;
+    for (int i = lane; i < sc; i += kWaveSize) {
+        const float e = expf(w[i] - m);
+        w[i] = e;
+        l += e;
+    }
+    l = wave_sum(l);
+    wave_lds_sync();
+
+    const int col = blockIdx.y * (NCH * kWaveSize * VEC) + lane * VEC;
+    bool ok[NCH];
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+        ok[ch] = col + ch * kWaveSize * VEC < d;
+    float acc[NCH][VEC];
+    mix_rows<T, VEC, NCH, FULLCOLS>(V + (size_t)i0 * plane + (size_t)n * d + col, plane, sc, w, ok,
+                                    acc);
+    float *arow = ACC + ((size_t)c * N + n) * d + col;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+        if (FULLCOLS || ok[ch])
+            store_f32<VEC>(arow + ch * kWaveSize * VEC, acc[ch]);
+    if (blockIdx.y == 0 && lane == 0) {
+        M[(size_t)c * N + n] = m;
+        L[(size_t)c * N + n] = l;
+    }
+}
+
+// H = (sum_p exp(M_p - m) ACC_p) / (sum_p exp(M_p - m) L_p), m = max_p M_p:
+// the routing over the union of the P chunks whose states are given (Sec.
+// 3.5's merge).  One wave per token; grid y = column blocks.
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock)
+route_merge(const float *__restrict__ M, const float *__restrict__ L,
+            const float *__restrict__ ACC, int P, int N, int d, T *__restrict__ H)
+{
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x * kWaves + wave;
+    if (n >= N)
+        return;
+    float m = -INFINITY;
+    for (int p = lane; p < P; p += kWaveSize)
+        m = fmaxf(m, M[(size_t)p * N + n]);
+    m = wave_max(m);
+    float ls = 0.0f;
+    for (int p = lane; p < P; p += kWaveSize)
+        ls = fmaf(expf(M[(size_t)p * N + n] - m), L[(size_t)p * N + n], ls);
+    ls = wave_sum(ls);
+    const int col = blockIdx.y * (NCH * kWaveSize * VEC) + lane * VEC;
+    bool ok[NCH];
+    float acc[NCH][VEC];
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+        ok[ch] = col + ch * kWaveSize * VEC < d;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[ch][e] = 0.0f;
+    }
+    for (int p = 0; p < P; ++p) {
+        const float wgt = expf(M[(size_t)p * N + n] - m);
+        const float *arow = ACC + ((size_t)p * N + n) * d + col;
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+            if (FULLCOLS || ok[ch]) {
+#pragma unroll
+                for (int e = 0; e < VEC; e += (VEC % 4 == 0 ? 4 : 1)) {
+                    if constexpr (VEC % 4 == 0) {
+                        const f32x4_t x = *reinterpret_cast<const f32x4_t *>(arow + ch * kWaveSize * VEC + e);
+                        acc[ch][e] = fmaf(wgt, x.x, acc[ch][e]);
+                        acc[ch][e + 1] = fmaf(wgt, x.y, acc[ch][e + 1]);
+                        acc[ch][e + 2] = fmaf(wgt, x.z, acc[ch][e + 2]);
+                        acc[ch][e + 3] = fmaf(wgt, x.w, acc[ch][e + 3]);
+                    } else {
+                        acc[ch][e] = fmaf(wgt, arow[ch * kWaveSize * VEC + e], acc[ch][e]);
+                    }
+                }
+            }
+        }
+    }
+    const float inv = 1.0f / ls;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[ch][e] *= inv;
+    store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)n * d + col, ok, acc);
+}
+
 // Full-rank AttnRes in one pass over the rows: an online softmax over depth.
 // Per batch of 4 sources the rows stay in registers while one batched wave
 // reduction forms their sum(o^2) and q.o; the running maximum m, the
 // normaliser l and the accumulator are rescaled only when m grows.  Reads
 // every row once, like the low-rank kernels.
-template <typename T, int VEC, int NCH, bool FULLCOLS>
+// STATE: the online-softmax state of chunk c = blockIdx.z (sources c chunk ..
+// min(S, (c + 1) chunk) - 1) goes to M, L, ACC as in route_state_lr, instead
+// of H.
+template <typename T, int VEC, int NCH, bool FULLCOLS, bool STATE = false>
 __global__ void __launch_bounds__(kBlock)
 route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__restrict__ H,
-                  int S, int N, int d, float eps)
+                  int S, int N, int d, float eps, float *__restrict__ M = nullptr,
+                  float *__restrict__ L = nullptr, float *__restrict__ ACC = nullptr, int chunk = 0)
 {
     typedef typename Raw<T, VEC>::type raw_t;
     const int lane = threadIdx.x & (kWaveSize - 1);
@@ -67,6 +207,11 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
         }
     }
     const size_t plane = (size_t)N * d;
+    if constexpr (STATE) {
+        const int i0 = blockIdx.z * chunk;
+        V += (size_t)i0 * plane;
+        S = min(chunk, S - i0);
+    }
     const T *vbase = V + (size_t)n * d + col;
     float m = -INFINITY, l = 0.0f;
     for (int i0 = 0; i0 < S; i0 += 4) {
@@ -138,6 +283,18 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
             }
         }
     }
+    if constexpr (STATE) {
+        float *arow = ACC + ((size_t)blockIdx.z * N + n) * d + col;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+            if (FULLCOLS || ok[c])
+                store_f32<VEC>(arow + c * kWaveSize * VEC, acc[c]);
+        if (lane == 0) {
+            M[(size_t)blockIdx.z * N + n] = m;
+            L[(size_t)blockIdx.z * N + n] = l;
+        }
+        return;
+    }
     const float inv = 1.0f / l;
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
@@ -174,7 +331,94 @@ hipError_t launch_fwd_t(const Problem &p, const Plan &pl, void *H, hipStream_t s
     });
 }
 
+template <typename T, int VEC>
+hipError_t launch_state_t(const Problem &p, const Plan &pl, int chunk, float *M, float *L,
+                          float *ACC, hipStream_t st)
+{
+    const T *V = static_cast<const T *>(p.V);
+    const T *keys = p.mode == LRAR_MODE_PROJECTED ? static_cast<const T *>(p.K) : V;
+    const int krow = p.mode == LRAR_MODE_PROJECTED ? (int)p.r : (int)p.d;
+    const int koff = p.mode == LRAR_MODE_SLICED ? (int)(p.d - p.r) : 0;
+    const unsigned nchunk = (unsigned)((p.S + chunk - 1) / chunk);
+    return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
+        constexpr int NCH = decltype(nch)::value;
+        constexpr bool FC = decltype(fc)::value;
+        if (p.mode == LRAR_MODE_FULL)
+            hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC, true>),
+                               dim3(pl.nblocks, 1, nchunk), dim3(kBlock), 0, st, V, p.q,
+                               static_cast<T *>(nullptr), (int)p.S, (int)p.N, (int)p.d, p.eps,
+                               M, L, ACC, chunk);
+        else
+            hipLaunchKernelGGL((route_state_lr<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit, nchunk),
+                               dim3(kBlock), pl.lds, st, V, keys, p.q, M, L, ACC, (int)p.S,
+                               (int)p.N, (int)p.d, (int)p.r, krow, koff, p.eps, pl.s_pad, chunk);
+        return hipGetLastError();
+    });
+}
+
+template <typename T, int VEC>
+hipError_t launch_merge_t(const Plan &pl, const float *M, const float *L, const float *ACC, int P,
+                          int N, int d, void *H, hipStream_t st)
+{
+    return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
+        constexpr int NCH = decltype(nch)::value;
+        constexpr bool FC = decltype(fc)::value;
+        hipLaunchKernelGGL((route_merge<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit),
+                           dim3(kBlock), 0, st, M, L, ACC, P, N, d, static_cast<T *>(H));
+        return hipGetLastError();
+    });
+}
+
 }  // namespace
+
+int launch_state(const Problem &p, int64_t chunk, float *M, float *L, float *ACC, hipStream_t st,
+                 std::string *err)
+{
+    Problem pc = p;
+    pc.S = chunk < p.S ? chunk : p.S;  // the plan of one chunk
+    Plan pl;
+    if (!make_plan(pc, false, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    if ((p.S + chunk - 1) / chunk > 65535) {
+        *err = "more than 65535 source chunks";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N == 0)
+        return LRAR_OK;
+    hipError_t e;
+    if (p.dtype == LRAR_DTYPE_BF16)
+        e = pl.vec > 1 ? launch_state_t<uint16_t, 8>(p, pl, (int)chunk, M, L, ACC, st)
+                       : launch_state_t<uint16_t, 1>(p, pl, (int)chunk, M, L, ACC, st);
+    else
+        e = pl.vec > 1 ? launch_state_t<float, 4>(p, pl, (int)chunk, M, L, ACC, st)
+                       : launch_state_t<float, 1>(p, pl, (int)chunk, M, L, ACC, st);
+    return hip_status(e, "route_state launch", err);
+}
+
+int launch_merge(const float *M, const float *L, const float *ACC, int64_t P, int64_t N, int64_t d,
+                 int dtype, void *H, hipStream_t st, std::string *err)
+{
+    // The column split of a forward over the same rows (the merge has no
+    // scores; S only sizes LDS, which the merge does not use).
+    Problem pc{nullptr, nullptr, nullptr, 1, N, d, 1, LRAR_MODE_SLICED, dtype, 0.0f, dtype};
+    Plan pl;
+    if (!make_plan(pc, false, &pl, err))
+        return LRAR_EUNSUPPORTED;
+    if (P > 1024) {
+        *err = "the merge supports at most 1024 states";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (N == 0)
+        return LRAR_OK;
+    hipError_t e;
+    if (dtype == LRAR_DTYPE_BF16)
+        e = pl.vec > 1 ? launch_merge_t<uint16_t, 8>(pl, M, L, ACC, (int)P, (int)N, (int)d, H, st)
+                       : launch_merge_t<uint16_t, 1>(pl, M, L, ACC, (int)P, (int)N, (int)d, H, st);
+    else
+        e = pl.vec > 1 ? launch_merge_t<float, 4>(pl, M, L, ACC, (int)P, (int)N, (int)d, H, st)
+                       : launch_merge_t<float, 1>(pl, M, L, ACC, (int)P, (int)N, (int)d, H, st);
+    return hip_status(e, "route_merge launch", err);
+}
 
 int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err)
 {

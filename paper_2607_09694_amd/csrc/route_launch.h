@@ -30,6 +30,13 @@ int check_supported(const Problem &p, bool bwd, std::string *why);
 size_t bwd_workspace_bytes(const Problem &p);
 
 int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err);
+// Online-softmax states of the sources in chunks of `chunk` (see
+// lr_attnres_route_state_fwd): M, L [P][N], ACC [P][N][d] fp32.
+int launch_state(const Problem &p, int64_t chunk, float *M, float *L, float *ACC, hipStream_t st,
+                 std::string *err);
+// H [N][d] (storage dtype) from P states (see lr_attnres_route_merge_fwd).
+int launch_merge(const float *M, const float *L, const float *ACC, int64_t P, int64_t N, int64_t d,
+                 int dtype, void *H, hipStream_t st, std::string *err);
 // accumulate: add the gradients into dV, dK and dq instead of overwriting.
 int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
                bool accumulate, hipStream_t st, std::string *err);

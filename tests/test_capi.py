@@ -47,6 +47,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_block_route_bwd_deferred", "lr_attnres_block_gather_bwd",
                             "lr_attnres_route_all_bwd", "lr_attnres_route_all_bwd_workspace_bytes",
                             "lr_attnres_route_bwd_deferred", "lr_attnres_route_gather_bwd",
+                            "lr_attnres_route_state_fwd", "lr_attnres_route_merge_fwd",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -515,3 +516,43 @@ def test_deferred_reverse_pass_unsupported(lib):
     assert dbwd(lib, d=66) == EUNSUPPORTED
     assert gath(lib, n_sites=1025, stride=24) == EUNSUPPORTED
     assert gath(lib, d=4096) == EUNSUPPORTED
+
+
+def state_call(lib, V=A, K=None, q=B, M=C, L=D, ACC=G, S=10, N=8, d=64, r=8, chunk=4, mode=SL,
+               dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_state_fwd(V, K, q, M, L, ACC, S, N, d, r, chunk, mode, dtype, eps,
+                                          None)
+
+
+def merge_call(lib, M=C, L=D, ACC=G, H=A, P=3, N=8, d=64, dtype=BF16):
+    return lib.lr_attnres_route_merge_fwd(M, L, ACC, H, P, N, d, dtype, None)
+
+
+STATE_INVALID = [
+    (state_call, "chunk zero", dict(chunk=0), "chunk"),
+    (state_call, "M NULL", dict(M=None), "M is NULL"),
+    (state_call, "ACC misaligned", dict(ACC=G + 4), "16-byte aligned"),
+    (state_call, "K outside projected", dict(K=E), "must be NULL"),
+    (state_call, "K NULL when projected", dict(mode=P), "K is NULL"),
+    # 3 chunks x 8 tokens x 4 bytes of M reach into L 64 bytes on.
+    (state_call, "L overlaps M", dict(L=C + 64), "overlap"),
+    (state_call, "ACC overlaps V", dict(ACC=A + 256), "overlaps"),
+    (merge_call, "P zero", dict(P=0), "P must be"),
+    (merge_call, "H NULL", dict(H=None), "H is NULL"),
+    (merge_call, "unknown dtype", dict(dtype=5), "dtype"),
+    (merge_call, "H overlaps ACC", dict(H=G + 256), "overlaps"),
+    (merge_call, "ACC misaligned", dict(ACC=G + 8), "16-byte aligned"),
+]
+
+
+@pytest.mark.parametrize("fn,name,kw,msg", STATE_INVALID, ids=[c[1] for c in STATE_INVALID])
+def test_split_sources_rejects(lib, fn, name, kw, msg):
+    assert fn(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_split_sources_unsupported(lib):
+    assert state_call(lib, S=2000, chunk=1025) == EUNSUPPORTED and "1024" in err(lib)
+    assert state_call(lib, S=70000, chunk=1, N=2) == EUNSUPPORTED and "65535" in err(lib)
+    assert state_call(lib, mode=F, d=8192, r=8192) == EUNSUPPORTED
+    assert merge_call(lib, P=1025) == EUNSUPPORTED and "1024" in err(lib)

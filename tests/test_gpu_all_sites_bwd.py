@@ -95,6 +95,8 @@ CASES = [
     (SLICED, 33, 30, 4, 26, 520, 32),       # group boundary, ragged slab, 2 key tiles
     (PROJECTED, 5, 1, 5, 9, 128, 8),        # a single site reading every source
     (SLICED, 12, 11, 1, 1100, 128, 16),     # several tokens per workgroup
+    (PROJECTED, 8, 8, 1, 16, 2048, 32),     # the widest rows (16 slabs)
+    (SLICED, 17, 16, 2, 13, 2048, 64),
 ]
 
 
