@@ -220,10 +220,16 @@ struct Plan {
     int s_pad = 4;
     int r_pad = 4;
     size_t lds = 0;
+    bool wg_split = false;  // forward: the sources of a token split over a workgroup
 };
 
 // Fills *pl for a validated problem, or returns false with the reason.
 bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why);
+
+// Switches a forward plan to one token per workgroup, its sources split
+// over the waves (route_fwd_lr_wg, route_fwd_full_1p<kFullWg>), when the
+// tokens are too few to fill the device with one wave each.
+void plan_wg_split(const Problem &p, Plan *pl);
 
 // LRAR_OK, or LRAR_EHIP with the HIP error text in *err.
 int hip_status(hipError_t e, const char *what, std::string *err);

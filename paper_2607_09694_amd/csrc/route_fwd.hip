@@ -52,6 +52,123 @@ __device__ __forceinline__ void store_f32(float *p, const float (&x)[VEC])
     }
 }
 
+// The end of a workgroup-split forward: wave w holds the online-softmax
+// state (m, l, acc) of its range of one token's sources; the waves publish
+// theirs in LDS (stat: 2 kWaves floats; part: the accumulators of waves
+// 1..kWaves-1) and wave 0 merges them,
+//     m* = max_w m_w,  h = sum_w e^(m_w - m*) acc_w / sum_w e^(m_w - m*) l_w,
+// and stores h.  Every wave of the workgroup calls it.
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__device__ __forceinline__ void wg_merge_store(float (&acc)[NCH][VEC], float m, float l,
+                                               float *stat, float *part, const bool (&ok)[NCH],
+                                               T *__restrict__ hrow, int wave, int lane)
+{
+    constexpr int kRow = NCH * kWaveSize * VEC;
+    if (lane == 0) {
+        stat[wave] = m;
+        stat[kWaves + wave] = l;
+    }
+    if (wave > 0) {
+        float *dst = part + (wave - 1) * kRow + lane * VEC;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+            store_f32<VEC>(dst + c * kWaveSize * VEC, acc[c]);
+    }
+    __syncthreads();
+    if (wave != 0)
+        return;
+    float mg = stat[0];
+#pragma unroll
+    for (int u = 1; u < kWaves; ++u)
+        mg = fmaxf(mg, stat[u]);
+    float scale[kWaves];
+    float lsum = 0.0f;
+#pragma unroll
+    for (int u = 0; u < kWaves; ++u) {
+        scale[u] = expf(stat[u] - mg);  // 0 for a wave without sources
+        lsum = fmaf(scale[u], stat[kWaves + u], lsum);
+    }
+    const float inv = 1.0f / lsum;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[c][e] *= scale[0];
+#pragma unroll
+        for (int u = 1; u < kWaves; ++u) {
+            const float *src = part + (u - 1) * kRow + c * kWaveSize * VEC + lane * VEC;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[c][e] = fmaf(scale[u], src[e], acc[c][e]);
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[c][e] *= inv;
+    }
+    store_row<T, VEC, NCH, FULLCOLS>(hrow, ok, acc);
+}
+
+// The low-rank forward for few tokens: one token per workgroup, its sources
+// cut into kWaves consecutive ranges, one per wave.  Each wave keeps the
+// online-softmax state of its range (max m_w, sum l_w, accumulator a_w, as
+// in route_state_lr) and wave 0 merges the four through LDS (the merge of
+// Sec. 3.5 inside one workgroup):
+//     m = max_w m_w,  h = sum_w e^(m_w - m) a_w / sum_w e^(m_w - m) l_w.
+// Each wave's chain of dependent loads is a quarter as long as in
+// route_fwd_lr, which is what bounds a launch with few tokens.  Grid x =
+// tokens, y = column blocks; LDS: kWaves * s_pad scores, 2 * kWaves
+// statistics, and the accumulators of waves 1..3.
+template <typename T, int VEC, int NCH, bool FULLCOLS>
+__global__ void __launch_bounds__(kBlock)
+route_fwd_lr_wg(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
+                T *__restrict__ H, int S, int N, int d, int r, int krow, int koff, float eps,
+                int s_pad)
+{
+    extern __shared__ float lds[];
+    constexpr int kRow = NCH * kWaveSize * VEC;  // accumulator floats per wave
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const int n = blockIdx.x;
+    const int per = (S + kWaves - 1) / kWaves;
+    const int i0 = min(S, wave * per);
+    const int sc = min(S, i0 + per) - i0;  // 0 for trailing waves when S < 4 per wave
+    float *w = lds + wave * s_pad;
+    float *stat = lds + kWaves * s_pad;
+    float *part = stat + 2 * kWaves;
+    const size_t plane = (size_t)N * d;
+    const int col = blockIdx.y * kRow + lane * VEC;
+    bool ok[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+        ok[c] = col + c * kWaveSize * VEC < d;
+    float acc[NCH][VEC];
+    float m = -INFINITY, l = 0.0f;
+    if (sc > 0) {  // wave-uniform
+        lr_scores<T, VEC>(keys + (size_t)i0 * N * krow, q, sc, N, r, krow, koff, eps, n, lane, w,
+                          nullptr);
+        for (int i = lane; i < sc; i += kWaveSize)
+            m = fmaxf(m, w[i]);
+        m = wave_max(m);
+        for (int i = lane; i < sc; i += kWaveSize) {
+            const float e = expf(w[i] - m);
+            w[i] = e;
+            l += e;
+        }
+        l = wave_sum(l);
+        wave_lds_sync();
+        mix_rows<T, VEC, NCH, FULLCOLS>(V + (size_t)i0 * plane + (size_t)n * d + col, plane, sc,
+                                        w, ok, acc);
+    } else {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[c][e] = 0.0f;
+    }
+    wg_merge_store<T, VEC, NCH, FULLCOLS>(acc, m, l, stat, part, ok, H + (size_t)n * d + col, wave,
+                                          lane);
+}
+
 // Online-softmax state of the routing over one chunk of the sources (Sec.
 // 3.5, the two-phase form that merges partial routings): chunk c =
 // blockIdx.z holds sources c chunk .. min(S, (c + 1) chunk) - 1, and per
@@ -178,10 +295,17 @@ route_merge(const float *__restrict__ M, const float *__restrict__ L,
 // reduction forms their sum(o^2) and q.o; the running maximum m, the
 // normaliser l and the accumulator are rescaled only when m grows.  Reads
 // every row once, like the low-rank kernels.
-// STATE: the online-softmax state of chunk c = blockIdx.z (sources c chunk ..
-// min(S, (c + 1) chunk) - 1) goes to M, L, ACC as in route_state_lr, instead
-// of H.
-template <typename T, int VEC, int NCH, bool FULLCOLS, bool STATE = false>
+// KIND selects what is written:
+//   kFullH     h, one wave per token;
+//   kFullState the online-softmax state of chunk c = blockIdx.z (sources
+//              c chunk .. min(S, (c + 1) chunk) - 1) to M, L, ACC, as in
+//              route_state_lr;
+//   kFullWg    h, one token per workgroup (grid x = tokens), its sources
+//              cut into kWaves ranges merged by wg_merge_store, as in
+//              route_fwd_lr_wg (dynamic LDS: 2 kWaves + (kWaves - 1) row
+//              floats).
+constexpr int kFullH = 0, kFullState = 1, kFullWg = 2;
+template <typename T, int VEC, int NCH, bool FULLCOLS, int KIND = kFullH>
 __global__ void __launch_bounds__(kBlock)
 route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__restrict__ H,
                   int S, int N, int d, float eps, float *__restrict__ M = nullptr,
@@ -190,9 +314,9 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
     typedef typename Raw<T, VEC>::type raw_t;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
-    const int n = blockIdx.x * kWaves + wave;
-    if (n >= N)
-        return;  // wave-uniform; no workgroup barrier below
+    const int n = KIND == kFullWg ? (int)blockIdx.x : (int)blockIdx.x * kWaves + wave;
+    if (KIND != kFullWg && n >= N)
+        return;  // wave-uniform; no workgroup barrier on this path
 
     const int col = lane * VEC;
     bool ok[NCH];
@@ -207,10 +331,15 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
         }
     }
     const size_t plane = (size_t)N * d;
-    if constexpr (STATE) {
+    if constexpr (KIND == kFullState) {
         const int i0 = blockIdx.z * chunk;
         V += (size_t)i0 * plane;
         S = min(chunk, S - i0);
+    } else if constexpr (KIND == kFullWg) {
+        const int per = (S + kWaves - 1) / kWaves;
+        const int i0 = min(S, wave * per);
+        V += (size_t)i0 * plane;
+        S = min(S, i0 + per) - i0;  // 0 for trailing waves: the loop below is skipped
     }
     const T *vbase = V + (size_t)n * d + col;
     float m = -INFINITY, l = 0.0f;
@@ -283,7 +412,13 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
             }
         }
     }
-    if constexpr (STATE) {
+    if constexpr (KIND == kFullWg) {
+        extern __shared__ float lds[];
+        wg_merge_store<T, VEC, NCH, FULLCOLS>(acc, m, l, lds, lds + 2 * kWaves, ok,
+                                              H + (size_t)n * d + col, wave, lane);
+        return;
+    }
+    if constexpr (KIND == kFullState) {
         float *arow = ACC + ((size_t)blockIdx.z * N + n) * d + col;
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
@@ -317,10 +452,19 @@ hipError_t launch_fwd_t(const Problem &p, const Plan &pl, void *H, hipStream_t s
     return dispatch_chunks<VEC>(pl, [&](auto nch, auto fc) -> hipError_t {
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
-        if (full) {
+        if (full && pl.wg_split) {
+            hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC, kFullWg>), dim3(pl.nblocks),
+                               dim3(kBlock), pl.lds, st, V, p.q, static_cast<T *>(H), (int)p.S,
+                               (int)p.N, (int)p.d, p.eps);
+        } else if (full) {
             hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC>), dim3(pl.nblocks),
                                dim3(kBlock), 0, st, V, p.q, static_cast<T *>(H), (int)p.S,
                                (int)p.N, (int)p.d, p.eps);
+        } else if (pl.wg_split) {
+            hipLaunchKernelGGL((route_fwd_lr_wg<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit),
+                               dim3(kBlock), pl.lds, st, V, keys, p.q, static_cast<T *>(H),
+                               (int)p.S, (int)p.N, (int)p.d, (int)p.r, krow, koff, p.eps,
+                               pl.s_pad);
         } else {
             hipLaunchKernelGGL((route_fwd_lr<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit),
                                dim3(kBlock), pl.lds, st, V, keys, p.q, static_cast<T *>(H),
@@ -344,7 +488,7 @@ hipError_t launch_state_t(const Problem &p, const Plan &pl, int chunk, float *M,
         constexpr int NCH = decltype(nch)::value;
         constexpr bool FC = decltype(fc)::value;
         if (p.mode == LRAR_MODE_FULL)
-            hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC, true>),
+            hipLaunchKernelGGL((route_fwd_full_1p<T, VEC, NCH, FC, kFullState>),
                                dim3(pl.nblocks, 1, nchunk), dim3(kBlock), 0, st, V, p.q,
                                static_cast<T *>(nullptr), (int)p.S, (int)p.N, (int)p.d, p.eps,
                                M, L, ACC, chunk);
@@ -427,6 +571,7 @@ int launch_fwd(const Problem &p, void *H, hipStream_t st, std::string *err)
         return LRAR_EUNSUPPORTED;
     if (p.N == 0)
         return LRAR_OK;
+    plan_wg_split(p, &pl);
     hipError_t e;
     if (p.dtype == LRAR_DTYPE_BF16)
         e = pl.vec > 1 ? launch_fwd_t<uint16_t, 8>(p, pl, H, st)

@@ -11,9 +11,35 @@ constexpr int kMaxSourcesFwd = 1024;
 constexpr int kMaxSourcesBwd = 512;
 constexpr int kMaxRankBwd = 256;
 
+// Token counts up to which the forward splits each token's sources over the
+// four waves of a workgroup (measured on MI355X at 49 sources, d = 1024: the
+// split is ahead up to these counts, level with or behind one wave per token
+// above them).  LRAR_WG_SPLIT_MAX_TOKENS overrides both.
+#ifdef LRAR_WG_SPLIT_MAX_TOKENS
+constexpr int64_t kWgSplitLowRank = LRAR_WG_SPLIT_MAX_TOKENS;
+constexpr int64_t kWgSplitFull = LRAR_WG_SPLIT_MAX_TOKENS;
+#else
+constexpr int64_t kWgSplitLowRank = 2048;
+constexpr int64_t kWgSplitFull = 1024;
+#endif
+
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
 }  // namespace
+
+void plan_wg_split(const Problem &p, Plan *pl)
+{
+    if (p.N > (p.mode == LRAR_MODE_FULL ? kWgSplitFull : kWgSplitLowRank) || p.S < 2)
+        return;
+    pl->wg_split = true;
+    pl->nblocks = (int)p.N;
+    const size_t row = (size_t)pl->nch * kWaveSize * pl->vec;
+    // Scores in LDS (low-rank keys only), per-wave statistics, the
+    // accumulators of waves 1..kWaves-1.
+    pl->s_pad = round_up((int)((p.S + kWaves - 1) / kWaves), 4);
+    const size_t scores = p.mode == LRAR_MODE_FULL ? 0 : (size_t)kWaves * pl->s_pad;
+    pl->lds = (scores + 2 * kWaves + (kWaves - 1) * row) * sizeof(float);
+}
 
 bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why)
 {

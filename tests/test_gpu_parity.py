@@ -246,6 +246,30 @@ def test_beyond_the_limits_is_refused(dev):
     check_values("H", "bf16", to_host(H), oracle.route_fwd(p.V, p.K, p.q, PROJECTED))
 
 
+# Above 2048 tokens (1024 with full-rank keys) the forward runs one wave per
+# token; below, the sources of a token are split over the waves of a
+# workgroup (the cases above).  These cover the first kernels' paths with
+# ragged tails.
+MANY_TOKEN_CASES = [
+    (FULL, "bf16", 9, 1030, 512, 512),
+    (FULL, "f32", 5, 1025, 100, 100),
+    (PROJECTED, "bf16", 49, 2051, 256, 16),
+    (SLICED, "f32", 7, 2049, 200, 12),
+    (PROJECTED, "bf16", 3, 2053, 100, 4),      # scalar path
+    (SLICED, "bf16", 3, 2050, 8200, 16),       # column blocks
+    (PROJECTED, "f32", 70, 2100, 64, 8),       # S above one wave
+]
+
+
+@pytest.mark.parametrize("case", MANY_TOKEN_CASES, ids=_id)
+def test_forward_many_tokens_matches_oracle(dev, case):
+    mode, dtype, S, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=S * 1000 + N)
+    H = lr.route_fwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev), mode)
+    torch.cuda.synchronize()
+    check_values("H", dtype, to_host(H), oracle.route_fwd(p.V, p.K, p.q, mode, r=p.r))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("mode", [PROJECTED, SLICED])
 def test_column_split_forward(dev, mode, dtype):
