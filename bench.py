@@ -15,6 +15,7 @@ S = 49, the forward alone) under "extra".
 from __future__ import annotations
 
 import argparse
+import platform
 import hashlib
 import json
 import os
@@ -147,28 +148,86 @@ def time_calls(torch, fn, reps, warmup, flush=None):
     return [a.elapsed_time(b) for a, b in ts]
 
 
-def cpu_baseline(g, q, target_s=10.0, chunk=1024):
+def cpu_baseline(g, q, target_s=10.0, chunk=1024, single_s=4.0):
     """fp64 oracle (as it stands) on the host: fwd + bwd of the main workload
     in 1024-token chunks, in order, repeated over the whole token set until
-    about target_s seconds have passed.  Host copies of the inputs are made
-    before timing."""
+    about target_s seconds have passed, on every host thread; then the same
+    on one thread for about single_s seconds.  Host copies of the inputs are
+    made before timing."""
     import oracle
     from paper_2607_09694_amd.inputs import bf16_tensor_to_bits
 
     V, K, dH = (bf16_tensor_to_bits(g[k]) for k in ("V", "K", "dH"))
-    done, spent = 0, 0.0
-    while spent < target_s:
-        n0 = done % N5
-        n1 = min(N5, n0 + chunk)
-        t0 = time.perf_counter()
-        oracle.route_fwd(V, K, q, oracle.PROJECTED, n0=n0, n1=n1)
-        oracle.route_bwd(V, K, q, dH, oracle.PROJECTED, n0=n0, n1=n1)
-        spent += time.perf_counter() - t0
-        done += n1 - n0
-    return {"value": round(done / spent, 1), "unit": "tokens/s", "cores": oracle.num_threads(),
+
+    def run(limit, step):
+        done, spent = 0, 0.0
+        while spent < limit:
+            n0 = done % N5
+            n1 = min(N5, n0 + step)
+            t0 = time.perf_counter()
+            oracle.route_fwd(V, K, q, oracle.PROJECTED, n0=n0, n1=n1)
+            oracle.route_bwd(V, K, q, dH, oracle.PROJECTED, n0=n0, n1=n1)
+            spent += time.perf_counter() - t0
+            done += n1 - n0
+        return done, spent
+
+    cores = oracle.num_threads()
+    done, spent = run(target_s, chunk)
+    oracle.set_num_threads(1)
+    done1, spent1 = run(single_s, 64)
+    oracle.set_num_threads(cores)
+    cpu = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    return {"value": round(done / spent, 1), "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{done} tokens ({done / N5:.2f} passes over all {N5} tokens) of the main "
-                      f"workload, fwd+bwd in fp64, {spent:.1f} s"}
+                      f"workload, fwd+bwd in fp64, {spent:.1f} s",
+            "single_thread_value": round(done1 / spent1, 1),
+            "single_thread_sample": f"{done1} tokens in 64-token chunks, {spent1:.1f} s",
+            "cpu": cpu}
+
+
+def device_state(torch, dev):
+    """Clock levels and power of the GPU, read from its sysfs entries
+    (read-only; empty where the files are not readable)."""
+    import glob
+
+    p = torch.cuda.get_device_properties(dev)
+    out = {"name": p.name, "arch": p.gcnArchName, "compute_units": p.multi_processor_count}
+    bdf = f"{p.pci_domain_id:04x}:{p.pci_bus_id:02x}:{p.pci_device_id:02x}.0"
+    base = f"/sys/bus/pci/devices/{bdf}"
+    for key, fname in (("sclk", "pp_dpm_sclk"), ("mclk", "pp_dpm_mclk"),
+                       ("fclk", "pp_dpm_fclk")):
+        try:
+            with open(f"{base}/{fname}") as f:
+                cur = [l.split(":", 1)[1].strip() for l in f if l.rstrip().endswith("*")]
+            if cur:
+                out[key] = cur[0].rstrip("*").strip()
+        except OSError:
+            pass
+    try:
+        with open(f"{base}/power_dpm_force_performance_level") as f:
+            out["perf_level"] = f.read().strip()
+    except OSError:
+        pass
+    for hw in glob.glob(f"{base}/hwmon/hwmon*"):
+        for name in ("power1_average", "power1_input"):
+            try:
+                with open(f"{hw}/{name}") as f:
+                    out["power_W"] = round(int(f.read().strip()) / 1e6, 1)
+                break
+            except (OSError, ValueError):
+                continue
+        try:
+            with open(f"{hw}/power1_cap") as f:
+                out["power_cap_W"] = round(int(f.read().strip()) / 1e6, 1)
+        except (OSError, ValueError):
+            pass
+    return out
 
 
 def all_sites_bytes(S, T, N, d, r, mode, es=2):
@@ -885,6 +944,7 @@ def main():
         step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gpu_state = device_state(torch, dev)  # right after the timed steps
     bwd_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
     ms_per_step = elapsed * 1e3 / args.steps
 
@@ -918,6 +978,7 @@ def main():
                    "global_batch": N5, "seq_len": 4096, "sources": S5, "d": D5, "r": R5,
                    "storage": "bf16", "parallelism": "single GPU"},
         "roofline": roofline,
+        "device": gpu_state,
         "fwd": {"avg_ms": round(fwd_ms, 4),
                 "tokens_per_s": round(N5 / (fwd_ms * 1e-3), 1),
                 "algo_GBps": round(fwd_bytes(S5, N5, D5, R5, 0) / (fwd_ms * 1e-3) / 1e9, 1)},

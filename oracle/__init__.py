@@ -51,6 +51,8 @@ def _load():
     for f in (lib.orc_route_weights, lib.orc_route_fwd, lib.orc_route_bwd):
         f.restype = ctypes.c_int
     lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_set_num_threads.argtypes = [i]
+    lib.orc_set_num_threads.restype = None
     lib.orc_block_num_sources.argtypes = [ll, ll]
     lib.orc_block_num_sources.restype = ll
     lib.orc_block_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll]
@@ -76,6 +78,11 @@ def _load():
 
 def num_threads() -> int:
     return _load().orc_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's later parallel regions (timing only)."""
+    _load().orc_set_num_threads(int(n))
 
 
 def _ptr(a):

@@ -690,6 +690,18 @@ int orc_key_projection(const void *A, const void *W, double *O, double *Kout, lo
     return 0;
 }
 
+/* Sets the number of OpenMP threads later parallel regions use (n >= 1);
+ * no effect in a build without OpenMP.  Timing harness only. */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Number of OpenMP threads a parallel region of this library would use. */
 int orc_num_threads(void)
 {

@@ -17,20 +17,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 constexpr int kAllSlab = 128;                     // columns per wave pass
 constexpr int kAlphaRow = kAllMaxSources + 4;     // floats per LDS alpha row
 constexpr int kKeyRow = kAllMaxRank + 8;          // bf16 per LDS key row
-// s_waitcnt immediate: lgkmcnt(0); vmcnt and expcnt left at their maxima.
-constexpr int kWaitLdsOnly = 0x000F | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
-
-// Workgroup barrier that orders LDS only: this wave's LDS accesses complete,
-// then s_barrier.  Unlike __syncthreads it does not wait for outstanding
-// global loads, so loads issued ahead stay in flight across it.  The
-// kernels that use it communicate between waves through LDS alone.
-__device__ __forceinline__ void lds_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(kWaitLdsOnly);
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
 
 struct AllArgs {
     const void *V;       // [S][N][d]

@@ -41,6 +41,22 @@ constexpr bool kNtLoad = true;
 constexpr bool kNtStore = true;
 
 // Sources whose value rows one lane has in flight in the forward mix.
+// s_waitcnt immediate (gfx9 encoding) that waits for this wave's LDS
+// accesses only (lgkmcnt 0; vmcnt and expcnt at their maxima).
+constexpr int kWaitLdsOnly = 0x000F | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
+
+// Workgroup barrier that orders LDS only: this wave's LDS accesses complete,
+// then s_barrier.  Unlike __syncthreads it does not wait for outstanding
+// global loads, so loads issued ahead stay in flight across it.  The
+// kernels that use it communicate between waves through LDS alone.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(kWaitLdsOnly);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
 // Sources loaded ahead in the backward stream (divides 8, the number of
 // sources per batched reduction of the dots dH . o_i).
