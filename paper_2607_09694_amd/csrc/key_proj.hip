@@ -18,17 +18,15 @@
 // most 9 column tiles of v_mfma_f32_16x16x32_bf16 with fp32 accumulators
 // (at most 144 per lane, so two waves fit a SIMD's registers).  Both
 // operands are k-contiguous in memory (A row-major, W in the [out][in]
-// layout of a linear layer).  32-wide k-slices (one MFMA k-step) of both go
-// straight from memory to LDS with buffer loads (no register staging), in a
-// ring of four stages: a slice is issued three k-steps before it is used,
-// so its loads have two k-steps of matrix work to land behind, which is
-// what the activation streamed from HBM needs.  The buffer resources cover
-// only the workgroup's rows, so rows past N or past the output read as
-// zero.  LDS rows are 64 bytes with the 16-byte chunks XOR-swizzled by
-// (row / 4) mod 4, so that the 16 consecutive rows that one MFMA operand
-// read touches fall on distinct banks.  Within a k-step the MFMAs go column
-// tile by column tile; the B fragments are read a few columns ahead and the
-// next k-step's A fragments during the first columns.
+// layout of a linear layer).  64-wide k-slices of both go straight from
+// memory to LDS with buffer loads (no register staging), double-buffered:
+// the next slice is in flight while the current one feeds the MFMAs.  The
+// buffer resources cover only the workgroup's rows, so rows past N or past
+// the output read as zero.  LDS rows are 128 bytes with the 16-byte chunks
+// XOR-swizzled by (row / 2) mod 8, so that the 16 consecutive rows that one
+// MFMA operand read touches fall on distinct banks.  Within a k-step the
+// MFMAs go column tile by column tile; the B fragments are read a few
+// columns ahead and the next k-step's A fragments during the first columns.
 // Workgroups are ordered so that the column tiles of one row tile run on
 // one XCD and share its L2 copy of the A slice.  The epilogue rounds to bf16
 // (nearest even), stages half of the tile at a time through LDS and writes
@@ -50,30 +48,20 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 constexpr int kPM = 256;             // tokens per workgroup tile
 constexpr int kPN = 256;             // output columns per full column tile
 constexpr int kPNMax = kPN + 32;     // the last column tile may reach 288
-constexpr int kPK = 32;              // k per LDS stage (one MFMA k-step)
-constexpr int kStages = 4;           // LDS ring
+constexpr int kPK = 64;              // k per LDS stage
 constexpr int kRow = kPK * 2;        // bytes per LDS row of a stage (unpadded)
-constexpr int kBlockRows = 1024 / kRow;          // rows per 1 KB block (16)
-constexpr int kABlocks = kPM / kBlockRows;       // 1 KB blocks: A part of a stage
-constexpr int kBBlocks = kPNMax / kBlockRows;    // ... and W part
+constexpr int kABlocks = kPM / 8;    // 1 KB blocks of 8 rows: A part of a stage
+constexpr int kBBlocks = kPNMax / 8; // ... and W part
 constexpr int kStageBytes = (kPM + kPNMax) * kRow;
 constexpr int kWaves8 = 8;           // waves per workgroup (2 per SIMD)
 constexpr int kLoads = (kABlocks + kBBlocks + kWaves8 - 1) / kWaves8;  // direct loads per wave
-// Waves 0 .. kLongWaves-1 issue kLoads loads per stage, the others one fewer.
-constexpr int kLongWaves = (kABlocks + kBBlocks) % kWaves8 == 0 ? kWaves8
-                                                                 : (kABlocks + kBBlocks) % kWaves8;
 constexpr int kCd = kPNMax + 8;      // LDS row stride of the output half-tile (elements)
 constexpr int kPThreads = kWaves8 * kWaveSize;
 // Buffer resource word 3 for raw (untyped) loads on gfx9-family parts.
 constexpr int kRawBufferFlags = 0x00020000;
 
 static_assert(kABlocks % kWaves8 == 0, "A blocks split evenly over the waves");
-static_assert(kStages * kStageBytes >= kPM / 2 * kCd * 2, "output half-tile fits the stages");
-static_assert(kLoads <= 15, "loads per stage fit the vmcnt immediates below");
-
-// s_waitcnt immediate (gfx9 encoding): at most n vector-memory operations
-// outstanding; expcnt and lgkmcnt left at their maxima (not waited on).
-constexpr int vmcnt_at_most(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+static_assert(2 * kStageBytes >= kPM / 2 * kCd * 2, "output half-tile fits the stages");
 
 struct ProjArgs {
     const uint16_t *A;  // [N][m]
@@ -91,10 +79,10 @@ int key_proj_col_tiles(int64_t nout)
     return nout <= kPNMax ? 1 : (int)((nout - kPNMax + kPN - 1) / kPN) + 1;
 }
 
-// LDS placement of 16-byte chunk c (0..3) of stage row `row`: rows are 64
-// bytes, and the chunk is XOR-swizzled with (row / 4) mod 4, so the 16
+// LDS placement of 16-byte chunk c (0..7) of stage row `row`: rows are 128
+// bytes, and the chunk is XOR-swizzled with (row / 2) mod 8, so the 16
 // consecutive rows that one MFMA operand read touches spread over all banks.
-__device__ __forceinline__ int chunk_at(int row, int c) { return row * kRow + 16 * (c ^ ((row >> 2) & 3)); }
+__device__ __forceinline__ int chunk_at(int row, int c) { return row * kRow + 16 * (c ^ ((row >> 1) & 7)); }
 
 // The k loop and epilogue of one workgroup; each wave computes NJ column
 // tiles of 16 (compile time, so that no MFMA sits behind a branch).
@@ -109,17 +97,18 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     const int nk = (a.m + kPK - 1) / kPK;
 
     // Stage kt into LDS buffer `buf` with buffer loads straight to LDS.  The
-    // wave's u-th load fills 1 KB block blk = wave + 8 u, 16 rows of 64
-    // bytes: lane l writes bytes 16 l .. 16 l + 15 of the block, i.e. block
-    // row l / 4, placed chunk l mod 4, which holds global chunk
-    // (l mod 4) ^ swizzle.  Blocks 0 .. kABlocks-1 are A's rows, the rest
-    // W's.  The swizzle (row / 4) mod 4 of block row l / 4 is (l / 16) mod 4
-    // for every block, so each lane needs one offset; the block's first row
-    // and the k offset are scalar.  The buffer resources cover the
-    // workgroup's rows of A and of W only, so rows past N, past the tile or
-    // past d + r read as zero.  A chunk past m reads the next row's first
-    // elements; it is zeroed in LDS (zero_tail).
-    const int voff = (lane >> 2) * a.m * 2 + 16 * ((lane & 3) ^ ((lane >> 4) & 3));
+    // wave's u-th load fills 1 KB block (wave + 4 u), rows 8 blk .. 8 blk + 7:
+    // lane l writes bytes 16 l .. 16 l + 15 of the block, i.e. row l / 8,
+    // placed chunk l mod 8, which holds global chunk (l mod 8) ^ swizzle.
+    // The buffer resources cover the workgroup's rows of A and of W only, so
+    // rows past N, past the tile or past d + r read as zero.  A chunk past m
+    // reads the next row's first elements; it is zeroed in LDS (zero_tail).
+    // Each lane needs one offset; the row group and the k offset are scalar.
+    // Block blk = wave + 8 u holds rows 8 blk .. 8 blk + 7 of A (blk < 32) or
+    // of W; its swizzle (row / 2) mod 8 = (4 (blk mod 2) + l / 16) mod 8 only
+    // depends on the wave's parity, so each lane needs one offset.
+    const int rl = 8 * wave + (lane >> 3);             // row within a 64-row group
+    const int voff = rl * a.m * 2 + 16 * ((lane & 7) ^ ((rl >> 1) & 7));
     const int arows = (int)min((int64_t)kPM, a.N - n0);
     const int brows = max(0, min(width, nout - j0));
     const __amdgpu_buffer_rsrc_t ares = __builtin_amdgcn_make_buffer_rsrc(
@@ -134,12 +123,11 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
             const int blk = wave + kWaves8 * u;
             if (u < kABlocks / kWaves8)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(ares, (lds_void_t *)(sb + 1024 * blk), 16,
-                                                         voff, blk * kBlockRows * a.m * 2 + kbytes,
-                                                         0, 0);
+                                                         voff, u * 128 * a.m + kbytes, 0, 0);
             else if (blk < kABlocks + kBBlocks)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
                     bres, (lds_void_t *)(sb + 1024 * blk), 16, voff,
-                    (blk - kABlocks) * kBlockRows * a.m * 2 + kbytes, 0, 0);
+                    (u - kABlocks / kWaves8) * 128 * a.m + kbytes, 0, 0);
         }
     };
 
@@ -150,45 +138,29 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
         for (int j = 0; j < NJ; ++j)
             acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // Operand fragments: lane l reads row base + l mod 16, k chunk l / 16
-    // of stage kt.
+    // Operand fragments: lane l reads row base + l mod 16, k chunk
+    // 4 ks + l / 16 of stage kt.
     const int fr = lane & 15, fq = lane >> 4;
     const int c0 = wn * 16 * half;  // first column of this wave's tiles
-    // sbase: byte offset of the stage's buffer, recomputed (not hoisted) at
-    // every k-step so that one address register serves each of the ring's
-    // four buffers.
-    const int aoff = chunk_at(wm * 64 + fr, fq), boff = kPM * kRow + chunk_at(c0 + fr, fq);
-    auto stage_base = [&](int kt) {
-        int sbase = (kt % kStages) * kStageBytes;
-        asm volatile("" : "+s"(sbase));
-        return sbase;
+    auto aload = [&](int kt, int ks, int i) {
+        const unsigned char *sa = lds + (kt & 1) * kStageBytes;
+        return *reinterpret_cast<const bf16x8_t *>(
+            sa + chunk_at(wm * 64 + 16 * i + fr, 4 * ks + fq));
     };
-    auto aload = [&](int sbase, int i) {
-        return *reinterpret_cast<const bf16x8_t *>(lds + sbase + aoff + 16 * kRow * i);
-    };
-    auto bload = [&](int sbase, int j) {
-        return *reinterpret_cast<const bf16x8_t *>(lds + sbase + boff + 16 * kRow * j);
+    auto bload = [&](int kt, int ks, int j) {
+        const unsigned char *sb = lds + (kt & 1) * kStageBytes + kPM * kRow;
+        return *reinterpret_cast<const bf16x8_t *>(sb + chunk_at(c0 + 16 * j + fr, 4 * ks + fq));
     };
     // A ragged last stage: the A chunks past m hold the next row's elements;
     // zero them in LDS once the stage has landed.
     auto zero_tail = [&](int kt) {
         const int valid = (a.m - kt * kPK) / 8;  // whole chunks still inside m
-        unsigned char *sa = lds + (kt % kStages) * kStageBytes;
-        for (int f = tid; f < kPM * 4; f += kPThreads) {
-            const int row = f >> 2, c = f & 3;
+        unsigned char *sa = lds + (kt & 1) * kStageBytes;
+        for (int f = tid; f < kPM * 8; f += kPThreads) {
+            const int row = f >> 3, c = f & 7;
             if (c >= valid)
                 *reinterpret_cast<u32x4_t *>(sa + chunk_at(row, c)) = u32x4_t{0u, 0u, 0u, 0u};
         }
-    };
-    // Wait until at most the last `ahead` stages issued by this wave are
-    // still in flight (waves 0 .. kLongWaves-1 issue one load more).
-    auto wait_stages = [&](int ahead) {
-        if (ahead == 0)
-            __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));
-        else if (wave < kLongWaves)
-            __builtin_amdgcn_s_waitcnt(vmcnt_at_most(kLoads));
-        else
-            __builtin_amdgcn_s_waitcnt(vmcnt_at_most(kLoads - 1));
     };
 
     // One k-step, column tile by column tile: B fragment j against the 4 A
@@ -197,16 +169,16 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
     // on the SIMD covers what remains of the LDS latency.
     constexpr int RING = NJ % 4 == 0 ? 4 : 3;
     bf16x8_t a0[4], a1[4], br[RING];
-    auto kstep = [&](int kt, bf16x8_t(&acur)[4], bf16x8_t(&anext)[4], bool more) {
-        const int scur = stage_base(kt), snext = stage_base(kt + 1);
+    auto kstep = [&](int kt, int ks, bf16x8_t(&acur)[4], bf16x8_t(&anext)[4], bool more) {
+        const int nkt = ks ? kt + 1 : kt, nks = ks ^ 1;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             if (j + RING - 1 < NJ)
-                br[(j + RING - 1) % RING] = bload(scur, j + RING - 1);
+                br[(j + RING - 1) % RING] = bload(kt, ks, j + RING - 1);
             else if (more)
-                br[(j + RING - 1) % RING] = bload(snext, j + RING - 1 - NJ);
+                br[(j + RING - 1) % RING] = bload(nkt, nks, j + RING - 1 - NJ);
             if (more && j < 4)
-                anext[j] = aload(snext, j);
+                anext[j] = aload(nkt, nks, j);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -217,61 +189,43 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
         if (more && NJ < 4) {
 #pragma unroll
             for (int i = NJ; i < 4; ++i)
-                anext[i] = aload(snext, i);
+                anext[i] = aload(nkt, nks, i);
         }
     };
 
-    // The ring: before k-step kt runs, stages kt and kt + 1 have landed and
-    // are visible, stage kt + 2 is in flight and stage kt + 3 is issued into
-    // the buffer that k-step kt - 1 has just released.  The barrier at the
-    // end of k-step kt makes stage kt + 2 visible (k-step kt reads its
-    // successor's first fragments) and releases stage kt's buffer.  The
-    // barriers order LDS only, so the stages issued ahead stay in flight.
     const bool ragged = a.m % kPK != 0;
-    for (int s = 0; s < kStages - 1 && s < nk; ++s)
-        issue(s, s);
-    // Stages 0 and 1 visible; stage 2 may stay in flight.
-    wait_stages(nk > 2 ? 1 : 0);
-    lds_barrier();
-    if (ragged && nk <= 2) {
-        zero_tail(nk - 1);
-        lds_barrier();
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (ragged && nk == 1) {
+        zero_tail(0);
+        __syncthreads();
     }
+    if (nk > 1)
+        issue(1, 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        a0[i] = aload(0, i);
+        a0[i] = aload(0, 0, i);
 #pragma unroll
     for (int j = 0; j < RING - 1; ++j)
-        br[j] = bload(0, j);
-    // Main loop: two k-steps per trip (so the A fragment registers
-    // alternate), each with a successor, so every prefetch is unconditional.
-    int kt = 0;
-    for (; kt + 2 < nk; kt += 2) {
-        if (kt + 3 < nk)
-            issue(kt + 3, (kt + 3) % kStages);
-        kstep(kt, a0, a1, true);
-        wait_stages(kt + 3 < nk ? 1 : 0);
-        lds_barrier();
-        if (ragged && kt + 3 == nk) {
-            zero_tail(kt + 2);
-            lds_barrier();
+        br[j] = bload(0, 0, j);
+    for (int kt = 0; kt < nk; ++kt) {
+        // First k-step: its successor is in the same stage.
+        kstep(kt, 0, a0, a1, true);
+        // Stage kt+1 (issued two k-steps ago) becomes visible before the
+        // second k-step prefetches from it.
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (ragged && kt + 2 == nk) {
+            zero_tail(kt + 1);
+            __syncthreads();
         }
-        if (kt + 4 < nk)
-            issue(kt + 4, (kt + 4) % kStages);
-        kstep(kt + 1, a1, a0, true);
-        wait_stages(kt + 4 < nk ? 1 : 0);
-        lds_barrier();
-        if (ragged && kt + 4 == nk) {
-            zero_tail(kt + 3);
-            lds_barrier();
-        }
+        kstep(kt, 1, a1, a0, kt + 1 < nk);
+        // Every wave is done with stage kt's buffer: refill it.
+        __syncthreads();
+        if (kt + 2 < nk)
+            issue(kt + 2, kt & 1);
     }
-    // The last one or two k-steps: every stage has landed, is visible and,
-    // if ragged, zeroed; nothing more is written to LDS before the epilogue.
-    kstep(kt, a0, a1, kt + 1 < nk);
-    if (kt + 1 < nk)
-        kstep(kt + 1, a1, a0, false);
-    lds_barrier();
 
     // Epilogue, one half of the rows at a time: lane holds C[wm*128 + 16 i +
     // 4 (lane / 16) + e][c0 + 16 j + (lane mod 16)]; round to bf16 into an LDS
@@ -325,7 +279,7 @@ __device__ __forceinline__ void key_proj_tile(const ProjArgs &a, unsigned char *
 
 __global__ __launch_bounds__(kPThreads, 1) void key_proj_gemm(ProjArgs a)
 {
-    __shared__ __align__(16) unsigned char lds[kStages * kStageBytes];
+    __shared__ __align__(16) unsigned char lds[2 * kStageBytes];
     // Workgroup b runs on XCD b mod 8; each XCD takes a contiguous range of
     // logical tiles, so the column tiles of one row tile share its L2.
     const int nb = gridDim.x, per = (nb + 7) / 8, xcd = blockIdx.x % 8, slot = blockIdx.x / 8;

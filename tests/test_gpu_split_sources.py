@@ -60,6 +60,7 @@ CASES = [
     (FULL, "f32", 9, 4, 5, 100, 100),            # full-rank, ragged slab
     (PROJECTED, "bf16", 300, 128, 6, 8192, 32),  # rows in two column blocks
     (SLICED, "bf16", 2048, 512, 3, 64, 8),       # beyond the one-call source limit
+    (FULL, "f32", 1100, 300, 3, 64, 64),         # full-rank keys beyond it
     (PROJECTED, "f32", 12, 50, 9, 64, 5),        # one chunk wider than the stack
     (SLICED, "bf16", 1, 1, 4, 136, 8),           # one source
     (PROJECTED, "bf16", 16, 1, 33, 264, 24),     # one source per chunk, ragged slab
