@@ -809,7 +809,6 @@ def extras(torch, lr, dev, reps, warmup):
         torch, lr, dev, V, PROJECTED, 32, 6, 5, 1)
     out["decode_model_pass_projected_r16_N128"] = decode_model_pass(torch, lr, dev, reps, warmup)
     out["key_producer_d1024_N16384"] = key_producer(torch, lr, dev, reps, warmup, flush)
-    out["hbm_ceilings"] = probe_ceilings(torch, dev, reps, warmup)
     del g, V, K, H, flush
     torch.cuda.empty_cache()
     return out
@@ -818,7 +817,8 @@ def extras(torch, lr, dev, reps, warmup):
 def focused(torch, lr, dev, names, reps=20, warmup=3):
     """Only the named workloads (for profiling one kernel at a time):
     'key_producer', 'split_sources' (the deepest site at decode token counts,
-    one call against states + merge), 'block_training', 'model_training' and
+    one call against states + merge), 'decode' (a 49-site pass at N = 128,
+    eager and as one graph), 'block_training', 'model_training' and
     'all_sites' (sites 2..49 of the 49-source pass, P-LR r = 16 and S-LR
     r = 64, cold; with 'per_site', also the per-site accumulating backward)."""
     from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_device_problem
@@ -830,6 +830,9 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
     if "split_sources" in names:
         out["split_sources_49src_d1024_projected_r16"] = split_sources(torch, lr, dev, reps,
                                                                        warmup, flush)
+    if "decode" in names:
+        out["decode_model_pass_projected_r16_N128"] = decode_model_pass(torch, lr, dev, reps,
+                                                                        warmup)
     if "block_training" in names:
         N, d = 16384, 1024
         g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=1)
@@ -878,7 +881,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--extra-only", default="",
                     help="comma-separated workloads to run alone, without the main step "
-                         "(key_producer, all_sites, block_training, model_training; per_site "
+                         "(key_producer, split_sources, decode, all_sites, block_training, "
+                         "model_training; per_site "
                          "adds the per-site backward beside the all-sites one); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
@@ -988,6 +992,14 @@ def main():
         result["cpu_baseline"] = cpu_baseline(g, q.cpu().numpy())
     del g, V, K, dH, dV, dK, H, ws
     torch.cuda.empty_cache()
+    # The same fractions against what this GPU's plain streaming kernels
+    # reach: the backward reads and writes (copy), the forward reads.
+    print("bench: HBM ceilings", file=sys.stderr, flush=True)
+    ceil = probe_ceilings(torch, dev, 10, 2)
+    result["hbm_ceilings"] = ceil
+    roofline["frac_of_measured_copy"] = round(achieved / ceil["copy_GBps"], 4)
+    result["fwd"]["frac_of_measured_read"] = round(
+        result["fwd"]["algo_GBps"] / ceil["read_GBps"], 4)
     if not args.no_extra:
         print("bench: other workloads", file=sys.stderr, flush=True)
         result["extra"] = extras(torch, lr, dev, reps=20, warmup=3)
