@@ -182,8 +182,10 @@ def cpu_baseline(g, q, target_s=10.0, chunk=1024, single_s=4.0):
             cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
         pass
+    per_token = (fwd_bytes(S5, N5, D5, R5, 0) + bwd_bytes(S5, N5, D5, R5)) / N5
     return {"value": round(done / spent, 1), "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
+            "algo_GBps": round(done / spent * per_token / 1e9, 2),
             "sample": f"{done} tokens ({done / N5:.2f} passes over all {N5} tokens) of the main "
                       f"workload, fwd+bwd in fp64, {spent:.1f} s",
             "single_thread_value": round(done1 / spent1, 1),
@@ -949,7 +951,8 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     gpu_state = device_state(torch, dev)  # right after the timed steps
-    bwd_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    bwd_all = [a.elapsed_time(b) for a, b in events]
+    bwd_ms = float(np.mean(bwd_all))
     ms_per_step = elapsed * 1e3 / args.steps
 
     # Forward alone (same inputs), for the record.
@@ -962,7 +965,9 @@ def main():
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(b_bwd),
-                "algo_bytes_per_launch": b_bwd, "avg_launch_ms": round(bwd_ms, 4)}
+                "algo_bytes_per_launch": b_bwd, "avg_launch_ms": round(bwd_ms, 4),
+                "median_launch_ms": round(float(np.median(bwd_all)), 4),
+                "min_launch_ms": round(float(np.min(bwd_all)), 4)}
 
     result = {
         "metric": METRIC,
@@ -983,7 +988,7 @@ def main():
                    "storage": "bf16", "parallelism": "single GPU"},
         "roofline": roofline,
         "device": gpu_state,
-        "fwd": {"avg_ms": round(fwd_ms, 4),
+        "fwd": {"avg_ms": round(fwd_ms, 4), "min_ms": round(float(np.min(fwd_ts)), 4),
                 "tokens_per_s": round(N5 / (fwd_ms * 1e-3), 1),
                 "algo_GBps": round(fwd_bytes(S5, N5, D5, R5, 0) / (fwd_ms * 1e-3) / 1e9, 1)},
     }
