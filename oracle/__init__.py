@@ -57,6 +57,10 @@ def _load():
     lib.orc_block_num_sources.restype = ll
     lib.orc_block_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll]
     lib.orc_block_route_fwd.restype = ctypes.c_int
+    lib.orc_block_route_fwd2.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll, i]
+    lib.orc_block_route_fwd2.restype = ctypes.c_int
+    lib.orc_block_completed_bf16.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, ll, ll]
+    lib.orc_block_completed_bf16.restype = ctypes.c_int
     lib.orc_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d,
                                         ll, ll]
     lib.orc_block_route_bwd.restype = ctypes.c_int
@@ -165,12 +169,16 @@ def block_num_sources(t: int, c: int) -> int:
     return _load().orc_block_num_sources(t, c)
 
 
-def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
+def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None,
+                    completed_bf16=False):
     """Block-source forward at site t (Sec. 3.1 Eqs. block_attnres_sum /
     block_attnres_partial_sum with the routing of Sec. 3.2).
 
     O [t, N, d] holds o_0 .. o_{t-1}; KO [t, N, r] their projected keys (or
-    None for sliced keys).  Returns H [n1-n0, d] in fp64.
+    None for sliced keys).  Returns H [n1-n0, d] in fp64.  completed_bf16:
+    the completed block summaries (every slot but the last) are the fp32 sums
+    of their members in order, rounded once to bf16, as in
+    block_completed_bf16.
     """
     O = np.ascontiguousarray(O)
     if O.dtype not in _STORE or O.ndim != 3 or O.shape[0] < t:
@@ -185,12 +193,40 @@ def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
     q = np.ascontiguousarray(np.asarray(q, dtype=np.float64))
     n1 = N if n1 is None else n1
     out = np.empty((n1 - n0, d), dtype=np.float64)
-    rc = _load().orc_block_route_fwd(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
-                                     _ptr(out), t, c, N, d, r, mode, _STORE[O.dtype], float(eps),
-                                     n0, n1)
+    rc = _load().orc_block_route_fwd2(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
+                                      _ptr(out), t, c, N, d, r, mode, _STORE[O.dtype],
+                                      float(eps), n0, n1, int(bool(completed_bf16)))
     if rc:
         raise ValueError("oracle: invalid block problem")
     return out
+
+
+def block_completed_bf16(O, KO, t, c, mode, r=None, n0=0, n1=None):
+    """The completed block summaries that site t reads (every slot but the
+    last: S - 1 of them, S = block_num_sources(t, c)), each the fp32 sum of
+    its members in order rounded once to bf16 (nearest even); projected keys
+    the same.  Returns (B [S-1, n1-n0, d], KB [S-1, n1-n0, r] or None) as
+    fp64 arrays holding bf16 values."""
+    O = np.ascontiguousarray(O)
+    if O.dtype not in _STORE or O.ndim != 3 or O.shape[0] < t:
+        raise ValueError("oracle: O must be [>=t, N, d] in a supported storage")
+    O = np.ascontiguousarray(O[:t])
+    _, N, d = O.shape
+    if mode == PROJECTED:
+        KO = np.ascontiguousarray(np.ascontiguousarray(KO)[:t])
+        r = KO.shape[2]
+    elif r is None:
+        raise ValueError("oracle: sliced keys need r")
+    S = block_num_sources(t, c)
+    n1 = N if n1 is None else n1
+    B = np.empty((S - 1, n1 - n0, d), dtype=np.float64)
+    KB = np.empty((S - 1, n1 - n0, r), dtype=np.float64) if mode == PROJECTED else None
+    rc = _load().orc_block_completed_bf16(_ptr(O), _ptr(KO if mode == PROJECTED else None),
+                                          _ptr(B), _ptr(KB), t, c, N, d, r, mode,
+                                          _STORE[O.dtype], n0, n1)
+    if rc:
+        raise ValueError("oracle: invalid block problem (site t must have a completed slot)")
+    return B, KB
 
 
 def block_route_bwd(O, KO, q, dH, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):

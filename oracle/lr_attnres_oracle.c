@@ -342,14 +342,103 @@ long long orc_block_num_sources(long long t, long long c)
     return 1 + (t - 1) / c + ((t - 1) % c != 0);
 }
 
+/* Round-to-nearest-even of an fp32 value to bf16 (the upper 16 bits of the
+ * fp32 pattern, with the discarded lower 16 bits deciding and ties going to
+ * an even result), widened back to double.  Finite inputs only. */
+static double round_to_bf16(float x)
+{
+    uint32_t bits;
+    memcpy(&bits, &x, sizeof bits);
+    const uint32_t low = bits & 0xFFFFu, keep = bits >> 16;
+    uint32_t up = keep;
+    if (low > 0x8000u || (low == 0x8000u && (keep & 1u)))
+        up = keep + 1u;
+    const uint32_t out = up << 16;
+    float f;
+    memcpy(&f, &out, sizeof f);
+    return (double)f;
+}
+
+/* Slot of output i: 0 for the embedding, block ceil(i / c) otherwise. */
+static long long block_slot(long long i, long long c) { return i == 0 ? 0 : (i - 1) / c + 1; }
+
+/* Completed block summaries in the model's bf16 (a storage reading, not the
+ * paper's): at site t every slot but the last (the one that receives
+ * o_{t-1}) is complete, and its summary is the fp32 sum of its members in
+ * their order, rounded once to bf16 (nearest even); a projected key the
+ * same.  Writes those slots' rounded values (as doubles) into B [S][nt][d]
+ * and KB [S][nt][r] (projected) for tokens [n0, n1); the last slot's rows
+ * are left as they are. */
+static void round_completed_slots(const void *O, const void *KO, double *B, double *KB,
+                                  long long t, long long c, long long S, long long N,
+                                  long long d, long long r, int store, long long n0,
+                                  long long n1)
+{
+    const long long nt = n1 - n0;
+    for (long long slot = 0; slot + 1 < S; ++slot) {
+        const long long first = slot == 0 ? 0 : (slot - 1) * c + 1;
+        const long long last = slot == 0 ? 0 : slot * c;  /* inclusive; < t - 1 here */
+        for (long long n = n0; n < n1; ++n) {
+            for (long long j = 0; j < d; ++j) {
+                float acc = 0.0f;
+                for (long long i = first; i <= last; ++i)
+                    acc += (float)widen(O, store, (i * N + n) * d + j);
+                B[(slot * nt + (n - n0)) * d + j] = round_to_bf16(acc);
+            }
+            if (KB)
+                for (long long j = 0; j < r; ++j) {
+                    float acc = 0.0f;
+                    for (long long i = first; i <= last; ++i)
+                        acc += (float)widen(KO, store, (i * N + n) * r + j);
+                    KB[(slot * nt + (n - n0)) * r + j] = round_to_bf16(acc);
+                }
+        }
+    }
+    (void)t;
+}
+
+/* The completed block summaries of site t (see round_completed_slots), for
+ * tokens [n0, n1): B [S-1][n1-n0][d], KB [S-1][n1-n0][r] (projected, else
+ * NULL), as doubles holding bf16 values.  S = orc_block_num_sources(t, c). */
+int orc_block_completed_bf16(const void *O, const void *KO, double *B, double *KB, long long t,
+                             long long c, long long N, long long d, long long r, int mode,
+                             int store, long long n0, long long n1)
+{
+    const long long S = orc_block_num_sources(t, c);
+    if (S < 2 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
+        B == NULL || (mode != ORC_KEYS_PROJECTED && mode != ORC_KEYS_SLICED) ||
+        (mode == ORC_KEYS_PROJECTED) != (KO != NULL) || (mode == ORC_KEYS_PROJECTED) != (KB != NULL) ||
+        store < 0 || store > 1)
+        return 1;
+    /* S slots of scratch, the last one unused, then copied out. */
+    const long long nt = n1 - n0;
+    double *Bs = (double *)calloc((size_t)(S * nt * d), sizeof(double));
+    double *KBs = KB ? (double *)calloc((size_t)(S * nt * r), sizeof(double)) : NULL;
+    if (Bs == NULL || (KB && KBs == NULL)) {
+        free(Bs);
+        free(KBs);
+        return 1;
+    }
+    round_completed_slots(O, KO, Bs, KBs, t, c, S, N, d, r, store, n0, n1);
+    memcpy(B, Bs, sizeof(double) * (size_t)((S - 1) * nt * d));
+    if (KB)
+        memcpy(KB, KBs, sizeof(double) * (size_t)((S - 1) * nt * r));
+    free(Bs);
+    free(KBs);
+    return 0;
+}
+
 /* Forward at site t: O is [t][N][d] (o_0 .. o_{t-1}), KO is [t][N][r]
  * (projected keys) or NULL.  H[n - n0][:] as in orc_route_fwd, with the
  * block summaries of the outputs as sources, for tokens [n0, n1).  The
  * summaries are formed in double; then the routing of Sec. 3.2 applies to
- * them unchanged (sliced keys: the tail of each summary). */
-int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *H,
-                        long long t, long long c, long long N, long long d, long long r,
-                        int mode, int store, double eps, long long n0, long long n1)
+ * them unchanged (sliced keys: the tail of each summary).  completed_bf16:
+ * the completed summaries (every slot but the last) are instead the bf16
+ * roundings of round_completed_slots. */
+int orc_block_route_fwd2(const void *O, const void *KO, const double *q, double *H,
+                         long long t, long long c, long long N, long long d, long long r,
+                         int mode, int store, double eps, long long n0, long long n1,
+                         int completed_bf16)
 {
     const long long S = orc_block_num_sources(t, c);
     if (S < 1 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
@@ -369,7 +458,7 @@ int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *
     }
     for (long long i = 0; i < t; ++i) {
         /* output i belongs to slot 0 (embedding) or block ceil(i / c) */
-        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
+        const long long slot = block_slot(i, c);
         for (long long n = n0; n < n1; ++n) {
             for (long long j = 0; j < d; ++j)
                 B[(slot * nt + (n - n0)) * d + j] += widen(O, store, (i * N + n) * d + j);
@@ -378,10 +467,19 @@ int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *
                     KB[(slot * nt + (n - n0)) * r + j] += widen(KO, store, (i * N + n) * r + j);
         }
     }
+    if (completed_bf16)
+        round_completed_slots(O, KO, B, KB, t, c, S, N, d, r, store, n0, n1);
     const int rc = orc_route_fwd(B, KB, q, H, S, nt, d, r, mode, ORC_STORE_F64, eps, 0, nt);
     free(B);
     free(KB);
     return rc;
+}
+
+int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *H,
+                        long long t, long long c, long long N, long long d, long long r,
+                        int mode, int store, double eps, long long n0, long long n1)
+{
+    return orc_block_route_fwd2(O, KO, q, H, t, c, N, d, r, mode, store, eps, n0, n1, 0);
 }
 
 /* Backward of the block-source forward at site t for L = sum_n dH[n] . h[n]:

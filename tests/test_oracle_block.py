@@ -132,3 +132,83 @@ def test_block_backward_of_blocks_of_one_is_the_routing_backward(orc):
     np.testing.assert_allclose(dO, dV, rtol=0, atol=1e-14)
     np.testing.assert_allclose(dKO, dK, rtol=0, atol=1e-14)
     np.testing.assert_allclose(dq, dq2, rtol=0, atol=1e-13)
+
+
+# --- Completed block summaries stored in bf16 (a storage reading: every slot
+# but the last holds the fp32 sum of its members in order, rounded once to
+# bf16 with ties to even).  The expected values below are worked by hand.
+
+def _bits(x):
+    """bf16 raw bits of values that are exactly representable in bf16."""
+    return (np.asarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_completed_bf16_ties_and_nearest_by_hand(orc):
+    """Site t = 4 with blocks of c = 2 reads slot 0 = o_0, slot 1 = o_1 + o_2
+    (completed) and slot 2 = o_3 (the newest).  Column 0: 1 + 2^-8 lies
+    halfway between bf16 1 and 1 + 2^-7 and goes to 1 (even); column 1:
+    1 + 3 2^-8, halfway between 1 + 2^-7 and 1 + 2^-6, goes to 1 + 2^-6
+    (even); column 2: 1 + 5 2^-9 is nearest 1 + 2^-7.  With q = 0 the weights
+    are equal, so h is the mean of the three summaries."""
+    O = _bits([[[0.5, 0.25, 2.0, 0.0]],
+               [[1.0, 1.0, 1.0, 0.0]],
+               [[2.0 ** -8, 3 * 2.0 ** -8, 2.0 ** -9, 0.0]],
+               [[4.0, 8.0, 0.0, 0.0]]])
+    O[2, 0, 2] = _bits(5 * 2.0 ** -9)  # 5 2^-9 = 1.25 2^-7 is a bf16 value
+    B, KB = orc.block_completed_bf16(O, None, 4, 2, SLICED, r=1)
+    assert KB is None and B.shape == (2, 1, 4)
+    assert B[1, 0, :3].tolist() == [1.0, 1.0 + 2.0 ** -6, 1.0 + 2.0 ** -7]
+    assert B[0, 0].tolist() == [0.5, 0.25, 2.0, 0.0]
+    h = orc.block_route_fwd(O, None, np.zeros(1), 4, 2, SLICED, r=1, completed_bf16=True)
+    want = (B[0, 0] + B[1, 0] + np.array([4.0, 8.0, 0.0, 0.0])) / 3
+    np.testing.assert_allclose(h[0], want, rtol=0, atol=1e-15)
+    exact = orc.block_route_fwd(O, None, np.zeros(1), 4, 2, SLICED, r=1)
+    assert exact[0, 0] == pytest.approx((0.5 + 1.0 + 2.0 ** -8 + 4.0) / 3, abs=1e-15)
+
+
+def test_completed_bf16_leaves_the_newest_slot_exact(orc):
+    """At site t = 3 with c = 2, slot 1 = o_1 + o_2 is full but it is the
+    slot that receives o_2, so it is read unrounded; slot 0 is the only
+    completed one."""
+    O = _bits([[[1.0]], [[1.0]], [[2.0 ** -8]]])
+    h = orc.block_route_fwd(O, None, np.zeros(1), 3, 2, SLICED, r=1, completed_bf16=True)
+    assert h[0, 0] == pytest.approx((1.0 + 1.0 + 2.0 ** -8) / 2, abs=1e-15)
+
+
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_completed_bf16_blocks_of_one_are_exact(orc, mode):
+    """With blocks of one output every completed summary is a single bf16
+    output, which rounds to itself: the result equals the exact one."""
+    p = make_host_problem(mode, 9, 5, 32, 8, dtype="bf16", seed=3, q_scale=4.0)
+    for t in (2, 5, 9):
+        a = orc.block_route_fwd(p.V, p.K, p.q, t, 1, mode, r=p.r, completed_bf16=True)
+        b = orc.block_route_fwd(p.V, p.K, p.q, t, 1, mode, r=p.r)
+        assert np.array_equal(a, b)
+
+
+def test_completed_bf16_projected_key_rounding_by_hand(orc):
+    """P-LR at t = 4, c = 2: the completed slot's key (1, 1 + 3 2^-8) rounds
+    to (1, 1 + 2^-6), which changes its score; the expected h is the plain
+    routing (the oracle's single-site forward, pinned on its own) over the
+    hand-rounded summaries."""
+    O = _bits([[[1.0, 0.0]], [[0.0, 1.0]], [[2.0, 0.0]], [[0.0, 0.0]]])
+    KO = _bits([[[1.0, 0.5]], [[1.0, 1.0]], [[0.0, 3 * 2.0 ** -8]], [[0.5, 1.0]]])
+    q = np.array([0.7, -1.3])
+    B = np.array([[[1.0, 0.0]], [[2.0, 1.0]], [[0.0, 0.0]]])
+    K = np.array([[[1.0, 0.5]], [[1.0, 1.0 + 2.0 ** -6]], [[0.5, 1.0]]])
+    want = orc.route_fwd(B, K, q, PROJECTED, eps=1e-6)
+    got = orc.block_route_fwd(O, KO, q, 4, 2, PROJECTED, completed_bf16=True)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-14)
+    KB = orc.block_completed_bf16(O, KO, 4, 2, PROJECTED)[1]
+    assert KB[1, 0].tolist() == [1.0, 1.0 + 2.0 ** -6]
+    exact = orc.block_route_fwd(O, KO, q, 4, 2, PROJECTED)
+    assert np.abs(exact - got).max() > 1e-4  # the rounding is visible
+
+
+def test_completed_bf16_token_ranges_compose(orc):
+    p = make_host_problem(SLICED, 20, 13, 48, 8, dtype="bf16", seed=8, q_scale=3.0)
+    full = orc.block_route_fwd(p.V, None, p.q, 20, 6, SLICED, r=8, completed_bf16=True)
+    part = np.concatenate([orc.block_route_fwd(p.V, None, p.q, 20, 6, SLICED, r=8, n0=a, n1=b,
+                                               completed_bf16=True)
+                           for a, b in ((0, 4), (4, 13))])
+    assert np.array_equal(full, part)
