@@ -359,27 +359,37 @@ def model_training_pass(torch, lr, dev, V, K, mode, r, reps, warmup):
     return res
 
 
-def block_pass_bytes(t, c, N, d, r, mode, es=2):
+def block_pass_bytes(t, c, N, d, r, mode, es=2, completed_bf16=False):
     """Algorithmic HBM bytes of the fused block call at site t: the earlier
     fp32 slots (with their fp32 key slots for projected keys) read once, the
-    updated slot read (unless it starts) and written, o_{t-1} read, h written."""
+    updated slot read (unless it starts) and written, o_{t-1} read, h written.
+    completed_bf16: the earlier slots are bf16 copies (2 bytes), and a call
+    that completes its block also writes the slot's bf16 copy."""
     if t == 1:
-        j, start = 0, True
+        j, start, finish = 0, True, True
     else:
-        j, start = (t - 2) // c + 1, (t - 2) % c == 0
+        j, start, finish = (t - 2) // c + 1, (t - 2) % c == 0, (t - 1) % c == 0
     row = d + (r if mode == 0 else 0)
-    b = j * N * row * 4 + (0 if start else N * row * 4) + N * row * 4
+    eb = 2 if completed_bf16 else 4
+    b = j * N * row * eb + (0 if start else N * row * 4) + N * row * 4
+    if completed_bf16 and finish:
+        b += N * row * 2
     return b + N * row * es + N * d * es
 
 
-def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush):
+def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush, completed_bf16=False):
     """49-site block-source forward pass over the output stack O [49, N, d].
     Each site's real call (with its own start flag) is timed `reps` times;
-    before each, untimed, the updated slot is restored and the MALL flushed."""
+    before each, untimed, the updated slot is restored and the MALL flushed.
+    completed_bf16: the completed summaries are read from bf16 copies."""
     T, N, d = O.shape
     nslots = (T - 2) // c + 2
     B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
     KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev) if mode == 0 else None
+    BC = KBC = None
+    if completed_bf16:
+        BC = torch.zeros((nslots, N, d), dtype=torch.bfloat16, device=dev)
+        KBC = torch.zeros((nslots, N, r), dtype=torch.bfloat16, device=dev) if mode == 0 else None
     gen = torch.Generator(device=dev).manual_seed(100 + r)
     KO = (torch.randn((T, N, r), generator=gen, device=dev).to(torch.bfloat16)
           if mode == 0 else None)
@@ -399,8 +409,14 @@ def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush):
             if KB is not None:
                 KB[j].copy_(ksaved)
 
+        finish = t == 1 or (t - 1) % c == 0
+
         def call():
-            lr.block_route_fwd(B, KB, O[t - 1], kn, Q[t - 1], n_src, start, mode, out=H)
+            if completed_bf16:
+                lr.block_route_fwd_bf16c(B, KB, BC, KBC, O[t - 1], kn, Q[t - 1], n_src, start,
+                                         finish, mode, out=H)
+            else:
+                lr.block_route_fwd(B, KB, O[t - 1], kn, Q[t - 1], n_src, start, mode, out=H)
 
         for _ in range(warmup):
             restore()
@@ -416,9 +432,9 @@ def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush):
             ev.append((a, b))
         torch.cuda.synchronize()
         total += float(np.median([a.elapsed_time(b) for a, b in ev]))
-        nbytes += block_pass_bytes(t, c, N, d, r, mode)
+        nbytes += block_pass_bytes(t, c, N, d, r, mode, completed_bf16=completed_bf16)
         del saved, ksaved
-    del B, KB, KO
+    del B, KB, KO, BC, KBC
     return {"total_ms": total, "tokens_per_s": N / (total * 1e-3),
             "algo_GBps": nbytes / (total * 1e-3) / 1e9,
             "frac_of_peak": nbytes / (total * 1e-3) / 1e9 / HBM_PEAK_GBS}
@@ -797,6 +813,10 @@ def extras(torch, lr, dev, reps, warmup):
                                                             6, reps, warmup, flush)
     out["block_model_pass_projected_r32_8blocks"] = block_pass(torch, lr, dev, V, PROJECTED,
                                                                32, 6, reps, warmup, flush)
+    for mode, r in ((SLICED, 64), (PROJECTED, 32)):
+        key = f"block_model_pass_{'sliced' if mode == SLICED else 'projected'}_r{r}_8blocks"
+        out[key + "_bf16_completed"] = block_pass(torch, lr, dev, V, mode, r, 6, reps, warmup,
+                                                  flush, completed_bf16=True)
     out["model_training_pass_projected_r16"] = model_training_pass(
         torch, lr, dev, V, K, PROJECTED, 16, 3, 1)
     out["model_training_pass_sliced_r64"] = model_training_pass(
@@ -820,7 +840,8 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
     """Only the named workloads (for profiling one kernel at a time):
     'key_producer', 'split_sources' (the deepest site at decode token counts,
     one call against states + merge), 'decode' (a 49-site pass at N = 128,
-    eager and as one graph), 'block_training', 'model_training' and
+    eager and as one graph), 'block_forward' (the 8-block forward pass, fp32 and
+    bf16 completed summaries), 'block_training', 'model_training' and
     'all_sites' (sites 2..49 of the 49-source pass, P-LR r = 16 and S-LR
     r = 64, cold; with 'per_site', also the per-site accumulating backward)."""
     from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_device_problem
@@ -835,6 +856,16 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
     if "decode" in names:
         out["decode_model_pass_projected_r16_N128"] = decode_model_pass(torch, lr, dev, reps,
                                                                         warmup)
+    if "block_forward" in names:
+        N, d = 16384, 1024
+        g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=1)
+        for mode, r in ((SLICED, 64), (PROJECTED, 32)):
+            key = f"block_model_pass_{'sliced' if mode == SLICED else 'projected'}_r{r}_8blocks"
+            out[key] = block_pass(torch, lr, dev, g["V"], mode, r, 6, reps, warmup, flush)
+            out[key + "_bf16_completed"] = block_pass(torch, lr, dev, g["V"], mode, r, 6, reps,
+                                                      warmup, flush, completed_bf16=True)
+        del g
+        torch.cuda.empty_cache()
     if "block_training" in names:
         N, d = 16384, 1024
         g = make_device_problem(PROJECTED, 49, N, d, 16, dev, seed=0, n_queries=1)
@@ -883,7 +914,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--extra-only", default="",
                     help="comma-separated workloads to run alone, without the main step "
-                         "(key_producer, split_sources, decode, all_sites, block_training, "
+                         "(key_producer, split_sources, decode, all_sites, block_forward, "
+                         "block_training, "
                          "model_training; per_site "
                          "adds the per-site backward beside the all-sites one); prints their JSON")
     ap.add_argument("--counters-pass", action="store_true",

@@ -173,6 +173,33 @@ int lr_attnres_block_route_fwd(float *B, float *KB, const void *o_new, const voi
                                void *stream);
 
 /*
+ * The same site with the completed block summaries stored in bf16 (bf16
+ * storage only).  Block AttnRes (Sec. 3.1) reads every completed summary at
+ * every later site; this keeps them as bf16 copies, which halves those
+ * reads.  The paper states no precision for the summaries; this storage
+ * option is the library's reading:
+ *   - slot n_src-1 (the one o_new joins) is updated in the fp32 B / KB
+ *     exactly as in lr_attnres_block_route_fwd and routed from fp32;
+ *   - slots 0..n_src-2 (completed) are read from BC [.][N][d] bf16 and, for
+ *     projected keys, KBC [.][N][r] bf16, instead of B and KB;
+ *   - finish = 1 (o_new is the last member of its block, or the embedding)
+ *     also writes BC[n_src-1] (and KBC[n_src-1]): the updated fp32 row
+ *     rounded once to bf16, round to nearest even.
+ * A model pass sets finish at site 1 (the embedding) and at every site
+ * whose o_new completes a block of c, t - 1 = jc, so each copy is the fp32
+ * member-order sum of its block, rounded once.
+ * BC / KBC need 16-byte alignment.  BC is required when N > 0 and either
+ * n_src > 1 or finish = 1; KBC likewise with projected keys, NULL
+ * otherwise.  Errors and limits as for lr_attnres_block_route_fwd, plus
+ * EINVAL for finish not 0/1; BC and KBC must not overlap any other
+ * argument.
+ */
+int lr_attnres_block_route_fwd_bf16c(float *B, float *KB, void *BC, void *KBC,
+                                     const void *o_new, const void *k_new, const float *q,
+                                     void *H, int64_t n_src, int start, int finish, int64_t N,
+                                     int64_t d, int64_t r, int mode, float eps, void *stream);
+
+/*
  * Block-source backward at one residual site, for the reverse pass of a
  * model that ran lr_attnres_block_route_fwd at every site (Sec. 3.1 "Block
  * AttnRes" with Sec. 3.2; the gradient of L = sum_n dH[n] . h[n]).  Sites are

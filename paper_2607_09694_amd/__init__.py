@@ -59,6 +59,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                ctypes.c_size_t, i64, i64, i64, i64, i, i, f, vp]
     lib.lr_attnres_block_route_bwd.restype = ctypes.c_int
+    lib.lr_attnres_block_route_fwd_bf16c.argtypes = [vp] * 8 + [i64, i, i, i64, i64, i64, i, f,
+                                                                vp]
+    lib.lr_attnres_block_route_fwd_bf16c.restype = ctypes.c_int
     lib.lr_attnres_block_inter_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64,
                                                i, f, vp]
     lib.lr_attnres_block_inter_fwd.restype = ctypes.c_int
@@ -484,6 +487,39 @@ def block_route_fwd(B, KB, o_new, k_new, q, n_src: int, start: bool, mode, eps: 
         _dev(B, "B"), _dev(KB, "KB"), _dev(o_new, "o_new"), _dev(k_new, "k_new", o_new.dtype),
         _dev(q, "q", torch.float32), _dev(H, "H", o_new.dtype), int(n_src), int(bool(start)),
         N, d, r, mode, _dtype_code(o_new), float(eps), _stream(B))
+    _check(lib, rc)
+    return H
+
+
+def block_route_fwd_bf16c(B, KB, BC, KBC, o_new, k_new, q, n_src: int, start: bool,
+                          finish: bool, mode, eps: float = 1e-6, out=None):
+    """block_route_fwd with the completed block summaries stored in bf16:
+    slots 0..n_src-2 are read from BC [>=n_src, N, d] bf16 (KBC [>=n_src,
+    N, r] bf16 for projected keys, else None); slot n_src-1 is updated in
+    the fp32 B / KB as in block_route_fwd and, when ``finish`` (o_new is its
+    block's last member, or the embedding), also rounded into BC / KBC.
+    bf16 storage only.  Returns H [N, d] bf16."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    if B.dtype != torch.float32 or (KB is not None and KB.dtype != torch.float32):
+        raise TypeError("summary slots must be float32")
+    if B.dim() != 3 or B.shape[0] < n_src or BC.dim() != 3 or BC.shape[0] < n_src:
+        raise ValueError("B and BC must be [>= n_src, N, d]")
+    _, N, d = B.shape
+    if tuple(BC.shape[1:]) != (N, d):
+        raise ValueError("BC must match B's [N, d]")
+    r = KB.shape[2] if mode == PROJECTED else q.shape[0]
+    if tuple(o_new.shape) != (N, d):
+        raise ValueError("o_new must be [N, d]")
+    bf = torch.bfloat16
+    H = out if out is not None else torch.empty((N, d), dtype=bf, device=B.device)
+    rc = lib.lr_attnres_block_route_fwd_bf16c(
+        _dev(B, "B"), _dev(KB, "KB"), _dev(BC, "BC", bf), _dev(KBC, "KBC", bf),
+        _dev(o_new, "o_new", bf), _dev(k_new, "k_new", bf), _dev(q, "q", torch.float32),
+        _dev(H, "H", bf), int(n_src), int(bool(start)), int(bool(finish)), N, d, r, mode,
+        float(eps), _stream(B))
     _check(lib, rc)
     return H
 

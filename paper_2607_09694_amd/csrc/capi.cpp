@@ -322,6 +322,59 @@ int lr_attnres_block_route_bwd(float *B, float *KB, float *dB, float *dKB, const
     return LRAR_OK;
 }
 
+int lr_attnres_block_route_fwd_bf16c(float *B, float *KB, void *BC, void *KBC,
+                                     const void *o_new, const void *k_new, const float *q,
+                                     void *H, int64_t n_src, int start, int finish, int64_t N,
+                                     int64_t d, int64_t r, int mode, float eps, void *stream)
+{
+    g_last_error.clear();
+    if (int krc = block_keys(&mode, d, r))
+        return krc;
+    if (start != 0 && start != 1)
+        return fail(LRAR_EINVAL, "start must be 0 or 1");
+    if (finish != 0 && finish != 1)
+        return fail(LRAR_EINVAL, "finish must be 0 or 1");
+    const int dtype = LRAR_DTYPE_BF16;
+    int64_t ve, ke, he;
+    int rc = check_shape(n_src, N, d, r, mode, dtype, eps, &ve, &ke, &he);
+    if (rc)
+        return rc;
+    const bool data = N > 0;
+    const bool proj = mode == LRAR_MODE_PROJECTED;
+    // The copies are read for the completed slots (n_src > 1) and written
+    // for slot n_src - 1 when it finishes.
+    const bool copies = data && (n_src > 1 || finish);
+    if ((rc = check_ptr(B, "B", 16, data)) || (rc = check_ptr(o_new, "o_new", 16, data)) ||
+        (rc = check_ptr(q, "q", 4, true)) || (rc = check_ptr(H, "H", 16, data)) ||
+        (rc = check_ptr(KB, "KB", 16, data && proj)) ||
+        (rc = check_ptr(k_new, "k_new", 2, data && proj)) ||
+        (rc = check_ptr(BC, "BC", 16, copies)) || (rc = check_ptr(KBC, "KBC", 16, copies && proj)))
+        return rc;
+    if (!proj && (KB || k_new || KBC))
+        return fail(LRAR_EINVAL, "KB, k_new and KBC must be NULL unless keys are projected");
+    int64_t nr;
+    if (!mul_ok(N, r, &nr))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    // B, KB, BC and KBC are read and rewritten: checked as outputs.
+    const Span outs[] = {span("H", H, he * 2), span("B", B, ve * 4), span("KB", KB, ke * 4),
+                         span("BC", BC, ve * 2), span("KBC", KBC, ke * 2)};
+    const Span ins[] = {span("o_new", o_new, he * 2), span("k_new", k_new, nr * 2),
+                        span("q", q, r * 4)};
+    if ((rc = check_aliasing(outs, 5, ins, 3)))
+        return rc;
+    lrar::BlockProblem p{B, KB, o_new, k_new, q, H, n_src, N, d, r, start, mode, dtype, eps};
+    p.completed_bf16 = 1;
+    p.BC = BC;
+    p.KBC = KBC;
+    p.finish = finish;
+    std::string why;
+    if ((rc = lrar::check_block_supported(p, &why)))
+        return fail(rc, why);
+    if ((rc = lrar::launch_block_fwd(p, static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 int lr_attnres_block_inter_fwd(const float *B, const float *KB, const float *Q, float *M,
                                float *L, float *ACC, int64_t n_prev, int64_t n_queries,
                                int64_t N, int64_t d, int64_t r, int mode, float eps,

@@ -11,17 +11,27 @@
 // slot j comes from the registers.  A summary's key is the sum of its
 // members' keys: for sliced keys the tail of the summed row, for projected
 // keys a second fp32 slot stack [slot][N][r] updated the same way.
+//
+// Completed summaries in bf16 (TC = bf16, a storage option): the earlier
+// slots are read from bf16 copies BC [slot][N][d] (and KBC [slot][N][r])
+// instead of the fp32 slots, which halves what a site reads of them; the
+// partial slot stays fp32.  When `finish` is set, the call that adds a
+// block's last member also writes that slot's copy: the updated fp32 row,
+// rounded once to bf16.  With TC = float, BC and KBC are the fp32 slots
+// themselves and nothing is written to them beyond the slot update.
 #include <algorithm>
+#include <type_traits>
 
 #include "route_common.h"
 
 namespace lrar {
 
-template <typename TO, int NCH, bool FULLCOLS>
+template <typename TO, typename TC, int NCH, bool FULLCOLS>
 __global__ void __launch_bounds__(kBlock)
-route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restrict__ o_new,
-                const TO *__restrict__ k_new, const float *__restrict__ q, TO *__restrict__ H,
-                int nsrc, int start, int N, int d, int r, int sliced, float eps, int s_pad)
+route_fwd_block(float *__restrict__ B, float *__restrict__ KB, TC *BC, TC *KBC,
+                const TO *__restrict__ o_new, const TO *__restrict__ k_new,
+                const float *__restrict__ q, TO *__restrict__ H, int nsrc, int start, int finish,
+                int N, int d, int r, int sliced, float eps, int s_pad)
 {
     constexpr int VEC = 4;  // fp32 slot rows move in 16-byte vectors of 4
     extern __shared__ float lds[];
@@ -56,9 +66,9 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
         }
     }
 
-    // 2. Scores of the earlier slots from their fp32 keys.
-    lr_scores<float, VEC>(sliced ? B : KB, q, j, N, r, sliced ? d : r, sliced ? d - r : 0, eps,
-                          n, lane, s, nullptr);
+    // 2. Scores of the earlier (completed) slots from their keys.
+    lr_scores<TC, VEC>(sliced ? BC : KBC, q, j, N, r, sliced ? d : r, sliced ? d - r : 0, eps, n,
+                       lane, s, nullptr);
 
     // 3. The updated summary row of slot j (Eqs. block_attnres_sum /
     //    block_attnres_partial_sum: one more member added), kept in registers,
@@ -80,6 +90,11 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
             for (int e = 0; e < VEC; ++e)
                 nw[c][e] = x[e];
             store_raw<float, VEC>(brow + c * kWaveSize * VEC, Narrow<float, VEC>::run(nw[c]));
+            if constexpr (!std::is_same<TC, float>::value)
+                if (finish)
+                    store_raw<TC, VEC>(BC + (size_t)j * plane + (size_t)n * d + col +
+                                           c * kWaveSize * VEC,
+                                       Narrow<TC, VEC>::run(nw[c]));
         } else {
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
@@ -104,6 +119,9 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
         for (int jj = lane; jj < r; jj += kWaveSize) {
             const float k = (start ? 0.0f : krow[jj]) + load_elem(knew + jj);
             krow[jj] = k;
+            if constexpr (!std::is_same<TC, float>::value)
+                if (finish)
+                    store_elem(KBC + ((size_t)j * N + n) * r + jj, k);
             ss = fmaf(k, k, ss);
             dot = fmaf(q[jj], k, dot);
         }
@@ -117,7 +135,7 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, const TO *__restr
 
     // 4. h = sum_i alpha_i b_i: slots 0..j-1 from HBM, slot j from registers.
     float acc[NCH][VEC];
-    mix_rows<float, VEC, NCH, FULLCOLS>(B + (size_t)n * d + col, plane, j, s, ok, acc);
+    mix_rows<TC, VEC, NCH, FULLCOLS>(BC + (size_t)n * d + col, plane, j, s, ok, acc);
     const float aj = s[j];
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
@@ -417,20 +435,24 @@ hipError_t launch_retire_t(const BlockRetire &br, hipStream_t st)
 
 namespace {
 
-template <typename TO>
+template <typename TO, typename TC>
 hipError_t launch_block_t(const BlockProblem &p, int nch, bool fullcols, size_t lds, int nblocks,
                           hipStream_t st)
 {
     const int s_pad = (int)((p.nsrc + 3) / 4 * 4);
     const int sliced = p.mode == LRAR_MODE_SLICED ? 1 : 0;
+    // fp32 completed slots are the slots themselves.
+    TC *BC = std::is_same<TC, float>::value ? reinterpret_cast<TC *>(p.B) : static_cast<TC *>(p.BC);
+    TC *KBC = std::is_same<TC, float>::value ? reinterpret_cast<TC *>(p.KB)
+                                             : static_cast<TC *>(p.KBC);
     auto go = [&](auto nchc, auto fc) {
         constexpr int NCH = decltype(nchc)::value;
         constexpr bool FC = decltype(fc)::value;
-        hipLaunchKernelGGL((route_fwd_block<TO, NCH, FC>), dim3(nblocks), dim3(kBlock), lds, st,
-                           p.B, p.KB, static_cast<const TO *>(p.o_new),
+        hipLaunchKernelGGL((route_fwd_block<TO, TC, NCH, FC>), dim3(nblocks), dim3(kBlock), lds,
+                           st, p.B, p.KB, BC, KBC, static_cast<const TO *>(p.o_new),
                            static_cast<const TO *>(p.k_new), p.q, static_cast<TO *>(p.H),
-                           (int)p.nsrc, p.start, (int)p.N, (int)p.d, (int)p.r, sliced, p.eps,
-                           s_pad);
+                           (int)p.nsrc, p.start, p.finish, (int)p.N, (int)p.d, (int)p.r, sliced,
+                           p.eps, s_pad);
         return hipGetLastError();
     };
     typedef std::true_type Y;
@@ -757,10 +779,13 @@ int launch_block_fwd(const BlockProblem &p, hipStream_t st, std::string *err)
     const bool fullcols = p.d % (256 * nch) == 0;
     const size_t lds = (size_t)kWaves * ((p.nsrc + 3) / 4 * 4) * sizeof(float);
     const int nblocks = (int)((p.N + kWaves - 1) / kWaves);
-    const hipError_t e =
-        p.dtype == LRAR_DTYPE_BF16
-            ? launch_block_t<uint16_t>(p, nch, fullcols, lds, nblocks, st)
-            : launch_block_t<float>(p, nch, fullcols, lds, nblocks, st);
+    hipError_t e;
+    if (p.completed_bf16)  // bf16 completed summaries (bf16 storage only)
+        e = launch_block_t<uint16_t, uint16_t>(p, nch, fullcols, lds, nblocks, st);
+    else
+        e = p.dtype == LRAR_DTYPE_BF16
+                ? launch_block_t<uint16_t, float>(p, nch, fullcols, lds, nblocks, st)
+                : launch_block_t<float, float>(p, nch, fullcols, lds, nblocks, st);
     return hip_status(e, "block_route_fwd launch", err);
 }
 

@@ -52,6 +52,13 @@ struct BlockProblem {
     int64_t nsrc, N, d, r;
     int start, mode, dtype;
     float eps;
+    // completed_bf16: the completed summaries are read from bf16 copies BC
+    // [nsrc][N][d] (and KBC [nsrc][N][r], projected) instead of the fp32
+    // slots (bf16 storage only), and `finish` writes slot nsrc-1's copy.
+    int completed_bf16 = 0;
+    void *BC = nullptr;
+    void *KBC = nullptr;
+    int finish = 0;
 };
 
 int check_block_supported(const BlockProblem &p, std::string *why);

@@ -48,6 +48,7 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_route_all_bwd", "lr_attnres_route_all_bwd_workspace_bytes",
                             "lr_attnres_route_bwd_deferred", "lr_attnres_route_gather_bwd",
                             "lr_attnres_route_state_fwd", "lr_attnres_route_merge_fwd",
+                            "lr_attnres_block_route_fwd_bf16c",
                             "lr_attnres_route_bwd_workspace_bytes", "lr_attnres_last_error",
                             "lr_attnres_abi_version"])
     out = subprocess.run(["nm", "-D", "--defined-only", lr.LIB_PATH], capture_output=True,
@@ -556,3 +557,33 @@ def test_split_sources_unsupported(lib):
     assert state_call(lib, S=70000, chunk=1, N=2) == EUNSUPPORTED and "65535" in err(lib)
     assert state_call(lib, mode=F, d=8192, r=8192) == EUNSUPPORTED
     assert merge_call(lib, P=1025) == EUNSUPPORTED and "1024" in err(lib)
+
+
+def bfc_call(lib, B=A, KB=None, BC=C, KBC=None, o_new=D, k_new=None, q=E, H=G, n_src=3, start=0,
+             finish=0, N=8, d=64, r=8, mode=SL, eps=1e-6):
+    return lib.lr_attnres_block_route_fwd_bf16c(B, KB, BC, KBC, o_new, k_new, q, H, n_src, start,
+                                                finish, N, d, r, mode, eps, None)
+
+
+BFC_INVALID = [
+    ("finish not 0/1", dict(finish=2), "finish"),
+    ("BC NULL with completed slots", dict(BC=None), "BC is NULL"),
+    ("BC NULL when finishing", dict(BC=None, n_src=1, finish=1), "BC is NULL"),
+    ("BC misaligned", dict(BC=C + 8), "16-byte aligned"),
+    ("KBC outside projected", dict(KBC=W), "must be NULL"),
+    ("KBC NULL when projected", dict(mode=P, KB=W, k_new=B_, KBC=None), "KBC is NULL"),
+    ("BC overlaps B", dict(BC=A + 64), "overlap"),
+    ("H overlaps BC", dict(H=C + 16), "overlap"),
+    ("BC overlaps o_new", dict(BC=D - 64), "overlap"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", BFC_INVALID, ids=[c[0] for c in BFC_INVALID])
+def test_block_bf16_copies_rejects(lib, name, kw, msg):
+    assert bfc_call(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_block_bf16_copies_unsupported(lib):
+    assert bfc_call(lib, d=66) == EUNSUPPORTED
+    assert bfc_call(lib, d=4096) == EUNSUPPORTED

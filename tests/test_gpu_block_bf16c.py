@@ -1,0 +1,166 @@
+"""GPU parity of the block-source forward with the completed block summaries
+stored in bf16 (Sec. 3.1 Block AttnRes with the keys of Sec. 3.2; the bf16
+storage of completed summaries is the library's reading): a whole model pass
+driven site by site, every site's h against the fp64 oracle with the same
+reading, and the bf16 copies against the oracle's rounded summaries bit for
+bit (both round the fp32 member-order sum once, to nearest even).
+
+Cases: both key modes, blocks of one (every copy is a single output), a
+single partial block, scalar key paths (r or the sliced key offset not a
+multiple of 4), the widest row, and the paper's 8-block pass at full size
+(sampled tokens)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_tensor_to_bits,
+                                         f32_from_bf16_bits, make_host_problem)
+from parity import check_bf16_key_grad
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(x, dev):
+    if x is None:
+        return None
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(x).to(dev)
+
+
+def to_host(t):
+    return f32_from_bf16_bits(bf16_tensor_to_bits(t))
+
+
+def site_args(t, c):
+    """Slot count, start and finish flags of site t (1-based), blocks of c:
+    o_{t-1} starts its block when (t-2) mod c == 0 and completes it when
+    (t-1) mod c == 0; the embedding (site 1) is a block of its own."""
+    if t == 1:
+        return 1, True, True
+    return (t - 2) // c + 2, (t - 2) % c == 0, (t - 1) % c == 0
+
+
+def drive_pass(dev, O, KO, Q, c, mode, sites):
+    T, N, d = O.shape
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    BC = torch.zeros((nslots, N, d), dtype=torch.bfloat16, device=dev)
+    KB = KBC = None
+    if mode == PROJECTED:
+        r = KO.shape[2]
+        KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev)
+        KBC = torch.zeros((nslots, N, r), dtype=torch.bfloat16, device=dev)
+    out = {}
+    for t in range(1, max(sites) + 1):
+        n_src, start, finish = site_args(t, c)
+        knew = KO[t - 1] if mode == PROJECTED else None
+        H = lr.block_route_fwd_bf16c(B, KB, BC, KBC, O[t - 1], knew, Q[t - 1], n_src, start,
+                                     finish, mode)
+        if t in sites:
+            out[t] = H
+    torch.cuda.synchronize()
+    return out, BC, KBC
+
+
+def expected_copies(Oh, KOh, T, c, mode, r):
+    """The oracle's rounded summaries of every block completed by site T's
+    output, as bf16 bits: read at a site T + 1 (one zero output appended)."""
+    pad = np.zeros((1,) + Oh.shape[1:], dtype=Oh.dtype)
+    O1 = np.concatenate([Oh, pad])
+    K1 = None if KOh is None else np.concatenate([KOh, np.zeros((1,) + KOh.shape[1:], KOh.dtype)])
+    B, KB = oracle.block_completed_bf16(O1, K1, T + 1, c, mode, r=r)
+    to_bits = lambda a: (a.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return to_bits(B), None if KB is None else to_bits(KB)
+
+
+# (mode, T, N, d, r, c)
+CASES = [
+    (PROJECTED, 13, 70, 256, 16, 3),
+    (SLICED, 13, 70, 256, 16, 3),
+    (SLICED, 9, 21, 2048, 8, 1),     # blocks of one: each copy is one output
+    (PROJECTED, 9, 24, 100, 7, 20),  # one partial block; r = 7 scalar key loads
+    (SLICED, 11, 33, 256, 10, 2),    # sliced key offset 246: scalar key loads
+    (PROJECTED, 17, 40, 1024, 32, 4),
+    (SLICED, 16, 19, 520, 64, 5),    # last site completes its block; ragged slab
+]
+
+
+@pytest.mark.parametrize("case", CASES,
+                         ids=lambda c: f"{'P' if c[0] == 0 else 'S'}-T{c[1]}-N{c[2]}-d{c[3]}-r{c[4]}-c{c[5]}")
+def test_bf16_copies_model_pass_matches_oracle(dev, case):
+    mode, T, N, d, r, c = case
+    p = make_host_problem(mode, T, N, d, r, dtype="bf16", seed=T * 31 + c)
+    rng = np.random.default_rng(T + c)
+    Qh = (rng.standard_normal((T, r)) * 2.0 / np.sqrt(r)).astype(np.float32)
+    O, KO, Q = to_dev(p.V, dev), to_dev(p.K, dev), torch.from_numpy(Qh).to(dev)
+    sites = list(range(1, T + 1))
+    out, BC, KBC = drive_pass(dev, O, KO, Q, c, mode, sites)
+    for t in sites:
+        ref = oracle.block_route_fwd(p.V, p.K, Qh[t - 1], t, c, mode, r=r, completed_bf16=True)
+        check_bf16_key_grad(f"H at site {t}", to_host(out[t]), ref)
+    Bx, KBx = expected_copies(p.V, p.K, T, c, mode, r)
+    nfin = Bx.shape[0]  # slots completed by the end of the pass
+    got = bf16_tensor_to_bits(BC[:nfin])
+    assert np.array_equal(got, Bx), "bf16 copies differ from the rounded member-order sums"
+    if mode == PROJECTED:
+        assert np.array_equal(bf16_tensor_to_bits(KBC[:nfin]), KBx)
+
+
+def test_bf16_copies_differ_from_fp32_slots_only_by_rounding(dev):
+    """The same pass with fp32 completed slots: the two outputs differ by
+    less than the bf16 bar of either against its own oracle."""
+    mode, T, N, d, r, c = SLICED, 13, 40, 512, 32, 3
+    p = make_host_problem(mode, T, N, d, r, dtype="bf16", seed=4)
+    Qh = (np.random.default_rng(2).standard_normal((T, r)) / np.sqrt(r)).astype(np.float32)
+    O, Q = to_dev(p.V, dev), torch.from_numpy(Qh).to(dev)
+    out16, _, _ = drive_pass(dev, O, None, Q, c, mode, [T])
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    for t in range(1, T + 1):
+        n_src, start, _ = site_args(t, c)
+        H32 = lr.block_route_fwd(B, None, O[t - 1], None, Q[t - 1], n_src, start, mode)
+    torch.cuda.synchronize()
+    a, b = to_host(out16[T]), to_host(H32)
+    ref16 = oracle.block_route_fwd(p.V, None, Qh[T - 1], T, c, mode, r=r, completed_bf16=True)
+    ref32 = oracle.block_route_fwd(p.V, None, Qh[T - 1], T, c, mode, r=r)
+    check_bf16_key_grad("bf16 copies", a, ref16)
+    check_bf16_key_grad("fp32 slots", b, ref32)
+    assert np.abs(a - b).max() < 0.1 and np.abs(a - b).max() > 0.0
+
+
+@pytest.mark.parametrize("mode,r", [(SLICED, 64), (PROJECTED, 32)], ids=["S-r64", "P-r32"])
+def test_bf16_copies_full_size(dev, mode, r):
+    """The paper's 8-block pass (d = 1024, 49 sites, blocks of 6, N = 16384)
+    with bf16 completed summaries: sampled tokens at sites around block
+    boundaries against the oracle with the same reading."""
+    T, N, d, c = 49, 16384, 1024, 6
+    g = torch.Generator(device=dev).manual_seed(3)
+    O = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+    for i in range(T):
+        O[i].copy_(torch.randn((N, d), generator=g, device=dev))
+    KO = (torch.randn((T, N, r), generator=g, device=dev).to(torch.bfloat16)
+          if mode == PROJECTED else None)
+    Q = torch.randn((T, r), generator=g, device=dev) / r ** 0.5
+    sites = [1, 2, 7, 8, 13, 25, 49]
+    out, BC, _ = drive_pass(dev, O, KO, Q, c, mode, sites)
+    idx = np.sort(np.concatenate([[0, 1, N - 1], np.random.default_rng(5).choice(N, 29, replace=False)]))
+    ti = torch.from_numpy(idx).to(dev)
+    Os = bf16_tensor_to_bits(O.index_select(1, ti))
+    Ks = bf16_tensor_to_bits(KO.index_select(1, ti)) if KO is not None else None
+    for t in sites:
+        ref = oracle.block_route_fwd(Os, Ks, Q[t - 1].cpu().numpy(), t, c, mode, r=r,
+                                     completed_bf16=True)
+        check_bf16_key_grad(f"H at site {t}", to_host(out[t].index_select(0, ti)), ref)
+    Bx, _ = expected_copies(Os, Ks, T, c, mode, r)
+    assert np.array_equal(bf16_tensor_to_bits(BC[:Bx.shape[0]].index_select(1, ti)), Bx)
