@@ -258,6 +258,8 @@ MANY_TOKEN_CASES = [
     (PROJECTED, "bf16", 3, 2053, 100, 4),      # scalar path
     (SLICED, "bf16", 3, 2050, 8200, 16),       # column blocks
     (PROJECTED, "f32", 70, 2100, 64, 8),       # S above one wave
+    (SLICED, "bf16", 5, 2048, 128, 8),         # the last token count split over waves
+    (FULL, "f32", 4, 1024, 64, 64),            # the same for full-rank keys
 ]
 
 
