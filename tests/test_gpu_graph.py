@@ -101,3 +101,70 @@ def test_captured_block_model_pass_replays(dev):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(ref.view(torch.int16), Hs.view(torch.int16)), f"replay {k}"
+
+
+def _replays_match(pass_, outs):
+    """Eager result, then a captured graph replayed three times with eager
+    work (zeroing the outputs) and host synchronisations between replays."""
+    pass_()
+    torch.cuda.synchronize()
+    refs = [o.clone() for o in outs]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pass_()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pass_()
+    for k in range(3):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for ref, o in zip(refs, outs):
+            assert torch.equal(ref.view(torch.uint8), o.view(torch.uint8)), f"replay {k}"
+
+
+def test_captured_block_pass_with_bf16_copies_replays(dev):
+    """A 13-site projected-key block pass with bf16 completed summaries in one
+    graph: every site's h and every copy written match the eager pass."""
+    T, N, d, r, c = 13, 40, 256, 16, 3
+    p = make_host_problem(PROJECTED, T, N, d, r, dtype="bf16", seed=9)
+    O, KO = to_dev(p.V, dev), to_dev(p.K, dev)
+    Q = torch.randn((T, r), generator=torch.Generator(device=dev).manual_seed(2), device=dev)
+    nslots = (T - 2) // c + 2
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    KB = torch.zeros((nslots, N, r), dtype=torch.float32, device=dev)
+    BC = torch.zeros((nslots, N, d), dtype=torch.bfloat16, device=dev)
+    KBC = torch.zeros((nslots, N, r), dtype=torch.bfloat16, device=dev)
+    Hs = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+
+    def pass_():
+        for t in range(1, T + 1):
+            n_src, start = (1, True) if t == 1 else ((t - 2) // c + 2, (t - 2) % c == 0)
+            finish = t == 1 or (t - 1) % c == 0
+            lr.block_route_fwd_bf16c(B, KB, BC, KBC, O[t - 1], KO[t - 1], Q[t - 1], n_src, start,
+                                     finish, PROJECTED, out=Hs[t - 1])
+
+    _replays_match(pass_, [Hs, BC, KBC])
+
+
+def test_captured_split_sources_replays(dev):
+    """Per-chunk states and their merge (a 49-source site at N = 64) in one
+    graph, replays against the eager result."""
+    S, N, d, r, chunk = 49, 64, 1024, 16, 7
+    p = make_host_problem(PROJECTED, S, N, d, r, dtype="bf16", seed=11)
+    V, K, q = to_dev(p.V, dev), to_dev(p.K, dev), to_dev(p.q, dev)
+    P = -(-S // chunk)
+    st = (torch.empty((P, N), dtype=torch.float32, device=dev),
+          torch.empty((P, N), dtype=torch.float32, device=dev),
+          torch.empty((P, N, d), dtype=torch.float32, device=dev))
+    H = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+
+    def pass_():
+        lr.route_state_fwd(V, K, q, PROJECTED, chunk, out=st)
+        lr.route_merge_fwd(*st, out=H)
+
+    _replays_match(pass_, [H, *st])
