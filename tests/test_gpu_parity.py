@@ -493,3 +493,29 @@ def test_model_shape_backward_site49(dev, model_stack, mode, r):
         _, _, part = oracle.route_bwd(Vh, Kh, qn, dHh, mode, r=r, n0=n0, n1=n0 + 2048)
         dq_ref += part
     check_dq("dq", to_host(dq), dq_ref)
+
+
+def test_rank_one_key_gradient_within_its_term_bound(dev):
+    """With r = 1 a normalised key is k / sqrt(k^2 + eps), about +-1, so the
+    key gradient (ds / rho)(q - kbar s / r) = (ds / rho) q (1 - kbar^2) is
+    O(eps): the two terms cancel about 10^4-fold and no normwise bar fits.
+    dK is held to the error bound of the formula's terms instead: fp32
+    arithmetic on terms of size |ds / rho| (|q| + |kbar s / r|)."""
+    S, N, d, r = 4, 5, 72, 1
+    p = make_host_problem(PROJECTED, S, N, d, r, dtype="f32", seed=404, with_dH=True)
+    V, K, q, dH = (to_dev(x, dev) for x in (p.V, p.K, p.q, p.dH))
+    _, dK, _ = lr.route_bwd(V, K, q, dH, PROJECTED)
+    torch.cuda.synchronize()
+    _, dK_ref, _ = oracle.route_bwd(p.V, p.K, p.q, p.dH, PROJECTED)
+    Kw, Vw, qw = p.K.astype(np.float64), p.V.astype(np.float64), p.q.astype(np.float64)
+    rho = np.sqrt((Kw ** 2).mean(axis=2) + 1e-6)
+    kb = Kw / rho[..., None]
+    s = (kb * qw).sum(axis=2)
+    a = np.exp(s - s.max(axis=0))
+    a /= a.sum(axis=0)
+    g = np.einsum("snd,nd->sn", Vw, p.dH.astype(np.float64))
+    ds = a * (g - (a * g).sum(axis=0))
+    terms = np.abs(ds / rho)[..., None] * (np.abs(qw) + np.abs(kb * s[..., None] / r))
+    assert terms.max() / np.abs(dK_ref).max() > 100  # the cancelling case it is meant to be
+    err = np.abs(to_host(dK) - dK_ref)
+    assert (err <= 32 * 2.0 ** -24 * terms).all(), (err / terms).max()
