@@ -1,0 +1,94 @@
+"""Seeded random shapes inside the documented limits for the calls beyond the
+single-site forward / backward (which test_gpu_parity.py covers the same
+way): every read site in one call (forward and backward), the split-sources
+states and merge, and the block forward with bf16 completed summaries; each
+against the fp64 oracle through the case functions of their own test files.
+
+Shapes keep r >= 2 and N >= 3: with rank-1 keys, or with one or two tokens,
+a sum can cancel by orders of magnitude, which the normwise bars do not
+cover (test_gpu_parity.py and test_gpu_all_sites_bwd.py hold such cases to
+the error bound of their terms)."""
+import numpy as np
+import pytest
+
+import test_gpu_all_sites as all_fwd
+import test_gpu_all_sites_bwd as all_bwd
+import test_gpu_block_bf16c as bf16c
+import test_gpu_split_sources as split
+from paper_2607_09694_amd.inputs import FULL, PROJECTED, SLICED
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+dev = all_fwd.dev  # the module fixture
+
+WIDTHS = [8, 16, 24, 64, 72, 128, 136, 200, 256, 264, 512, 520, 1000, 1024, 1032, 2048]
+
+
+def _rank(rng, mode, d, cap):
+    return int(rng.integers(2, min(d, cap) + 1)) if mode == SLICED else int(rng.integers(2, cap + 1))
+
+
+def _all_sites_cases(n, seed, storages):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        mode = int(rng.integers(0, 2))
+        dtype = storages[int(rng.integers(0, len(storages)))]
+        S = int(rng.integers(1, 65))
+        first = int(rng.integers(1, S + 1))
+        T = min(int(rng.integers(1, S - first + 2)), 64)
+        d = int(rng.choice([w for w in WIDTHS if w % 8 == 0]))
+        r = _rank(rng, mode, d, 64)
+        N = int(rng.integers(3, 120))
+        out.append((mode, dtype, S, T, first, N, d, r))
+    return out
+
+
+def _split_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        mode = int(rng.integers(0, 3))
+        dtype = ["f32", "bf16"][int(rng.integers(0, 2))]
+        d = int(rng.choice(WIDTHS))
+        S = int(rng.integers(1, 130))
+        chunk = int(rng.integers(1, S + 3))
+        N = int(rng.integers(3, 80))
+        r = d if mode == FULL else _rank(rng, mode, d, 128 if mode == SLICED else 64)
+        out.append((mode, dtype, S, chunk, N, d, r))
+    return out
+
+
+def _bf16c_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        mode = int(rng.integers(0, 2))
+        d = int(rng.choice([w for w in WIDTHS if w % 4 == 0]))
+        T = int(rng.integers(2, 20))
+        c = int(rng.integers(1, 8))
+        N = int(rng.integers(3, 60))
+        r = _rank(rng, mode, d, 32 if mode == PROJECTED else 64)
+        out.append((mode, T, N, d, r, c))
+    return out
+
+
+@pytest.mark.parametrize("case", _all_sites_cases(16, 71, ["f32", "bf16"]), ids=str)
+def test_random_all_sites_forward(dev, case):
+    all_fwd.test_all_sites_match_oracle(dev, case)
+
+
+@pytest.mark.parametrize("case", [c[:1] + c[2:] for c in _all_sites_cases(16, 72, ["bf16"])],
+                         ids=str)
+def test_random_all_sites_backward(dev, case):
+    all_bwd.test_all_sites_backward_matches_oracle(dev, case)
+
+
+@pytest.mark.parametrize("case", _split_cases(16, 73), ids=str)
+def test_random_split_sources(dev, case):
+    split.test_states_and_merge_match_oracle(dev, case)
+
+
+@pytest.mark.parametrize("case", _bf16c_cases(12, 74), ids=str)
+def test_random_block_bf16_copies(dev, case):
+    bf16c.test_bf16_copies_model_pass_matches_oracle(dev, case)
