@@ -157,19 +157,22 @@ __device__ inline void depth_softmax(const float *s, float *alpha, int S, int la
 // ---------------------------------------------------------------------------
 
 // vbase points at column (col0 + lane*VEC) of source 0's row of the token;
-// chunk c of source i is at vbase + i*plane + c*64*VEC.
-template <typename T, int VEC, int NCH, bool FULLCOLS>
+// chunk c of source i is at vbase + i*plane + c*64*VEC.  acc starts at zero,
+// or (CONTINUE) goes on from the sum it holds, in source order.
+template <typename T, int VEC, int NCH, bool FULLCOLS, bool CONTINUE = false>
 __device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t plane, int S,
                                          const float *alpha, const bool (&ok)[NCH],
                                          float (&acc)[NCH][VEC])
 {
     typedef typename Raw<T, VEC>::type raw_t;
     constexpr int U = MixUnroll<NCH>::value;
+    if constexpr (!CONTINUE) {
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+        for (int c = 0; c < NCH; ++c)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e)
-            acc[c][e] = 0.0f;
+            for (int e = 0; e < VEC; ++e)
+                acc[c][e] = 0.0f;
+    }
     int i = 0;
     for (; i + U <= S; i += U) {
         raw_t raw[U][NCH];

@@ -144,6 +144,20 @@ route_fwd_lr_wg(const T *__restrict__ V, const T *__restrict__ keys, const float
     float acc[NCH][VEC];
     float m = -INFINITY, l = 0.0f;
     if (sc > 0) {  // wave-uniform
+        // The first rows of the range do not depend on the scores: their
+        // loads go out before the key loads, so the two wait together.
+        typedef typename Raw<T, VEC>::type raw_t;
+        constexpr int PRE = MixUnroll<NCH>::value;
+        const T *vb = V + (size_t)i0 * plane + (size_t)n * d + col;
+        raw_t pre[PRE][NCH];
+#pragma unroll
+        for (int u = 0; u < PRE; ++u)
+            if (u < sc)
+#pragma unroll
+                for (int c = 0; c < NCH; ++c)
+                    if (FULLCOLS || ok[c])
+                        pre[u][c] = load_stream<T, VEC, kNtLoad>(vb + (size_t)u * plane +
+                                                                 c * kWaveSize * VEC);
         lr_scores<T, VEC>(keys + (size_t)i0 * N * krow, q, sc, N, r, krow, koff, eps, n, lane, w,
                           nullptr);
         for (int i = lane; i < sc; i += kWaveSize)
@@ -156,8 +170,31 @@ route_fwd_lr_wg(const T *__restrict__ V, const T *__restrict__ keys, const float
         }
         l = wave_sum(l);
         wave_lds_sync();
-        mix_rows<T, VEC, NCH, FULLCOLS>(V + (size_t)i0 * plane + (size_t)n * d + col, plane, sc,
-                                        w, ok, acc);
+        // In source order: the prefetched rows, then the rest of the range.
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[c][e] = 0.0f;
+#pragma unroll
+        for (int u = 0; u < PRE; ++u) {
+            if (u < sc) {
+                const float a = w[u];
+#pragma unroll
+                for (int c = 0; c < NCH; ++c) {
+                    if (FULLCOLS || ok[c]) {
+                        float x[VEC];
+                        widen(pre[u][c], x);
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            acc[c][e] = fmaf(a, x[e], acc[c][e]);
+                    }
+                }
+            }
+        }
+        if (sc > PRE)
+            mix_rows<T, VEC, NCH, FULLCOLS, true>(vb + (size_t)PRE * plane, plane, sc - PRE,
+                                                  w + PRE, ok, acc);
     } else {
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
