@@ -290,12 +290,16 @@ int lr_attnres_block_gather_bwd(const float *B, const float *KB, int64_t slot, c
  *   M [P][N] = max score, L [P][N] = sum exp(s - M),
  *   ACC [P][N][d] = sum exp(s - M) o_i      (all fp32, overwritten),
  * with the scores of lr_attnres_route_fwd (same V, K, q, mode, dtype, eps).
- * ACC / L is the routing over that chunk alone.  Each chunk is its own set of
- * workgroups, so a small token count (decoding) still fills the device, and
- * the states are what a pass whose sources are spread over several devices
- * would exchange.  lr_attnres_route_merge_fwd turns them into h.
+ * ACC / L is the routing over that chunk alone.  The states are what a pass
+ * whose sources are spread over several devices would exchange, and they
+ * route a stack deeper than one call takes (S above 1024);
+ * lr_attnres_route_merge_fwd turns them into h.  (For few tokens on one
+ * device, lr_attnres_route_fwd already splits each token's sources over a
+ * workgroup and merges in on-chip memory, which is faster than states plus
+ * a merge.)  M and L need 4-byte alignment, ACC 16 bytes; V, K and q as for
+ * lr_attnres_route_fwd.
  * EINVAL: chunk < 1, or as lr_attnres_route_fwd.  EUNSUPPORTED: chunk above
- * 1024 (P any, up to 65535), or the row limits of lr_attnres_route_fwd.
+ * 1024, more than 65535 chunks, or the row limits of lr_attnres_route_fwd.
  */
 int lr_attnres_route_state_fwd(const void *V, const void *K, const float *q, float *M, float *L,
                                float *ACC, int64_t S, int64_t N, int64_t d, int64_t r,
@@ -306,8 +310,10 @@ int lr_attnres_route_state_fwd(const void *V, const void *K, const float *q, flo
  * m = max_p M_p: the routing over the union of the P chunks whose states
  * (layout of lr_attnres_route_state_fwd) are given; with the states of all
  * chunks of one site it equals lr_attnres_route_fwd's h up to rounding.
+ * M and L need 4-byte alignment, ACC and H 16 bytes.
  * EINVAL: P < 1, N < 0, d < 1, unknown dtype, misaligned or overlapping
- * buffers.  EUNSUPPORTED: P above 1024.
+ * buffers.  EUNSUPPORTED: P above 1024, or a row wider than
+ * lr_attnres_route_fwd takes.
  */
 int lr_attnres_route_merge_fwd(const float *M, const float *L, const float *ACC, void *H,
                                int64_t P, int64_t N, int64_t d, int dtype, void *stream);
