@@ -312,8 +312,8 @@ int lr_attnres_route_state_fwd(const void *V, const void *K, const float *q, flo
  * chunks of one site it equals lr_attnres_route_fwd's h up to rounding.
  * M and L need 4-byte alignment, ACC and H 16 bytes.
  * EINVAL: P < 1, N < 0, d < 1, unknown dtype, misaligned or overlapping
- * buffers.  EUNSUPPORTED: P above 1024, or a row wider than
- * lr_attnres_route_fwd takes.
+ * buffers.  EUNSUPPORTED: P above 1024 or N above 2^30 (any row width:
+ * wide rows are split into column blocks).
  */
 int lr_attnres_route_merge_fwd(const float *M, const float *L, const float *ACC, void *H,
                                int64_t P, int64_t N, int64_t d, int dtype, void *stream);
