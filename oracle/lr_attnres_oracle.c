@@ -365,8 +365,8 @@ static long long block_slot(long long i, long long c) { return i == 0 ? 0 : (i -
 /* Completed block summaries in the model's bf16 (a storage reading, not the
  * paper's): at site t every slot but the last (the one that receives
  * o_{t-1}) is complete, and its summary is the fp32 sum of its members in
- * their order, rounded once to bf16 (nearest even); a projected key the
- * same.  Writes those slots' rounded values (as doubles) into B [S][nt][d]
+ * their order (from the first member on), rounded once to bf16 (nearest
+ * even); a projected key the same.  Writes those slots' rounded values (as doubles) into B [S][nt][d]
  * and KB [S][nt][r] (projected) for tokens [n0, n1); the last slot's rows
  * are left as they are. */
 static void round_completed_slots(const void *O, const void *KO, double *B, double *KB,
@@ -378,17 +378,20 @@ static void round_completed_slots(const void *O, const void *KO, double *B, doub
     for (long long slot = 0; slot + 1 < S; ++slot) {
         const long long first = slot == 0 ? 0 : (slot - 1) * c + 1;
         const long long last = slot == 0 ? 0 : slot * c;  /* inclusive; < t - 1 here */
+        /* The sum starts from the first member (a one-member summary is
+         * that member, the sign of a zero included), then adds the others
+         * in order. */
         for (long long n = n0; n < n1; ++n) {
             for (long long j = 0; j < d; ++j) {
-                float acc = 0.0f;
-                for (long long i = first; i <= last; ++i)
+                float acc = (float)widen(O, store, (first * N + n) * d + j);
+                for (long long i = first + 1; i <= last; ++i)
                     acc += (float)widen(O, store, (i * N + n) * d + j);
                 B[(slot * nt + (n - n0)) * d + j] = round_to_bf16(acc);
             }
             if (KB)
                 for (long long j = 0; j < r; ++j) {
-                    float acc = 0.0f;
-                    for (long long i = first; i <= last; ++i)
+                    float acc = (float)widen(KO, store, (first * N + n) * r + j);
+                    for (long long i = first + 1; i <= last; ++i)
                         acc += (float)widen(KO, store, (i * N + n) * r + j);
                     KB[(slot * nt + (n - n0)) * r + j] = round_to_bf16(acc);
                 }

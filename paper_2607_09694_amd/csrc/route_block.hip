@@ -117,7 +117,8 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, TC *BC, TC *KBC,
         float *krow = KB + ((size_t)j * N + n) * r;
         const TO *knew = k_new + (size_t)n * r;
         for (int jj = lane; jj < r; jj += kWaveSize) {
-            const float k = (start ? 0.0f : krow[jj]) + load_elem(knew + jj);
+            const float kn = load_elem(knew + jj);
+            const float k = start ? kn : krow[jj] + kn;  // from the first member, as the rows
             krow[jj] = k;
             if constexpr (!std::is_same<TC, float>::value)
                 if (finish)
@@ -349,7 +350,8 @@ route_block_merge(float *__restrict__ B, float *__restrict__ KB, const TO *__res
         float *krow = KB + ((size_t)j * N + n) * r;
         const TO *knew = k_new + (size_t)n * r;
         for (int jj = lane; jj < r; jj += kWaveSize) {
-            const float k = (start ? 0.0f : krow[jj]) + load_elem(knew + jj);
+            const float kn = load_elem(knew + jj);
+            const float k = start ? kn : krow[jj] + kn;  // from the first member, as the rows
             krow[jj] = k;
             ss = fmaf(k, k, ss);
             dot = fmaf(q[jj], k, dot);

@@ -93,6 +93,7 @@ CASES = [
     (SLICED, 11, 33, 256, 10, 2),    # sliced key offset 246: scalar key loads
     (PROJECTED, 17, 40, 1024, 32, 4),
     (SLICED, 16, 19, 520, 64, 5),    # last site completes its block; ragged slab
+    (PROJECTED, 6, 54, 2048, 8, 3),  # the embedding holds a -0.0, which its copy keeps
 ]
 
 

@@ -212,3 +212,15 @@ def test_completed_bf16_token_ranges_compose(orc):
                                                completed_bf16=True)
                            for a, b in ((0, 4), (4, 13))])
     assert np.array_equal(full, part)
+
+
+def test_completed_bf16_sum_starts_from_the_first_member(orc):
+    """A one-member block's summary is the member itself, a negative zero
+    included (0x8000); two members that cancel give +0 (an IEEE sum)."""
+    O = _bits([[[1.0, 2.0]], [[3.0, 5.0]], [[-3.0, 0.5]], [[0.0, 0.0]]])
+    O[0, 0, 0] = 0x8000          # -0.0 in the embedding (slot 0, one member)
+    B, _ = orc.block_completed_bf16(O, None, 4, 2, SLICED, r=1)
+    bits = (B.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert bits[0, 0, 0] == 0x8000                      # -0 kept
+    assert bits[1, 0, 0] == 0x0000                      # 3 + (-3) = +0
+    assert B[1, 0, 1] == 5.5
