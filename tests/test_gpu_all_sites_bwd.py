@@ -243,3 +243,40 @@ def test_cancelling_query_gradient_within_its_term_bound(dev):
     kappa = abs_terms.max() / np.abs(ref[2]).max()
     assert kappa > 100  # the case is the cancelling one it is meant to be
     check_sum_by_terms("dQ", dQ, ref[2], abs_terms, N * S, 2.0 ** -16)
+
+
+def test_stack_beyond_2_31_elements(dev):
+    """A stack of more than 2^31 elements (S = 64, N = 33000, d = 1024), so
+    that plane offsets need 64 bits, through the all-sites forward and
+    backward; sampled tokens, the last ones included, against the oracle."""
+    mode, r = PROJECTED, 16
+    S, T, first, N, d = 64, 48, 17, 33000, 1024
+    assert S * N * d > 2 ** 31
+    g = torch.Generator(device=dev)
+    g.manual_seed(99)
+    V = torch.empty((S, N, d), dtype=torch.bfloat16, device=dev)
+    for i in range(S):
+        V[i].copy_(torch.randn((N, d), generator=g, device=dev))
+    K = torch.randn((S, N, r), generator=g, device=dev).to(torch.bfloat16)
+    Q = torch.randn((T, r), generator=g, device=dev) * (2.0 / r ** 0.5)
+    dH = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+    for j in range(T):
+        dH[j].copy_(torch.randn((N, d), generator=g, device=dev))
+    H, ne = lr.route_all_fwd(V, K, Q, mode, first)
+    dV, dK, dQ = lr.route_all_bwd(V, K, Q, dH, mode, first)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([[0, N // 2, N - 2, N - 1],
+                                     np.random.default_rng(3).integers(0, N, 8)]))
+    idx = torch.as_tensor(toks, device=dev)
+    Vs = bf16_tensor_to_bits(V[:, idx].contiguous())
+    Ks = bf16_tensor_to_bits(K[:, idx].contiguous())
+    dHs = bf16_tensor_to_bits(dH[:, idx].contiguous())
+    Qh = Q.cpu().numpy().astype(np.float64)
+    rH, rne = oracle.route_all_fwd(Vs, Ks, Qh, mode, first, r=r)
+    check_bf16_grown("H", to_host(H[:, idx].contiguous()), rH)
+    got_ne = ne[:, idx].contiguous().cpu().numpy()
+    assert np.abs(got_ne - rne).max() <= 1e-5 * np.abs(rne).max()
+    rV, rK, rQ = oracle.route_all_bwd(Vs, Ks, Qh, dHs, mode, first, r=r)
+    # dQ sums over all N tokens, which the sampled oracle does not see.
+    _check("", mode, (dV[:, idx].contiguous(), dK[:, idx].contiguous(),
+                      torch.as_tensor(rQ, device=dev)), (rV, rK, rQ))
