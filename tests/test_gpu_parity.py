@@ -519,3 +519,29 @@ def test_rank_one_key_gradient_within_its_term_bound(dev):
     assert terms.max() / np.abs(dK_ref).max() > 100  # the cancelling case it is meant to be
     err = np.abs(to_host(dK) - dK_ref)
     assert (err <= 32 * 2.0 ** -24 * terms).all(), (err / terms).max()
+
+
+@pytest.mark.parametrize("mode,r", [(PROJECTED, 32), (SLICED, 64)], ids=["P-r32", "S-r64"])
+def test_single_site_beyond_2_31_elements(dev, mode, r):
+    """A value stack of more than 2^31 elements (S = 70, N = 16384, d = 2048),
+    so that element offsets need 64 bits: H, dV (and dK) on sampled tokens,
+    the first and last four included."""
+    S, N, d = 70, 16384, 2048
+    assert S * N * d > 2 ** 31
+    g = make_device_problem(mode, S, N, d, r, dev, seed=3, with_dH=True)
+    V, K, q, dH = g["V"], g["K"], g["q"][0].contiguous(), g["dH"]
+    H = lr.route_fwd(V, K, q, mode)
+    dV, dK, _ = lr.route_bwd(V, K, q, dH, mode)
+    torch.cuda.synchronize()
+    idx = sample_tokens(N, seed=9)
+    ti = torch.from_numpy(idx).to(dev)
+    Vs, dHs = sampled(V, idx, 1), sampled(dH, idx, 0)
+    Ks = sampled(K, idx, 1) if K is not None else None
+    qn = q.cpu().numpy()
+    check_bf16_value("H", to_host(H.index_select(0, ti)), oracle.route_fwd(Vs, Ks, qn, mode, r=r))
+    dV_ref, dK_ref, _ = oracle.route_bwd(Vs, Ks, qn, dHs, mode, r=r)
+    check_value_grad(mode, "bf16", to_host(dV.index_select(1, ti)), dV_ref, r)
+    if mode == PROJECTED:
+        check_bf16_key_grad("dK", to_host(dK.index_select(1, ti)), dK_ref)
+    del g, V, K, dH, H, dV, dK
+    torch.cuda.empty_cache()
