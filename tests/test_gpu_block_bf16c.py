@@ -165,3 +165,37 @@ def test_bf16_copies_full_size(dev, mode, r):
         check_bf16_key_grad(f"H at site {t}", to_host(out[t].index_select(0, ti)), ref)
     Bx, _ = expected_copies(Os, Ks, T, c, mode, r)
     assert np.array_equal(bf16_tensor_to_bits(BC[:Bx.shape[0]].index_select(1, ti)), Bx)
+
+
+def test_block_slots_beyond_2_31_elements(dev):
+    """A 13-site pass (blocks of 3, 5 slots) over N = 220000 tokens at
+    d = 2048: the fp32 slot stack and the bf16 copies each hold more than
+    2^31 values (64-bit slot offsets).  fp32 slots and bf16 copies both;
+    sampled tokens, the last included, at the last site."""
+    mode, T, N, d, r, c = SLICED, 13, 220000, 2048, 64, 3
+    nslots = (T - 2) // c + 2
+    assert nslots * N * d > 2 ** 31
+    g = torch.Generator(device=dev).manual_seed(21)
+    O = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+    for i in range(T):
+        O[i].copy_(torch.randn((N, d), generator=g, device=dev))
+    Q = torch.randn((T, r), generator=g, device=dev) / r ** 0.5
+    out16, BC, _ = drive_pass(dev, O, None, Q, c, mode, [T])
+    H16 = out16[T]
+    B = torch.zeros((nslots, N, d), dtype=torch.float32, device=dev)
+    for t in range(1, T + 1):
+        n_src, start, _ = site_args(t, c)
+        H32 = lr.block_route_fwd(B, None, O[t - 1], None, Q[t - 1], n_src, start, mode)
+    torch.cuda.synchronize()
+    idx = np.sort(np.concatenate([[0, N - 2, N - 1], np.random.default_rng(6).choice(N, 13, replace=False)]))
+    ti = torch.from_numpy(idx).to(dev)
+    Os = bf16_tensor_to_bits(O.index_select(1, ti))
+    qh = Q[T - 1].cpu().numpy()
+    check_bf16_key_grad("H bf16 copies", to_host(H16.index_select(0, ti)),
+                        oracle.block_route_fwd(Os, None, qh, T, c, mode, r=r, completed_bf16=True))
+    check_bf16_key_grad("H fp32 slots", to_host(H32.index_select(0, ti)),
+                        oracle.block_route_fwd(Os, None, qh, T, c, mode, r=r))
+    Bx, _ = expected_copies(Os, None, T, c, mode, r)
+    assert np.array_equal(bf16_tensor_to_bits(BC[:Bx.shape[0]].index_select(1, ti)), Bx)
+    del O, B, BC, out16
+    torch.cuda.empty_cache()

@@ -158,3 +158,29 @@ def test_deepest_site_full_size(dev, mode, r, chunk):
     check_f32("M[0]", M[0, idx].cpu().numpy(), Mr)
     check_f32("L[0]", L[0, idx].cpu().numpy(), Lr)
     check_f32("ACC[0]", ACC[0, idx].cpu().numpy(), Ar)
+
+
+def test_states_beyond_2_31_elements(dev):
+    """Chunks of one source over a 70-source stack at N = 16384, d = 2048:
+    ACC holds more than 2^31 fp32 values (64-bit state offsets).  Sampled
+    tokens, the last included, against the oracle."""
+    mode, S, N, d, r, chunk = PROJECTED, 70, 16384, 2048, 16, 1
+    assert S * N * d > 2 ** 31
+    prob = make_device_problem(mode, S, N, d, r, dev, seed=12)
+    q = prob["q"][0].contiguous()
+    M, L, ACC = lr.route_state_fwd(prob["V"], prob["K"], q, mode, chunk)
+    H = lr.route_merge_fwd(M, L, ACC)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([[0, N - 2, N - 1], np.random.default_rng(4).integers(0, N, 13)]))
+    idx = torch.as_tensor(toks, device=dev)
+    Vb = bf16_tensor_to_bits(prob["V"][:, idx].contiguous())
+    Kb = bf16_tensor_to_bits(prob["K"][:, idx].contiguous())
+    qh = q.cpu().numpy()
+    check_bf16_value("H", to_host(H[idx].contiguous()), oracle.route_fwd(Vb, Kb, qh, mode, r=r))
+    last = S - 1  # the last chunk's state lies past 2^31 values
+    Mr, Lr, Ar = oracle.route_state(Vb[last:], Kb[last:], qh, mode, r=r)
+    check_f32("M[last]", M[last, idx].cpu().numpy(), Mr)
+    check_f32("L[last]", L[last, idx].cpu().numpy(), Lr)
+    check_f32("ACC[last]", ACC[last, idx].cpu().numpy(), Ar)
+    del prob, M, L, ACC, H
+    torch.cuda.empty_cache()
