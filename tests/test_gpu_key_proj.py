@@ -142,3 +142,30 @@ def test_rejected_outside_limits(dev):
         lr.key_proj_fwd(A, W, 4)
     with pytest.raises(lr.RoutingError, match="bf16"):
         lr.key_proj_fwd(A.float()[:, :8].contiguous(), W.float()[:, :8].contiguous(), 4)
+
+
+def test_activations_beyond_2_31_elements(dev):
+    """N = 770000 tokens at the SwiGLU width m = 2816: the activation holds
+    more than 2^31 elements (64-bit row offsets); sampled rows, the last
+    included, against the oracle."""
+    N, m, d, r = 770000, 2816, 1024, 16
+    assert N * m > 2 ** 31
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    A = torch.empty((N, m), dtype=torch.bfloat16, device=dev)
+    for n0 in range(0, N, 1 << 17):
+        n1 = min(N, n0 + (1 << 17))
+        A[n0:n1].copy_(torch.randn((n1 - n0, m), generator=g, device=dev))
+    W = (torch.randn((d + r, m), generator=g, device=dev) / m ** 0.5).to(torch.bfloat16)
+    O, K = lr.key_proj_fwd(A, W, d)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, N // 2, N - 257, N - 256, N - 1],
+                                     np.random.default_rng(8).integers(0, N, 11)]))
+    idx = torch.as_tensor(rows, device=dev)
+    Ab = bf16_tensor_to_bits(A[idx].contiguous())
+    Wb = bf16_tensor_to_bits(W)
+    Or, Kr = oracle.key_projection(Ab, Wb, d)
+    check_projection("O", to_host(O[idx].contiguous()), Or, Ab, Wb[:d])
+    check_projection("K", to_host(K[idx].contiguous()), Kr, Ab, Wb[d:])
+    del A, O, K
+    torch.cuda.empty_cache()
