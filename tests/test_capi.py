@@ -587,3 +587,32 @@ def test_block_bf16_copies_rejects(lib, name, kw, msg):
 def test_block_bf16_copies_unsupported(lib):
     assert bfc_call(lib, d=66) == EUNSUPPORTED
     assert bfc_call(lib, d=4096) == EUNSUPPORTED
+
+
+def test_last_error_is_per_thread(lib):
+    """Two threads make different invalid calls, interleaved; each reads back
+    its own message afterwards (the error string is thread-local)."""
+    import threading
+
+    step = threading.Barrier(2)
+    seen = {}
+
+    def first():
+        assert fwd(lib, V=None) == EINVAL       # "V is NULL"
+        step.wait()                             # the other thread fails now
+        step.wait()
+        seen["first"] = err(lib)
+
+    def second():
+        step.wait()
+        assert fwd(lib, N=-1) == EINVAL         # "N >= 0"
+        step.wait()
+        seen["second"] = err(lib)
+
+    threads = [threading.Thread(target=first), threading.Thread(target=second)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=30)
+    assert "V is NULL" in seen["first"]
+    assert "N >= 0" in seen["second"]
