@@ -76,6 +76,8 @@ def _load():
     lib.orc_route_all_bwd.restype = ctypes.c_int
     lib.orc_key_projection.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, i, ll, ll]
     lib.orc_key_projection.restype = ctypes.c_int
+    lib.orc_key_projection_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, i]
+    lib.orc_key_projection_bwd.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -358,3 +360,33 @@ def key_projection(A, W, d, n0=0, n1=None):
     if rc:
         raise ValueError("oracle: invalid projection")
     return O, K
+
+
+def key_projection_bwd(A, W, dO, dK):
+    """Backward of [o_n; k_n] = [W^O; W^K] a_n (Sec. 3.3, Eq.
+    fused_projection) in fp64, by the chain rule through the linear map:
+    dA = [dO, dK] W and dW = [dO, dK]^T A.
+
+    A [N, m], W [d + r, m], dO [N, d] or None (d = 0), dK [N, r] or None
+    (r = 0), all in one storage.  Returns (dA [N, m], dW [d + r, m])."""
+    A = np.ascontiguousarray(A)
+    W = np.ascontiguousarray(W)
+    if A.dtype not in _STORE or W.dtype != A.dtype or A.ndim != 2 or W.ndim != 2:
+        raise ValueError("oracle: A [N, m] and W [d + r, m] in one supported storage")
+    N, m = A.shape
+    d = 0 if dO is None else dO.shape[1]
+    r = 0 if dK is None else dK.shape[1]
+    if W.shape != (d + r, m):
+        raise ValueError("oracle: W must be [d + r, m]")
+    for g, w in ((dO, d), (dK, r)):
+        if g is not None and (g.dtype != A.dtype or g.shape != (N, w)):
+            raise ValueError("oracle: dO [N, d] and dK [N, r] in A's storage")
+    dO = None if dO is None else np.ascontiguousarray(dO)
+    dK = None if dK is None else np.ascontiguousarray(dK)
+    dA = np.empty((N, m), dtype=np.float64)
+    dW = np.empty((d + r, m), dtype=np.float64)
+    rc = _load().orc_key_projection_bwd(_ptr(A), _ptr(W), _ptr(dO), _ptr(dK), _ptr(dA),
+                                        _ptr(dW), N, m, d, r, _STORE[A.dtype])
+    if rc:
+        raise ValueError("oracle: invalid projection backward")
+    return dA, dW

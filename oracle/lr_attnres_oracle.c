@@ -791,6 +791,50 @@ int orc_key_projection(const void *A, const void *W, double *O, double *Kout, lo
     return 0;
 }
 
+/* Backward of the projected-key producer [o_n; k_n] = [W^O; W^K] a_n
+ * (Sec. 3.3, Eq. fused_projection).  The paper states no backward; for a
+ * loss with upstream gradients g_n = [dO[n]; dK[n]] of the d + r outputs of
+ * token n, the chain rule through the linear map C = A W^T gives
+ *     dA[n][c] = sum_j g_n[j] W[j][c]        (j over the d + r outputs)
+ *     dW[j][c] = sum_n g_n[j] A[n][c]        (n over the N tokens)
+ * written out here as plain sums in fp64.  A [N][m], W [d + r][m], dO [N][d]
+ * (NULL when d = 0), dK [N][r] (NULL when r = 0), all in storage `store`;
+ * dA [N][m] and dW [d + r][m] are fp64.  Returns 0, or 1 on invalid input. */
+int orc_key_projection_bwd(const void *A, const void *W, const void *dO, const void *dK,
+                           double *dA, double *dW, long long N, long long m, long long d,
+                           long long r, int store)
+{
+    if (N < 0 || m < 1 || d < 0 || r < 0 || d + r < 1 || store < 0 || store > 2)
+        return 1;
+    if (A == NULL || W == NULL || dA == NULL || dW == NULL || (d > 0 && dO == NULL) ||
+        (r > 0 && dK == NULL))
+        return 1;
+    const long long nout = d + r;
+#pragma omp parallel for schedule(static)
+    for (long long n = 0; n < N; ++n) {
+        for (long long c = 0; c < m; ++c) {
+            double acc = 0.0;
+            for (long long j = 0; j < nout; ++j) {
+                const double g = j < d ? widen(dO, store, n * d + j) : widen(dK, store, n * r + (j - d));
+                acc += g * widen(W, store, j * m + c);
+            }
+            dA[n * m + c] = acc;
+        }
+    }
+#pragma omp parallel for schedule(static)
+    for (long long j = 0; j < nout; ++j) {
+        for (long long c = 0; c < m; ++c) {
+            double acc = 0.0;
+            for (long long n = 0; n < N; ++n) {
+                const double g = j < d ? widen(dO, store, n * d + j) : widen(dK, store, n * r + (j - d));
+                acc += g * widen(A, store, n * m + c);
+            }
+            dW[j * m + c] = acc;
+        }
+    }
+    return 0;
+}
+
 /* Sets the number of OpenMP threads later parallel regions use (n >= 1);
  * no effect in a build without OpenMP.  Timing harness only. */
 void orc_set_num_threads(int n)
