@@ -497,6 +497,33 @@ int lr_attnres_route_neff(const void *V, const void *K, const float *q, float *n
 int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int64_t N, int64_t m,
                             int64_t d, int64_t r, int dtype, void *stream);
 
+/* Backward of the projected-key producer (Sec. 3.3, Eq. fused_projection).
+ * The paper gives no backward; with upstream gradients G = [dO, dK] of the
+ * d value and r key outputs of each token, the chain rule through
+ * [o_n; k_n] = [W^O; W^K] a_n gives
+ *   dA [N][m]     = dO W^O + dK W^K, storage `dtype`, rounded to nearest
+ *                   even from fp32 sums over the d + r outputs;
+ *   dW [d + r][m] = [dO^T A; dK^T A], fp32 (overwritten, not accumulated),
+ *                   fp32 sums over the N tokens, in a fixed order (bitwise
+ *                   reproducible); N = 0 gives dW = 0.
+ * A [N][m] and W [d + r][m] are the forward's inputs, dO [N][d] (NULL when
+ * d = 0) and dK [N][r] (NULL when r = 0) the upstream gradients, all in
+ * storage `dtype`.  `workspace` is caller-owned device memory of at least
+ * lr_attnres_key_proj_bwd_workspace_bytes(N, m, d, r, dtype) bytes (the
+ * fp32 partials of dW when its token sum is split; may be NULL when that
+ * is 0); its contents on entry do not matter.  Asynchronous on `stream`.
+ * EINVAL: N < 0, m < 1, d or r < 0, d + r < 1, a required pointer NULL or
+ * not 16-byte aligned, dO (dK) non-NULL with d = 0 (r = 0), the workspace
+ * too small, outputs (dA, dW, workspace) overlapping each other or the
+ * inputs.  EUNSUPPORTED: fp32 storage, m, d or r not a multiple of 8, m or
+ * d + r above 2^20, N above 2^30.
+ */
+size_t lr_attnres_key_proj_bwd_workspace_bytes(int64_t N, int64_t m, int64_t d, int64_t r,
+                                               int dtype);
+int lr_attnres_key_proj_bwd(const void *A, const void *W, const void *dO, const void *dK,
+                            void *dA, float *dW, void *workspace, size_t workspace_bytes,
+                            int64_t N, int64_t m, int64_t d, int64_t r, int dtype, void *stream);
+
 /* Text of the last error raised on the calling thread ("" if none); valid
  * until the next call into the library on that thread. */
 const char *lr_attnres_last_error(void);

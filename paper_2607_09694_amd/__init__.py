@@ -97,6 +97,11 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_neff.restype = ctypes.c_int
     lib.lr_attnres_key_proj_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i, vp]
     lib.lr_attnres_key_proj_fwd.restype = ctypes.c_int
+    lib.lr_attnres_key_proj_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i]
+    lib.lr_attnres_key_proj_bwd_workspace_bytes.restype = ctypes.c_size_t
+    lib.lr_attnres_key_proj_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, i64,
+                                            i64, i64, i64, i, vp]
+    lib.lr_attnres_key_proj_bwd.restype = ctypes.c_int
     lib.lr_attnres_last_error.argtypes = []
     lib.lr_attnres_last_error.restype = ctypes.c_char_p
     lib.lr_attnres_abi_version.argtypes = []
@@ -413,6 +418,43 @@ def key_proj_fwd(A, W, d: int, out=None):
                                      _stream(A))
     _check(lib, rc)
     return O, K
+
+
+def key_proj_bwd(A, W, dO, dK, out=None):
+    """Backward of [o_n; k_n] = [W^O; W^K] a_n (Sec. 3.3, Eq.
+    fused_projection): dA = dO W^O + dK W^K and dW = [dO^T A; dK^T A].
+
+    A [N,m] bf16; W [d+r,m] bf16; dO [N,d] or None (d = 0); dK [N,r] or
+    None (r = 0), bf16.  Returns (dA [N,m] bf16, dW [d+r,m] fp32); ``out``
+    may supply (dA, dW).
+    """
+    import torch
+
+    lib = load_library()
+    if A.dim() != 2 or W.dim() != 2 or W.shape[1] != A.shape[1]:
+        raise ValueError("A must be [N, m] and W [d + r, m]")
+    N, m = A.shape
+    d = 0 if dO is None else dO.shape[1]
+    r = 0 if dK is None else dK.shape[1]
+    if W.shape[0] != d + r:
+        raise ValueError("W must have d + r rows")
+    for g, w, name in ((dO, d, "dO"), (dK, r, "dK")):
+        if g is not None and (g.dim() != 2 or g.shape[0] != N or g.shape[1] != w):
+            raise ValueError(f"{name} must be [N, {w}]")
+    if out is not None:
+        dA, dW = out
+    else:
+        dA = torch.empty((N, m), dtype=A.dtype, device=A.device)
+        dW = torch.empty((d + r, m), dtype=torch.float32, device=A.device)
+    code = _dtype_code(A)
+    nbytes = lib.lr_attnres_key_proj_bwd_workspace_bytes(N, m, d, r, code)
+    ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=A.device)
+    rc = lib.lr_attnres_key_proj_bwd(_dev(A, "A"), _dev(W, "W", A.dtype), _dev(dO, "dO", A.dtype),
+                                     _dev(dK, "dK", A.dtype), _dev(dA, "dA", A.dtype),
+                                     _dev(dW, "dW", torch.float32), _dev(ws, "workspace"), nbytes,
+                                     N, m, d, r, code, _stream(A))
+    _check(lib, rc)
+    return dA, dW
 
 
 def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:

@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblrattnres.so")
 SOURCES = ["route_fwd.hip", "route_bwd.hip", "route_block.hip", "route_all.hip",
-           "route_all_bwd.hip", "key_proj.hip", "route_plan.cpp", "capi.cpp"]
+           "route_all_bwd.hip", "key_proj.hip", "key_proj_bwd.hip", "route_plan.cpp", "capi.cpp"]
 # Benchmark-only helper: streaming copy / read kernels of known traffic.
 PROBE_LIB = os.path.join(PKG, "libhbmprobe.so")
 PROBE_SOURCES = ["hbm_probe.hip"]

@@ -665,6 +665,60 @@ int lr_attnres_key_proj_fwd(const void *A, const void *W, void *O, void *K, int6
     return LRAR_OK;
 }
 
+size_t lr_attnres_key_proj_bwd_workspace_bytes(int64_t N, int64_t m, int64_t d, int64_t r,
+                                               int dtype)
+{
+    if (dtype != LRAR_DTYPE_BF16 || N < 0 || m < 1 || d < 0 || r < 0 || d + r < 1 ||
+        N > ((int64_t)1 << 30) || m > (1 << 20) || d + r > (1 << 20))
+        return 0;
+    return lrar::key_proj_bwd_workspace_bytes(N, m, d, r);
+}
+
+int lr_attnres_key_proj_bwd(const void *A, const void *W, const void *dO, const void *dK,
+                            void *dA, float *dW, void *workspace, size_t workspace_bytes,
+                            int64_t N, int64_t m, int64_t d, int64_t r, int dtype, void *stream)
+{
+    g_last_error.clear();
+    if (dtype != LRAR_DTYPE_F32 && dtype != LRAR_DTYPE_BF16)
+        return fail(LRAR_EINVAL, "unknown storage type " + std::to_string(dtype));
+    if (N < 0 || m < 1 || d < 0 || r < 0 || d + r < 1)
+        return fail(LRAR_EINVAL, "sizes must satisfy N >= 0, m >= 1, d >= 0, r >= 0, d + r >= 1");
+    const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+    int64_t ae, we, oe, ke, wf;
+    if (!mul_ok(N, m, &ae) || !mul_ok(d + r, m, &we) || !mul_ok(N, d, &oe) || !mul_ok(N, r, &ke) ||
+        !mul_ok(we, 4, &wf) || !mul_ok(ae, es, &ae) || !mul_ok(we, es, &we) ||
+        !mul_ok(oe, es, &oe) || !mul_ok(ke, es, &ke))
+        return fail(LRAR_EINVAL, "tensor size overflows int64");
+    const bool data = N > 0;
+    int rc;
+    if ((rc = check_ptr(A, "A", 16, data)) || (rc = check_ptr(W, "W", 16, data)) ||
+        (rc = check_ptr(dO, "dO", 16, data && d > 0)) ||
+        (rc = check_ptr(dK, "dK", 16, data && r > 0)) || (rc = check_ptr(dA, "dA", 16, data)) ||
+        (rc = check_ptr(dW, "dW", 16, true)) || (rc = check_ptr(workspace, "workspace", 16, false)))
+        return rc;
+    if (d == 0 && dO)
+        return fail(LRAR_EINVAL, "dO must be NULL when d = 0");
+    if (r == 0 && dK)
+        return fail(LRAR_EINVAL, "dK must be NULL when r = 0");
+    lrar::KeyProjProblem p{A, W, nullptr, nullptr, N, m, d, r, dtype};
+    std::string why;
+    if ((rc = lrar::check_key_proj_bwd_supported(p, &why)))
+        return fail(rc, why);
+    const size_t need = lrar::key_proj_bwd_workspace_bytes(N, m, d, r);
+    if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    const Span outs[] = {span("dA", dA, ae), span("dW", dW, wf),
+                         span("workspace", workspace, (int64_t)need)};
+    const Span ins[] = {span("A", A, ae), span("W", W, we), span("dO", dO, oe),
+                        span("dK", dK, ke)};
+    if ((rc = check_aliasing(outs, 3, ins, 4)))
+        return rc;
+    if ((rc = lrar::launch_key_proj_bwd(p, dO, dK, dA, dW, workspace,
+                                        static_cast<hipStream_t>(stream), &why)))
+        return fail(rc, why);
+    return LRAR_OK;
+}
+
 int lr_attnres_route_neff(const void *V, const void *K, const float *q, float *neff, int64_t S,
                           int64_t N, int64_t d, int64_t r, int mode, int dtype, float eps,
                           void *stream)

@@ -1,0 +1,341 @@
+// Backward of the projected-key producer (Sec. 3.3, Eq. fused_projection).
+// The forward is one linear map C = A W^T with C = [O, K] (the d value
+// columns, then the r key columns).  For upstream gradients G = [dO, dK]
+// ([N][d + r], split at column d like C) the chain rule gives two GEMMs:
+//     dA[N][m]     = G W            (reduction over the d + r outputs)
+//     dW[d + r][m] = G^T A          (reduction over the N tokens)
+// so the key rows of W cost r more reduction steps in dA and r more rows of
+// dW, the same r / d overhead as in the forward.
+//
+// One tile kernel serves both.  A workgroup of 4 waves computes a 128 x 128
+// output tile with v_mfma_f32_16x16x32_bf16 and fp32 accumulators (each
+// wave a 64 x 64 quarter, 16 MFMA tiles).  The reduction runs in stages of
+// 64: every stage is loaded from memory into registers while the previous
+// one feeds the MFMAs, then written to LDS, where both operands sit with the
+// reduction index contiguous in each row (what an MFMA operand read needs).
+// Of the four operand reads only G in dA is stored that way in memory; W in
+// dA and both G and A in dW have the output index contiguous instead.  Those
+// are transposed on the way into LDS: a lane loads 8 consecutive output
+// indices at two consecutive reduction steps and writes 8 words, each the
+// pair of steps for one output index.  LDS rows are padded to 72 elements
+// (36 words), which spreads the 16 rows of one operand read over all banks.
+//
+// dA rounds to bf16 (nearest even).  dW is written in fp32, so that a caller
+// can add it to fp32 master gradients without a second rounding; its token
+// reduction is split over P workgroups per tile when the tile grid alone
+// would not fill the chip, each writing an fp32 partial into the caller's
+// workspace, and a second kernel sums the partials in split order.  Every
+// sum has a fixed order, so the results are bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <string>
+
+#include "route_common.h"
+
+namespace lrar {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+constexpr int kBM = 128;                          // output rows per tile
+constexpr int kBN = 128;                          // output columns per tile
+constexpr int kBK = 64;                           // reduction steps per stage
+constexpr int kLd = kBK + 8;                      // LDS row stride (elements)
+constexpr int kBThreads = 256;                    // 4 waves
+constexpr int kRowChunks = kBM * kBK / 8 / kBThreads;       // 4: k-contiguous loads per lane
+constexpr int kPairs = kBK / 2 * kBN / 8 / kBThreads;       // 2: transposed pair loads per lane
+constexpr int kTargetGroups = 512;                // dW: workgroups wanted per launch
+
+static_assert(kRowChunks == 4 && kPairs == 2, "stage loads split evenly over the lanes");
+
+struct BwdArgs {
+    const uint16_t *A;   // [N][m]
+    const uint16_t *W;   // [d + r][m]
+    const uint16_t *dO;  // [N][d] or NULL (d = 0)
+    const uint16_t *dK;  // [N][r] or NULL (r = 0)
+    uint16_t *dA;        // [N][m]
+    float *dst;          // dW [d + r][m] (one split) or partials [P][d + r][m]
+    int64_t N;
+    int64_t per;         // tokens per split (a multiple of kBK)
+    int m, d, r;
+    int ntn;             // column tiles
+};
+
+__device__ __forceinline__ u32x4_t zero4() { return u32x4_t{0u, 0u, 0u, 0u}; }
+
+// 8 consecutive outputs o .. o+7 of token n from [dO, dK] (o % 8 == 0, and
+// d % 8 == 0, so the 8 never straddle the split).
+__device__ __forceinline__ u32x4_t g_chunk(const BwdArgs &a, int64_t n, int o)
+{
+    if (o < a.d)
+        return *reinterpret_cast<const u32x4_t *>(a.dO + n * a.d + o);
+    return *reinterpret_cast<const u32x4_t *>(a.dK + n * a.r + (o - a.d));
+}
+
+// Word e of the transposed pair: element e of row k (low half) and of row
+// k + 1 (high half).
+__device__ __forceinline__ unsigned pair_word(const u32x4_t &lo, const u32x4_t &hi, int e)
+{
+    const unsigned x = lo[e >> 1], y = hi[e >> 1];
+    return (e & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+}
+
+// DW = false: C = dA tile (rows: tokens, columns: input features, reduction:
+//             the d + r outputs).  X = G rows (k-contiguous), Y = W (transposed).
+// DW = true:  C = dW tile (rows: outputs, columns: input features, reduction:
+//             the tokens of split blockIdx.y).  X = G (transposed), Y = A
+//             (transposed).
+template <bool DW>
+__global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
+{
+    __shared__ __align__(16) uint16_t Xs[kBM * kLd];
+    __shared__ __align__(16) uint16_t Ys[kBN * kLd];
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int nout = a.d + a.r;
+    const int64_t tm = blockIdx.x / a.ntn;
+    const int tn = blockIdx.x % a.ntn;
+    const int64_t row0 = tm * kBM;  // token (dA) or output (dW)
+    const int col0 = tn * kBN;      // input feature
+    const int64_t rows = DW ? nout : a.N;
+    const int64_t kbeg = DW ? (int64_t)blockIdx.y * a.per : 0;
+    const int64_t kend = DW ? min(a.N, kbeg + a.per) : nout;
+    const int nk = (int)((kend - kbeg + kBK - 1) / kBK);
+
+    // Stage registers: X is 4 row chunks (dA) or 2 transposed pairs (dW).
+    u32x4_t xr[4], yr[4];
+
+    // Transposed pair u of this lane: reduction steps 2 kp, 2 kp + 1 of the
+    // stage, output indices 8 mc .. 8 mc + 7 of the tile.
+    const int kp_lane = lane & 15, mc_lane = (lane >> 4) + 4 * wave;
+    auto fetch = [&](int kt) {
+        const int64_t k0 = kbeg + (int64_t)kt * kBK;
+        if (!DW) {
+#pragma unroll
+            for (int u = 0; u < kRowChunks; ++u) {
+                const int q = tid + kBThreads * u, row = q >> 3, kc = q & 7;
+                const int64_t n = row0 + row;
+                const int64_t o = k0 + 8 * kc;
+                xr[u] = (n < a.N && o < kend) ? g_chunk(a, n, (int)o) : zero4();
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kPairs; ++u) {
+            const int kp = kp_lane + 16 * u;
+            const int64_t k = k0 + 2 * kp;
+            if (DW) {
+                const int64_t o = row0 + 8 * mc_lane;
+                const bool ok = o < nout;
+                xr[2 * u] = (ok && k < kend) ? g_chunk(a, k, (int)o) : zero4();
+                xr[2 * u + 1] = (ok && k + 1 < kend) ? g_chunk(a, k + 1, (int)o) : zero4();
+            }
+            const int j = col0 + 8 * mc_lane;
+            const bool ok = j < a.m;
+            const uint16_t *Y = DW ? a.A : a.W;
+            yr[2 * u] = (ok && k < kend)
+                            ? *reinterpret_cast<const u32x4_t *>(Y + k * a.m + j) : zero4();
+            yr[2 * u + 1] = (ok && k + 1 < kend)
+                                ? *reinterpret_cast<const u32x4_t *>(Y + (k + 1) * a.m + j)
+                                : zero4();
+        }
+    };
+    auto put_pairs = [&](uint16_t *S, const u32x4_t *v) {
+#pragma unroll
+        for (int u = 0; u < kPairs; ++u) {
+            const int kp = kp_lane + 16 * u;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                *reinterpret_cast<unsigned *>(S + (8 * mc_lane + e) * kLd + 2 * kp) =
+                    pair_word(v[2 * u], v[2 * u + 1], e);
+        }
+    };
+    auto put = [&]() {
+        if (!DW) {
+#pragma unroll
+            for (int u = 0; u < kRowChunks; ++u) {
+                const int q = tid + kBThreads * u, row = q >> 3, kc = q & 7;
+                *reinterpret_cast<u32x4_t *>(Xs + row * kLd + 8 * kc) = xr[u];
+            }
+        } else {
+            put_pairs(Xs, xr);
+        }
+        put_pairs(Ys, yr);
+    };
+
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // Operand fragments: lane l reads row 16 i + l mod 16 of its quarter,
+    // elements 32 ks + 8 (l / 16) .. +7 of the stage.
+    const int fr = lane & 15, fq = lane >> 4;
+    if (nk > 0) {
+        fetch(0);
+        put();
+        __syncthreads();
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+        if (kt + 1 < nk)
+            fetch(kt + 1);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            bf16x8_t xf[4], yf[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                xf[i] = *reinterpret_cast<const bf16x8_t *>(
+                    Xs + (wm * 64 + 16 * i + fr) * kLd + 32 * ks + 8 * fq);
+                yf[i] = *reinterpret_cast<const bf16x8_t *>(
+                    Ys + (wn * 64 + 16 * i + fr) * kLd + 32 * ks + 8 * fq);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[i], yf[j], acc[i][j],
+                                                                        0, 0, 0);
+        }
+        __syncthreads();
+        if (kt + 1 < nk) {
+            put();
+            __syncthreads();
+        }
+    }
+
+    // Lane holds C[16 i + 4 (l / 16) + e][16 j + l mod 16] of its quarter.
+    float *dst = DW ? a.dst + (int64_t)blockIdx.y * nout * a.m : nullptr;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = col0 + wn * 64 + 16 * j + fr;
+            if (c >= a.m)
+                continue;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t row = row0 + wm * 64 + 16 * i + 4 * fq + e;
+                if (row >= rows)
+                    continue;
+                if (DW)
+                    dst[row * a.m + c] = acc[i][j][e];
+                else
+                    a.dA[row * a.m + c] = to_bf16(acc[i][j][e]);
+            }
+        }
+}
+
+// dW[x] = sum over the P partials in split order (P = 0 writes zeros: the
+// gradient of W over no tokens).
+__global__ __launch_bounds__(kBThreads) void key_proj_bwd_reduce(const float *part, float *dW,
+                                                               int64_t count4, int P)
+{
+    const int64_t stride = (int64_t)gridDim.x * kBThreads;
+    const int64_t plane = count4 * 4;
+    for (int64_t x = (int64_t)blockIdx.x * kBThreads + threadIdx.x; x < count4; x += stride) {
+        f32x4_t s = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int p = 0; p < P; ++p)
+            s += *reinterpret_cast<const f32x4_t *>(part + p * plane + 4 * x);
+        *reinterpret_cast<f32x4_t *>(dW + 4 * x) = s;
+    }
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+// Token splits of dW: enough workgroups to fill the chip, each split a
+// multiple of one stage.  P = 0 when there are no tokens.
+void key_proj_bwd_splits(int64_t N, int64_t m, int64_t nout, int64_t *P, int64_t *per)
+{
+    if (N == 0) {
+        *P = 0;
+        *per = kBK;
+        return;
+    }
+    const int64_t tiles = ceil_div(nout, kBM) * ceil_div(m, kBN);
+    const int64_t want = std::max((int64_t)1, std::min(ceil_div(kTargetGroups, tiles), ceil_div(N, kBK)));
+    *per = ceil_div(ceil_div(N, want), kBK) * kBK;
+    *P = ceil_div(N, *per);
+}
+
+size_t key_proj_bwd_workspace_bytes(int64_t N, int64_t m, int64_t d, int64_t r)
+{
+    int64_t P, per;
+    key_proj_bwd_splits(N, m, d + r, &P, &per);
+    return P > 1 ? (size_t)P * (size_t)(d + r) * (size_t)m * sizeof(float) : 0;
+}
+
+int check_key_proj_bwd_supported(const KeyProjProblem &p, std::string *why)
+{
+    if (p.dtype != LRAR_DTYPE_BF16) {
+        *why = "the key producer's backward runs on bf16 storage (the matrix cores' input type)";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.m % 8 != 0 || p.d % 8 != 0 || p.r % 8 != 0) {
+        *why = "the key producer's backward needs m, d and r multiples of 8";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.m > (1 << 20) || p.d + p.r > (1 << 20)) {
+        *why = "the key producer's backward supports m and d + r up to 2^20";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (p.N > ((int64_t)1 << 30)) {
+        *why = "N above 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (ceil_div(p.N, kBM) * ceil_div(p.m, kBN) > INT32_MAX) {
+        *why = "too many output tiles for one launch";
+        return LRAR_EUNSUPPORTED;
+    }
+    return LRAR_OK;
+}
+
+int launch_key_proj_bwd(const KeyProjProblem &p, const void *dO, const void *dK, void *dA,
+                        float *dW, void *workspace, hipStream_t st, std::string *err)
+{
+    BwdArgs a;
+    a.A = static_cast<const uint16_t *>(p.A);
+    a.W = static_cast<const uint16_t *>(p.W);
+    a.dO = static_cast<const uint16_t *>(dO);
+    a.dK = static_cast<const uint16_t *>(dK);
+    a.dA = static_cast<uint16_t *>(dA);
+    a.N = p.N;
+    a.m = (int)p.m;
+    a.d = (int)p.d;
+    a.r = (int)p.r;
+    a.ntn = (int)ceil_div(p.m, kBN);
+    const int64_t nout = p.d + p.r;
+    int64_t P;
+    key_proj_bwd_splits(p.N, p.m, nout, &P, &a.per);
+    if (p.N > 0) {
+        const int64_t tiles = ceil_div(p.N, kBM) * a.ntn;
+        hipLaunchKernelGGL(key_proj_bwd_gemm<false>, dim3((unsigned)tiles), dim3(kBThreads), 0,
+                           st, a);
+        int rc = hip_status(hipGetLastError(), "key_proj_bwd_gemm (dA) launch", err);
+        if (rc)
+            return rc;
+        a.dst = P > 1 ? static_cast<float *>(workspace) : dW;
+        hipLaunchKernelGGL(key_proj_bwd_gemm<true>,
+                           dim3((unsigned)(ceil_div(nout, kBM) * a.ntn), (unsigned)P),
+                           dim3(kBThreads), 0, st, a);
+        if ((rc = hip_status(hipGetLastError(), "key_proj_bwd_gemm (dW) launch", err)))
+            return rc;
+    }
+    if (P != 1) {
+        const int64_t count4 = nout * p.m / 4;
+        const int64_t groups = std::max((int64_t)1, std::min(ceil_div(count4, kBThreads), (int64_t)4096));
+        hipLaunchKernelGGL(key_proj_bwd_reduce, dim3((unsigned)groups), dim3(kBThreads), 0, st,
+                           static_cast<const float *>(workspace), dW, count4, (int)P);
+        return hip_status(hipGetLastError(), "key_proj_bwd_reduce launch", err);
+    }
+    return LRAR_OK;
+}
+
+}  // namespace lrar

@@ -180,6 +180,13 @@ struct KeyProjProblem {
 
 int check_key_proj_supported(const KeyProjProblem &p, std::string *why);
 int launch_key_proj(const KeyProjProblem &p, hipStream_t st, std::string *err);
+// Backward of the key producer: p.O and p.K are unused.  dW is fp32; the
+// workspace holds the token splits' partials (key_proj_bwd_workspace_bytes).
+void key_proj_bwd_splits(int64_t N, int64_t m, int64_t nout, int64_t *P, int64_t *per);
+size_t key_proj_bwd_workspace_bytes(int64_t N, int64_t m, int64_t d, int64_t r);
+int check_key_proj_bwd_supported(const KeyProjProblem &p, std::string *why);
+int launch_key_proj_bwd(const KeyProjProblem &p, const void *dO, const void *dK, void *dA,
+                        float *dW, void *workspace, hipStream_t st, std::string *err);
 int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err);
 
 }  // namespace lrar

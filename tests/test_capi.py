@@ -43,7 +43,8 @@ def test_exports_every_declared_symbol(lib):
                             "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
-                            "lr_attnres_key_proj_fwd", "lr_attnres_route_neff",
+                            "lr_attnres_key_proj_fwd", "lr_attnres_key_proj_bwd",
+                            "lr_attnres_key_proj_bwd_workspace_bytes", "lr_attnres_route_neff",
                             "lr_attnres_block_route_bwd_deferred", "lr_attnres_block_gather_bwd",
                             "lr_attnres_route_all_bwd", "lr_attnres_route_all_bwd_workspace_bytes",
                             "lr_attnres_route_bwd_deferred", "lr_attnres_route_gather_bwd",
@@ -465,6 +466,52 @@ def test_key_projection_unsupported(lib):
     assert "bf16" in err(lib)
     assert kproj(lib, m=60) == EUNSUPPORTED
     assert kproj(lib, N=(1 << 30) + 1, m=8, d=8, r=8) == EUNSUPPORTED
+
+
+def kproj_bwd(lib, A_=A, W=B, dO=C, dK=D, dA=E, dW=G, ws=None, wsb=0, N=8, m=64, d=32, r=16,
+              dtype=BF16):
+    return lib.lr_attnres_key_proj_bwd(A_, W, dO, dK, dA, dW, ws, wsb, N, m, d, r, dtype, None)
+
+
+KPROJ_BWD_INVALID = [
+    ("no outputs", dict(d=0, r=0), "d + r >= 1"),
+    ("negative N", dict(N=-1), "N >= 0"),
+    ("A NULL", dict(A_=None), "A is NULL"),
+    ("dA NULL", dict(dA=None), "dA is NULL"),
+    ("dW NULL", dict(dW=None), "dW is NULL"),
+    ("dK misaligned", dict(dK=D + 8), "16-byte aligned"),
+    ("dO given with d = 0", dict(d=0), "dO must be NULL"),
+    ("dK given with r = 0", dict(r=0), "dK must be NULL"),
+    ("dA overlaps A", dict(dA=A + 64), "overlaps"),
+    ("dW overlaps dA", dict(dW=E + 256), "overlap"),
+    ("workspace too small", dict(N=4096, m=512, d=512, r=16), "workspace too small"),
+    ("unknown storage", dict(dtype=7), "storage"),
+]
+
+
+@pytest.mark.parametrize("name,kw,msg", KPROJ_BWD_INVALID, ids=[c[0] for c in KPROJ_BWD_INVALID])
+def test_key_projection_bwd_rejects(lib, name, kw, msg):
+    assert kproj_bwd(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_key_projection_bwd_unsupported(lib):
+    assert kproj_bwd(lib, dtype=F32) == EUNSUPPORTED
+    assert "bf16" in err(lib)
+    assert kproj_bwd(lib, m=60) == EUNSUPPORTED
+    assert kproj_bwd(lib, r=12) == EUNSUPPORTED
+    assert kproj_bwd(lib, N=(1 << 30) + 1, m=8, d=8, r=8) == EUNSUPPORTED
+
+
+def test_key_projection_bwd_workspace(lib):
+    """Token splits only when the dW tile grid alone is small: the paper's
+    projection shape splits 16384 tokens 8 ways; a 512-tile grid and no
+    tokens need none; unsupported inputs report 0."""
+    ws = lib.lr_attnres_key_proj_bwd_workspace_bytes
+    assert ws(16384, 1024, 1024, 16, BF16) == 8 * 1040 * 1024 * 4
+    assert ws(100, 8192, 1024, 0, BF16) == 0
+    assert ws(0, 1024, 1024, 16, BF16) == 0
+    assert ws(64, 64, 32, 16, F32) == 0
 
 
 def neff_call(lib, V=A, K=None, q=B, ne=C, S=4, N=8, d=64, r=8, mode=SL, dtype=BF16, eps=1e-6):

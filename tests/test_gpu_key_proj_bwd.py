@@ -1,0 +1,147 @@
+"""GPU parity of the projected-key producer's backward (Sec. 3.3, Eq.
+fused_projection; chain rule through the linear map) through the C ABI,
+against the fp64 oracle.
+
+dA is bf16, rounded once from an fp32 sum over the d + r outputs: it must lie
+within 2^-8 |ref| (twice bf16's half-ulp) plus twice the fp32 sum's error
+bound n 2^-24 sum |term| of the exact value.  dW is fp32, a sum over the N
+tokens (split into partials and summed in split order): it is held to twice
+that error bound.  sum |term| comes from the oracle run on the operands'
+magnitudes.  Cases cover ragged token, output and feature tiles, several
+token splits with a ragged last one, keys only (d = 0), values only (r = 0),
+a tile grid wide enough for one split (dW written directly), no tokens, the
+paper's projection shape at full size (sampled rows of dA and columns of
+dW), and bitwise reproducibility.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_09694_amd as lr
+from paper_2607_09694_amd.inputs import bf16_bits_from_f32, bf16_tensor_to_bits, f32_from_bf16_bits
+from parity import check_sum_by_terms
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lr.load_library()
+    return torch.device("cuda:0")
+
+
+def to_dev(bits, dev):
+    return None if bits is None else torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+def host_operands(N, m, d, r, seed):
+    rng = np.random.default_rng(seed)
+    A = bf16_bits_from_f32(rng.standard_normal((N, m)).astype(np.float32))
+    W = bf16_bits_from_f32((rng.standard_normal((d + r, m)) / np.sqrt(m)).astype(np.float32))
+    dO = bf16_bits_from_f32(rng.standard_normal((N, d)).astype(np.float32)) if d else None
+    dK = bf16_bits_from_f32(rng.standard_normal((N, r)).astype(np.float32)) if r else None
+    return A, W, dO, dK
+
+
+def magnitudes(*xs):
+    return [None if x is None else x & np.uint16(0x7FFF) for x in xs]
+
+
+def check_dA(got, ref, terms, n_terms):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.isfinite(got).all(), "non-finite values in dA"
+    bar = 2.0 ** -8 * np.abs(ref) + 2.0 * n_terms * 2.0 ** -24 * terms
+    worst = (np.abs(got - ref) / np.maximum(bar, 1e-300)).max(initial=0.0)
+    assert worst <= 1.0, f"dA: max error / bar {worst:.3f}"
+
+
+def splits(N, m, nout):
+    tiles = -(-nout // 128) * -(-m // 128)
+    want = max(1, min(-(-512 // tiles), -(-N // 64)))
+    per = -(-(-(-N // want)) // 64) * 64
+    return -(-N // per)
+
+
+# (N, m, d, r)
+CASES = [
+    (300, 136, 64, 16),     # ragged tokens, features and outputs; 5 splits, last ragged
+    (1000, 256, 256, 32),   # 3 output tiles, the last one partial
+    (77, 64, 0, 16),        # keys only (the embedding key projection)
+    (129, 200, 96, 0),      # values only, ragged feature tile
+    (64, 8, 8, 8),          # one tile of each
+    (100, 8192, 1024, 0),   # 512 dW tiles: one split, written directly
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "N{}-m{}-d{}-r{}".format(*c))
+def test_matches_oracle(dev, case):
+    N, m, d, r = case
+    A, W, dO, dK = host_operands(N, m, d, r, seed=N + m + d + r)
+    dA, dW = lr.key_proj_bwd(to_dev(A, dev), to_dev(W, dev), to_dev(dO, dev), to_dev(dK, dev))
+    torch.cuda.synchronize()
+    refA, refW = oracle.key_projection_bwd(A, W, dO, dK)
+    tA, tW = oracle.key_projection_bwd(*magnitudes(A, W, dO, dK))
+    check_dA(f32_from_bf16_bits(bf16_tensor_to_bits(dA)), refA, tA, d + r)
+    check_sum_by_terms("dW", dW.cpu().numpy(), refW, tW, N + splits(N, m, d + r), 0.0)
+
+
+def test_no_tokens_gives_zero_weight_gradient(dev):
+    m, d, r = 64, 32, 8
+    A = torch.zeros((0, m), dtype=torch.bfloat16, device=dev)
+    W = torch.ones((d + r, m), dtype=torch.bfloat16, device=dev)
+    dO = torch.zeros((0, d), dtype=torch.bfloat16, device=dev)
+    dK = torch.zeros((0, r), dtype=torch.bfloat16, device=dev)
+    dWo = torch.full((d + r, m), 7.0, dtype=torch.float32, device=dev)
+    dA, dW = lr.key_proj_bwd(A, W, dO, dK, out=(torch.empty((0, m), dtype=torch.bfloat16,
+                                                            device=dev), dWo))
+    torch.cuda.synchronize()
+    assert tuple(dA.shape) == (0, m) and bool((dW == 0).all())
+
+
+def test_bitwise_reproducible(dev):
+    N, m, d, r = 3000, 512, 512, 32
+    A, W, dO, dK = (to_dev(x, dev) for x in host_operands(N, m, d, r, seed=7))
+    a1, w1 = lr.key_proj_bwd(A, W, dO, dK)
+    a2, w2 = lr.key_proj_bwd(A, W, dO, dK)
+    torch.cuda.synchronize()
+    assert torch.equal(a1.view(torch.int16), a2.view(torch.int16))
+    assert torch.equal(w1.view(torch.int32), w2.view(torch.int32))
+
+
+def test_unsupported_shapes_raise(dev):
+    A = torch.zeros((4, 12), dtype=torch.bfloat16, device=dev)
+    W = torch.zeros((16, 12), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lr.RoutingError, match="EUNSUPPORTED"):
+        lr.key_proj_bwd(A, W, torch.zeros((4, 8), dtype=torch.bfloat16, device=dev),
+                        torch.zeros((4, 8), dtype=torch.bfloat16, device=dev))
+
+
+@pytest.mark.parametrize("r", [16, 32])
+def test_full_size_sampled(dev, r):
+    """The paper's projection shape (m = d = 1024) at N = 16384 tokens:
+    sampled token rows of dA and feature columns of dW against the oracle."""
+    N, m, d = 16384, 1024, 1024
+    g = torch.Generator(device=dev).manual_seed(r)
+    A = torch.randn((N, m), generator=g, device=dev).to(torch.bfloat16)
+    W = (torch.randn((d + r, m), generator=g, device=dev) / m ** 0.5).to(torch.bfloat16)
+    dO = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
+    dK = torch.randn((N, r), generator=g, device=dev).to(torch.bfloat16)
+    dA, dW = lr.key_proj_bwd(A, W, dO, dK)
+    torch.cuda.synchronize()
+    rows = np.sort(np.concatenate([[0, 127, 128, N - 1],
+                                   np.random.default_rng(r).choice(N, 28, replace=False)]))
+    cols = np.sort(np.concatenate([[0, m - 1], np.random.default_rng(r + 1).choice(m, 14,
+                                                                                   replace=False)]))
+    bits = lambda t: bf16_tensor_to_bits(t)
+    Ah, Wh, dOh, dKh = bits(A), bits(W), bits(dO), bits(dK)
+    refA, _ = oracle.key_projection_bwd(Ah[rows], Wh, dOh[rows], dKh[rows])
+    tA, _ = oracle.key_projection_bwd(*magnitudes(Ah[rows], Wh, dOh[rows], dKh[rows]))
+    check_dA(f32_from_bf16_bits(bits(dA)[rows]), refA, tA, d + r)
+    _, refW = oracle.key_projection_bwd(np.ascontiguousarray(Ah[:, cols]),
+                                        np.ascontiguousarray(Wh[:, cols]), dOh, dKh)
+    _, tW = oracle.key_projection_bwd(*magnitudes(np.ascontiguousarray(Ah[:, cols]),
+                                                  np.ascontiguousarray(Wh[:, cols]), dOh, dKh))
+    check_sum_by_terms("dW", dW[:, cols].cpu().numpy(), refW, tW, N + splits(N, m, d + r), 0.0)
