@@ -704,6 +704,29 @@ def key_producer(torch, lr, dev, reps, warmup, flush):
         torch.cuda.synchronize()
         res["bitwise_equal_to_library_fused_gemm"] = bool(torch.equal(V[1], C[:, :d]) and
                                                           torch.equal(K[1], C[:, d:]))
+        # Backward: dA = [dO, dK] W (bf16) and dW = [dO, dK]^T A (fp32), against
+        # the library's two GEMMs on the concatenated gradient (dW in bf16).
+        dO = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
+        dK = torch.randn((N, r), generator=g, device=dev).to(torch.bfloat16)
+        dA = torch.empty((N, m), dtype=torch.bfloat16, device=dev)
+        dW = torch.empty((d + r, m), dtype=torch.float32, device=dev)
+        Gc = torch.cat([dO, dK], dim=1)
+        Gt = Gc.t().contiguous()
+        dA2 = torch.empty_like(dA)
+        dW2 = torch.empty((d + r, m), dtype=torch.bfloat16, device=dev)
+
+        def lib_bwd():
+            torch.matmul(Gc, W, out=dA2)
+            torch.matmul(Gt, A, out=dW2)
+
+        for name, fn in (("backward", lambda: lr.key_proj_bwd(A, W, dO, dK, out=(dA, dW))),
+                         ("library_backward_two_gemms", lib_bwd)):
+            ts = time_calls(torch, fn, reps, warmup, flush)
+            med = float(np.median(ts))
+            res[name] = {"median_ms": med, "min_ms": float(np.min(ts)),
+                         "TFLOPs": 2 * flops / (med * 1e-3) / 1e12,
+                         "frac_of_bf16_peak": 2 * flops / (med * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}
+        del dO, dK, dA, dW, Gc, Gt, dA2, dW2
         out[f"m{m}_r{r}"] = res
         del A, W, V, K, C
         torch.cuda.empty_cache()

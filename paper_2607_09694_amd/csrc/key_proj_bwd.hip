@@ -47,7 +47,7 @@ constexpr int kLd = kBK + 8;                      // LDS row stride (elements)
 constexpr int kBThreads = 256;                    // 4 waves
 constexpr int kRowChunks = kBM * kBK / 8 / kBThreads;       // 4: k-contiguous loads per lane
 constexpr int kPairs = kBK / 2 * kBN / 8 / kBThreads;       // 2: transposed pair loads per lane
-constexpr int kTargetGroups = 512;                // dW: workgroups wanted per launch
+constexpr int kSlots = 2 * 256;                   // workgroups resident at once (2 per CU)
 
 static_assert(kRowChunks == 4 && kPairs == 2, "stage loads split evenly over the lanes");
 
@@ -250,8 +250,10 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace
 
-// Token splits of dW: enough workgroups to fill the chip, each split a
-// multiple of one stage.  P = 0 when there are no tokens.
+// Token splits of dW: as many as let every workgroup of the launch be
+// resident at once (a second, partial round of workgroups would cost a
+// whole round's time), each split a multiple of one stage.  P = 0 when there
+// are no tokens.
 void key_proj_bwd_splits(int64_t N, int64_t m, int64_t nout, int64_t *P, int64_t *per)
 {
     if (N == 0) {
@@ -260,7 +262,7 @@ void key_proj_bwd_splits(int64_t N, int64_t m, int64_t nout, int64_t *P, int64_t
         return;
     }
     const int64_t tiles = ceil_div(nout, kBM) * ceil_div(m, kBN);
-    const int64_t want = std::max((int64_t)1, std::min(ceil_div(kTargetGroups, tiles), ceil_div(N, kBK)));
+    const int64_t want = std::max((int64_t)1, std::min(kSlots / tiles, ceil_div(N, kBK)));
     *per = ceil_div(ceil_div(N, want), kBK) * kBK;
     *P = ceil_div(N, *per);
 }

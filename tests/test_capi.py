@@ -505,10 +505,12 @@ def test_key_projection_bwd_unsupported(lib):
 
 def test_key_projection_bwd_workspace(lib):
     """Token splits only when the dW tile grid alone is small: the paper's
-    projection shape splits 16384 tokens 8 ways; a 512-tile grid and no
-    tokens need none; unsupported inputs report 0."""
+    projection shape (72 tiles) splits 16384 tokens 7 ways, 504 workgroups
+    resident at once; a 512-tile grid and no tokens need none; unsupported
+    inputs report 0."""
     ws = lib.lr_attnres_key_proj_bwd_workspace_bytes
-    assert ws(16384, 1024, 1024, 16, BF16) == 8 * 1040 * 1024 * 4
+    assert ws(16384, 1024, 1024, 16, BF16) == 7 * 1040 * 1024 * 4
+    assert ws(16384, 2816, 1024, 16, BF16) == 2 * 1040 * 2816 * 4
     assert ws(100, 8192, 1024, 0, BF16) == 0
     assert ws(0, 1024, 1024, 16, BF16) == 0
     assert ws(64, 64, 32, 16, F32) == 0

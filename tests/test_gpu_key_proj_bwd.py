@@ -60,7 +60,7 @@ def check_dA(got, ref, terms, n_terms):
 
 def splits(N, m, nout):
     tiles = -(-nout // 128) * -(-m // 128)
-    want = max(1, min(-(-512 // tiles), -(-N // 64)))
+    want = max(1, min(512 // tiles, -(-N // 64)))
     per = -(-(-(-N // want)) // 64) * 64
     return -(-N // per)
 
