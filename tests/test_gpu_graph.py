@@ -168,3 +168,25 @@ def test_captured_split_sources_replays(dev):
         lr.route_merge_fwd(*st, out=H)
 
     _replays_match(pass_, [H, *st])
+
+
+def test_captured_key_producer_forward_and_backward_replays(dev):
+    """The key producer and its backward (token splits and their ordered
+    sum included) in one graph: every replay matches the eager call bit for
+    bit."""
+    N, m, d, r = 700, 256, 128, 16
+    g = torch.Generator(device=dev).manual_seed(4)
+    A = torch.randn((N, m), generator=g, device=dev).to(torch.bfloat16)
+    W = (torch.randn((d + r, m), generator=g, device=dev) / m ** 0.5).to(torch.bfloat16)
+    dO = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
+    dK = torch.randn((N, r), generator=g, device=dev).to(torch.bfloat16)
+    O = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((N, r), dtype=torch.bfloat16, device=dev)
+    dA = torch.empty((N, m), dtype=torch.bfloat16, device=dev)
+    dW = torch.empty((d + r, m), dtype=torch.float32, device=dev)
+
+    def pass_():
+        lr.key_proj_fwd(A, W, d, out=(O, K))
+        lr.key_proj_bwd(A, W, dO, dK, out=(dA, dW))
+
+    _replays_match(pass_, [O, K, dA, dW])

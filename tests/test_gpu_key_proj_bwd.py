@@ -145,3 +145,30 @@ def test_full_size_sampled(dev, r):
     _, tW = oracle.key_projection_bwd(*magnitudes(np.ascontiguousarray(Ah[:, cols]),
                                                   np.ascontiguousarray(Wh[:, cols]), dOh, dKh))
     check_sum_by_terms("dW", dW[:, cols].cpu().numpy(), refW, tW, N + splits(N, m, d + r), 0.0)
+
+
+def _random_shapes(count, seed):
+    rng = np.random.default_rng(seed)
+    shapes = []
+    for _ in range(count):
+        N = int(rng.integers(1, 1500))
+        m = 8 * int(rng.integers(1, 80))
+        d = 8 * int(rng.integers(0, 40))
+        r = 8 * int(rng.integers(0 if d else 1, 9))
+        shapes.append((N, m, d, r))
+    return shapes
+
+
+@pytest.mark.parametrize("case", _random_shapes(16, 2026), ids=lambda c: "N{}-m{}-d{}-r{}".format(*c))
+def test_random_shapes_match_oracle(dev, case):
+    """Seeded random shapes (every size a multiple of 8 where the entry
+    point needs it, tokens anywhere in 1 .. 1499): token, output and
+    feature tiles ragged in every combination, and split counts from 1 up."""
+    N, m, d, r = case
+    A, W, dO, dK = host_operands(N, m, d, r, seed=N * 7 + m)
+    dA, dW = lr.key_proj_bwd(to_dev(A, dev), to_dev(W, dev), to_dev(dO, dev), to_dev(dK, dev))
+    torch.cuda.synchronize()
+    refA, refW = oracle.key_projection_bwd(A, W, dO, dK)
+    tA, tW = oracle.key_projection_bwd(*magnitudes(A, W, dO, dK))
+    check_dA(f32_from_bf16_bits(bf16_tensor_to_bits(dA)), refA, tA, d + r)
+    check_sum_by_terms("dW", dW.cpu().numpy(), refW, tW, N + splits(N, m, d + r), 0.0)
