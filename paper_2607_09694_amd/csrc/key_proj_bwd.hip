@@ -11,14 +11,20 @@
 // output tile with v_mfma_f32_16x16x32_bf16 and fp32 accumulators (each
 // wave a 64 x 64 quarter, 16 MFMA tiles).  The reduction runs in stages of
 // 64: every stage is loaded from memory into registers while the previous
-// one feeds the MFMAs, then written to LDS, where both operands sit with the
-// reduction index contiguous in each row (what an MFMA operand read needs).
-// Of the four operand reads only G in dA is stored that way in memory; W in
-// dA and both G and A in dW have the output index contiguous instead.  Those
-// are transposed on the way into LDS: a lane loads 8 consecutive output
-// indices at two consecutive reduction steps and writes 8 words, each the
-// pair of steps for one output index.  LDS rows are padded to 72 elements
-// (36 words), which spreads the 16 rows of one operand read over all banks.
+// one feeds the MFMAs, then written to LDS.  An MFMA operand fragment holds,
+// per lane, 8 consecutive reduction steps of one output index.  Of the four
+// operand reads only G in dA has the reduction index contiguous in memory
+// (its LDS rows are output indices, read 16 bytes a lane); W in dA and both
+// G and A in dW have the output index contiguous instead.  Those
+// stay in that layout in LDS (rows are reduction steps, 16-byte chunks
+// copied as loaded) and are transposed by the read: gfx950's ds_read_b64_tr_b16
+// gives lane i of a 16-lane group element i mod 4 of the 8 bytes addressed
+// by lane i / 4 + 4 e, for e = 0..3.  Pointing lane s of the group at
+// reduction step s / 4 and output indices 4 (s mod 4) .. +3 therefore hands
+// lane i four consecutive reduction steps of output index i; two such reads
+// make an MFMA operand fragment.  Rows of the reduction-contiguous operand
+// are padded to 72 elements and rows of a transposed one to 144, which
+// spreads one operand read over the banks.
 //
 // dA rounds to bf16 (nearest even).  dW is written in fp32, so that a caller
 // can add it to fp32 master gradients without a second rounding; its token
@@ -46,10 +52,16 @@ constexpr int kBK = 64;                           // reduction steps per stage
 constexpr int kLd = kBK + 8;                      // LDS row stride (elements)
 constexpr int kBThreads = 256;                    // 4 waves
 constexpr int kRowChunks = kBM * kBK / 8 / kBThreads;       // 4: k-contiguous loads per lane
-constexpr int kPairs = kBK / 2 * kBN / 8 / kBThreads;       // 2: transposed pair loads per lane
+constexpr int kTs = kBN + 16;                     // LDS row stride of a transposed operand
+constexpr int kTChunks = kBK * kBN / 8 / kBThreads;         // 4: transposed-operand loads per lane
 constexpr int kSlots = 2 * 256;                   // workgroups resident at once (2 per CU)
 
-static_assert(kRowChunks == 4 && kPairs == 2, "stage loads split evenly over the lanes");
+static_assert(kRowChunks == 4 && kTChunks == 4, "stage loads split evenly over the lanes");
+static_assert(kBK * kTs == kBM * kLd, "both LDS layouts of an operand take the same space");
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+typedef __attribute__((address_space(3))) char lds_char_t;
 
 struct BwdArgs {
     const uint16_t *A;   // [N][m]
@@ -75,12 +87,19 @@ __device__ __forceinline__ u32x4_t g_chunk(const BwdArgs &a, int64_t n, int o)
     return *reinterpret_cast<const u32x4_t *>(a.dK + n * a.r + (o - a.d));
 }
 
-// Word e of the transposed pair: element e of row k (low half) and of row
-// k + 1 (high half).
-__device__ __forceinline__ unsigned pair_word(const u32x4_t &lo, const u32x4_t &hi, int e)
+// MFMA operand fragment from a transposed operand in LDS (row = reduction
+// step, kTs elements per row): lane l receives reduction steps 32 ks +
+// 8 (l / 16) .. +7 of output index base + l mod 16.  Within each 16-lane
+// group, lane s addresses step s / 4 (then s / 4 + 4) and output indices
+// base + 4 (s mod 4) .. +3; the transposing read regroups the elements.
+__device__ __forceinline__ bf16x8_t frag_tr(const uint16_t *S, int ks, int base, int lane)
 {
-    const unsigned x = lo[e >> 1], y = hi[e >> 1];
-    return (e & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+    const int row = 32 * ks + 8 * (lane >> 4) + ((lane & 15) >> 2);
+    const int col = base + 4 * (lane & 3);
+    lds_char_t *p = (lds_char_t *)(S) + 2 * (row * kTs + col);
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)p);
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(p + 2 * 4 * kTs));
+    return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // DW = false: C = dA tile (rows: tokens, columns: input features, reduction:
@@ -107,12 +126,10 @@ __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
     const int64_t kend = DW ? min(a.N, kbeg + a.per) : nout;
     const int nk = (int)((kend - kbeg + kBK - 1) / kBK);
 
-    // Stage registers: X is 4 row chunks (dA) or 2 transposed pairs (dW).
+    // Stage registers: 4 chunks of 8 elements per operand.  A transposed
+    // operand's chunk u is reduction step q / 16 of the stage, output indices
+    // 8 (q mod 16) .. +7 of the tile, with q = tid + 256 u.
     u32x4_t xr[4], yr[4];
-
-    // Transposed pair u of this lane: reduction steps 2 kp, 2 kp + 1 of the
-    // stage, output indices 8 mc .. 8 mc + 7 of the tile.
-    const int kp_lane = lane & 15, mc_lane = (lane >> 4) + 4 * wave;
     auto fetch = [&](int kt) {
         const int64_t k0 = kbeg + (int64_t)kt * kBK;
         if (!DW) {
@@ -124,34 +141,25 @@ __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
                 xr[u] = (n < a.N && o < kend) ? g_chunk(a, n, (int)o) : zero4();
             }
         }
+        const uint16_t *Y = DW ? a.A : a.W;
 #pragma unroll
-        for (int u = 0; u < kPairs; ++u) {
-            const int kp = kp_lane + 16 * u;
-            const int64_t k = k0 + 2 * kp;
+        for (int u = 0; u < kTChunks; ++u) {
+            const int q = tid + kBThreads * u, ks = q >> 4, mc = q & 15;
+            const int64_t k = k0 + ks;
             if (DW) {
-                const int64_t o = row0 + 8 * mc_lane;
-                const bool ok = o < nout;
-                xr[2 * u] = (ok && k < kend) ? g_chunk(a, k, (int)o) : zero4();
-                xr[2 * u + 1] = (ok && k + 1 < kend) ? g_chunk(a, k + 1, (int)o) : zero4();
+                const int64_t o = row0 + 8 * mc;
+                xr[u] = (o < nout && k < kend) ? g_chunk(a, k, (int)o) : zero4();
             }
-            const int j = col0 + 8 * mc_lane;
-            const bool ok = j < a.m;
-            const uint16_t *Y = DW ? a.A : a.W;
-            yr[2 * u] = (ok && k < kend)
-                            ? *reinterpret_cast<const u32x4_t *>(Y + k * a.m + j) : zero4();
-            yr[2 * u + 1] = (ok && k + 1 < kend)
-                                ? *reinterpret_cast<const u32x4_t *>(Y + (k + 1) * a.m + j)
-                                : zero4();
+            const int j = col0 + 8 * mc;
+            yr[u] = (j < a.m && k < kend)
+                        ? *reinterpret_cast<const u32x4_t *>(Y + k * a.m + j) : zero4();
         }
     };
-    auto put_pairs = [&](uint16_t *S, const u32x4_t *v) {
+    auto put_tr = [&](uint16_t *S, const u32x4_t *v) {
 #pragma unroll
-        for (int u = 0; u < kPairs; ++u) {
-            const int kp = kp_lane + 16 * u;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                *reinterpret_cast<unsigned *>(S + (8 * mc_lane + e) * kLd + 2 * kp) =
-                    pair_word(v[2 * u], v[2 * u + 1], e);
+        for (int u = 0; u < kTChunks; ++u) {
+            const int q = tid + kBThreads * u, ks = q >> 4, mc = q & 15;
+            *reinterpret_cast<u32x4_t *>(S + ks * kTs + 8 * mc) = v[u];
         }
     };
     auto put = [&]() {
@@ -162,9 +170,9 @@ __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
                 *reinterpret_cast<u32x4_t *>(Xs + row * kLd + 8 * kc) = xr[u];
             }
         } else {
-            put_pairs(Xs, xr);
+            put_tr(Xs, xr);
         }
-        put_pairs(Ys, yr);
+        put_tr(Ys, yr);
     };
 
     f32x4_t acc[4][4];
@@ -190,10 +198,10 @@ __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
             bf16x8_t xf[4], yf[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                xf[i] = *reinterpret_cast<const bf16x8_t *>(
-                    Xs + (wm * 64 + 16 * i + fr) * kLd + 32 * ks + 8 * fq);
-                yf[i] = *reinterpret_cast<const bf16x8_t *>(
-                    Ys + (wn * 64 + 16 * i + fr) * kLd + 32 * ks + 8 * fq);
+                xf[i] = DW ? frag_tr(Xs, ks, wm * 64 + 16 * i, lane)
+                           : *reinterpret_cast<const bf16x8_t *>(
+                                 Xs + (wm * 64 + 16 * i + fr) * kLd + 32 * ks + 8 * fq);
+                yf[i] = frag_tr(Ys, ks, wn * 64 + 16 * i, lane);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
