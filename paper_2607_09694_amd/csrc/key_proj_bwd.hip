@@ -57,7 +57,11 @@ constexpr int kTChunks = kBK * kBN / 8 / kBThreads;         // 4: transposed-ope
 constexpr int kSlots = 2 * 256;                   // workgroups resident at once (2 per CU)
 
 static_assert(kRowChunks == 4 && kTChunks == 4, "stage loads split evenly over the lanes");
+constexpr int kCs = kBN + 8;                      // LDS row stride of the staged bf16 dA tile
+constexpr int kCf = kBN + 4;                      // ... of a staged fp32 dW half-tile (floats)
 static_assert(kBK * kTs == kBM * kLd, "both LDS layouts of an operand take the same space");
+static_assert(kBM * kCs <= 2 * kBM * kLd && (kBM / 2) * kCf * 2 <= 2 * kBM * kLd,
+              "the staged output fits the operand stages");
 
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
@@ -110,8 +114,9 @@ __device__ __forceinline__ bf16x8_t frag_tr(const uint16_t *S, int ks, int base,
 template <bool DW>
 __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
 {
-    __shared__ __align__(16) uint16_t Xs[kBM * kLd];
-    __shared__ __align__(16) uint16_t Ys[kBN * kLd];
+    __shared__ __align__(16) uint16_t lds[2 * kBM * kLd];
+    uint16_t *const Xs = lds;
+    uint16_t *const Ys = lds + kBM * kLd;
 
     const int tid = threadIdx.x;
     const int lane = tid % kWaveSize, wave = tid / kWaveSize;
@@ -217,26 +222,53 @@ __global__ __launch_bounds__(kBThreads) void key_proj_bwd_gemm(BwdArgs a)
         }
     }
 
-    // Lane holds C[16 i + 4 (l / 16) + e][16 j + l mod 16] of its quarter.
-    float *dst = DW ? a.dst + (int64_t)blockIdx.y * nout * a.m : nullptr;
+    // Epilogue (every wave is past its last LDS read): lane holds
+    // C[16 i + 4 (l / 16) + e][16 j + l mod 16] of its quarter.  The tile is
+    // staged through LDS and written as 16-byte row segments: dA whole, as
+    // bf16; dW in two halves of 64 rows, as fp32.
+    if (!DW) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int c = col0 + wn * 64 + 16 * j + fr;
-            if (c >= a.m)
-                continue;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int64_t row = row0 + wm * 64 + 16 * i + 4 * fq + e;
-                if (row >= rows)
-                    continue;
-                if (DW)
-                    dst[row * a.m + c] = acc[i][j][e];
-                else
-                    a.dA[row * a.m + c] = to_bf16(acc[i][j][e]);
-            }
+                for (int e = 0; e < 4; ++e)
+                    lds[(wm * 64 + 16 * i + 4 * fq + e) * kCs + wn * 64 + 16 * j + fr] =
+                        to_bf16(acc[i][j][e]);
+        __syncthreads();
+        for (int f = tid; f < kBM * (kBN / 8); f += kBThreads) {
+            const int row = f >> 4, ch = f & 15;
+            const int64_t n = row0 + row;
+            const int c = col0 + 8 * ch;
+            if (n < rows && c < a.m)
+                *reinterpret_cast<u32x4_t *>(a.dA + n * a.m + c) =
+                    *reinterpret_cast<const u32x4_t *>(lds + row * kCs + 8 * ch);
         }
+    } else {
+        float *const Cf = reinterpret_cast<float *>(lds);
+        float *const dst = a.dst + (int64_t)blockIdx.y * nout * a.m;
+        for (int h = 0; h < 2; ++h) {
+            if (wm == h) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            Cf[(16 * i + 4 * fq + e) * kCf + wn * 64 + 16 * j + fr] = acc[i][j][e];
+            }
+            __syncthreads();
+            for (int f = tid; f < (kBM / 2) * (kBN / 4); f += kBThreads) {
+                const int row = f >> 5, ch = f & 31;
+                const int64_t o = row0 + (kBM / 2) * h + row;
+                const int c = col0 + 4 * ch;
+                if (o < rows && c < a.m)
+                    *reinterpret_cast<f32x4_t *>(dst + o * a.m + c) =
+                        *reinterpret_cast<const f32x4_t *>(Cf + row * kCf + 4 * ch);
+            }
+            __syncthreads();
+        }
+    }
 }
 
 // dW[x] = sum over the P partials in split order (P = 0 writes zeros: the
