@@ -420,13 +420,14 @@ def key_proj_fwd(A, W, d: int, out=None):
     return O, K
 
 
-def key_proj_bwd(A, W, dO, dK, out=None):
+def key_proj_bwd(A, W, dO, dK, out=None, workspace=None):
     """Backward of [o_n; k_n] = [W^O; W^K] a_n (Sec. 3.3, Eq.
     fused_projection): dA = dO W^O + dK W^K and dW = [dO^T A; dK^T A].
 
     A [N,m] bf16; W [d+r,m] bf16; dO [N,d] or None (d = 0); dK [N,r] or
     None (r = 0), bf16.  Returns (dA [N,m] bf16, dW [d+r,m] fp32); ``out``
-    may supply (dA, dW).
+    may supply (dA, dW), ``workspace`` a uint8 device buffer of at least
+    key_proj_bwd_workspace_bytes(...) bytes.
     """
     import torch
 
@@ -447,14 +448,24 @@ def key_proj_bwd(A, W, dO, dK, out=None):
         dA = torch.empty((N, m), dtype=A.dtype, device=A.device)
         dW = torch.empty((d + r, m), dtype=torch.float32, device=A.device)
     code = _dtype_code(A)
-    nbytes = lib.lr_attnres_key_proj_bwd_workspace_bytes(N, m, d, r, code)
-    ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=A.device)
+    need = lib.lr_attnres_key_proj_bwd_workspace_bytes(N, m, d, r, code)
+    if workspace is None:
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=A.device)
     rc = lib.lr_attnres_key_proj_bwd(_dev(A, "A"), _dev(W, "W", A.dtype), _dev(dO, "dO", A.dtype),
                                      _dev(dK, "dK", A.dtype), _dev(dA, "dA", A.dtype),
-                                     _dev(dW, "dW", torch.float32), _dev(ws, "workspace"), nbytes,
-                                     N, m, d, r, code, _stream(A))
+                                     _dev(dW, "dW", torch.float32), _dev(workspace, "workspace"),
+                                     workspace.numel() * workspace.element_size(), N, m, d, r, code,
+                                     _stream(A))
     _check(lib, rc)
     return dA, dW
+
+
+def key_proj_bwd_workspace_bytes(N, m, d, r, dtype) -> int:
+    """Workspace of key_proj_bwd: the fp32 partials of dW's token splits."""
+    import torch
+
+    code = _BF16 if dtype == torch.bfloat16 else _F32
+    return load_library().lr_attnres_key_proj_bwd_workspace_bytes(N, m, d, r, code)
 
 
 def route_bwd_workspace_bytes(S, N, d, r, mode, dtype) -> int:

@@ -172,3 +172,21 @@ def test_random_shapes_match_oracle(dev, case):
     tA, tW = oracle.key_projection_bwd(*magnitudes(A, W, dO, dK))
     check_dA(f32_from_bf16_bits(bf16_tensor_to_bits(dA)), refA, tA, d + r)
     check_sum_by_terms("dW", dW.cpu().numpy(), refW, tW, N + splits(N, m, d + r), 0.0)
+
+
+def test_caller_workspace_reused_across_calls(dev):
+    """A caller-owned workspace sized by the query, reused by two calls in a
+    row (the second with fewer tokens): each call's result matches a call
+    with a workspace of its own, bit for bit (the partials are overwritten,
+    never accumulated)."""
+    m, d, r = 256, 256, 16
+    need = lr.key_proj_bwd_workspace_bytes(3000, m, d, r, torch.bfloat16)
+    assert need > 0
+    ws = torch.full((need,), 0x7F, dtype=torch.uint8, device=dev)
+    for N, seed in ((3000, 1), (1100, 2)):
+        A, W, dO, dK = (to_dev(x, dev) for x in host_operands(N, m, d, r, seed=seed))
+        a1, w1 = lr.key_proj_bwd(A, W, dO, dK, workspace=ws)
+        a2, w2 = lr.key_proj_bwd(A, W, dO, dK)
+        torch.cuda.synchronize()
+        assert torch.equal(a1.view(torch.int16), a2.view(torch.int16))
+        assert torch.equal(w1.view(torch.int32), w2.view(torch.int32))
