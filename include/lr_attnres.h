@@ -136,6 +136,31 @@ int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q
                                     float eps, void *stream);
 
 /*
+ * lr_attnres_route_bwd without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  The per-workgroup dq partials go to a
+ * device array that the library holds, 8 MiB on every device it runs on,
+ * kept until the process ends (its address is looked up once per device, on
+ * that device's first call).  The call itself allocates nothing, on the
+ * device or through any library routine.
+ *   Arguments, results, validation and errors are those of
+ *   lr_attnres_route_bwd with the workspace removed, plus LRAR_EUNSUPPORTED
+ *   when the problem needs more than 8 MiB of partials
+ *   (lr_attnres_route_bwd_workspace_bytes > 8388608: e.g. r = 32 beyond
+ *   2^19 tokens with projected keys, or full rank at d = 1024 beyond
+ *   32768 tokens).
+ *   All calls on one device share the array, and each call leaves its
+ *   partials there: two calls that can run at the same time on one device
+ *   (different streams, or different host threads without ordering) race
+ *   and may return wrong dq.  Calls ordered on one stream are safe; nothing
+ *   in the array needs to start at zero.
+ */
+int lr_attnres_route_bwd_noalloc(const void *V, const void *K, const float *q,
+                                 const void *dH, void *dV, void *dK, float *dq, int64_t S,
+                                 int64_t N, int64_t d, int64_t r, int mode, int dtype,
+                                 float eps, void *stream);
+
+/*
  * Block-source routing forward at one residual site: Block AttnRes (Sec. 3.1,
  * Eqs. block_attnres_sum and block_attnres_partial_sum) with the low-rank
  * keys of Sec. 3.2.  The 2L sub-layer outputs are grouped into consecutive

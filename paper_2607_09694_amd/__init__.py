@@ -53,6 +53,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.lr_attnres_route_bwd.restype = ctypes.c_int
     lib.lr_attnres_route_bwd_accumulate.argtypes = lib.lr_attnres_route_bwd.argtypes
     lib.lr_attnres_route_bwd_accumulate.restype = ctypes.c_int
+    lib.lr_attnres_route_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64,
+                                                 i, i, f, vp]
+    lib.lr_attnres_route_bwd_noalloc.restype = ctypes.c_int
     lib.lr_attnres_block_route_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i, i64, i64, i64,
                                                i, i, f, vp]
     lib.lr_attnres_block_route_fwd.restype = ctypes.c_int
@@ -508,6 +511,26 @@ def route_bwd(V, K, q, dH, mode, eps: float = 1e-6, out=None, workspace=None,
             _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
             _dev(dq, "dq", torch.float32), _dev(workspace, "workspace"),
             workspace.numel(), S, N, d, r, mode, code, float(eps), _stream(V))
+    _check(lib, rc)
+    return dV, dK, dq
+
+
+def route_bwd_noalloc(V, K, q, dH, mode, out, eps: float = 1e-6):
+    """route_bwd into the caller's ``out`` = (dV, dK, dq) buffers with no
+    workspace: the library keeps the dq partials in its own device array
+    (at most 8 MiB of them; see lr_attnres_route_bwd_noalloc), so the call
+    allocates nothing.  Calls that may overlap on one device race."""
+    import torch
+
+    lib = load_library()
+    mode = _mode(mode)
+    S, N, d, r = _shape(V, K, q, mode)
+    dV, dK, dq = out
+    rc = lib.lr_attnres_route_bwd_noalloc(_dev(V, "V"), _dev(K, "K", V.dtype),
+                                          _dev(q, "q", torch.float32), _dev(dH, "dH", V.dtype),
+                                          _dev(dV, "dV", V.dtype), _dev(dK, "dK", V.dtype),
+                                          _dev(dq, "dq", torch.float32), S, N, d, r, mode,
+                                          _dtype_code(V), float(eps), _stream(V))
     _check(lib, rc)
     return dV, dK, dq
 

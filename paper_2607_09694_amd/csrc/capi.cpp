@@ -159,9 +159,12 @@ size_t lr_attnres_route_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int
 
 namespace {
 
+// noalloc: the dq partials go to the library's own device array (workspace
+// must then be NULL with size 0).
 int route_bwd(const void *V, const void *K, const float *q, const void *dH, void *dV, void *dK,
               float *dq, void *workspace, size_t workspace_bytes, int64_t S, int64_t N, int64_t d,
-              int64_t r, int mode, int dtype, float eps, bool accumulate, void *stream)
+              int64_t r, int mode, int dtype, float eps, bool accumulate, void *stream,
+              bool noalloc = false)
 {
     g_last_error.clear();
     int64_t ve, ke, he;
@@ -182,7 +185,7 @@ int route_bwd(const void *V, const void *K, const float *q, const void *dH, void
     std::string why;
     if ((rc = lrar::check_supported(p, true, &why)))
         return fail(rc, why);
-    const size_t need = lrar::bwd_workspace_bytes(p);
+    const size_t need = noalloc ? 0 : lrar::bwd_workspace_bytes(p);
     if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(LRAR_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
     const int64_t es = dtype == LRAR_DTYPE_BF16 ? 2 : 4;
@@ -192,8 +195,12 @@ int route_bwd(const void *V, const void *K, const float *q, const void *dH, void
                         span("dH", dH, he * es)};
     if ((rc = check_aliasing(outs, 4, ins, 4)))
         return rc;
-    if ((rc = lrar::launch_bwd(p, dH, dV, dK, dq, workspace, accumulate,
-                               static_cast<hipStream_t>(stream), &why)))
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (noalloc)
+        rc = lrar::launch_bwd_noalloc(p, dH, dV, dK, dq, st, &why);
+    else
+        rc = lrar::launch_bwd(p, dH, dV, dK, dq, workspace, accumulate, st, &why);
+    if (rc)
         return fail(rc, why);
     return LRAR_OK;
 }
@@ -209,6 +216,14 @@ int lr_attnres_route_bwd(const void *V, const void *K, const float *q, const voi
 {
     return route_bwd(V, K, q, dH, dV, dK, dq, workspace, workspace_bytes, S, N, d, r, mode, dtype,
                      eps, false, stream);
+}
+
+int lr_attnres_route_bwd_noalloc(const void *V, const void *K, const float *q, const void *dH,
+                                 void *dV, void *dK, float *dq, int64_t S, int64_t N, int64_t d,
+                                 int64_t r, int mode, int dtype, float eps, void *stream)
+{
+    return route_bwd(V, K, q, dH, dV, dK, dq, nullptr, 0, S, N, d, r, mode, dtype, eps, false,
+                     stream, true);
 }
 
 int lr_attnres_route_bwd_accumulate(const void *V, const void *K, const float *q, const void *dH,

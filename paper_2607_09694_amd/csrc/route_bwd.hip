@@ -3,6 +3,8 @@
 // dq reduction, and their launcher.
 #include "route_common.h"
 
+#include <mutex>
+
 namespace lrar {
 
 // ---------------------------------------------------------------------------
@@ -703,6 +705,79 @@ int launch_block_bwd(const Problem &p, const BlockRetire &br, const void *dH, vo
     if (e == hipSuccess && p.N > 0)
         e = launch_block_retire(br, st);
     return hip_status(e, "block_route_bwd launch", err);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free backward: the dq partials in a file-scope device array
+// ---------------------------------------------------------------------------
+
+// The per-workgroup dq partials of lr_attnres_route_bwd_noalloc live here
+// instead of in a caller workspace.  Every device the library runs on holds
+// its own copy until the process ends; all calls on one device share it, and
+// each launch overwrites the rows it later reads, so nothing has to start at
+// zero.  Host code never passes this name to a kernel: it stands for a host
+// shadow, and the device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+float *g_scratch_addr[kMaxDevices];
+
+// Device address of `scratch` on device `dev`, looked up once per device
+// with that device current.
+int scratch_address(int dev, float **out, std::string *err)
+{
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = "device index " + std::to_string(dev) + " beyond the allocation-free backward's " +
+               std::to_string(kMaxDevices) + " devices";
+        return LRAR_EUNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_addr[dev]) {
+        int cur = -1;
+        hipError_t e = hipGetDevice(&cur);
+        if (e != hipSuccess)
+            return hip_status(e, "hipGetDevice", err);
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess)
+            return hip_status(e, "hipSetDevice", err);
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t back = hipSetDevice(cur);
+            if (e == hipSuccess)
+                e = back;
+        }
+        if (e != hipSuccess)
+            return hip_status(e, "hipGetSymbolAddress(scratch)", err);
+        g_scratch_addr[dev] = static_cast<float *>(p);
+    }
+    *out = g_scratch_addr[dev];
+    return LRAR_OK;
+}
+
+}  // namespace
+
+int launch_bwd_noalloc(const Problem &p, const void *dH, void *dV, void *dK, float *dq,
+                       hipStream_t st, std::string *err)
+{
+    const size_t need = bwd_workspace_bytes(p);
+    if (need > kNoAllocScratchBytes) {
+        *err = "the allocation-free backward needs " + std::to_string(need) +
+               " bytes of dq partials; its device array holds " +
+               std::to_string(kNoAllocScratchBytes);
+        return LRAR_EUNSUPPORTED;
+    }
+    int dev = -1;
+    hipError_t e = st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_status(e, st ? "hipStreamGetDevice" : "hipGetDevice", err);
+    float *ws = nullptr;
+    const int rc = scratch_address(dev, &ws, err);
+    if (rc != LRAR_OK)
+        return rc;
+    return launch_bwd(p, dH, dV, dK, dq, ws, false, st, err);
 }
 
 }  // namespace lrar

@@ -41,6 +41,16 @@ int launch_merge(const float *M, const float *L, const float *ACC, int64_t P, in
 int launch_bwd(const Problem &p, const void *dH, void *dV, void *dK, float *dq, void *ws,
                bool accumulate, hipStream_t st, std::string *err);
 
+// Largest dq-partial workspace the allocation-free backward serves from its
+// file-scope device array (8 MiB per device).
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+
+// launch_bwd (overwriting) with the dq partials in that device array instead
+// of a caller workspace; LRAR_EUNSUPPORTED when the problem needs more.
+// Allocates nothing; concurrent calls on one device race on the array.
+int launch_bwd_noalloc(const Problem &p, const void *dH, void *dV, void *dK, float *dq,
+                       hipStream_t st, std::string *err);
+
 // One residual site of block-source routing (see lr_attnres_block_route_fwd).
 struct BlockProblem {
     float *B;           // [nsrc][N][d] fp32 summary slots; slot nsrc-1 updated

@@ -40,7 +40,8 @@ def _declared_functions():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert names == sorted(["lr_attnres_route_fwd", "lr_attnres_route_bwd",
-                            "lr_attnres_route_bwd_accumulate", "lr_attnres_block_route_fwd",
+                            "lr_attnres_route_bwd_accumulate", "lr_attnres_route_bwd_noalloc",
+                            "lr_attnres_block_route_fwd",
                             "lr_attnres_block_route_bwd", "lr_attnres_block_inter_fwd",
                             "lr_attnres_block_merge_fwd", "lr_attnres_route_all_fwd",
                             "lr_attnres_key_proj_fwd", "lr_attnres_key_proj_bwd",
@@ -138,6 +139,39 @@ def test_backward_rejects(lib, name, kw, msg):
 def test_accumulating_backward_rejects(lib, name, kw, msg):
     assert bwd(lib, accumulate=True, **kw) == EINVAL
     assert msg in err(lib)
+
+
+def bwd_noalloc(lib, V=A, K=None, q=B, dH=C, dV=D, dK=None, dq=E, S=4, N=8, d=64, r=8, mode=SL,
+                dtype=BF16, eps=1e-6):
+    return lib.lr_attnres_route_bwd_noalloc(V, K, q, dH, dV, dK, dq, S, N, d, r, mode, dtype,
+                                            eps, None)
+
+
+NOALLOC_INVALID = [c for c in BWD_INVALID if "workspace" not in c[0]]
+
+
+@pytest.mark.parametrize("name,kw,msg", NOALLOC_INVALID, ids=[c[0] for c in NOALLOC_INVALID])
+def test_noalloc_backward_rejects(lib, name, kw, msg):
+    kw = {k: v for k, v in kw.items() if k not in ("ws", "wsb")}
+    assert bwd_noalloc(lib, **kw) == EINVAL
+    assert msg in err(lib)
+
+
+def test_noalloc_backward_limit(lib):
+    """Problems whose dq partials exceed the 8 MiB device array are refused
+    before any HIP call; the workspace query says how much they need."""
+    q = lib.lr_attnres_route_bwd_workspace_bytes
+    limit = 8 << 20
+    # projected r = 32 at d = 2048: two tokens per wave, 8 per workgroup
+    assert q(64, 1 << 19, 2048, 32, P, BF16) == limit
+    assert q(64, (1 << 19) + 8, 2048, 32, P, BF16) > limit
+    big = dict(mode=P, K=G, dK=G + 0x1_0000_0000, S=1, d=2048, r=32, N=(1 << 19) + 8)
+    assert bwd_noalloc(lib, **big) == EUNSUPPORTED
+    assert "8388608" in err(lib)
+    # full rank, d = 1024: four tokens per wave, 16 per workgroup
+    assert q(1, 32768, 1024, 1024, F, BF16) == limit
+    assert bwd_noalloc(lib, mode=F, S=1, d=1024, r=1024, N=32768 + 16) == EUNSUPPORTED
+    assert bwd_noalloc(lib, S=513) == EUNSUPPORTED
 
 
 def test_unsupported_shapes(lib):
