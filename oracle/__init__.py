@@ -57,10 +57,8 @@ def _load():
     lib.orc_block_num_sources.restype = ll
     lib.orc_block_route_fwd.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll]
     lib.orc_block_route_fwd.restype = ctypes.c_int
-    lib.orc_block_route_fwd2.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d, ll, ll, i]
-    lib.orc_block_route_fwd2.restype = ctypes.c_int
-    lib.orc_block_completed_bf16.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, ll, ll]
-    lib.orc_block_completed_bf16.restype = ctypes.c_int
+    lib.orc_block_summaries.argtypes = [vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, ll, ll]
+    lib.orc_block_summaries.restype = ctypes.c_int
     lib.orc_block_route_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, ll, ll, ll, ll, ll, i, i, d,
                                         ll, ll]
     lib.orc_block_route_bwd.restype = ctypes.c_int
@@ -89,6 +87,11 @@ def num_threads() -> int:
 def set_num_threads(n: int) -> None:
     """Threads of the oracle's later parallel regions (timing only)."""
     _load().orc_set_num_threads(int(n))
+
+
+def _eps(eps):
+    """eps as the kernels receive it: an fp32 value, widened exactly."""
+    return float(np.float32(eps))
 
 
 def _ptr(a):
@@ -126,7 +129,7 @@ def route_weights(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
     n1 = N if n1 is None else n1
     out = np.empty((n1 - n0, S), dtype=np.float64)
     rc = _load().orc_route_weights(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
-                                   _STORE[V.dtype], float(eps), n0, n1)
+                                   _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return out
@@ -138,7 +141,7 @@ def route_fwd(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
     n1 = N if n1 is None else n1
     out = np.empty((n1 - n0, d), dtype=np.float64)
     rc = _load().orc_route_fwd(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
-                               _STORE[V.dtype], float(eps), n0, n1)
+                               _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return out
@@ -160,7 +163,7 @@ def route_bwd(V, K, q, dH, mode, r=None, eps=1e-6, n0=0, n1=None):
     dK = np.empty((S, nt, r), dtype=np.float64) if mode == PROJECTED else None
     dq = np.empty((r,), dtype=np.float64)
     rc = _load().orc_route_bwd(_ptr(V), _ptr(K), _ptr(q), _ptr(dH), _ptr(dV), _ptr(dK),
-                               _ptr(dq), S, N, d, r, mode, _STORE[V.dtype], float(eps), n0, n1)
+                               _ptr(dq), S, N, d, r, mode, _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return dV, dK, dq
@@ -171,63 +174,55 @@ def block_num_sources(t: int, c: int) -> int:
     return _load().orc_block_num_sources(t, c)
 
 
-def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None,
-                    completed_bf16=False):
-    """Block-source forward at site t (Sec. 3.1 Eqs. block_attnres_sum /
-    block_attnres_partial_sum with the routing of Sec. 3.2).
-
-    O [t, N, d] holds o_0 .. o_{t-1}; KO [t, N, r] their projected keys (or
-    None for sliced keys).  Returns H [n1-n0, d] in fp64.  completed_bf16:
-    the completed block summaries (every slot but the last) are the fp32 sums
-    of their members in order, rounded once to bf16, as in
-    block_completed_bf16.
-    """
+def _block_prep(O, KO, t, mode, r):
     O = np.ascontiguousarray(O)
     if O.dtype not in _STORE or O.ndim != 3 or O.shape[0] < t:
         raise ValueError("oracle: O must be [>=t, N, d] in a supported storage")
     O = np.ascontiguousarray(O[:t])
-    _, N, d = O.shape
     if mode == PROJECTED:
         KO = np.ascontiguousarray(np.ascontiguousarray(KO)[:t])
         r = KO.shape[2]
     elif r is None:
         raise ValueError("oracle: sliced keys need r")
+    return O, KO, r
+
+
+def block_route_fwd(O, KO, q, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
+    """Block-source forward at site t (Sec. 3.1 Eqs. block_attnres_sum /
+    block_attnres_partial_sum with the routing of Sec. 3.2).
+
+    O [t, N, d] holds o_0 .. o_{t-1}; KO [t, N, r] their projected keys (or
+    None for sliced keys).  Returns H [n1-n0, d] in fp64.
+    """
+    O, KO, r = _block_prep(O, KO, t, mode, r)
+    _, N, d = O.shape
     q = np.ascontiguousarray(np.asarray(q, dtype=np.float64))
     n1 = N if n1 is None else n1
     out = np.empty((n1 - n0, d), dtype=np.float64)
-    rc = _load().orc_block_route_fwd2(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
-                                      _ptr(out), t, c, N, d, r, mode, _STORE[O.dtype],
-                                      float(eps), n0, n1, int(bool(completed_bf16)))
+    rc = _load().orc_block_route_fwd(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
+                                     _ptr(out), t, c, N, d, r, mode, _STORE[O.dtype],
+                                     _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid block problem")
     return out
 
 
-def block_completed_bf16(O, KO, t, c, mode, r=None, n0=0, n1=None):
-    """The completed block summaries that site t reads (every slot but the
-    last: S - 1 of them, S = block_num_sources(t, c)), each the fp32 sum of
-    its members in order rounded once to bf16 (nearest even); projected keys
-    the same.  Returns (B [S-1, n1-n0, d], KB [S-1, n1-n0, r] or None) as
-    fp64 arrays holding bf16 values."""
-    O = np.ascontiguousarray(O)
-    if O.dtype not in _STORE or O.ndim != 3 or O.shape[0] < t:
-        raise ValueError("oracle: O must be [>=t, N, d] in a supported storage")
-    O = np.ascontiguousarray(O[:t])
+def block_summaries(O, KO, t, c, mode, r=None, n0=0, n1=None):
+    """The block summaries site t reads (Sec. 3.1 Eqs. block_attnres_sum /
+    block_attnres_partial_sum), exact in fp64: slot 0 the embedding, slot j
+    the sum of block j's outputs written before site t.  Returns
+    (B [S, n1-n0, d], KB [S, n1-n0, r] or None), S = block_num_sources(t, c);
+    a projected summary's key is the sum of its members' keys."""
+    O, KO, r = _block_prep(O, KO, t, mode, r)
     _, N, d = O.shape
-    if mode == PROJECTED:
-        KO = np.ascontiguousarray(np.ascontiguousarray(KO)[:t])
-        r = KO.shape[2]
-    elif r is None:
-        raise ValueError("oracle: sliced keys need r")
     S = block_num_sources(t, c)
     n1 = N if n1 is None else n1
-    B = np.empty((S - 1, n1 - n0, d), dtype=np.float64)
-    KB = np.empty((S - 1, n1 - n0, r), dtype=np.float64) if mode == PROJECTED else None
-    rc = _load().orc_block_completed_bf16(_ptr(O), _ptr(KO if mode == PROJECTED else None),
-                                          _ptr(B), _ptr(KB), t, c, N, d, r, mode,
-                                          _STORE[O.dtype], n0, n1)
+    B = np.empty((S, n1 - n0, d), dtype=np.float64)
+    KB = np.empty((S, n1 - n0, r), dtype=np.float64) if mode == PROJECTED else None
+    rc = _load().orc_block_summaries(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(B),
+                                     _ptr(KB), t, c, N, d, r, mode, _STORE[O.dtype], n0, n1)
     if rc:
-        raise ValueError("oracle: invalid block problem (site t must have a completed slot)")
+        raise ValueError("oracle: invalid block problem")
     return B, KB
 
 
@@ -254,7 +249,7 @@ def block_route_bwd(O, KO, q, dH, t, c, mode, r=None, eps=1e-6, n0=0, n1=None):
     dq = np.empty((r,), dtype=np.float64)
     rc = _load().orc_block_route_bwd(_ptr(O), _ptr(KO if mode == PROJECTED else None), _ptr(q),
                                      _ptr(dH), _ptr(dO), _ptr(dKO), _ptr(dq), t, c, N, d, r,
-                                     mode, _STORE[O.dtype], float(eps), n0, n1)
+                                     mode, _STORE[O.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid block problem")
     return dO, dKO, dq
@@ -270,7 +265,7 @@ def route_state(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
     L = np.empty((n1 - n0,), dtype=np.float64)
     A = np.empty((n1 - n0, d), dtype=np.float64)
     rc = _load().orc_route_state(_ptr(V), _ptr(K), _ptr(q), _ptr(M), _ptr(L), _ptr(A), S, N, d,
-                                 r, mode, _STORE[V.dtype], float(eps), n0, n1)
+                                 r, mode, _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return M, L, A
@@ -283,7 +278,7 @@ def effective_sources(V, K, q, mode, r=None, eps=1e-6, n0=0, n1=None):
     n1 = N if n1 is None else n1
     out = np.empty((n1 - n0,), dtype=np.float64)
     rc = _load().orc_effective_sources(_ptr(V), _ptr(K), _ptr(q), _ptr(out), S, N, d, r, mode,
-                                       _STORE[V.dtype], float(eps), n0, n1)
+                                       _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return out
@@ -305,7 +300,7 @@ def route_all_fwd(V, K, Q, mode, first, r=None, eps=1e-6, n0=0, n1=None):
     H = np.empty((T, n1 - n0, d), dtype=np.float64)
     NEFF = np.empty((T, n1 - n0), dtype=np.float64)
     rc = _load().orc_route_all_fwd(_ptr(V), _ptr(K), _ptr(Q), _ptr(H), _ptr(NEFF), S, N, d, r,
-                                   first, T, mode, _STORE[V.dtype], float(eps), n0, n1)
+                                   first, T, mode, _STORE[V.dtype], _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return H, NEFF
@@ -332,7 +327,7 @@ def route_all_bwd(V, K, Q, dH, mode, first, r=None, eps=1e-6, n0=0, n1=None):
     dQ = np.empty((T, r), dtype=np.float64)
     rc = _load().orc_route_all_bwd(_ptr(V), _ptr(K), _ptr(Q), _ptr(dH), _ptr(dV), _ptr(dK),
                                    _ptr(dQ), S, N, d, r, first, T, mode, _STORE[V.dtype],
-                                   float(eps), n0, n1)
+                                   _eps(eps), n0, n1)
     if rc:
         raise ValueError("oracle: invalid problem")
     return dV, dK, dQ

@@ -342,123 +342,19 @@ long long orc_block_num_sources(long long t, long long c)
     return 1 + (t - 1) / c + ((t - 1) % c != 0);
 }
 
-/* Round-to-nearest-even of an fp32 value to bf16 (the upper 16 bits of the
- * fp32 pattern, with the discarded lower 16 bits deciding and ties going to
- * an even result), widened back to double.  Finite inputs only. */
-static double round_to_bf16(float x)
-{
-    uint32_t bits;
-    memcpy(&bits, &x, sizeof bits);
-    const uint32_t low = bits & 0xFFFFu, keep = bits >> 16;
-    uint32_t up = keep;
-    if (low > 0x8000u || (low == 0x8000u && (keep & 1u)))
-        up = keep + 1u;
-    const uint32_t out = up << 16;
-    float f;
-    memcpy(&f, &out, sizeof f);
-    return (double)f;
-}
-
 /* Slot of output i: 0 for the embedding, block ceil(i / c) otherwise. */
 static long long block_slot(long long i, long long c) { return i == 0 ? 0 : (i - 1) / c + 1; }
 
-/* Completed block summaries in the model's bf16 (a storage reading, not the
- * paper's): at site t every slot but the last (the one that receives
- * o_{t-1}) is complete, and its summary is the fp32 sum of its members in
- * their order (from the first member on), rounded once to bf16 (nearest
- * even); a projected key the same.  Writes those slots' rounded values (as doubles) into B [S][nt][d]
- * and KB [S][nt][r] (projected) for tokens [n0, n1); the last slot's rows
- * are left as they are. */
-static void round_completed_slots(const void *O, const void *KO, double *B, double *KB,
-                                  long long t, long long c, long long S, long long N,
-                                  long long d, long long r, int store, long long n0,
-                                  long long n1)
+/* The block summaries site t reads (Sec. 3.1, Eqs. block_attnres_sum and
+ * block_attnres_partial_sum), exact in double: slot 0 is the embedding o_0,
+ * slot j >= 1 the sum of the outputs of block j written before site t (the
+ * last slot may be partial).  B [S][nt][d] and KB [S][nt][r] (projected keys;
+ * else NULL) must be zero on entry; tokens [n0, n1), nt = n1 - n0. */
+static void block_sums(const void *O, const void *KO, double *B, double *KB, long long t,
+                       long long c, long long N, long long d, long long r, int store,
+                       long long n0, long long n1)
 {
     const long long nt = n1 - n0;
-    for (long long slot = 0; slot + 1 < S; ++slot) {
-        const long long first = slot == 0 ? 0 : (slot - 1) * c + 1;
-        const long long last = slot == 0 ? 0 : slot * c;  /* inclusive; < t - 1 here */
-        /* The sum starts from the first member (a one-member summary is
-         * that member, the sign of a zero included), then adds the others
-         * in order. */
-        for (long long n = n0; n < n1; ++n) {
-            for (long long j = 0; j < d; ++j) {
-                float acc = (float)widen(O, store, (first * N + n) * d + j);
-                for (long long i = first + 1; i <= last; ++i)
-                    acc += (float)widen(O, store, (i * N + n) * d + j);
-                B[(slot * nt + (n - n0)) * d + j] = round_to_bf16(acc);
-            }
-            if (KB)
-                for (long long j = 0; j < r; ++j) {
-                    float acc = (float)widen(KO, store, (first * N + n) * r + j);
-                    for (long long i = first + 1; i <= last; ++i)
-                        acc += (float)widen(KO, store, (i * N + n) * r + j);
-                    KB[(slot * nt + (n - n0)) * r + j] = round_to_bf16(acc);
-                }
-        }
-    }
-    (void)t;
-}
-
-/* The completed block summaries of site t (see round_completed_slots), for
- * tokens [n0, n1): B [S-1][n1-n0][d], KB [S-1][n1-n0][r] (projected, else
- * NULL), as doubles holding bf16 values.  S = orc_block_num_sources(t, c). */
-int orc_block_completed_bf16(const void *O, const void *KO, double *B, double *KB, long long t,
-                             long long c, long long N, long long d, long long r, int mode,
-                             int store, long long n0, long long n1)
-{
-    const long long S = orc_block_num_sources(t, c);
-    if (S < 2 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
-        B == NULL || (mode != ORC_KEYS_PROJECTED && mode != ORC_KEYS_SLICED) ||
-        (mode == ORC_KEYS_PROJECTED) != (KO != NULL) || (mode == ORC_KEYS_PROJECTED) != (KB != NULL) ||
-        store < 0 || store > 1)
-        return 1;
-    /* S slots of scratch, the last one unused, then copied out. */
-    const long long nt = n1 - n0;
-    double *Bs = (double *)calloc((size_t)(S * nt * d), sizeof(double));
-    double *KBs = KB ? (double *)calloc((size_t)(S * nt * r), sizeof(double)) : NULL;
-    if (Bs == NULL || (KB && KBs == NULL)) {
-        free(Bs);
-        free(KBs);
-        return 1;
-    }
-    round_completed_slots(O, KO, Bs, KBs, t, c, S, N, d, r, store, n0, n1);
-    memcpy(B, Bs, sizeof(double) * (size_t)((S - 1) * nt * d));
-    if (KB)
-        memcpy(KB, KBs, sizeof(double) * (size_t)((S - 1) * nt * r));
-    free(Bs);
-    free(KBs);
-    return 0;
-}
-
-/* Forward at site t: O is [t][N][d] (o_0 .. o_{t-1}), KO is [t][N][r]
- * (projected keys) or NULL.  H[n - n0][:] as in orc_route_fwd, with the
- * block summaries of the outputs as sources, for tokens [n0, n1).  The
- * summaries are formed in double; then the routing of Sec. 3.2 applies to
- * them unchanged (sliced keys: the tail of each summary).  completed_bf16:
- * the completed summaries (every slot but the last) are instead the bf16
- * roundings of round_completed_slots. */
-int orc_block_route_fwd2(const void *O, const void *KO, const double *q, double *H,
-                         long long t, long long c, long long N, long long d, long long r,
-                         int mode, int store, double eps, long long n0, long long n1,
-                         int completed_bf16)
-{
-    const long long S = orc_block_num_sources(t, c);
-    if (S < 1 || N < 0 || d < 1 || r < 1 || n0 < 0 || n1 < n0 || n1 > N || O == NULL ||
-        q == NULL || H == NULL || (mode != ORC_KEYS_PROJECTED && mode != ORC_KEYS_SLICED) ||
-        (mode == ORC_KEYS_PROJECTED) != (KO != NULL) || (mode == ORC_KEYS_SLICED && r > d) ||
-        store < 0 || store > 2)
-        return 1;
-    const long long nt = n1 - n0;
-    /* Summaries of the token range, double: B [S][nt][d], KB [S][nt][r]. */
-    double *B = (double *)calloc((size_t)(S * nt * d), sizeof(double));
-    double *KB = mode == ORC_KEYS_PROJECTED ? (double *)calloc((size_t)(S * nt * r), sizeof(double))
-                                            : NULL;
-    if (B == NULL || (mode == ORC_KEYS_PROJECTED && KB == NULL)) {
-        free(B);
-        free(KB);
-        return 1;
-    }
     for (long long i = 0; i < t; ++i) {
         /* output i belongs to slot 0 (embedding) or block ceil(i / c) */
         const long long slot = block_slot(i, c);
@@ -470,19 +366,63 @@ int orc_block_route_fwd2(const void *O, const void *KO, const double *q, double 
                     KB[(slot * nt + (n - n0)) * r + j] += widen(KO, store, (i * N + n) * r + j);
         }
     }
-    if (completed_bf16)
-        round_completed_slots(O, KO, B, KB, t, c, S, N, d, r, store, n0, n1);
-    const int rc = orc_route_fwd(B, KB, q, H, S, nt, d, r, mode, ORC_STORE_F64, eps, 0, nt);
-    free(B);
-    free(KB);
-    return rc;
 }
 
+static int block_args_ok(const void *O, const void *KO, long long S, long long N, long long d,
+                         long long r, int mode, int store, long long n0, long long n1)
+{
+    return S >= 1 && N >= 0 && d >= 1 && r >= 1 && n0 >= 0 && n1 >= n0 && n1 <= N &&
+           O != NULL && (mode == ORC_KEYS_PROJECTED || mode == ORC_KEYS_SLICED) &&
+           (mode == ORC_KEYS_PROJECTED) == (KO != NULL) &&
+           !(mode == ORC_KEYS_SLICED && r > d) && store >= 0 && store <= 2;
+}
+
+/* The summaries themselves (see block_sums): B [S][n1-n0][d], KB
+ * [S][n1-n0][r] for projected keys (else NULL), S = orc_block_num_sources(t, c).
+ * O is [t][N][d] (o_0 .. o_{t-1}), KO [t][N][r] or NULL. */
+int orc_block_summaries(const void *O, const void *KO, double *B, double *KB, long long t,
+                        long long c, long long N, long long d, long long r, int mode,
+                        int store, long long n0, long long n1)
+{
+    const long long S = orc_block_num_sources(t, c);
+    if (!block_args_ok(O, KO, S, N, d, r, mode, store, n0, n1) || B == NULL ||
+        (mode == ORC_KEYS_PROJECTED) != (KB != NULL))
+        return 1;
+    const long long nt = n1 - n0;
+    memset(B, 0, sizeof(double) * (size_t)(S * nt * d));
+    if (KB)
+        memset(KB, 0, sizeof(double) * (size_t)(S * nt * r));
+    block_sums(O, KO, B, KB, t, c, N, d, r, store, n0, n1);
+    return 0;
+}
+
+/* Forward at site t: O is [t][N][d] (o_0 .. o_{t-1}), KO is [t][N][r]
+ * (projected keys) or NULL.  H[n - n0][:] as in orc_route_fwd, with the
+ * block summaries of the outputs as sources, for tokens [n0, n1).  The
+ * summaries are formed in double; then the routing of Sec. 3.2 applies to
+ * them unchanged (sliced keys: the tail of each summary). */
 int orc_block_route_fwd(const void *O, const void *KO, const double *q, double *H,
                         long long t, long long c, long long N, long long d, long long r,
                         int mode, int store, double eps, long long n0, long long n1)
 {
-    return orc_block_route_fwd2(O, KO, q, H, t, c, N, d, r, mode, store, eps, n0, n1, 0);
+    const long long S = orc_block_num_sources(t, c);
+    if (!block_args_ok(O, KO, S, N, d, r, mode, store, n0, n1) || q == NULL || H == NULL)
+        return 1;
+    const long long nt = n1 - n0;
+    /* Summaries of the token range, double: B [S][nt][d], KB [S][nt][r]. */
+    double *B = (double *)calloc((size_t)(S * nt * d), sizeof(double));
+    double *KB = mode == ORC_KEYS_PROJECTED ? (double *)calloc((size_t)(S * nt * r), sizeof(double))
+                                            : NULL;
+    if (B == NULL || (mode == ORC_KEYS_PROJECTED && KB == NULL)) {
+        free(B);
+        free(KB);
+        return 1;
+    }
+    block_sums(O, KO, B, KB, t, c, N, d, r, store, n0, n1);
+    const int rc = orc_route_fwd(B, KB, q, H, S, nt, d, r, mode, ORC_STORE_F64, eps, 0, nt);
+    free(B);
+    free(KB);
+    return rc;
 }
 
 /* Backward of the block-source forward at site t for L = sum_n dH[n] . h[n]:
@@ -514,16 +454,7 @@ int orc_block_route_bwd(const void *O, const void *KO, const double *q, const vo
     int rc = 1;
     if (B == NULL || dHr == NULL || dB == NULL || (proj && (KB == NULL || dKB == NULL)))
         goto done;
-    for (long long i = 0; i < t; ++i) {
-        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
-        for (long long n = n0; n < n1; ++n) {
-            for (long long j = 0; j < d; ++j)
-                B[(slot * nt + (n - n0)) * d + j] += widen(O, store, (i * N + n) * d + j);
-            if (proj)
-                for (long long j = 0; j < r; ++j)
-                    KB[(slot * nt + (n - n0)) * r + j] += widen(KO, store, (i * N + n) * r + j);
-        }
-    }
+    block_sums(O, KO, B, KB, t, c, N, d, r, store, n0, n1);
     for (long long n = n0; n < n1; ++n)
         for (long long j = 0; j < d; ++j)
             dHr[(n - n0) * d + j] = widen(dH, store, n * d + j);
@@ -531,7 +462,7 @@ int orc_block_route_bwd(const void *O, const void *KO, const double *q, const vo
     if (rc)
         goto done;
     for (long long i = 0; i < t; ++i) {
-        const long long slot = i == 0 ? 0 : (i - 1) / c + 1;
+        const long long slot = block_slot(i, c);
         memcpy(dO + i * nt * d, dB + slot * nt * d, sizeof(double) * (size_t)(nt * d));
         if (proj)
             memcpy(dKO + i * nt * r, dKB + slot * nt * r, sizeof(double) * (size_t)(nt * r));

@@ -143,84 +143,69 @@ def _bits(x):
     return (np.asarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
 
 
-def test_completed_bf16_ties_and_nearest_by_hand(orc):
+def test_summaries_by_hand(orc):
     """Site t = 4 with blocks of c = 2 reads slot 0 = o_0, slot 1 = o_1 + o_2
-    (completed) and slot 2 = o_3 (the newest).  Column 0: 1 + 2^-8 lies
-    halfway between bf16 1 and 1 + 2^-7 and goes to 1 (even); column 1:
-    1 + 3 2^-8, halfway between 1 + 2^-7 and 1 + 2^-6, goes to 1 + 2^-6
-    (even); column 2: 1 + 5 2^-9 is nearest 1 + 2^-7.  With q = 0 the weights
-    are equal, so h is the mean of the three summaries."""
+    (completed) and slot 2 = o_3 (partial).  The sums are exact: 1 + 2^-8
+    and 1 + 5 2^-9 are not bf16 values, and the oracle does not round them.
+    With q = 0 the weights are equal, so h is the mean of the three."""
     O = _bits([[[0.5, 0.25, 2.0, 0.0]],
                [[1.0, 1.0, 1.0, 0.0]],
-               [[2.0 ** -8, 3 * 2.0 ** -8, 2.0 ** -9, 0.0]],
+               [[2.0 ** -8, 3 * 2.0 ** -8, 5 * 2.0 ** -9, 0.0]],
                [[4.0, 8.0, 0.0, 0.0]]])
-    O[2, 0, 2] = _bits(5 * 2.0 ** -9)  # 5 2^-9 = 1.25 2^-7 is a bf16 value
-    B, KB = orc.block_completed_bf16(O, None, 4, 2, SLICED, r=1)
-    assert KB is None and B.shape == (2, 1, 4)
-    assert B[1, 0, :3].tolist() == [1.0, 1.0 + 2.0 ** -6, 1.0 + 2.0 ** -7]
+    B, KB = orc.block_summaries(O, None, 4, 2, SLICED, r=1)
+    assert KB is None and B.shape == (3, 1, 4)
     assert B[0, 0].tolist() == [0.5, 0.25, 2.0, 0.0]
-    h = orc.block_route_fwd(O, None, np.zeros(1), 4, 2, SLICED, r=1, completed_bf16=True)
-    want = (B[0, 0] + B[1, 0] + np.array([4.0, 8.0, 0.0, 0.0])) / 3
-    np.testing.assert_allclose(h[0], want, rtol=0, atol=1e-15)
-    exact = orc.block_route_fwd(O, None, np.zeros(1), 4, 2, SLICED, r=1)
-    assert exact[0, 0] == pytest.approx((0.5 + 1.0 + 2.0 ** -8 + 4.0) / 3, abs=1e-15)
+    assert B[1, 0].tolist() == [1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 5 * 2.0 ** -9, 0.0]
+    assert B[2, 0].tolist() == [4.0, 8.0, 0.0, 0.0]
+    h = orc.block_route_fwd(O, None, np.zeros(1), 4, 2, SLICED, r=1)
+    np.testing.assert_allclose(h[0], B[:, 0].mean(axis=0), rtol=0, atol=1e-15)
 
 
-def test_completed_bf16_leaves_the_newest_slot_exact(orc):
-    """At site t = 3 with c = 2, slot 1 = o_1 + o_2 is full but it is the
-    slot that receives o_2, so it is read unrounded; slot 0 is the only
-    completed one."""
-    O = _bits([[[1.0]], [[1.0]], [[2.0 ** -8]]])
-    h = orc.block_route_fwd(O, None, np.zeros(1), 3, 2, SLICED, r=1, completed_bf16=True)
-    assert h[0, 0] == pytest.approx((1.0 + 1.0 + 2.0 ** -8) / 2, abs=1e-15)
-
-
-@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
-def test_completed_bf16_blocks_of_one_are_exact(orc, mode):
-    """With blocks of one output every completed summary is a single bf16
-    output, which rounds to itself: the result equals the exact one."""
-    p = make_host_problem(mode, 9, 5, 32, 8, dtype="bf16", seed=3, q_scale=4.0)
-    for t in (2, 5, 9):
-        a = orc.block_route_fwd(p.V, p.K, p.q, t, 1, mode, r=p.r, completed_bf16=True)
-        b = orc.block_route_fwd(p.V, p.K, p.q, t, 1, mode, r=p.r)
-        assert np.array_equal(a, b)
-
-
-def test_completed_bf16_projected_key_rounding_by_hand(orc):
-    """P-LR at t = 4, c = 2: the completed slot's key (1, 1 + 3 2^-8) rounds
-    to (1, 1 + 2^-6), which changes its score; the expected h is the plain
-    routing (the oracle's single-site forward, pinned on its own) over the
-    hand-rounded summaries."""
+def test_projected_summary_keys_by_hand(orc):
+    """P-LR at t = 4, c = 2: the completed slot's key is the sum of its two
+    members' keys, (1, 1 + 3 2^-8), kept exactly; h is the single-site
+    routing (pinned on its own) over the hand-summed sources."""
     O = _bits([[[1.0, 0.0]], [[0.0, 1.0]], [[2.0, 0.0]], [[0.0, 0.0]]])
     KO = _bits([[[1.0, 0.5]], [[1.0, 1.0]], [[0.0, 3 * 2.0 ** -8]], [[0.5, 1.0]]])
     q = np.array([0.7, -1.3])
     B = np.array([[[1.0, 0.0]], [[2.0, 1.0]], [[0.0, 0.0]]])
-    K = np.array([[[1.0, 0.5]], [[1.0, 1.0 + 2.0 ** -6]], [[0.5, 1.0]]])
+    K = np.array([[[1.0, 0.5]], [[1.0, 1.0 + 3 * 2.0 ** -8]], [[0.5, 1.0]]])
+    Bo, Ko = orc.block_summaries(O, KO, 4, 2, PROJECTED)
+    assert np.array_equal(Bo, B) and np.array_equal(Ko, K)
     want = orc.route_fwd(B, K, q, PROJECTED, eps=1e-6)
-    got = orc.block_route_fwd(O, KO, q, 4, 2, PROJECTED, completed_bf16=True)
+    got = orc.block_route_fwd(O, KO, q, 4, 2, PROJECTED)
     np.testing.assert_allclose(got, want, rtol=0, atol=1e-14)
-    KB = orc.block_completed_bf16(O, KO, 4, 2, PROJECTED)[1]
-    assert KB[1, 0].tolist() == [1.0, 1.0 + 2.0 ** -6]
-    exact = orc.block_route_fwd(O, KO, q, 4, 2, PROJECTED)
-    assert np.abs(exact - got).max() > 1e-4  # the rounding is visible
 
 
-def test_completed_bf16_token_ranges_compose(orc):
-    p = make_host_problem(SLICED, 20, 13, 48, 8, dtype="bf16", seed=8, q_scale=3.0)
-    full = orc.block_route_fwd(p.V, None, p.q, 20, 6, SLICED, r=8, completed_bf16=True)
-    part = np.concatenate([orc.block_route_fwd(p.V, None, p.q, 20, 6, SLICED, r=8, n0=a, n1=b,
-                                               completed_bf16=True)
-                           for a, b in ((0, 4), (4, 13))])
-    assert np.array_equal(full, part)
+@pytest.mark.parametrize("mode", [PROJECTED, SLICED])
+def test_summaries_of_blocks_of_one_are_the_outputs(orc, mode):
+    p = make_host_problem(mode, 9, 5, 32, 8, dtype="bf16", seed=3)
+    B, KB = orc.block_summaries(p.V, p.K, 9, 1, mode, r=p.r)
+    O = (p.V.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert np.array_equal(B, O)
+    if mode == PROJECTED:
+        assert np.array_equal(KB, (p.K.astype(np.uint32) << 16).view(np.float32))
 
 
-def test_completed_bf16_sum_starts_from_the_first_member(orc):
-    """A one-member block's summary is the member itself, a negative zero
-    included (0x8000); two members that cancel give +0 (an IEEE sum)."""
-    O = _bits([[[1.0, 2.0]], [[3.0, 5.0]], [[-3.0, 0.5]], [[0.0, 0.0]]])
-    O[0, 0, 0] = 0x8000          # -0.0 in the embedding (slot 0, one member)
-    B, _ = orc.block_completed_bf16(O, None, 4, 2, SLICED, r=1)
-    bits = (B.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
-    assert bits[0, 0, 0] == 0x8000                      # -0 kept
-    assert bits[1, 0, 0] == 0x0000                      # 3 + (-3) = +0
-    assert B[1, 0, 1] == 5.5
+@pytest.mark.parametrize("t,c", [(2, 3), (7, 3), (8, 3), (13, 4), (49, 6)])
+def test_summaries_partition_the_outputs(orc, t, c):
+    """Every output lands in exactly one slot: with small-integer outputs
+    (exact sums), the slots add up to the sum of all outputs, slot 0 is the
+    embedding, and the last slot holds the (t - 2) mod c + 1 newest ones."""
+    rng = np.random.default_rng(t * 10 + c)
+    O = _bits(rng.integers(-8, 9, size=(t, 3, 5)).astype(np.float32))
+    B, _ = orc.block_summaries(O, None, t, c, SLICED, r=2)
+    Of = (O.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert B.shape[0] == orc.block_num_sources(t, c)
+    assert np.array_equal(B.sum(axis=0), Of.sum(axis=0))
+    assert np.array_equal(B[0], Of[0])
+    k = (t - 2) % c + 1
+    assert np.array_equal(B[-1], Of[t - k:t].sum(axis=0))
+
+
+def test_summaries_token_ranges_compose(orc):
+    p = make_host_problem(PROJECTED, 20, 13, 48, 8, dtype="bf16", seed=8)
+    full = orc.block_summaries(p.V, p.K, 20, 6, PROJECTED)
+    parts = [orc.block_summaries(p.V, p.K, 20, 6, PROJECTED, n0=a, n1=b) for a, b in ((0, 4), (4, 13))]
+    for k in range(2):
+        assert np.array_equal(full[k], np.concatenate([x[k] for x in parts], axis=1))
