@@ -114,6 +114,24 @@ def test_forward_matches_oracle(dev, case):
     check_values("H", dtype, to_host(H), ref)
 
 
+def test_small_sliced_fp32_workload_seed0(dev):
+    """The small S-LR workload as specified: fp32, N = 256 tokens, d = 64,
+    r = 8, S = 8 sources, values ~ N(0, 1), q ~ N(0, 1/r), key = RMSNorm of
+    the last 8 coordinates (Sec. 3.4 Eq. sliced_key), unit gain, drawn with
+    numpy PCG64(0) in the order V, q, dH.  Forward and backward against the
+    oracle at the fp32 bar."""
+    p = make_host_problem(SLICED, 8, 256, 64, 8, dtype="f32", seed=0, with_dH=True)
+    V, q, dH = to_dev(p.V, dev), to_dev(p.q, dev), to_dev(p.dH, dev)
+    H = lr.route_fwd(V, None, q, SLICED)
+    dV, dK, dq = lr.route_bwd(V, None, q, dH, SLICED)
+    torch.cuda.synchronize()
+    assert dK is None
+    check_f32("H", to_host(H), oracle.route_fwd(p.V, None, p.q, SLICED, r=8))
+    dV_ref, _, dq_ref = oracle.route_bwd(p.V, None, p.q, p.dH, SLICED, r=8)
+    check_f32("dV", to_host(dV), dV_ref)
+    check_dq("dq", to_host(dq), dq_ref, tol=1e-5)
+
+
 @pytest.mark.parametrize("case", CASES, ids=_id)
 def test_backward_matches_oracle(dev, case):
     mode, dtype, S, N, d, r = case
