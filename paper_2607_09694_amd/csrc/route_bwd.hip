@@ -102,8 +102,9 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
     }
     const size_t plane = (size_t)N * d;
 
+    const int bx = blockIdx.x;
     for (int t = 0; t < tpw; ++t) {
-        const int n = (blockIdx.x * tpw + t) * kWaves + wave;
+        const int n = (bx * tpw + t) * kWaves + wave;
         if (n >= N)
             break;  // wave-uniform; the workgroup barrier below is outside the loop
         lr_scores<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s, rho);
@@ -327,7 +328,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
         float sum = 0.0f;
         for (int w = 0; w < kWaves; ++w)
             sum += stage[w * r_pad + j];
-        partial[(size_t)blockIdx.x * r + j] = sum;
+        partial[(size_t)bx * r + j] = sum;
     }
 }
 
@@ -365,8 +366,9 @@ route_bwd_full(const T *__restrict__ V, const float *__restrict__ q, const T *__
     const size_t plane = (size_t)N * d;
     const float inv_d = 1.0f / (float)d;
 
+    const int bx = blockIdx.x;
     for (int t = 0; t < tpw; ++t) {
-        const int n = (blockIdx.x * tpw + t) * kWaves + wave;
+        const int n = (bx * tpw + t) * kWaves + wave;
         if (n >= N)
             break;  // wave-uniform; the workgroup barriers are after the loop
         float dh[NCH][VEC];
@@ -471,7 +473,7 @@ route_bwd_full(const T *__restrict__ V, const float *__restrict__ q, const T *__
         __syncthreads();
     }
     for (int j = threadIdx.x; j < d; j += kBlock)
-        partial[(size_t)blockIdx.x * d + j] = stage[j];
+        partial[(size_t)bx * d + j] = stage[j];
 }
 
 // dq[j] = sum_b partial[b][j] in a fixed order: one workgroup per column;

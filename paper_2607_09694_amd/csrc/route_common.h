@@ -57,6 +57,27 @@ __device__ __forceinline__ void lds_barrier()
     asm volatile("" ::: "memory");
 }
 
+// The workgroup a launched one stands for, so that each of the 8 XCDs of
+// the chip holds one contiguous range of the grid (row-major linear index
+// x + y * gridDim.x).  The hardware deals workgroups to the XCDs round-robin
+// (linear index mod 8); remapped, the rows an XCD reads at one time come
+// from one token range of each source plane.  Streams over the planes ran
+// about 10% faster this way on MI355X (reads of 49 planes at d = 1024:
+// 6.2 -> 6.9 TB/s).  A bijection of the grid for any size.
+constexpr int kXcds = 8;
+struct BlockXY {
+    int x, y;
+};
+__device__ __forceinline__ BlockXY xcd_block()
+{
+    const int nx = (int)gridDim.x, total = nx * (int)gridDim.y;
+    const int b = (int)blockIdx.x + (int)blockIdx.y * nx;
+    const int xcd = b % kXcds, i = b / kXcds;
+    const int full = total / kXcds, rem = total % kXcds;
+    const int m = xcd * full + min(xcd, rem) + i;
+    return BlockXY{m % nx, m / nx};
+}
+
 template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
 // Sources loaded ahead in the backward stream (divides 8, the number of
 // sources per batched reduction of the dots dH . o_i).
@@ -65,6 +86,45 @@ template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 8 ? 
 // chunks per lane: two for rows of 4+ chunks (d >= 2048 bf16), else one
 // (measured on MI355X at d = 1024 and 2048).
 constexpr int bwd_tokens_per_wave(int nch) { return nch >= 4 ? 2 : 1; }
+
+// Tokens per wave (TW) and sources per load batch (SB) of the forward of
+// projected / sliced keys.  A wave owns TW consecutive tokens, whose rows are
+// adjacent in every source plane, and each round trip loads SB sources
+// across them: SB plane visits of TW * 2d contiguous bytes.  Measured on
+// MI355X (49 planes, d = 1024, cold), the shape of that batch sets the read
+// rate: 2 tokens x 1 source ran at 6.5 TB/s, 1 token x 4 sources at 6.1,
+// and keeping a second batch in flight (two register buffers) was slower
+// in every shape tried.
+#ifndef LRAR_FWD_TW_NARROW
+#define LRAR_FWD_TW_NARROW 2  // rows of at most 2 chunks per lane (d <= 1024 bf16)
+#endif
+#ifndef LRAR_FWD_SB_NARROW
+#define LRAR_FWD_SB_NARROW 1
+#endif
+#ifndef LRAR_FWD_TW_WIDE
+#define LRAR_FWD_TW_WIDE 2    // rows of 4 chunks (d <= 2048 bf16)
+#endif
+#ifndef LRAR_FWD_SB_WIDE
+#define LRAR_FWD_SB_WIDE 1
+#endif
+constexpr int fwd_tokens_per_wave(int nch)
+{
+    return nch <= 2 ? LRAR_FWD_TW_NARROW : nch == 4 ? LRAR_FWD_TW_WIDE : 1;
+}
+constexpr int fwd_sources_per_batch(int nch)
+{
+    return nch <= 2 ? LRAR_FWD_SB_NARROW : nch == 4 ? LRAR_FWD_SB_WIDE : 1;
+}
+#ifndef LRAR_FWD_LPR_NARROW
+#define LRAR_FWD_LPR_NARROW 2
+#endif
+#ifndef LRAR_FWD_LPR_WIDE
+#define LRAR_FWD_LPR_WIDE 2
+#endif
+constexpr int fwd_loads_per_trip(int nch)
+{
+    return nch <= 2 ? LRAR_FWD_LPR_NARROW : nch == 4 ? LRAR_FWD_LPR_WIDE : 2;
+}
 
 // ---------------------------------------------------------------------------
 // Scores and softmax (Eqs. lr_key_norm and lr_attnres_weight)
@@ -89,6 +149,54 @@ __device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__r
         lps <<= 1;
     const int spi = kWaveSize / lps;
     const int isub = lane / lps, v = lane % lps;
+    if (nkv <= lps) {
+        // At most one key vector per lane and source: the loads of KP
+        // groups of sources go out together (sources past S re-read source
+        // S-1 and lanes past the key re-read its last vector; neither
+        // counts), then the scores of the KP groups are formed.
+        constexpr int KP = 4;
+        typedef typename Raw<T, KV>::type raw_t;
+        const bool vok = v < nkv;
+        const int vv = min(v, nkv - 1);
+        float qv[KV];
+#pragma unroll
+        for (int e = 0; e < KV; ++e)
+            qv[e] = vok ? q[vv * KV + e] : 0.0f;
+        for (int i0 = 0; i0 < S; i0 += KP * spi) {
+            raw_t kr[KP];
+#pragma unroll
+            for (int p = 0; p < KP; ++p) {
+                const int i = min(i0 + p * spi + isub, S - 1);
+                kr[p] = load_raw<T, KV>(keys + ((size_t)i * N + n) * krow + koff + vv * KV);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int p = 0; p < KP; ++p) {
+                float x[KV];
+                widen(kr[p], x);
+                float ss = 0.0f, dot = 0.0f;
+#pragma unroll
+                for (int e = 0; e < KV; ++e) {
+                    ss = fmaf(x[e], x[e], ss);
+                    dot = fmaf(qv[e], x[e], dot);
+                }
+                if (!vok)
+                    ss = dot = 0.0f;
+                for (int m = 1; m < lps; m <<= 1) {
+                    ss += __shfl_xor(ss, m, kWaveSize);
+                    dot += __shfl_xor(dot, m, kWaveSize);
+                }
+                const int i = i0 + p * spi + isub;
+                if (v == 0 && i < S) {
+                    const float rho = sqrtf(ss / (float)r + eps);
+                    s_out[i] = dot / rho;
+                    if (rho_out)
+                        rho_out[i] = rho;
+                }
+            }
+        }
+        return;
+    }
     for (int i0 = 0; i0 < S; i0 += spi) {
         const int i = i0 + isub;
         float ss = 0.0f, dot = 0.0f;
@@ -128,6 +236,87 @@ __device__ inline void lr_scores(const T *__restrict__ keys, const float *__rest
         lr_scores_kv<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
     else
         lr_scores_kv<T, 1>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
+    wave_lds_sync();
+}
+
+// Scores of the TW consecutive tokens n0 .. n0+TW-1 into s_out[t * s_pad + i]
+// (tokens at or past N are read as token N-1 and not written).  With at most
+// one key vector per lane and source, the key loads of all TW tokens and KP
+// groups of sources go out together; otherwise token by token.
+template <typename T, int KV, int TW>
+__device__ inline void lr_scores_tokens_kv(const T *__restrict__ keys, const float *__restrict__ q,
+                                           int S, int N, int r, int krow, int koff, float eps,
+                                           int n0, int lane, float *s_out, int s_pad)
+{
+    const int nkv = r / KV;
+    int lps = 1;
+    while (lps < nkv && lps < kWaveSize)
+        lps <<= 1;
+    if (nkv > lps) {
+        for (int t = 0; t < TW; ++t)
+            if (n0 + t < N)
+                lr_scores_kv<T, KV>(keys, q, S, N, r, krow, koff, eps, n0 + t, lane,
+                                    s_out + t * s_pad, nullptr);
+        return;
+    }
+    constexpr int KP = TW >= 4 ? 1 : TW == 2 ? 2 : 4;
+    typedef typename Raw<T, KV>::type raw_t;
+    const int spi = kWaveSize / lps;
+    const int isub = lane / lps, v = lane % lps;
+    const bool vok = v < nkv;
+    const int vv = min(v, nkv - 1);
+    float qv[KV];
+#pragma unroll
+    for (int e = 0; e < KV; ++e)
+        qv[e] = vok ? q[vv * KV + e] : 0.0f;
+    for (int i0 = 0; i0 < S; i0 += KP * spi) {
+        raw_t kr[TW][KP];
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int n = min(n0 + t, N - 1);
+#pragma unroll
+            for (int p = 0; p < KP; ++p) {
+                const int i = min(i0 + p * spi + isub, S - 1);
+                kr[t][p] = load_raw<T, KV>(keys + ((size_t)i * N + n) * krow + koff + vv * KV);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+#pragma unroll
+            for (int p = 0; p < KP; ++p) {
+                float x[KV];
+                widen(kr[t][p], x);
+                float ss = 0.0f, dot = 0.0f;
+#pragma unroll
+                for (int e = 0; e < KV; ++e) {
+                    ss = fmaf(x[e], x[e], ss);
+                    dot = fmaf(qv[e], x[e], dot);
+                }
+                if (!vok)
+                    ss = dot = 0.0f;
+                for (int m = 1; m < lps; m <<= 1) {
+                    ss += __shfl_xor(ss, m, kWaveSize);
+                    dot += __shfl_xor(dot, m, kWaveSize);
+                }
+                const int i = i0 + p * spi + isub;
+                if (v == 0 && i < S && n0 + t < N)
+                    s_out[t * s_pad + i] = dot / sqrtf(ss / (float)r + eps);
+            }
+        }
+    }
+}
+
+template <typename T, int VEC, int TW>
+__device__ inline void lr_scores_tokens(const T *__restrict__ keys, const float *__restrict__ q,
+                                        int S, int N, int r, int krow, int koff, float eps,
+                                        int n0, int lane, float *s_out, int s_pad)
+{
+    if (VEC > 1 && r % VEC == 0 && krow % VEC == 0 && koff % VEC == 0)
+        lr_scores_tokens_kv<T, VEC, TW>(keys, q, S, N, r, krow, koff, eps, n0, lane, s_out,
+                                        s_pad);
+    else
+        lr_scores_tokens_kv<T, 1, TW>(keys, q, S, N, r, krow, koff, eps, n0, lane, s_out, s_pad);
     wave_lds_sync();
 }
 
@@ -183,6 +372,10 @@ __device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t pla
                 if (FULLCOLS || ok[c])
                     raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + (size_t)(i + u) * plane +
                                                              c * kWaveSize * VEC);
+        // Keep the batch's loads together ahead of their uses: without this
+        // the scheduler sinks each load next to its first use, leaving one
+        // source's row in flight at a time.
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const float a = alpha[i + u];
@@ -211,6 +404,87 @@ __device__ __forceinline__ void mix_rows(const T *__restrict__ vbase, size_t pla
                     acc[c][e] = fmaf(a, x[e], acc[c][e]);
             }
         }
+    }
+}
+
+// The same stream with two batches of U sources in registers: the loads of
+// batch b + 1 are issued before batch b is multiplied, so a wave keeps
+// between U and 2U rows in flight instead of draining to none between
+// batches.  Batch 0 is loaded by the caller into ra (mix_batch_load), which
+// lets it go out before the scores are known.  Loads past the last source
+// re-read source S-1 (the same lines, in flight together; no HBM traffic of
+// their own) and are not accumulated: with every load unconditional, the
+// compiler's wait counts leave the newer batch in flight while the older
+// one is used.  Sums in source order, like mix_rows (bit-identical).
+template <typename T, int VEC, int NCH, bool FULLCOLS, int U>
+__device__ __forceinline__ void mix_batch_load(typename Raw<T, VEC>::type (&r)[U][NCH],
+                                               const T *__restrict__ vbase, size_t plane, int i,
+                                               int S, const bool (&ok)[NCH])
+{
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int src = min(i + u, S - 1);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+            if (FULLCOLS || ok[c])
+                r[u][c] = load_stream<T, VEC, kNtLoad>(vbase + (size_t)src * plane +
+                                                       c * kWaveSize * VEC);
+    }
+}
+
+template <typename T, int VEC, int NCH, bool FULLCOLS, int U>
+__device__ __forceinline__ void mix_batch_fma(const typename Raw<T, VEC>::type (&r)[U][NCH],
+                                              const float *alpha, int i, int S,
+                                              const bool (&ok)[NCH], float (&acc)[NCH][VEC])
+{
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (i + u < S) {
+            const float a = alpha[i + u];
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                if (FULLCOLS || ok[c]) {
+                    float x[VEC];
+                    widen(r[u][c], x);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e)
+                        acc[c][e] = fmaf(a, x[e], acc[c][e]);
+                }
+            }
+        }
+    }
+}
+
+template <typename T, int VEC, int NCH, bool FULLCOLS, int U>
+__device__ __forceinline__ void mix_rows_pipelined(typename Raw<T, VEC>::type (&ra)[U][NCH],
+                                                   const T *__restrict__ vbase, size_t plane,
+                                                   int S, const float *alpha,
+                                                   const bool (&ok)[NCH], float (&acc)[NCH][VEC])
+{
+    typename Raw<T, VEC>::type rb[U][NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            acc[c][e] = 0.0f;
+    // ra holds batch 0 (sources 0 .. U-1) on entry; nb batches in all.
+    const int nb = (S + U - 1) / U;
+    int b = 0;
+    for (; b + 2 < nb; b += 2) {
+        mix_batch_load<T, VEC, NCH, FULLCOLS, U>(rb, vbase, plane, (b + 1) * U, S, ok);
+        __builtin_amdgcn_sched_barrier(0);
+        mix_batch_fma<T, VEC, NCH, FULLCOLS, U>(ra, alpha, b * U, S, ok, acc);
+        mix_batch_load<T, VEC, NCH, FULLCOLS, U>(ra, vbase, plane, (b + 2) * U, S, ok);
+        __builtin_amdgcn_sched_barrier(0);
+        mix_batch_fma<T, VEC, NCH, FULLCOLS, U>(rb, alpha, (b + 1) * U, S, ok, acc);
+    }
+    if (b + 1 < nb) {
+        mix_batch_load<T, VEC, NCH, FULLCOLS, U>(rb, vbase, plane, (b + 1) * U, S, ok);
+        __builtin_amdgcn_sched_barrier(0);
+        mix_batch_fma<T, VEC, NCH, FULLCOLS, U>(ra, alpha, b * U, S, ok, acc);
+        mix_batch_fma<T, VEC, NCH, FULLCOLS, U>(rb, alpha, (b + 1) * U, S, ok, acc);
+    } else {
+        mix_batch_fma<T, VEC, NCH, FULLCOLS, U>(ra, alpha, b * U, S, ok, acc);
     }
 }
 

@@ -8,33 +8,105 @@ namespace lrar {
 // Forward kernels
 // ---------------------------------------------------------------------------
 
-// Projected / sliced keys.  Grid: x = token groups of kWaves, y = column
-// blocks of NCH*64*VEC (more than one only for very wide rows; each column
-// block recomputes the cheap r-dimensional scores).
+// Projected / sliced keys.  Grid: x = token groups of kWaves * TW, y =
+// column blocks of NCH*64*VEC (more than one only for very wide rows; each
+// column block recomputes the cheap r-dimensional scores).  Wave w owns the
+// TW consecutive tokens n0 = (x * kWaves + w) * TW ..: it scores them, takes
+// each token's softmax into its own LDS slice, and streams the sources in
+// batches of SB, each batch loading the SB sources' rows of all TW tokens
+// (adjacent in each source plane) before accumulating them.  Tokens past N
+// re-read row N-1 and are not stored; sources past S re-read source S-1
+// (the same lines, in flight together) and are not accumulated.
 template <typename T, int VEC, int NCH, bool FULLCOLS>
 __global__ void __launch_bounds__(kBlock)
 route_fwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *__restrict__ q,
              T *__restrict__ H, int S, int N, int d, int r, int krow, int koff, float eps,
              int s_pad)
 {
+    constexpr int TW = fwd_tokens_per_wave(NCH);
+    constexpr int SB = fwd_sources_per_batch(NCH);
+    typedef typename Raw<T, VEC>::type raw_t;
     extern __shared__ float lds[];
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
-    const int n = blockIdx.x * kWaves + wave;
-    if (n >= N)
+    const int n0 = ((int)blockIdx.x * kWaves + wave) * TW;
+    if (n0 >= N)
         return;  // wave-uniform; this kernel has no workgroup barrier
-    float *alpha = lds + wave * s_pad;
-    lr_scores<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, alpha, nullptr);
-    depth_softmax(alpha, alpha, S, lane);
-
     const int col = blockIdx.y * (NCH * kWaveSize * VEC) + lane * VEC;
     bool ok[NCH];
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
         ok[c] = col + c * kWaveSize * VEC < d;
-    float acc[NCH][VEC];
-    mix_rows<T, VEC, NCH, FULLCOLS>(V + (size_t)n * d + col, (size_t)N * d, S, alpha, ok, acc);
-    store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)n * d + col, ok, acc);
+    const size_t plane = (size_t)N * d;
+    const T *rows[TW];
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+        rows[t] = V + (size_t)min(n0 + t, N - 1) * d + col;
+    float *s = lds + wave * TW * s_pad;
+
+    // One batch is SB sources x TW tokens x NCH column chunks, LPR of whose
+    // 16-byte loads are in flight at a time: each group of LPR loads is
+    // issued, then accumulated, before the next group goes out.
+    constexpr int UNITS = SB * TW * NCH;
+    constexpr int LPR = fwd_loads_per_trip(NCH) < UNITS ? fwd_loads_per_trip(NCH) : UNITS;
+    raw_t rr[LPR];
+    auto load = [&](int i0, int g) {
+#pragma unroll
+        for (int k = 0; k < LPR; ++k) {
+            const int unit = g + k;
+            const int u = unit / (TW * NCH), t = (unit / NCH) % TW, c = unit % NCH;
+            if (unit < UNITS && (FULLCOLS || ok[c]))
+                rr[k] = load_stream<T, VEC, kNtLoad>(rows[t] + (size_t)min(i0 + u, S - 1) * plane +
+                                                     c * kWaveSize * VEC);
+        }
+    };
+    float acc[TW][NCH][VEC];
+    auto fma = [&](int i0, int g) {
+#pragma unroll
+        for (int k = 0; k < LPR; ++k) {
+            const int unit = g + k;
+            const int u = unit / (TW * NCH), t = (unit / NCH) % TW, c = unit % NCH;
+            if (unit < UNITS && i0 + u < S && (FULLCOLS || ok[c])) {
+                const float a = s[t * s_pad + i0 + u];
+                float x[VEC];
+                widen(rr[k], x);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    acc[t][c][e] = fmaf(a, x[e], acc[t][c][e]);
+            }
+        }
+    };
+
+    // The first group does not depend on the scores: its loads go out before
+    // the key loads, so the two round trips overlap.
+    load(0, 0);
+    lr_scores_tokens<T, VEC, TW>(keys, q, S, N, r, krow, koff, eps, n0, lane, s, s_pad);
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+        if (n0 + t < N)
+            depth_softmax(s + t * s_pad, s + t * s_pad, S, lane);
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                acc[t][c][e] = 0.0f;
+    for (int i0 = 0; i0 < S; i0 += SB) {
+#pragma unroll
+        for (int g = 0; g < UNITS; g += LPR) {
+            if (i0 > 0 || g > 0)
+                load(i0, g);
+            // The group's loads stay together ahead of their uses.
+            __builtin_amdgcn_sched_barrier(0);
+            fma(i0, g);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < TW; ++t)
+        if (n0 + t < N)
+            store_row<T, VEC, NCH, FULLCOLS>(H + (size_t)(n0 + t) * d + col, ok, acc[t]);
 }
 
 // fp32 row segment of VEC values.
@@ -351,7 +423,9 @@ route_fwd_full_1p(const T *__restrict__ V, const float *__restrict__ q, T *__res
     typedef typename Raw<T, VEC>::type raw_t;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = threadIdx.x / kWaveSize;
-    const int n = KIND == kFullWg ? (int)blockIdx.x : (int)blockIdx.x * kWaves + wave;
+    const int n = KIND == kFullWg ? (int)blockIdx.x
+                  : KIND == kFullH ? xcd_block().x * kWaves + wave
+                                   : (int)blockIdx.x * kWaves + wave;
     if (KIND != kFullWg && n >= N)
         return;  // wave-uniform; no workgroup barrier on this path
 
@@ -503,8 +577,10 @@ hipError_t launch_fwd_t(const Problem &p, const Plan &pl, void *H, hipStream_t s
                                (int)p.S, (int)p.N, (int)p.d, (int)p.r, krow, koff, p.eps,
                                pl.s_pad);
         } else {
-            hipLaunchKernelGGL((route_fwd_lr<T, VEC, NCH, FC>), dim3(pl.nblocks, pl.ysplit),
-                               dim3(kBlock), pl.lds, st, V, keys, p.q, static_cast<T *>(H),
+            constexpr int TW = fwd_tokens_per_wave(NCH);
+            const int nb = (int)((p.N + kWaves * TW - 1) / (kWaves * TW));
+            hipLaunchKernelGGL((route_fwd_lr<T, VEC, NCH, FC>), dim3(nb, pl.ysplit),
+                               dim3(kBlock), pl.lds * TW, st, V, keys, p.q, static_cast<T *>(H),
                                (int)p.S, (int)p.N, (int)p.d, (int)p.r, krow, koff, p.eps,
                                pl.s_pad);
         }

@@ -84,7 +84,8 @@ bool make_plan(const Problem &p, bool bwd, Plan *pl, std::string *why)
     if (!bwd) {
         pl->nblocks = (int)((p.N + kWaves - 1) / kWaves);
         // The low-rank forward keeps the weights in LDS; the full-rank one
-        // holds its online-softmax state in registers.
+        // holds its online-softmax state in registers.  (The plan is that of
+        // one token per wave; route_fwd_lr's launch scales it to its TW.)
         pl->lds = p.mode == LRAR_MODE_FULL ? 0 : (size_t)kWaves * pl->s_pad * sizeof(float);
     } else {
         pl->tpw = p.mode == LRAR_MODE_FULL ? 4 : bwd_tokens_per_wave(pl->nch);
