@@ -65,7 +65,8 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
     float *__restrict__ coef = dfo.coef;
     extern __shared__ float lds[];
     const int lane = threadIdx.x & (kWaveSize - 1);
-    const int wave = threadIdx.x / kWaveSize;
+    // wave-uniform (scalar): the stream's buffer descriptors depend on it
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
     float *s = lds + (4 * wave + 0) * s_pad;
     float *rho = lds + (4 * wave + 1) * s_pad;
     float *alpha = lds + (4 * wave + 2) * s_pad;
@@ -126,33 +127,60 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
         const T *vbase = V + (size_t)n * d + col;
         T *dvbase = dV + (size_t)n * d + col;
         constexpr int L = BwdInflight<NCH>::value;
+        // With 16-byte vectors every access of the stream goes through a
+        // per-row buffer resource: source i's value row (no bytes past the
+        // last source) and its gradient row (bytes up to the key tail, none
+        // when the source takes no gradient row here).  Lanes past the row
+        // end and sources past S read zeros and store nothing, with no branch
+        // around any access, so the compiler's wait counts let the stores and
+        // the next loads stay in flight.  Scalar rows keep guarded accesses.
+        constexpr bool BUF = VEC > 1;
         for (int i0 = 0; i0 < S; i0 += 8) {
             float part[8];
 #pragma unroll
             for (int h = 0; h < 8; h += L) {
                 raw_t raw[L][NCH], old[ACC ? L : 1][NCH];
+                __amdgpu_buffer_rsrc_t rv[L], rd[L];
 #pragma unroll
-                for (int u = 0; u < L; ++u)
-                    if (i0 + h + u < S)
+                for (int u = 0; u < L; ++u) {
+                    const int i = i0 + h + u;
+                    const bool live = i < S;
+                    const bool takes = live && (!DEFER || (!DALL && i == S - 1));
+                    if constexpr (BUF) {
+                        const size_t ic = (size_t)min(i, S - 1);  // in-range base
+                        rv[u] = row_rsrc(V + (ic * N + n) * d, live ? d * (int)sizeof(T) : 0);
+                        // every source of a fully deferred step takes no row (dV may be NULL)
+                        rd[u] = row_rsrc(DALL ? nullptr : dV + (DEFER ? (size_t)n : ic * N + n) * d,
+                                         takes ? tail_start * (int)sizeof(T) : 0);
+#pragma unroll
+                        for (int c = 0; c < NCH; ++c) {
+                            const int off = (col + c * kWaveSize * VEC) * (int)sizeof(T);
+                            raw[u][c] = buffer_load16<T, VEC, kBwdNtLoad>(rv[u], off);
+                            if constexpr (ACC)
+                                old[u][c] = buffer_load16<T, VEC, kBwdNtLoad>(rd[u], off);
+                        }
+                    } else if (live) {
 #pragma unroll
                         for (int c = 0; c < NCH; ++c)
                             if (FULLCOLS || ok[c]) {
-                                const size_t off = (size_t)(i0 + h + u) * plane + c * kWaveSize * VEC;
+                                const size_t off = (size_t)i * plane + c * kWaveSize * VEC;
                                 raw[u][c] = load_stream<T, VEC, kNtLoad>(vbase + off);
                                 if constexpr (ACC)
-                                    if (wr[c] && (!DEFER || (!DALL && i0 + h + u == S - 1)))
+                                    if (wr[c] && takes)
                                         old[u][c] = load_stream<T, VEC, kNtLoad>(
                                             dvbase + (DEFER ? c * kWaveSize * VEC : off));
                             }
+                    }
+                }
 #pragma unroll
                 for (int u = 0; u < L; ++u) {
                     float p = 0.0f;
                     const int i = i0 + h + u;
-                    if (i < S) {
-                        const float a = alpha[i];
+                    if (BUF || i < S) {
+                        const float a = i < S ? alpha[min(i, S - 1)] : 0.0f;
 #pragma unroll
                         for (int c = 0; c < NCH; ++c) {
-                            if (FULLCOLS || ok[c]) {
+                            if (BUF || FULLCOLS || ok[c]) {
                                 float x[VEC], y[VEC];
                                 widen(raw[u][c], x);
 #pragma unroll
@@ -160,14 +188,22 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                                     p = fmaf(dh[c][e], x[e], p);
                                     y[e] = a * dh[c][e];
                                 }
-                                const bool wdv = wr[c] && (!DEFER || (!DALL && i == S - 1));
-                                if constexpr (ACC)
-                                    if (wdv)
+                                const bool wdv = wr[c] && i < S && (!DEFER || (!DALL && i == S - 1));
+                                if constexpr (BUF) {
+                                    if constexpr (ACC)
                                         add_stored(y, old[u][c]);
-                                if (wdv)
-                                    store_stream<T, VEC, kNtStore>(
-                                        dvbase + (DEFER ? 0 : (size_t)i * plane) + c * kWaveSize * VEC,
+                                    buffer_store16<T, VEC, kBwdNtStore>(
+                                        rd[u], (col + c * kWaveSize * VEC) * (int)sizeof(T),
                                         Narrow<T, VEC>::run(y));
+                                } else {
+                                    if constexpr (ACC)
+                                        if (wdv)
+                                            add_stored(y, old[u][c]);
+                                    if (wdv)
+                                        store_stream<T, VEC, kNtStore>(
+                                            dvbase + (DEFER ? 0 : (size_t)i * plane) + c * kWaveSize * VEC,
+                                            Narrow<T, VEC>::run(y));
+                                }
                                 if constexpr (DEFER && !DALL) {
                                     if (wdv) {
                                         // retire: dO = the new running row;
@@ -188,6 +224,12 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
                     }
                     part[h + u] = p;
                 }
+                // One step of L sources at a time: the dots of this step are
+                // formed before the next step's loads go out, so at most one
+                // step's rows are in flight per wave.
+#pragma unroll
+                for (int u = 0; u < L; ++u)
+                    asm volatile("" : "+v"(part[h + u])::"memory");
             }
             const float tot = multi_sum<8>(part, lane);
             const int idx = multi_sum_index<8>(lane);

@@ -79,9 +79,25 @@ __device__ __forceinline__ BlockXY xcd_block()
 }
 
 template <int NCH> struct MixUnroll { static constexpr int value = NCH >= 8 ? 1 : 8 / NCH; };
-// Sources loaded ahead in the backward stream (divides 8, the number of
-// sources per batched reduction of the dots dH . o_i).
-template <int NCH> struct BwdInflight { static constexpr int value = NCH >= 8 ? 1 : NCH >= 2 ? 2 : 4; };
+// Sources loaded per step of the backward stream (divides 8, the number of
+// sources per batched reduction of the dots dH . o_i).  At d = 2048 one
+// source per step (4 KB read, 4 KB written per wave) measured level with or
+// ahead of two on MI355X; both sit at the box's read + write copy rate.
+#ifndef LRAR_BWD_INFLIGHT_WIDE
+#define LRAR_BWD_INFLIGHT_WIDE 1  // rows of 4 chunks per lane (d = 2048 bf16)
+#endif
+template <int NCH> struct BwdInflight {
+    static constexpr int value = NCH >= 8 ? 1 : NCH == 4 ? LRAR_BWD_INFLIGHT_WIDE : NCH >= 2 ? 2 : 4;
+};
+// Cache policy of the backward's value-row loads and gradient-row stores.
+#ifndef LRAR_BWD_NT_LOAD
+#define LRAR_BWD_NT_LOAD 1
+#endif
+#ifndef LRAR_BWD_NT_STORE
+#define LRAR_BWD_NT_STORE 1
+#endif
+constexpr bool kBwdNtLoad = LRAR_BWD_NT_LOAD != 0;
+constexpr bool kBwdNtStore = LRAR_BWD_NT_STORE != 0;
 // Tokens per wave in the backward of projected / sliced keys, by column
 // chunks per lane: two for rows of 4+ chunks (d >= 2048 bf16), else one
 // (measured on MI355X at d = 1024 and 2048).

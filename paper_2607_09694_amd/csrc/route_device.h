@@ -78,6 +78,36 @@ __device__ __forceinline__ void store_stream(T *p, typename Raw<T, VEC>::type v)
         *reinterpret_cast<raw_t *>(p) = v;
 }
 
+// Raw (untyped) buffer accesses of 16 bytes.  A buffer resource describes
+// one row: its base address and its size in bytes.  An access at or past
+// the size is dropped by the hardware (a load returns zeros), so a range
+// check becomes a size in the scalar descriptor instead of a branch around
+// the access.  NT marks the access non-temporal.
+constexpr int kRawBufferWord3 = 0x00020000;  // word 3 of a raw buffer resource (gfx9 family)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void *base, int bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, kRawBufferWord3);
+}
+
+template <typename T, int VEC, bool NT>
+__device__ __forceinline__ typename Raw<T, VEC>::type buffer_load16(__amdgpu_buffer_rsrc_t r,
+                                                                    int byte_off)
+{
+    typedef typename Raw<T, VEC>::type raw_t;
+    static_assert(sizeof(raw_t) == 16, "16-byte accesses only");
+    return __builtin_bit_cast(raw_t, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, NT ? 2 : 0));
+}
+
+template <typename T, int VEC, bool NT>
+__device__ __forceinline__ void buffer_store16(__amdgpu_buffer_rsrc_t r, int byte_off,
+                                               typename Raw<T, VEC>::type v)
+{
+    static_assert(sizeof(v) == 16, "16-byte accesses only");
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, byte_off, 0,
+                                           NT ? 2 : 0);
+}
+
 // Widen one raw access to VEC fp32 values (exact).
 __device__ __forceinline__ void widen(const f32x4_t &r, float (&x)[4])
 {
