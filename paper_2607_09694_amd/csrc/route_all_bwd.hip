@@ -96,6 +96,14 @@ __device__ __forceinline__ void per_token(T &x)
     asm volatile("" : "+s"(x));
 }
 
+// The same for per-lane values: the LDS offsets and masks derived from the
+// lane's indices are formed where they are used instead of being
+// precomputed once and held (and spilled) for the kernel's lifetime.
+__device__ __forceinline__ void per_lane(int &x)
+{
+    asm volatile("" : "+v"(x));
+}
+
 template <int MT, int RT, bool ACC>
 __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
 {
@@ -113,15 +121,12 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
     __shared__ float qs[kAllMaxSources * kAllMaxRank];  // Q [T][r]
     static_assert(2 * kDhBufBytes >= kAllMaxSources * kAlphaRow * 4, "ds / rho fits the slabs");
 
-    const int tid = threadIdx.x;
-    const int lane = tid % kWaveSize, wave = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
-    const int lc = lane & 15, ks = lane >> 4;
-    const int src = 16 * wave + lc;  // this lane's source as a G operand
-    const int hch = tid & 15, hr0 = tid >> 4;
+    const int tid0 = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid0 / kWaveSize);
     float *dsr = reinterpret_cast<float *>(dhbuf);
     float *tailbuf = alpha + wave * 16 * kTailRow;  // this wave's 16 sources
 
-    for (int f = tid; f < b.f.T * b.f.r; f += kBlock)
+    for (int f = tid0; f < b.f.T * b.f.r; f += kBlock)
         qs[f] = b.f.Q[f];
 
     f32x4_t dq[RT];
@@ -130,6 +135,12 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
         dq[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
     for (int64_t n = blockIdx.x; n < b.f.N; n += gridDim.x) {
+        int tid = tid0;
+        per_lane(tid);
+        const int lane = tid % kWaveSize;
+        int lc = lane & 15, ks = lane >> 4;
+        int src = 16 * wave + lc;  // this lane's source as a G operand
+        int hch = tid & 15, hr0 = tid >> 4;
         AllArgs a = b.f;
         per_token(a.S);
         per_token(a.T);
@@ -215,6 +226,11 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
         for (int mt = 0; mt < MT; ++mt)
             G[mt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
         for (int s = 0; s < nslab; ++s) {
+            per_lane(lc);
+            per_lane(ks);
+            per_lane(src);
+            per_lane(hch);
+            per_lane(hr0);
             unsigned char *buf = dhbuf + (s & 1) * kDhBufBytes;
             // Rows past T, and rows 16 MT .. 32 KG - 1 that the last site
             // group's dV MFMAs read with weight 0, are written as zeros (the
@@ -472,6 +488,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
     }
 
     if (wave < MT) {
+        const int lc = (tid0 % kWaveSize) & 15, ks = (tid0 % kWaveSize) >> 4;
         float *part = b.partial + (size_t)blockIdx.x * b.f.T * b.f.r;
 #pragma unroll
         for (int ct = 0; ct < RT; ++ct)
