@@ -431,7 +431,7 @@ int lr_attnres_route_gather_bwd(const void *V, const void *K, int64_t source, co
 /*
  * Every read site of a pass over one stack of sources, in one call (Sec. 3.1,
  * Eq. full_attnres_source_set: site t reads the sources 0 .. t-1; routing of
- * Sec. 3.2 with projected or sliced keys, Sec. 3.3-3.4), with each site's
+ * Sec. 3.2 with any of the three key modes, Sec. 3.3-3.4), with each site's
  * effective number of sources (Sec. 4.5, Eq. effective_sources).  For use once
  * all outputs of the pass exist: recomputing the routed states of a pass,
  * probing a trained model.  Site j = 0 .. T-1 reads the first `first + j`
@@ -445,13 +445,18 @@ int lr_attnres_route_gather_bwd(const void *V, const void *K, int64_t source, co
  *        first + j sources with query Q[j]);
  *   neff [T][N] fp32, overwritten, or NULL: exp(-sum_i alpha_i log alpha_i)
  *        of site j's weights for token n.
- * The stack is read once for all sites.  EINVAL: first < 1, T < 1,
- * first + T - 1 > S, or the conditions of lr_attnres_route_fwd (V, H 16-byte
- * aligned; K, Q, neff element aligned; no output may overlap an input or the
- * other output).  EUNSUPPORTED: full-rank keys, S or T above 64, r above 64,
- * d not a multiple of 8, N above 2^30.  Non-finite source values are not
- * confined to the sites that read them: a source past a site's prefix enters
- * that site's product with weight 0, and 0 * inf is NaN.
+ * With projected or sliced keys, S, T and r at most 64 and d a multiple of
+ * 8, one fused launch reads the stack once for all sites; otherwise (full-rank
+ * keys, larger S, T or r, other d) the library runs the sites one after the
+ * other, each as lr_attnres_route_fwd over its prefix (and
+ * lr_attnres_route_neff), so every site's H row is bit for bit that call's.
+ * EINVAL: first < 1, T < 1, first + T - 1 > S, or the conditions of
+ * lr_attnres_route_fwd (V, H 16-byte aligned; K, Q, neff element aligned; no
+ * output may overlap an input or the other output).  EUNSUPPORTED: N above
+ * 2^30, or, site by site, what lr_attnres_route_fwd refuses for the last site
+ * (first + T - 1 sources).  In the fused launch non-finite source values are
+ * not confined to the sites that read them: a source past a site's prefix
+ * enters that site's product with weight 0, and 0 * inf is NaN.
  */
 int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void *H, float *neff,
                              int64_t S, int64_t N, int64_t d, int64_t r, int64_t first,
@@ -471,12 +476,21 @@ int lr_attnres_route_all_fwd(const void *V, const void *K, const float *Q, void 
  *   workspace: lr_attnres_route_all_bwd_workspace_bytes(...) bytes of device
  *        memory, 4-byte aligned (per-workgroup dQ partials).
  * accumulate = 0 overwrites dV, dK and dQ; 1 adds the gradients to them.
- * Each source row, upstream row and dV row is moved once for all sites.
- * dQ is reduced in a fixed order, so results are bitwise reproducible.
+ * Where the fused forward applies and storage is bf16, one fused launch moves
+ * each source row, upstream row and dV row once for all sites and rounds each
+ * gradient to bf16 once.  Otherwise (full-rank keys, fp32 storage, larger S,
+ * T or r, other d) the sites run one after the other as accumulating
+ * lr_attnres_route_bwd calls over their prefixes, after a fill kernel has
+ * zeroed dV, dK and dQ when overwriting (no memset); a source's gradient is
+ * then rounded to the storage after each site that reads it, and dQ row j is
+ * bit for bit site j's dq.  Either way dQ is reduced in a fixed order, so
+ * results are bitwise reproducible.
  * EINVAL as for lr_attnres_route_all_fwd, plus dH, dV 16-byte aligned, dK and
  * dQ element aligned, a too small workspace, accumulate not 0 or 1, and any
  * output (or the workspace) overlapping an input or another output.
- * EUNSUPPORTED: as for lr_attnres_route_all_fwd, and fp32 storage.
+ * EUNSUPPORTED: N above 2^30, or, site by site, what lr_attnres_route_bwd
+ * refuses for the last site.  The workspace query covers whichever path the
+ * problem takes (the single-site backward's workspace when site by site).
  */
 size_t lr_attnres_route_all_bwd_workspace_bytes(int64_t S, int64_t N, int64_t d, int64_t r,
                                                 int64_t first, int64_t T, int mode, int dtype);

@@ -253,9 +253,11 @@ def route_all_fwd(V, K, Q, mode, first: int, eps: float = 1e-6, with_neff: bool 
     """Every read site of a pass over the stack V in one call (Sec. 3.1):
     site j = 0..T-1 reads the first first+j sources with query Q[j].
 
-    V [S,N,d] bf16/fp32; K [S,N,r] (projected) or None (sliced); Q [T,r]
-    fp32.  Returns (H [T,N,d] in V's dtype, neff [T,N] fp32 or None), neff
-    per Eq. effective_sources.  ``out`` may supply (H, neff).
+    V [S,N,d] bf16/fp32; K [S,N,r] (projected) or None (sliced, full-rank);
+    Q [T,r] fp32 (full-rank: r = d).  Returns (H [T,N,d] in V's dtype, neff
+    [T,N] fp32 or None), neff per Eq. effective_sources.  ``out`` may supply
+    (H, neff).  Problems outside the fused kernel run site by site inside
+    the library.
     """
     import torch
 

@@ -278,25 +278,32 @@ __global__ __launch_bounds__(kBlock) void route_neff(const T *__restrict__ keys,
 
 }  // namespace
 
+bool all_fused(const AllProblem &p)
+{
+    return (p.mode == LRAR_MODE_PROJECTED || p.mode == LRAR_MODE_SLICED) &&
+           p.S <= kAllMaxSources && p.T <= kAllMaxSources && p.r <= kAllMaxRank && p.d % 8 == 0;
+}
+
+Problem all_site_problem(const AllProblem &p, int64_t j)
+{
+    return Problem{p.V, p.K, p.Q + j * p.r, p.first + j, p.N, p.d, p.r, p.mode, p.dtype, p.eps,
+                   p.dtype};
+}
+
 int check_all_supported(const AllProblem &p, std::string *why)
 {
-    if (p.mode != LRAR_MODE_PROJECTED && p.mode != LRAR_MODE_SLICED) {
-        *why = "all-sites routing takes projected or sliced keys (full-rank keys need the whole "
-               "row per score)";
-        return LRAR_EUNSUPPORTED;
-    }
-    if (p.S > kAllMaxSources || p.T > kAllMaxSources || p.r > kAllMaxRank) {
-        *why = "all-sites routing supports S <= " + std::to_string(kAllMaxSources) +
-               " sources, T <= " + std::to_string(kAllMaxSources) + " sites and r <= " +
-               std::to_string(kAllMaxRank);
-        return LRAR_EUNSUPPORTED;
-    }
-    if (p.d % 8 != 0) {
-        *why = "all-sites routing needs d % 8 == 0";
-        return LRAR_EUNSUPPORTED;
-    }
     if (p.N > ((int64_t)1 << 30)) {
         *why = "N above 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (all_fused(p))
+        return LRAR_OK;
+    // Full-rank keys, or more than 64 sources, sites or key columns: site by
+    // site, each site as the single-site forward over its prefix.  The last
+    // site reads the most sources and binds.
+    std::string w;
+    if (check_supported(all_site_problem(p, p.T - 1), false, &w) != LRAR_OK) {
+        *why = "all-sites routing, site by site: " + w;
         return LRAR_EUNSUPPORTED;
     }
     return LRAR_OK;
@@ -306,6 +313,25 @@ int launch_all_fwd(const AllProblem &p, hipStream_t st, std::string *err)
 {
     if (p.N == 0)
         return LRAR_OK;
+    if (!all_fused(p)) {
+        // One launch of the single-site forward (and N_eff) per site.
+        const size_t es = p.dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+        for (int64_t j = 0; j < p.T; ++j) {
+            const Problem ps = all_site_problem(p, j);
+            int rc = launch_fwd(ps, static_cast<char *>(p.H) + (size_t)j * p.N * p.d * es, st,
+                                err);
+            if (rc == LRAR_OK && p.neff) {
+                // Full rank: the key is the whole value, sliced keys with r = d.
+                Problem pn = ps;
+                if (pn.mode == LRAR_MODE_FULL)
+                    pn.mode = LRAR_MODE_SLICED;
+                rc = launch_neff(pn, p.neff + j * p.N, st, err);
+            }
+            if (rc != LRAR_OK)
+                return rc;
+        }
+        return LRAR_OK;
+    }
     AllArgs a;
     a.V = p.V;
     a.keys = p.mode == LRAR_MODE_PROJECTED ? p.K : p.V;

@@ -46,6 +46,8 @@
 // loads issued ahead stay in flight across them.
 #include "route_all_weights.h"
 
+#include <algorithm>
+
 namespace lrar {
 
 namespace {
@@ -533,18 +535,65 @@ void launch_all_bwd_acc(const AllBwdArgs &b, unsigned grid, hipStream_t st)
 
 int64_t all_bwd_workgroups(int64_t N) { return N < kAllBwdGrid ? N : kAllBwdGrid; }
 
+namespace {
+
+// The fused backward takes bf16 storage and what the fused forward takes.
+bool all_bwd_fused(const AllProblem &p) { return p.dtype == LRAR_DTYPE_BF16 && all_fused(p); }
+
+__global__ void __launch_bounds__(256) fill_zero16(u32x4_t *__restrict__ p, size_t n)
+{
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+        p[i] = u32x4_t{0u, 0u, 0u, 0u};
+}
+
+__global__ void __launch_bounds__(256) fill_zero2(uint16_t *__restrict__ p, size_t n)
+{
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+        p[i] = 0;
+}
+
+// Zeros `bytes` (even) bytes at p with a kernel (no memset node, so a
+// captured graph replays it like any other launch).
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t st)
+{
+    if (!p || bytes == 0)
+        return hipSuccess;
+    if (reinterpret_cast<uintptr_t>(p) % 16 == 0 && bytes % 16 == 0) {
+        const size_t n = bytes / 16;
+        const unsigned grid = (unsigned)std::min<size_t>((n + 255) / 256, 8192);
+        hipLaunchKernelGGL(fill_zero16, dim3(grid), dim3(256), 0, st, static_cast<u32x4_t *>(p),
+                           n);
+    } else {
+        const size_t n = bytes / 2;
+        const unsigned grid = (unsigned)std::min<size_t>((n + 255) / 256, 8192);
+        hipLaunchKernelGGL(fill_zero2, dim3(grid), dim3(256), 0, st, static_cast<uint16_t *>(p),
+                           n);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
 size_t all_bwd_workspace_bytes(const AllProblem &p)
 {
+    if (!all_bwd_fused(p))
+        return bwd_workspace_bytes(all_site_problem(p, p.T - 1));
     return (size_t)all_bwd_workgroups(p.N) * (size_t)p.T * (size_t)p.r * sizeof(float);
 }
 
 int check_all_bwd_supported(const AllProblem &p, std::string *why)
 {
-    int rc = check_all_supported(p, why);
-    if (rc)
-        return rc;
-    if (p.dtype != LRAR_DTYPE_BF16) {
-        *why = "the all-sites backward takes bf16 storage";
+    if (p.N > ((int64_t)1 << 30)) {
+        *why = "N above 2^30 tokens";
+        return LRAR_EUNSUPPORTED;
+    }
+    if (all_bwd_fused(p))
+        return LRAR_OK;
+    // Full-rank keys, fp32 storage, or more than 64 sources, sites or key
+    // columns: site by site, each site's accumulating single-site backward.
+    std::string w;
+    if (check_supported(all_site_problem(p, p.T - 1), true, &w) != LRAR_OK) {
+        *why = "all-sites backward, site by site: " + w;
         return LRAR_EUNSUPPORTED;
     }
     return LRAR_OK;
@@ -553,6 +602,28 @@ int check_all_bwd_supported(const AllProblem &p, std::string *why)
 int launch_all_bwd(const AllProblem &p, const void *dH, void *dV, void *dK, float *dQ, void *ws,
                    bool accumulate, hipStream_t st, std::string *err)
 {
+    if (!all_bwd_fused(p)) {
+        // Site by site: each site's backward adds into the gradients of its
+        // prefix and into its row of dQ, after one zero fill when overwriting.
+        const size_t es = p.dtype == LRAR_DTYPE_BF16 ? 2 : 4;
+        if (!accumulate) {
+            hipError_t e = launch_zero(dV, (size_t)p.S * p.N * p.d * es, st);
+            if (e == hipSuccess && p.mode == LRAR_MODE_PROJECTED)
+                e = launch_zero(dK, (size_t)p.S * p.N * p.r * es, st);
+            if (e == hipSuccess)
+                e = launch_zero(dQ, (size_t)p.T * p.r * sizeof(float), st);
+            if (e != hipSuccess)
+                return hip_status(e, "route_all_bwd zero fill", err);
+        }
+        for (int64_t j = 0; j < p.T; ++j) {
+            const int rc = launch_bwd(all_site_problem(p, j),
+                                      static_cast<const char *>(dH) + (size_t)j * p.N * p.d * es,
+                                      dV, dK, dQ + j * p.r, ws, true, st, err);
+            if (rc != LRAR_OK)
+                return rc;
+        }
+        return LRAR_OK;
+    }
     const unsigned grid = (unsigned)all_bwd_workgroups(p.N);
     float *partial = static_cast<float *>(ws);
     if (grid > 0) {

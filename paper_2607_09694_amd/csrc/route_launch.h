@@ -161,6 +161,11 @@ struct AllProblem {
 };
 
 int check_all_supported(const AllProblem &p, std::string *why);
+// Whether the fused all-sites kernels take the problem (projected or sliced
+// keys, S, T, r <= 64, d % 8 == 0); otherwise the sites run one by one.
+bool all_fused(const AllProblem &p);
+// The single-site problem of site j of an all-sites problem.
+Problem all_site_problem(const AllProblem &p, int64_t j);
 
 // Backward of every read site (see lr_attnres_route_all_bwd): dV [S][N][d],
 // dK [S][N][r] (projected keys) or NULL, dQ [T][r]; overwritten, or added

@@ -346,12 +346,13 @@ def test_all_sites_rejects(lib, name, kw, msg):
 
 
 def test_all_sites_unsupported(lib):
-    assert allf(lib, mode=F, r=64) == EUNSUPPORTED
-    assert "projected or sliced" in err(lib)
-    assert allf(lib, S=65, T=3) == EUNSUPPORTED
-    assert allf(lib, S=70, first=1, T=65) == EUNSUPPORTED
-    assert allf(lib, mode=P, K=E, r=65, d=128) == EUNSUPPORTED
-    assert allf(lib, d=68) == EUNSUPPORTED
+    # Beyond the fused kernel the sites run one by one, so the limits are
+    # those of the single-site forward at the last site (first + T - 1
+    # sources).
+    assert allf(lib, S=1026, first=1025, T=2) == EUNSUPPORTED
+    assert "site by site" in err(lib)
+    assert allf(lib, mode=F, r=8192, d=8192) == EUNSUPPORTED
+    assert allf(lib, N=(1 << 30) + 1, S=2, first=1, T=1, d=8, r=8) == EUNSUPPORTED
 
 
 def allb_ws(lib, S=6, N=8, d=64, r=8, first=2, T=5, mode=SL, dtype=BF16):
@@ -365,12 +366,19 @@ def allb(lib, V=A, K=None, Q=B, dH=C, dV=D, dK=None, dQ=E, ws=G, ws_bytes=1 << 2
 
 
 def test_all_sites_backward_workspace(lib):
-    # one fp32 partial row of T x r per workgroup, at most 512 workgroups
+    # fused: one fp32 partial row of T x r per workgroup, at most 512 workgroups
     assert allb_ws(lib) == 8 * 5 * 8 * 4
     assert allb_ws(lib, N=100000, S=49, first=1, T=48, r=16, d=1024) == 512 * 48 * 16 * 4
     assert allb_ws(lib, N=0) == 0
     assert allb_ws(lib, first=0) == 0
     assert allb_ws(lib, first=2, T=6) == 0
+    # site by site (full rank, fp32 storage, S > 64): the single-site
+    # backward's workspace, reused by every site
+    single = lib.lr_attnres_route_bwd_workspace_bytes
+    assert allb_ws(lib, mode=F, r=64) == single(6, 8, 64, 64, F, BF16) > 0
+    assert allb_ws(lib, dtype=F32) == single(6, 8, 64, 8, SL, F32) > 0
+    assert allb_ws(lib, S=100, first=30, T=71, N=5000, d=1024, r=16, mode=P) == \
+        single(100, 5000, 1024, 16, P, BF16)
 
 
 ALLB_INVALID = [
@@ -401,12 +409,14 @@ def test_all_sites_backward_rejects(lib, name, kw, msg):
 
 
 def test_all_sites_backward_unsupported(lib):
-    assert allb(lib, mode=F, r=64) == EUNSUPPORTED
-    assert allb(lib, dtype=F32) == EUNSUPPORTED
-    assert "bf16" in err(lib)
-    assert allb(lib, S=65, T=3) == EUNSUPPORTED
-    assert allb(lib, mode=P, K=W, dK=W + 0x1_0000_0000, r=65, d=128) == EUNSUPPORTED
-    assert allb(lib, d=68) == EUNSUPPORTED
+    # Beyond the fused kernel (full rank, fp32 storage, S, T or r above 64,
+    # d % 8 != 0) the sites run one by one: the limits are the single-site
+    # backward's at the last site.
+    assert allb(lib, S=514, first=513, T=2) == EUNSUPPORTED
+    assert "site by site" in err(lib)
+    assert allb(lib, mode=P, K=W, dK=W + 0x1_0000_0000, r=257, d=1024) == EUNSUPPORTED
+    assert allb(lib, mode=F, r=8192, d=8192) == EUNSUPPORTED
+    assert allb(lib, dtype=F32, mode=F, r=8192, d=8192) == EUNSUPPORTED
 
 
 def sdef(lib, V=A, K=None, q=B, dH=C, coef=D, dq=E, ws=G, ws_bytes=1 << 20, S=6, N=8, d=64, r=8,

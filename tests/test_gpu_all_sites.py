@@ -166,17 +166,73 @@ def test_all_sites_agree_with_per_site_routing(dev):
         check_bf16_value(f"site {j}", to_host(H[j]), to_host(h).astype(np.float64))
 
 
+# Problems the fused kernel does not take run site by site inside the
+# library: (mode, storage, S, T, first, N, d, r).
+SITE_BY_SITE = [
+    (FULL, "bf16", 9, 8, 2, 13, 256, 256),     # full-rank keys
+    (FULL, "f32", 12, 10, 3, 7, 200, 200),
+    (FULL, "bf16", 1, 1, 1, 6, 64, 64),        # one source: a copy
+    (SLICED, "bf16", 70, 8, 63, 9, 136, 16),   # S > 64
+    (PROJECTED, "f32", 20, 5, 3, 11, 128, 80),  # r > 64
+    (SLICED, "bf16", 10, 9, 2, 11, 68, 8),     # d % 8 != 0
+    (PROJECTED, "bf16", 66, 65, 2, 5, 64, 8),  # T > 64
+]
+
+
+def _sbs_ids(c):
+    return "{}-{}-S{}-T{}-f{}-N{}-d{}-r{}".format({PROJECTED: "P", SLICED: "S", FULL: "F"}[c[0]],
+                                                  *c[1:])
+
+
+@pytest.mark.parametrize("case", SITE_BY_SITE, ids=_sbs_ids)
+def test_all_sites_site_by_site_match_oracle(dev, case):
+    """Each site of the site-by-site path is the single-site forward of its
+    prefix (bit for bit) and matches the oracle to the storage's bar."""
+    mode, dtype, S, T, first, N, d, r = case
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=21)
+    Q = _queries(T, r, seed=22, scale=2.0)
+    V, K, Qd = to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev)
+    H, ne = lr.route_all_fwd(V, K, Qd, mode, first)
+    torch.cuda.synchronize()
+    Hr, NEr = oracle.route_all_fwd(p.V, p.K, Q.astype(np.float64), mode, first, r=r)
+    check_h("H", dtype, to_host(H), Hr)
+    check_neff("neff", to_host(ne), NEr)
+    for j in sorted({0, T // 2, T - 1}):
+        s = first + j
+        h = lr.route_fwd(V[:s], None if K is None else K[:s], Qd[j].contiguous(), mode)
+        torch.cuda.synchronize()
+        assert np.array_equal(host_bits(H[j]), host_bits(h)), f"site {j}"
+
+
+def test_all_sites_full_rank_model_pass_full_size(dev):
+    """Full-rank keys at the paper's model pass (49 sources, sites reading
+    2..49, d = 1024, N = 16384), site by site; sampled tokens against the
+    oracle token by token."""
+    S, T, first, N, d = 49, 48, 2, 16384, 1024
+    prob = make_device_problem(FULL, S, N, d, d, dev, seed=0, n_queries=T)
+    H, ne = lr.route_all_fwd(prob["V"], None, prob["q"], FULL, first)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([[0, N - 1], np.random.default_rng(1).integers(0, N, 10)]))
+    idx = torch.as_tensor(toks, device=dev)
+    Vs = host_bits(prob["V"][:, idx].contiguous())
+    Q = prob["q"].cpu().numpy().astype(np.float64)
+    ref, ref_ne = oracle.route_all_fwd(Vs, None, Q, FULL, first, r=d)
+    check_bf16_value("H", to_host(H[:, idx].contiguous()), ref)
+    check_neff("neff", to_host(ne[:, idx].contiguous()), ref_ne)
+
+
 def test_all_sites_rejected_outside_limits(dev):
     p = make_host_problem(PROJECTED, 4, 3, 64, 8, dtype="bf16", seed=9)
     V, K = to_dev(p.V, dev), to_dev(p.K, dev)
     with pytest.raises(lr.RoutingError):
         lr.route_all_fwd(V, K, torch.zeros((4, 8), device=dev), PROJECTED, 2)
-    big = torch.zeros((65, 2, 64), dtype=torch.bfloat16, device=dev)
-    with pytest.raises(lr.RoutingError, match="S <= 64"):
-        lr.route_all_fwd(big, None, torch.zeros((3, 8), device=dev), SLICED, 1)
-    full = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=dev)
-    with pytest.raises(lr.RoutingError, match="projected or sliced"):
-        lr.route_all_fwd(full, None, torch.zeros((2, 64), device=dev), 2, 1)
+    # site by site, the last site past the single-site forward's 1024 sources
+    big = torch.zeros((1026, 2, 64), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lr.RoutingError, match="site by site"):
+        lr.route_all_fwd(big, None, torch.zeros((2, 8), device=dev), SLICED, 1025)
+    wide = torch.zeros((2, 1, 8192), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(lr.RoutingError, match="site by site"):
+        lr.route_all_fwd(wide, None, torch.zeros((1, 8192), device=dev), FULL, 1)
 
 
 FULL_SIZE = [(PROJECTED, 16), (SLICED, 64)]

@@ -16,10 +16,10 @@ import pytest
 
 import oracle
 import paper_2607_09694_amd as lr
-from paper_2607_09694_amd.inputs import (PROJECTED, SLICED, bf16_bits_from_f32,
+from paper_2607_09694_amd.inputs import (FULL, PROJECTED, SLICED, bf16_bits_from_f32,
                                          bf16_tensor_to_bits, f32_from_bf16_bits,
                                          make_host_problem)
-from parity import check_sum_by_terms, check_bf16_grown, check_bf16_key_grad, check_dq
+from parity import check_bf16_grown, check_bf16_key_grad, check_dq, check_f32, check_sum_by_terms
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -302,3 +302,183 @@ def test_stack_beyond_2_31_elements(dev):
     _check("", mode, (dV[:, idx].contiguous(), dK[:, idx].contiguous(), None), (rV, rK, rQ))
     del H, ne, dV, dK
     check_dq("dQ", to_host(dQ), oracle_dQ_all_tokens(V, K, Q, dH, mode, first, r))
+
+
+# ---------------------------------------------------------------------------
+# Site by site: full-rank keys, fp32 storage, and S, T or r above 64 (or
+# d % 8 != 0) run as one accumulating single-site backward per site.  The
+# running gradient of a source is rounded to the storage after every site
+# that reads it, so the bf16 bar is the bound of those roundings: one
+# half-ulp (2^-9 relative) of each running sum, with a factor 2 (2^-8), plus
+# 1e-3 for the fp32 sums, floored at the value bar 2e-2.  fp32 storage keeps
+# the fp32 bar (48 roundings of 2^-24 stay far below 1e-5).
+# ---------------------------------------------------------------------------
+
+def _host(t):
+    if t.dtype == torch.bfloat16:
+        return bf16_tensor_to_bits(t)
+    return t.detach().contiguous().cpu().numpy()
+
+
+def _widen(x):
+    return f32_from_bf16_bits(x).astype(np.float64) if x.dtype == np.uint16 else \
+        x.astype(np.float64)
+
+
+def _sbs_problem(mode, dtype, S, T, first, N, d, r, seed):
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=seed)
+    rng = np.random.default_rng(seed + 2)
+    dH = rng.standard_normal((T, p.N, p.d)).astype(np.float32)
+    if dtype == "bf16":
+        dH = bf16_bits_from_f32(dH)
+    return p, _queries(T, p.r, seed + 1), dH
+
+
+def _site_parts(V, K, Q, dH, mode, first, r):
+    """Each site's oracle gradient of its prefix, in site order."""
+    return [oracle.route_bwd(V[:first + j], None if K is None else K[:first + j], Q[j], dH[j],
+                             mode, r=r)
+            for j in range(Q.shape[0])]
+
+
+def _check_accumulated(name, dtype, got, parts, start):
+    """got = start + parts[0] + parts[1] + ..., part j covering the first
+    parts[j].shape[0] sources, rounded to the storage after each part."""
+    P = start.astype(np.float64).copy()
+    bsum = np.zeros_like(P)
+    for G in parts:
+        s = G.shape[0]
+        P[:s] += G
+        bsum[:s] += np.abs(P[:s])
+    got = np.asarray(got, dtype=np.float64)
+    assert np.isfinite(got).all()
+    if dtype == "f32":
+        check_f32(name, got, P)
+        return
+    bar = np.maximum(2e-2, 2.0 ** -8 * bsum + 1e-3)
+    worst = (np.abs(got - P) / bar).max(initial=0.0)
+    assert worst <= 1.0, f"{name}: max error / rounding bound {worst:.3f}"
+
+
+def _check_site_by_site(mode, dtype, got, p, Q, dH, first, start=None):
+    dV, dK, dQ = got
+    Qh = Q.astype(np.float64)
+    parts = _site_parts(p.V, p.K, Qh, dH, mode, first, p.r)
+    S = p.V.shape[0]
+    zV = np.zeros((S, p.N, p.d)) if start is None else start[0]
+    _check_accumulated("dV", dtype, to_host(dV), [g[0] for g in parts], zV)
+    if mode == PROJECTED:
+        zK = np.zeros((S, p.N, p.r)) if start is None else start[1]
+        _check_accumulated("dK", dtype, to_host(dK), [g[1] for g in parts], zK)
+    else:
+        assert dK is None
+    rQ = np.stack([g[2] for g in parts]) + (0.0 if start is None else start[2])
+    check_dq("dQ", to_host(dQ), rQ, tol=1e-5 if dtype == "f32" else 1e-4)
+
+
+# (mode, storage, S, T, first, N, d, r)
+SITE_BY_SITE = [
+    (FULL, "bf16", 9, 8, 1, 21, 256, 256),
+    (FULL, "f32", 7, 5, 2, 13, 136, 136),
+    (PROJECTED, "f32", 12, 10, 2, 17, 264, 16),
+    (SLICED, "f32", 20, 17, 3, 19, 200, 12),
+    (SLICED, "bf16", 70, 6, 65, 9, 128, 16),     # S > 64
+    (PROJECTED, "bf16", 10, 8, 2, 15, 128, 80),  # r > 64
+    (SLICED, "bf16", 10, 9, 1, 11, 68, 8),       # d % 8 != 0
+    (FULL, "bf16", 20, 6, 3, 600, 128, 128),     # sources 8..19 read by no site
+]
+
+
+def _sbs_ids(c):
+    return "{}-{}-S{}-T{}-f{}-N{}-d{}-r{}".format({PROJECTED: "P", SLICED: "S", FULL: "F"}[c[0]],
+                                                  *c[1:])
+
+
+@pytest.mark.parametrize("case", SITE_BY_SITE, ids=_sbs_ids)
+def test_all_sites_backward_site_by_site(dev, case):
+    """The site-by-site path against the oracle's per-site gradients; a
+    source no site reads gets exactly zero; dQ row j is bit for bit the
+    single-site backward's dq of site j."""
+    mode, dtype, S, T, first, N, d, r = case
+    p, Q, dH = _sbs_problem(mode, dtype, S, T, first, N, d, r, seed=S + 3 * T + N)
+    V, K, Qd, dHd = to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev), to_dev(dH, dev)
+    got = lr.route_all_bwd(V, K, Qd, dHd, mode, first)
+    torch.cuda.synchronize()
+    _check_site_by_site(mode, dtype, got, p, Q, dH, first)
+    last = first + T - 1
+    if last < S:
+        assert not bool(got[0][last:].float().abs().max() > 0)
+    for j in sorted({0, T - 1}):
+        s = first + j
+        _, _, dq = lr.route_bwd(V[:s], None if K is None else K[:s], Qd[j].contiguous(), dHd[j],
+                                mode)
+        torch.cuda.synchronize()
+        assert torch.equal(got[2][j], dq), f"dQ row {j}"
+
+
+@pytest.mark.parametrize("mode,dtype", [(FULL, "bf16"), (PROJECTED, "f32")], ids=["F-bf16",
+                                                                                 "P-f32"])
+def test_all_sites_backward_site_by_site_accumulates(dev, mode, dtype):
+    S, T, first, N, d, r = 11, 9, 2, 23, 136, 16
+    p, Q, dH = _sbs_problem(mode, dtype, S, T, first, N, d, r, seed=61)
+    rng = np.random.default_rng(62)
+    dV0 = rng.standard_normal((S, N, p.d)).astype(np.float32)
+    dK0 = rng.standard_normal((S, N, p.r)).astype(np.float32)
+    dQ0 = rng.standard_normal((T, p.r)).astype(np.float32)
+    if dtype == "bf16":
+        dV0, dK0 = bf16_bits_from_f32(dV0), bf16_bits_from_f32(dK0)
+    out = (to_dev(dV0, dev), to_dev(dK0, dev) if mode == PROJECTED else None, to_dev(dQ0, dev))
+    got = lr.route_all_bwd(to_dev(p.V, dev), to_dev(p.K, dev), to_dev(Q, dev), to_dev(dH, dev),
+                           mode, first, out=out, accumulate=True)
+    torch.cuda.synchronize()
+    start = (_widen(dV0), _widen(dK0) if mode == PROJECTED else None, dQ0.astype(np.float64))
+    _check_site_by_site(mode, dtype, got, p, Q, dH, first, start=start)
+
+
+def test_all_sites_backward_site_by_site_overwrites(dev):
+    """Overwrite mode clears what the outputs held before the sites add in
+    (a kernel fill, no memset): a second call on dirty buffers matches the
+    first bit for bit."""
+    mode, S, T, first, N, d = FULL, 10, 7, 2, 40, 72
+    p, Q, dH = _sbs_problem(mode, "bf16", S, T, first, N, d, d, seed=71)
+    args = (to_dev(p.V, dev), None, to_dev(Q, dev), to_dev(dH, dev), mode, first)
+    a = lr.route_all_bwd(*args)
+    out = (torch.full_like(a[0], 3.0), None, torch.full_like(a[2], -7.0))
+    b = lr.route_all_bwd(*args, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0].view(torch.int16), b[0].view(torch.int16))
+    assert torch.equal(a[2], b[2])
+
+
+def test_all_sites_backward_full_rank_model_pass_full_size(dev):
+    """Full-rank keys at the paper's model pass (49 sources, 48 sites reading
+    2..49, d = 1024, N = 16384), site by site: sampled tokens against the
+    oracle's per-site gradients; dQ rows bit for bit the single-site
+    backward's dq of their sites (whose full-size parity with the oracle the
+    single-site tests hold)."""
+    mode, S, T, first, N, d = FULL, 49, 48, 2, 16384, 1024
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    V = torch.empty((S, N, d), dtype=torch.bfloat16, device=dev)
+    for i in range(S):
+        V[i].copy_(torch.randn((N, d), generator=g, device=dev))
+    Q = torch.randn((T, d), generator=g, device=dev) * (2.0 / d ** 0.5)
+    dH = torch.empty((T, N, d), dtype=torch.bfloat16, device=dev)
+    for j in range(T):
+        dH[j].copy_(torch.randn((N, d), generator=g, device=dev))
+    dV, _, dQ = lr.route_all_bwd(V, None, Q, dH, mode, first)
+    torch.cuda.synchronize()
+    toks = np.unique(np.concatenate([[0, N - 1], np.random.default_rng(4).integers(0, N, 8)]))
+    idx = torch.as_tensor(toks, device=dev)
+    Vs = _host(V[:, idx].contiguous())
+    dHs = _host(dH[:, idx].contiguous())
+    Qh = Q.cpu().numpy().astype(np.float64)
+    parts = _site_parts(Vs, None, Qh, dHs, mode, first, d)
+    _check_accumulated("dV", "bf16", to_host(dV[:, idx].contiguous()), [g[0] for g in parts],
+                       np.zeros((S, len(toks), d)))
+    del dV
+    for j in (0, 23, 47):
+        s = first + j
+        _, _, dq = lr.route_bwd(V[:s], None, Q[j].contiguous(), dH[j], mode)
+        torch.cuda.synchronize()
+        assert torch.equal(dQ[j], dq), f"dQ row {j}"
