@@ -956,6 +956,29 @@ def focused(torch, lr, dev, names, reps=20, warmup=3):
     return out
 
 
+def key_producer_pass(torch, lr, dev):
+    """Untimed calls of the SwiGLU key producer for counter runs: dispatches
+    4-13 of the kernel are cold (the memory-side cache flushed by a read
+    before each), 14-23 warm (back to back)."""
+    N, d, m, r = 16384, 1024, 2816, 16
+    g = torch.Generator(device=dev)
+    g.manual_seed(m + r)
+    A = torch.randn((N, m), generator=g, device=dev).to(torch.bfloat16)
+    W = (torch.randn((d + r, m), generator=g, device=dev) / m ** 0.5).to(torch.bfloat16)
+    O = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((N, r), dtype=torch.bfloat16, device=dev)
+    flush = Flusher(torch, dev)
+    for _ in range(3):
+        lr.key_proj_fwd(A, W, d, out=(O, K))
+    for _ in range(10):
+        flush()
+        lr.key_proj_fwd(A, W, d, out=(O, K))
+    for _ in range(10):
+        lr.key_proj_fwd(A, W, d, out=(O, K))
+    torch.cuda.synchronize()
+    print("bench: key producer pass done", file=sys.stderr, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -972,6 +995,10 @@ def main():
     ap.add_argument("--counters-pass", action="store_true",
                     help="no timing: 3 reference copies of 1 GiB, then 3 forward and 3 "
                          "backward calls of the main workload (for rocprofv3 --pmc runs)")
+    ap.add_argument("--key-producer-pass", action="store_true",
+                    help="no timing: the SwiGLU key producer (m = 2816, d = 1024, r = 16, "
+                         "N = 16384), 3 warm-up calls, 10 cold calls (a 1 GiB read before "
+                         "each), then 10 warm calls (for rocprofv3 --pmc runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: --gpus must be 1 (tokens are independent, so the "
@@ -986,6 +1013,9 @@ def main():
 
     lr.load_library()
     dev = torch.device("cuda:0")
+    if args.key_producer_pass:
+        key_producer_pass(torch, lr, dev)
+        return
     if args.extra_only:
         names = set(args.extra_only.split(","))
         print(json.dumps({"extra_only": focused(torch, lr, dev, names)}), flush=True)

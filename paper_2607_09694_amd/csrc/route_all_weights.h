@@ -252,13 +252,15 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
 // 8 x 8 block of bf16 (8 rows of 8 consecutive columns, one 16-byte row per
 // register quad) is transposed with these into MFMA operands that hold one
 // column of 8 rows.
+// Each is one byte permute (v_perm_b32: selector bytes 0-3 pick bytes of the
+// second operand, 4-7 of the first).
 __device__ __forceinline__ unsigned lo_pair(unsigned x, unsigned y)
 {
-    return (x & 0xffffu) | (y << 16);
+    return __builtin_amdgcn_perm(y, x, 0x05040100u);  // (x & 0xffff) | (y << 16)
 }
 __device__ __forceinline__ unsigned hi_pair(unsigned x, unsigned y)
 {
-    return (x >> 16) | (y & 0xffff0000u);
+    return __builtin_amdgcn_perm(y, x, 0x07060302u);  // (x >> 16) | (y & 0xffff0000)
 }
 
 }  // namespace
