@@ -398,6 +398,27 @@ def block_pass_bytes(t, c, N, d, r, mode, es=2, completed_bf16=False):
     return b + N * row * es + N * d * es
 
 
+def block_deferred_bwd_bytes(T, c, N, d, r, mode, es=2):
+    """Algorithmic HBM bytes of the deferred block reverse pass over T sites
+    with blocks of c outputs.  Site step with j completed slots: the j + 1
+    fp32 slot rows read, the partial slot's gradient rows read and written,
+    dH read, 3 fp32 coefficients per completed slot written, and the fused
+    retire (slot row written back, o_new / k_new read, dO / dK written).
+    Gather of slot p read as completed by u sites: their dH and
+    coefficients read, the slot's fp32 key read, its gradient written."""
+    row = d + (r if mode == 0 else 0)
+    nsrc = [1] + [(t - 2) // c + 2 for t in range(2, T + 1)]
+    total = 0
+    for n_src in nsrc:
+        j = n_src - 1
+        total += (j + 1) * N * row * 4 + N * row * 8 + N * d * es + j * 3 * N * 4 \
+            + N * row * (4 + es + es)
+    for p in sorted(set(n - 1 for n in nsrc)):
+        u = sum(1 for n in nsrc if n - 1 > p)
+        total += u * N * d * es + u * 3 * N * 4 + N * r * 4 + N * row * 4
+    return total
+
+
 def block_pass(torch, lr, dev, O, mode, r, c, reps, warmup, flush, completed_bf16=False):
     """49-site block-source forward pass over the output stack O [49, N, d].
     Each site's real call (with its own start flag) is timed `reps` times;
@@ -540,6 +561,15 @@ def block_training_pass(torch, lr, dev, O, mode, r, c, reps, warmup):
         f, b = float(np.median(tf)), float(np.median(tb))
         res.update({name + "fwd_pass_ms": f, name + "bwd_pass_ms": b, name + "step_ms": f + b,
                     name + "tokens_per_s": N / ((f + b) * 1e-3)})
+    # Roofline of the forward pass and of the deferred reverse pass and step
+    # on their algorithmic bytes (warm: the sites run back to back).
+    fb = sum(block_pass_bytes(t, c, N, d, r, mode) for t in range(1, T + 1))
+    bb = block_deferred_bwd_bytes(T, c, N, d, r, mode)
+    f, b = res["deferred_fwd_pass_ms"], res["deferred_bwd_pass_ms"]
+    res.update({"fwd_pass_algo_bytes": fb, "deferred_bwd_pass_algo_bytes": bb,
+                "fwd_pass_frac_of_peak": fb / (f * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "deferred_bwd_pass_frac_of_peak": bb / (b * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "deferred_step_frac_of_peak": (fb + bb) / ((f + b) * 1e-3) / 1e9 / HBM_PEAK_GBS})
     del B, dB, KB, dKB, KO, dHs, ws, coef
     return res
 
