@@ -136,6 +136,13 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
     for (int ct = 0; ct < RT; ++ct)
         dq[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
+    // The keys of the workgroup's next token are loaded once its current
+    // token's slabs are done, so that they arrive during the key-gradient
+    // phases instead of holding up the next token's scores.
+    u32x4_t kown[4 * KK];
+    if (blockIdx.x < b.f.N)
+        load_site_keys<RP>(b.f, blockIdx.x, kown);
+
     for (int64_t n = blockIdx.x; n < b.f.N; n += gridDim.x) {
         int tid = tid0;
         per_lane(tid);
@@ -154,6 +161,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
         per_token(a.N);
         const size_t plane = (size_t)a.N * a.d;
         const int nslab = (a.d + kAllSlab - 1) / kAllSlab;
+        const float inv_r = 1.0f / (float)a.r;
         // First column of the key octets (sliced keys; d past the row otherwise).
         const int tail0 = b.sliced ? (a.d - a.r) / 8 * 8 : a.d;
 
@@ -187,9 +195,6 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
                 vraw[u] = load_stream<uint16_t, 8, false>(ok ? vbase + src * plane + c : vbase);
             }
         };
-        // The keys first, so that waiting for them does not wait for the slab.
-        u32x4_t kown[4 * KK];
-        load_site_keys<RP>(a, n, kown);
         load_dh(0);
         load_v(0);
 
@@ -325,6 +330,9 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
             }
         }
 
+        if (n + gridDim.x < a.N)
+            load_site_keys<RP>(a, n + gridDim.x, kown);
+
         // Softmax gradient.  Lane (lc, ks) holds G[site 16 mt + 4 ks + e][src].
         float ds[MT][4];
 #pragma unroll
@@ -408,7 +416,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
             for (int o = 1; o < 16; o <<= 1)
                 dot += __shfl_xor(dot, o, kWaveSize);
             const float inv = i < a.S ? 1.0f / rho[i] : 0.0f;
-            const float scale = dot * inv * inv / (float)a.r;
+            const float scale = dot * inv * inv * inv_r;
 #pragma unroll
             for (int ct = 0; ct < RT; ++ct) {
                 const int c = 16 * ct + lc;

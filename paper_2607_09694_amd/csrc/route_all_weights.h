@@ -186,14 +186,17 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
 
     // Scores: lane l holds sites 16 w + 4 (l / 16) + e against sources
     // 16 nt + (l mod 16).
+    // One reciprocal per key instead of a division per score.
     float s[4][4];
     float m[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    const float inv_r = 1.0f / (float)a.r;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
         float t = ss[nt];
         t += __shfl_xor(t, 16, kWaveSize);
         t += __shfl_xor(t, 32, kWaveSize);
-        const float rho = sqrtf(t / (float)a.r + a.eps);
+        const float rho = sqrtf(fmaf(t, inv_r, a.eps));
+        const float irho = 1.0f / rho;
         const int i = 16 * nt + col;
         if (SAVE && wave == 0 && ks == 0)
             rho_out[i] = rho;
@@ -201,7 +204,7 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
         for (int e = 0; e < 4; ++e) {
             const int site = 16 * wave + 4 * ks + e;
             const bool v = site < a.T && i < a.first + site;
-            s[nt][e] = v ? D[nt][e] / rho : -INFINITY;
+            s[nt][e] = v ? D[nt][e] * irho : -INFINITY;
             m[e] = fmaxf(m[e], s[nt][e]);
         }
     }
