@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import paper_2607_09694_amd as lr
-from paper_2607_09694_amd.inputs import PROJECTED, SLICED, make_host_problem
+from paper_2607_09694_amd.inputs import FULL, PROJECTED, SLICED, make_host_problem
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -190,3 +190,52 @@ def test_captured_key_producer_forward_and_backward_replays(dev):
         lr.key_proj_bwd(A, W, dO, dK, out=(dA, dW))
 
     _replays_match(pass_, [O, K, dA, dW])
+
+
+@pytest.mark.parametrize("mode,dtype", [(FULL, "bf16"), (SLICED, "f32")],
+                         ids=["full-bf16", "sliced-f32"])
+def test_captured_all_sites_site_by_site_replays(dev, mode, dtype):
+    """The all-sites forward and backward on their site-by-site path (full-rank
+    keys; fp32 storage) inside one graph: the overwriting backward clears its
+    outputs with a fill kernel, so each replay over outputs left dirty by the
+    previous one matches the eager result bit for bit."""
+    S, T, first, N, d, r = 9, 7, 3, 40, 136, 16
+    p = make_host_problem(mode, S, N, d, r, dtype=dtype, seed=17)
+    r = p.r
+    V = to_dev(p.V, dev)
+    gq = torch.Generator(device=dev).manual_seed(2)
+    Q = torch.randn((T, r), generator=gq, device=dev) / r ** 0.5
+    dH = torch.randn((T, N, d), generator=gq, device=dev).to(V.dtype)
+    H = torch.empty((T, N, d), dtype=V.dtype, device=dev)
+    ne = torch.empty((T, N), dtype=torch.float32, device=dev)
+    dV = torch.empty_like(V)
+    dQ = torch.empty((T, r), dtype=torch.float32, device=dev)
+    ws = torch.empty((max(16, lr.route_all_bwd_workspace_bytes(S, N, d, r, first, T, mode,
+                                                                 V.dtype)),),
+                     dtype=torch.uint8, device=dev)
+
+    def step():
+        lr.route_all_fwd(V, None, Q, mode, first, out=(H, ne))
+        lr.route_all_bwd(V, None, Q, dH, mode, first, out=(dV, None, dQ), workspace=ws)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (H, ne, dV, dQ)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for k in range(3):
+        for t in (H, ne, dV, dQ):
+            t.fill_(3.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(ref, (H, ne, dV, dQ)):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {k}"
+        V.mul_(1.0)
+        torch.cuda.synchronize()
