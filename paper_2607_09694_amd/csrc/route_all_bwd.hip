@@ -340,9 +340,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int site = 16 * mt + 4 * ks + e;
-                float t = av[mt][e] * G[mt][e];
-                for (int o = 1; o < 16; o <<= 1)
-                    t += __shfl_xor(t, o, kWaveSize);
+                const float t = row16_sum(av[mt][e] * G[mt][e]);
                 if (lc == 0)
                     gpart[wave * kAllMaxSources + site] = t;
             }
@@ -413,8 +411,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
                 kv[ct] = c < a.r ? bf16_at(keys + i * kKeyRow + c) : 0.0f;
                 dot = fmaf(kv[ct], uk[ct][e], dot);
             }
-            for (int o = 1; o < 16; o <<= 1)
-                dot += __shfl_xor(dot, o, kWaveSize);
+            dot = row16_sum(dot);
             const float inv = i < a.S ? 1.0f / rho[i] : 0.0f;
             const float scale = dot * inv * inv * inv_r;
 #pragma unroll
