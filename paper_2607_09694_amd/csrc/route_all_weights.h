@@ -55,30 +55,9 @@ struct AllArgs {
 // so that they can be issued ahead of other loads) and the queries from LDS
 // (qlds, Q [T][r]); by default both are read here from global memory.
 // Sum and maximum over the 16 lanes of each row of the wave, returned to
-// all 16, with four data-parallel-primitive moves instead of four lane
-// permutes through LDS: lanes i^1 and i^2 (quad permutes), then the mirrored
-// quad within each half row and the mirrored half within the row.  After the
-// first two steps every lane of a quad holds the same bits, so the last two
-// pair exactly the values a xor butterfly over 4 and 8 pairs, and the result
-// is the same bits as that butterfly.
-#define LRAR_DPP(v, ctrl) \
-    __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), (ctrl), 0xF, 0xF, false))
-__device__ __forceinline__ float row16_sum(float x)
-{
-    x += LRAR_DPP(x, 0xB1);   // quad_perm [1, 0, 3, 2]: lane i^1
-    x += LRAR_DPP(x, 0x4E);   // quad_perm [2, 3, 0, 1]: lane i^2
-    x += LRAR_DPP(x, 0x141);  // row_half_mirror: the other quad of the half row
-    x += LRAR_DPP(x, 0x140);  // row_mirror: the other half of the row
-    return x;
-}
-__device__ __forceinline__ float row16_max(float x)
-{
-    x = fmaxf(x, LRAR_DPP(x, 0xB1));
-    x = fmaxf(x, LRAR_DPP(x, 0x4E));
-    x = fmaxf(x, LRAR_DPP(x, 0x141));
-    x = fmaxf(x, LRAR_DPP(x, 0x140));
-    return x;
-}
+// all 16: four DPP moves (group_sum / group_max over groups of 16).
+__device__ __forceinline__ float row16_sum(float x) { return group_sum(x, 16); }
+__device__ __forceinline__ float row16_max(float x) { return group_max(x, 16); }
 
 template <int RP>
 __device__ __forceinline__ void load_site_keys(const AllArgs &a, int64_t n, u32x4_t *kraw)

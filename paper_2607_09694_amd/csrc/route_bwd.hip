@@ -108,7 +108,8 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
         const int n = (bx * tpw + t) * kWaves + wave;
         if (n >= N)
             break;  // wave-uniform; the workgroup barrier below is outside the loop
-        lr_scores<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s, rho);
+        lr_scores<T, VEC, std::is_same<T, float>::value>(keys, q, S, N, r, krow, koff, eps, n,
+                                                          lane, s, rho);
         depth_softmax(s, alpha, S, lane);
 
         typedef typename Raw<T, VEC>::type raw_t;

@@ -154,7 +154,11 @@ constexpr int fwd_loads_per_trip(int nch)
 // vectors, and the group sums its partial dot products with lps-lane
 // butterflies, so 64 / lps sources are scored per step.  The group's first
 // lane writes s_out[i] (and rho_out[i]).
-template <typename T, int KV>
+// DPP: the lane-group butterflies with DPP moves (butterfly_sum2; same
+// bits).  Measured on MI355X: faster in the backward over fp32 block slots
+// (1-2% on the block reverse passes), slower in the bf16 forward and the
+// fp32 block forward, which keep the LDS lane permutes.
+template <typename T, int KV, bool DPP = false>
 __device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__restrict__ q,
                                     int S, int N, int r, int krow, int koff, float eps, int n,
                                     int lane, float *s_out, float *rho_out)
@@ -198,10 +202,7 @@ __device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__r
                 }
                 if (!vok)
                     ss = dot = 0.0f;
-                for (int m = 1; m < lps; m <<= 1) {
-                    ss += __shfl_xor(ss, m, kWaveSize);
-                    dot += __shfl_xor(dot, m, kWaveSize);
-                }
+                butterfly_sum2<DPP>(ss, dot, lps);
                 const int i = i0 + p * spi + isub;
                 if (v == 0 && i < S) {
                     const float rho = sqrtf(ss / (float)r + eps);
@@ -228,10 +229,7 @@ __device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__r
                 }
             }
         }
-        for (int m = 1; m < lps; m <<= 1) {
-            ss += __shfl_xor(ss, m, kWaveSize);
-            dot += __shfl_xor(dot, m, kWaveSize);
-        }
+        butterfly_sum2<DPP>(ss, dot, lps);
         if (v == 0 && i < S) {
             const float rho = sqrtf(ss / (float)r + eps);
             s_out[i] = dot / rho;
@@ -243,15 +241,15 @@ __device__ inline void lr_scores_kv(const T *__restrict__ keys, const float *__r
 
 // The scores with 16-byte key vectors when the key rows allow them, else
 // element by element.  Ends with the wave's LDS writes visible.
-template <typename T, int VEC>
+template <typename T, int VEC, bool DPP = false>
 __device__ inline void lr_scores(const T *__restrict__ keys, const float *__restrict__ q, int S,
                                  int N, int r, int krow, int koff, float eps, int n, int lane,
                                  float *s_out, float *rho_out)
 {
     if (VEC > 1 && r % VEC == 0 && krow % VEC == 0 && koff % VEC == 0)
-        lr_scores_kv<T, VEC>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
+        lr_scores_kv<T, VEC, DPP>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
     else
-        lr_scores_kv<T, 1>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
+        lr_scores_kv<T, 1, DPP>(keys, q, S, N, r, krow, koff, eps, n, lane, s_out, rho_out);
     wave_lds_sync();
 }
 
@@ -311,10 +309,7 @@ __device__ inline void lr_scores_tokens_kv(const T *__restrict__ keys, const flo
                 }
                 if (!vok)
                     ss = dot = 0.0f;
-                for (int m = 1; m < lps; m <<= 1) {
-                    ss += __shfl_xor(ss, m, kWaveSize);
-                    dot += __shfl_xor(dot, m, kWaveSize);
-                }
+                butterfly_sum2<false>(ss, dot, lps);
                 const int i = i0 + p * spi + isub;
                 if (v == 0 && i < S && n0 + t < N)
                     s_out[t * s_pad + i] = dot / sqrtf(ss / (float)r + eps);

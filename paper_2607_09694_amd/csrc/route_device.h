@@ -175,6 +175,53 @@ __device__ __forceinline__ float load_elem(const uint16_t *p)
 __device__ __forceinline__ void store_elem(float *p, float v) { *p = v; }
 __device__ __forceinline__ void store_elem(uint16_t *p, float v) { *p = to_bf16(v); }
 
+// One data-parallel-primitive move: lane i receives the value of the lane
+// that `ctrl` selects within its row of 16 (every lane active).
+#define LRAR_DPP(v, ctrl) \
+    __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), (ctrl), 0xF, 0xF, false))
+
+// Sum over aligned groups of g lanes (g a power of two, 1..64, the same on
+// every lane), every lane of a group receiving its group's sum, with the
+// pairings of a xor butterfly over lane bits 1, 2, 4, ...: bits 1 and 2 are
+// quad permutes; bits 4 and 8 mirror the quad within the half row and the
+// half within the row, which pair exactly as xor 4 and xor 8 do once the
+// earlier steps have made every quad (half row) hold one value; bits 16 and
+// 32 cross rows through LDS permutes.  Same bits as the butterfly, with four
+// of its six lane exchanges as DPP moves instead of LDS permutes.
+__device__ __forceinline__ float group_sum(float v, int g)
+{
+    if (g > 1)
+        v += LRAR_DPP(v, 0xB1);   // quad_perm [1, 0, 3, 2]: lane i^1
+    if (g > 2)
+        v += LRAR_DPP(v, 0x4E);   // quad_perm [2, 3, 0, 1]: lane i^2
+    if (g > 4)
+        v += LRAR_DPP(v, 0x141);  // row_half_mirror
+    if (g > 8)
+        v += LRAR_DPP(v, 0x140);  // row_mirror
+    if (g > 16)
+        v += __shfl_xor(v, 16, kWaveSize);
+    if (g > 32)
+        v += __shfl_xor(v, 32, kWaveSize);
+    return v;
+}
+
+__device__ __forceinline__ float group_max(float v, int g)
+{
+    if (g > 1)
+        v = fmaxf(v, LRAR_DPP(v, 0xB1));
+    if (g > 2)
+        v = fmaxf(v, LRAR_DPP(v, 0x4E));
+    if (g > 4)
+        v = fmaxf(v, LRAR_DPP(v, 0x141));
+    if (g > 8)
+        v = fmaxf(v, LRAR_DPP(v, 0x140));
+    if (g > 16)
+        v = fmaxf(v, __shfl_xor(v, 16, kWaveSize));
+    if (g > 32)
+        v = fmaxf(v, __shfl_xor(v, 32, kWaveSize));
+    return v;
+}
+
 // Butterfly reductions over the 64 lanes of a wave; every lane gets the result.
 __device__ __forceinline__ float wave_sum(float v)
 {
@@ -190,6 +237,42 @@ __device__ __forceinline__ float wave_max(float v)
     for (int m = 32; m >= 1; m >>= 1)
         v = fmaxf(v, __shfl_xor(v, m, kWaveSize));
     return v;
+}
+
+// Two sums over aligned groups of g lanes by the xor butterfly over lane
+// bits 1, 2, 4, ..., step by step together so that the two chains overlap:
+// with DPP moves for bits 1-8 (as group_sum) or with LDS lane permutes only
+// (same bits either way).
+template <bool DPP>
+__device__ __forceinline__ void butterfly_sum2(float &a, float &b, int g)
+{
+    if constexpr (DPP) {
+        if (g > 1) {
+            a += LRAR_DPP(a, 0xB1);
+            b += LRAR_DPP(b, 0xB1);
+        }
+        if (g > 2) {
+            a += LRAR_DPP(a, 0x4E);
+            b += LRAR_DPP(b, 0x4E);
+        }
+        if (g > 4) {
+            a += LRAR_DPP(a, 0x141);
+            b += LRAR_DPP(b, 0x141);
+        }
+        if (g > 8) {
+            a += LRAR_DPP(a, 0x140);
+            b += LRAR_DPP(b, 0x140);
+        }
+        for (int m = 16; m < g; m <<= 1) {
+            a += __shfl_xor(a, m, kWaveSize);
+            b += __shfl_xor(b, m, kWaveSize);
+        }
+        return;
+    }
+    for (int m = 1; m < g; m <<= 1) {
+        a += __shfl_xor(a, m, kWaveSize);
+        b += __shfl_xor(b, m, kWaveSize);
+    }
 }
 
 // Sum M per-lane values (M a power of two, M <= 64) over the wave with
