@@ -127,12 +127,12 @@ route_fwd_block(float *__restrict__ B, float *__restrict__ KB, TC *BC, TC *KBC,
             dot = fmaf(q[jj], k, dot);
         }
     }
-    ss = wave_sum(ss);
-    dot = wave_sum(dot);
+    ss = wave_sum_t<true>(ss);
+    dot = wave_sum_t<true>(dot);
     if (lane == 0)
         s[j] = dot / sqrtf(ss / (float)r + eps);
     wave_lds_sync();
-    depth_softmax(s, s, nsrc, lane);
+    depth_softmax<true>(s, s, nsrc, lane);
 
     // 4. h = sum_i alpha_i b_i: slots 0..j-1 from HBM, slot j from registers.
     float acc[NCH][VEC];

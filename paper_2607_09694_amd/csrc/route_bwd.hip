@@ -110,7 +110,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
             break;  // wave-uniform; the workgroup barrier below is outside the loop
         lr_scores<T, VEC, std::is_same<T, float>::value>(keys, q, S, N, r, krow, koff, eps, n,
                                                           lane, s, rho);
-        depth_softmax(s, alpha, S, lane);
+        depth_softmax<std::is_same<T, float>::value>(s, alpha, S, lane);
 
         typedef typename Raw<T, VEC>::type raw_t;
         float dh[NCH][VEC];
@@ -241,7 +241,7 @@ route_bwd_lr(const T *__restrict__ V, const T *__restrict__ keys, const float *_
         float gb = 0.0f;
         for (int i = lane; i < S; i += kWaveSize)
             gb = fmaf(alpha[i], g[i], gb);
-        gb = wave_sum(gb);
+        gb = wave_sum_t<std::is_same<T, float>::value>(gb);
         for (int i = lane; i < S; i += kWaveSize)
             g[i] = alpha[i] * (g[i] - gb);  // g now holds ds
         wave_lds_sync();

@@ -332,20 +332,22 @@ __device__ inline void lr_scores_tokens(const T *__restrict__ keys, const float 
 }
 
 // alpha_i = exp(s_i - max) / sum_l exp(s_l - max) over the S sources.
-// s and alpha may alias.  Ends with the wave's LDS writes visible.
+// s and alpha may alias.  Ends with the wave's LDS writes visible.  DPP: the
+// wave reductions with DPP moves (wave_sum_t), used over fp32 block slots.
+template <bool DPP = false>
 __device__ inline void depth_softmax(const float *s, float *alpha, int S, int lane)
 {
     float m = -INFINITY;
     for (int i = lane; i < S; i += kWaveSize)
         m = fmaxf(m, s[i]);
-    m = wave_max(m);
+    m = wave_max_t<DPP>(m);
     float z = 0.0f;
     for (int i = lane; i < S; i += kWaveSize) {
         const float e = expf(s[i] - m);
         alpha[i] = e;
         z += e;
     }
-    z = wave_sum(z);
+    z = wave_sum_t<DPP>(z);
     const float inv = 1.0f / z;
     for (int i = lane; i < S; i += kWaveSize)
         alpha[i] *= inv;

@@ -239,6 +239,19 @@ __device__ __forceinline__ float wave_max(float v)
     return v;
 }
 
+// Wave reductions with DPP moves for the lane bits within a row (DPP) or
+// the LDS-permute butterflies above; the sum's order differs between the two.
+template <bool DPP>
+__device__ __forceinline__ float wave_sum_t(float v)
+{
+    return DPP ? group_sum(v, kWaveSize) : wave_sum(v);
+}
+template <bool DPP>
+__device__ __forceinline__ float wave_max_t(float v)
+{
+    return DPP ? group_max(v, kWaveSize) : wave_max(v);
+}
+
 // Two sums over aligned groups of g lanes by the xor butterfly over lane
 // bits 1, 2, 4, ..., step by step together so that the two chains overlap:
 // with DPP moves for bits 1-8 (as group_sum) or with LDS lane permutes only
