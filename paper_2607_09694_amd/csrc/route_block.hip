@@ -165,14 +165,14 @@ __device__ inline float partial_softmax(float *s, int S, int lane, float *l)
     float m = -INFINITY;
     for (int i = lane; i < S; i += kWaveSize)
         m = fmaxf(m, s[i]);
-    m = wave_max(m);
+    m = wave_max_t<true>(m);
     float z = 0.0f;
     for (int i = lane; i < S; i += kWaveSize) {
         const float e = expf(s[i] - m);
         s[i] = e;
         z += e;
     }
-    *l = wave_sum(z);
+    *l = wave_sum_t<true>(z);
     return m;
 }
 
@@ -357,8 +357,8 @@ route_block_merge(float *__restrict__ B, float *__restrict__ KB, const TO *__res
             dot = fmaf(q[jj], k, dot);
         }
     }
-    ss = wave_sum(ss);
-    dot = wave_sum(dot);
+    ss = wave_sum_t<true>(ss);
+    dot = wave_sum_t<true>(dot);
     const float sj = dot / sqrtf(ss / (float)r + eps);
 
     const float m = has_state ? Ms[n] : -INFINITY;
@@ -638,7 +638,7 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
         ck[u] = cu[2 * N + n];
         ck_sum += ck[u];
     }
-    ck_sum = wave_sum(ck_sum);
+    ck_sum = wave_sum_t<true>(ck_sum);
     wave_lds_sync();
 
     // rho of the slot's key: the last r columns of the summary (sliced) or
@@ -650,7 +650,7 @@ __global__ void __launch_bounds__(kBlock) block_gather(GatherArgs a)
         const float x = load_elem(key + e);
         ss = fmaf(x, x, ss);
     }
-    const float rho = sqrtf(wave_sum(ss) / (float)a.r + a.eps);
+    const float rho = sqrtf(wave_sum_t<true>(ss) / (float)a.r + a.eps);
     const float kscale = a.n_sites > 0 ? ck_sum / rho : 0.0f;
     // The key-column term of key element e: sum_t cq_t q_t[e] - kscale * k[e].
     auto key_term = [&](int e) {
