@@ -92,3 +92,54 @@ def test_random_split_sources(dev, case):
 @pytest.mark.parametrize("case", _bf16c_cases(12, 74), ids=str)
 def test_random_block_bf16_copies(dev, case):
     bf16c.test_bf16_copies_model_pass_matches_oracle(dev, case)
+
+
+# Problems the fused all-sites kernels do not take run site by site inside
+# the library: full-rank keys, S or T above 64, r above 64, d % 8 != 0, and
+# (backward) fp32 storage.  Each case below is outside the fused limits for
+# one drawn reason.
+ODD_WIDTHS = [12, 36, 68, 100, 204, 260]
+
+
+def _site_by_site_cases(n, seed, backward):
+    rng = np.random.default_rng(seed)
+    reasons = ["full", "sources", "rank", "width"] + (["f32"] if backward else [])
+    out = []
+    for _ in range(n):
+        why = reasons[int(rng.integers(0, len(reasons)))]
+        dtype = ["f32", "bf16"][int(rng.integers(0, 2))]
+        mode = int(rng.integers(0, 2))
+        S = int(rng.integers(2, 40))
+        d = int(rng.choice([64, 128, 136, 256, 264]))
+        r = _rank(rng, mode, d, 48)
+        if why == "full":
+            mode, d = FULL, int(rng.choice([64, 72, 136, 200, 256]))
+            r = d
+        elif why == "sources":
+            S = int(rng.integers(65, 90))
+        elif why == "rank":
+            d = int(rng.choice([136, 256, 264]))
+            r = int(rng.integers(65, 97))
+        elif why == "width":
+            d = int(rng.choice(ODD_WIDTHS))
+            r = _rank(rng, mode, d, 32)
+        else:
+            dtype = "f32"
+        first = int(rng.integers(1, S + 1))
+        T = int(rng.integers(1, min(S - first + 1, 12) + 1))
+        if why == "sources":
+            first = int(rng.integers(60, S + 1))
+            T = int(rng.integers(1, S - first + 2))
+        N = int(rng.integers(3, 40))
+        out.append((mode, dtype, S, T, first, N, d, r))
+    return out
+
+
+@pytest.mark.parametrize("case", _site_by_site_cases(12, 75, False), ids=str)
+def test_random_all_sites_forward_site_by_site(dev, case):
+    all_fwd.test_all_sites_site_by_site_match_oracle(dev, case)
+
+
+@pytest.mark.parametrize("case", _site_by_site_cases(12, 76, True), ids=str)
+def test_random_all_sites_backward_site_by_site(dev, case):
+    all_bwd.test_all_sites_backward_site_by_site(dev, case)
