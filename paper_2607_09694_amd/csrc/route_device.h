@@ -176,9 +176,16 @@ __device__ __forceinline__ void store_elem(float *p, float v) { *p = v; }
 __device__ __forceinline__ void store_elem(uint16_t *p, float v) { *p = to_bf16(v); }
 
 // One data-parallel-primitive move: lane i receives the value of the lane
-// that `ctrl` selects within its row of 16 (every lane active).
-#define LRAR_DPP(v, ctrl) \
-    __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), (ctrl), 0xF, 0xF, false))
+// that CTRL selects within its row of 16 (every lane active).
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1, 0, 3, 2]: lane i^1
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2, 3, 0, 1]: lane i^2
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror: lane 7 - i within each 8
+constexpr int kDppMirror = 0x140;      // row_mirror: lane 15 - i within the row
 
 // Sum over aligned groups of g lanes (g a power of two, 1..64, the same on
 // every lane), every lane of a group receiving its group's sum, with the
@@ -191,13 +198,13 @@ __device__ __forceinline__ void store_elem(uint16_t *p, float v) { *p = to_bf16(
 __device__ __forceinline__ float group_sum(float v, int g)
 {
     if (g > 1)
-        v += LRAR_DPP(v, 0xB1);   // quad_perm [1, 0, 3, 2]: lane i^1
+        v += dpp_move<kDppXor1>(v);
     if (g > 2)
-        v += LRAR_DPP(v, 0x4E);   // quad_perm [2, 3, 0, 1]: lane i^2
+        v += dpp_move<kDppXor2>(v);
     if (g > 4)
-        v += LRAR_DPP(v, 0x141);  // row_half_mirror
+        v += dpp_move<kDppHalfMirror>(v);
     if (g > 8)
-        v += LRAR_DPP(v, 0x140);  // row_mirror
+        v += dpp_move<kDppMirror>(v);
     if (g > 16)
         v += __shfl_xor(v, 16, kWaveSize);
     if (g > 32)
@@ -208,13 +215,13 @@ __device__ __forceinline__ float group_sum(float v, int g)
 __device__ __forceinline__ float group_max(float v, int g)
 {
     if (g > 1)
-        v = fmaxf(v, LRAR_DPP(v, 0xB1));
+        v = fmaxf(v, dpp_move<kDppXor1>(v));
     if (g > 2)
-        v = fmaxf(v, LRAR_DPP(v, 0x4E));
+        v = fmaxf(v, dpp_move<kDppXor2>(v));
     if (g > 4)
-        v = fmaxf(v, LRAR_DPP(v, 0x141));
+        v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
     if (g > 8)
-        v = fmaxf(v, LRAR_DPP(v, 0x140));
+        v = fmaxf(v, dpp_move<kDppMirror>(v));
     if (g > 16)
         v = fmaxf(v, __shfl_xor(v, 16, kWaveSize));
     if (g > 32)
@@ -261,20 +268,20 @@ __device__ __forceinline__ void butterfly_sum2(float &a, float &b, int g)
 {
     if constexpr (DPP) {
         if (g > 1) {
-            a += LRAR_DPP(a, 0xB1);
-            b += LRAR_DPP(b, 0xB1);
+            a += dpp_move<kDppXor1>(a);
+            b += dpp_move<kDppXor1>(b);
         }
         if (g > 2) {
-            a += LRAR_DPP(a, 0x4E);
-            b += LRAR_DPP(b, 0x4E);
+            a += dpp_move<kDppXor2>(a);
+            b += dpp_move<kDppXor2>(b);
         }
         if (g > 4) {
-            a += LRAR_DPP(a, 0x141);
-            b += LRAR_DPP(b, 0x141);
+            a += dpp_move<kDppHalfMirror>(a);
+            b += dpp_move<kDppHalfMirror>(b);
         }
         if (g > 8) {
-            a += LRAR_DPP(a, 0x140);
-            b += LRAR_DPP(b, 0x140);
+            a += dpp_move<kDppMirror>(a);
+            b += dpp_move<kDppMirror>(b);
         }
         for (int m = 16; m < g; m <<= 1) {
             a += __shfl_xor(a, m, kWaveSize);
