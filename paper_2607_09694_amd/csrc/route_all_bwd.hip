@@ -27,8 +27,8 @@
 // and keep their share of dQ in registers; a fixed-order reduction adds the
 // per-workgroup partials, so dQ is bitwise reproducible.  Wave w owns
 // sources 16 w .. 16 w + 15.  The row is processed in 128-column slabs: the
-// workgroup stages the T upstream rows of a slab in LDS (16-byte chunks
-// XOR-swizzled by row, conflict-free in both read patterns below), each wave
+// workgroup stages the T upstream rows of a slab in LDS (rows padded by one
+// 16-byte chunk, conflict-free in both read patterns below), each wave
 // loads its 16 source rows of the slab into registers, then
 //   - G: A = dH rows from LDS (lane: one site, 8 columns), B = the source
 //     rows (lane: one source, the same 8 columns);
@@ -53,7 +53,7 @@ namespace lrar {
 namespace {
 
 constexpr int kAllBwdGrid = 512;                       // persistent workgroups
-constexpr int kDhRowBytes = kAllSlab * 2;              // one slab row of dH, bf16
+constexpr int kDhRowBytes = kAllSlab * 2 + 16;         // one slab row of dH, bf16, padded
 constexpr int kDhBufBytes = kAllMaxSources * kDhRowBytes;
 constexpr int kTailRow = 64;                           // floats per source: key-column octets
 
@@ -66,10 +66,12 @@ struct AllBwdArgs {
     bool sliced;         // the key is the last r columns of each value row
 };
 
-// LDS byte offset of 16-byte chunk c (0..15) of slab row `row`: rows are
-// 256 bytes and the chunk index is XOR-swizzled with row mod 16, so both 16
-// rows at one logical chunk and one row's 16 chunks fall on distinct banks.
-__device__ __forceinline__ int dh_chunk(int row, int c) { return row * kDhRowBytes + 16 * (c ^ (row & 15)); }
+// LDS byte offset of 16-byte chunk c (0..15) of slab row `row`: rows of 256
+// bytes are laid out 272 bytes apart, so both 16 consecutive rows at one
+// chunk and one row's 16 chunks fall on distinct banks, and the offsets of
+// the rows a lane reads differ by constants (immediate offsets, no per-read
+// address arithmetic).
+__device__ __forceinline__ int dh_chunk(int row, int c) { return row * kDhRowBytes + 16 * c; }
 
 __device__ __forceinline__ float bf16_at(const uint16_t *p) { return __uint_as_float((unsigned)*p << 16); }
 
@@ -176,23 +178,28 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
         // per load), so those loads go through the caches normally; the
         // upstream rows, read as whole lines, stream.
         u32x4_t hraw[MT], vraw[4];
+        // Each lane forms one 64-bit row address per slab; the rows it
+        // reads after that are whole planes (16 sites) or 32 columns further
+        // on, uniform steps.
         auto load_dh = [&](int s) {
             const int col = s * kAllSlab + 8 * hch;
             const uint16_t *hbase = b.dH + n * a.d;
+            const uint16_t *h0 = hbase + (size_t)(unsigned)hr0 * plane + col;
 #pragma unroll
             for (int q = 0; q < MT; ++q) {
                 const int row = hr0 + 16 * q;
                 const bool ok = row < a.T && col < a.d;
-                hraw[q] = load_stream<uint16_t, 8, kNtLoad>(ok ? hbase + row * plane + col : hbase);
+                hraw[q] = load_stream<uint16_t, 8, kNtLoad>(ok ? h0 + 16 * q * plane : hbase);
             }
         };
         auto load_v = [&](int s) {
             const uint16_t *vbase = static_cast<const uint16_t *>(a.V) + n * a.d;
+            const uint16_t *v0 = vbase + (size_t)(unsigned)src * plane + s * kAllSlab + 8 * ks;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int c = s * kAllSlab + 32 * u + 8 * ks;
                 const bool ok = src < a.S && c < a.d;
-                vraw[u] = load_stream<uint16_t, 8, false>(ok ? vbase + src * plane + c : vbase);
+                vraw[u] = load_stream<uint16_t, 8, false>(ok ? v0 + 32 * u : vbase);
             }
         };
         load_dh(0);
@@ -294,6 +301,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
             const int c0 = s * kAllSlab + 8 * lc;
             if (c0 < tail0) {
                 // Rounded and stored (added to the stored value when accumulating).
+                uint16_t *d0 = b.dV + (size_t)(unsigned)(16 * wave + 4 * ks) * plane + n * a.d + c0;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int i = 16 * wave + 4 * ks + e;
@@ -303,7 +311,7 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
 #pragma unroll
                     for (int p = 0; p < 8; ++p)
                         v[p] = acc[p][e];
-                    uint16_t *dst = b.dV + i * plane + n * a.d + c0;
+                    uint16_t *dst = d0 + e * plane;
                     if (ACC) {
                         float old[8];
                         widen(load_raw<uint16_t, 8>(dst), old);
@@ -385,11 +393,14 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
             for (int ct = 0; ct < RT; ++ct) {
                 __builtin_amdgcn_sched_barrier(0);
                 const int c = 16 * ct + lc;
+                // Q[site][c] for sites 4 ks + (a constant per e): the lane's
+                // row is formed once, the rest are uniform steps of r.
+                const float *qlane = qs + 4 * ks * a.r + c;
                 float qv[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const int site = 16 * (2 * kg + e / 4) + 4 * ks + e % 4;
-                    qv[e] = (site < a.T && c < a.r) ? qs[site * a.r + c] : 0.0f;
+                    const int so = 16 * (2 * kg + e / 4) + e % 4;
+                    qv[e] = (4 * ks + so < a.T && c < a.r) ? qlane[so * a.r] : 0.0f;
                 }
                 bf16x8_t Qhi, Qlo;
                 split_hilo(qv, Qhi, Qlo);
@@ -420,7 +431,8 @@ __global__ __launch_bounds__(kBlock, 2) void route_all_bwd_bf16(AllBwdArgs b)
                 const float dk = (uk[ct][e] - kv[ct] * scale) * inv;
                 if (i < a.S && c < a.r) {
                     if (b.dK) {
-                        uint16_t *dst = b.dK + (i * (size_t)a.N + n) * a.r + c;
+                        uint16_t *dst = b.dK + ((size_t)(unsigned)(16 * wave + 4 * ks) * a.N + n) * a.r +
+                                        (size_t)e * a.N * a.r + c;
                         float v = dk;
                         if (ACC)
                             v += bf16_at(dst);

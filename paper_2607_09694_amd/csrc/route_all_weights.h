@@ -70,13 +70,15 @@ __device__ __forceinline__ void load_site_keys(const AllArgs &a, int64_t n, u32x
     if (a.kvec) {
         // Sources past S and elements past r load a valid address; they are
         // zeroed where the keys are used.
+        // One 64-bit row address per lane; the other rows are 16 planes on.
+        const uint16_t *k0 = keys + (size_t)(unsigned)col * kplane + 8 * ks;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
                 const int i = 16 * nt + col, c = 32 * kk + 8 * ks;
                 const bool ok = i < a.S && c < a.r;
-                kraw[nt * KK + kk] = load_raw<uint16_t, 8>(ok ? keys + i * kplane + c : keys);
+                kraw[nt * KK + kk] = load_raw<uint16_t, 8>(ok ? k0 + 16 * nt * kplane + 32 * kk : keys);
             }
     } else {
 #pragma unroll
