@@ -51,11 +51,13 @@ __device__ __forceinline__ int tile_prefix(const AllArgs &a, int mt)
 __device__ __forceinline__ void load_group(const uint16_t *__restrict__ vrow, size_t plane,
                                            int S, int kg, int ks, bool ok, u32x4_t (&raw)[8])
 {
+    // One 64-bit row address per lane; the other sources are whole planes on.
+    const uint16_t *r0 = vrow + (size_t)(unsigned)(32 * kg + 8 * ks) * plane;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int i = 32 * kg + 8 * ks + e;
         if (ok && i < S)
-            raw[e] = load_stream<uint16_t, 8, kNtLoad>(vrow + i * plane);
+            raw[e] = load_stream<uint16_t, 8, kNtLoad>(r0 + e * plane);
     }
 }
 
@@ -143,6 +145,7 @@ __global__ __launch_bounds__(kBlock, MT <= 3 ? 2 : 1) void route_all_fwd_bf16(Al
         }
         // Lane l holds sites 16 mt + 4 (l / 16) + e, columns c0 .. c0 + 7.
         if (ok) {
+            uint16_t *h0 = H + (size_t)(unsigned)(4 * ks) * plane + slab * kAllSlab;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -153,7 +156,7 @@ __global__ __launch_bounds__(kBlock, MT <= 3 ? 2 : 1) void route_all_fwd_bf16(Al
 #pragma unroll
                         for (int h = 0; h < 4; ++h)
                             o[h] = pack_bf16x2(acc[mt][2 * h][e], acc[mt][2 * h + 1][e]);
-                        store_stream<uint16_t, 8, kNtStore>(H + site * plane + slab * kAllSlab, o);
+                        store_stream<uint16_t, 8, kNtStore>(h0 + (16 * mt + e) * plane, o);
                     }
                 }
         }
