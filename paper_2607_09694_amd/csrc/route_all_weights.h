@@ -108,7 +108,12 @@ __device__ __forceinline__ void all_site_weights(const AllArgs &a, int64_t n, fl
                                                  const u32x4_t *kpre = nullptr,
                                                  const float *qlds = nullptr)
 {
-    const int lane = threadIdx.x % kWaveSize, wave = threadIdx.x / kWaveSize;
+    // The lane's indices are formed here, each call, instead of being held
+    // across a persistent caller's token loop (where they would take
+    // registers for the kernel's lifetime).
+    unsigned tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid % kWaveSize, wave = tid / kWaveSize;
     const int col = lane & 15, ks = lane >> 4;
     const int qsite = 16 * wave + col;  // site of this lane's A-operand row
     const T *keys = static_cast<const T *>(a.keys) + n * a.krow + a.koff;
