@@ -74,6 +74,10 @@ CASES = [
     (PROJECTED, "bf16", 17, 5, 13, 12, 384, 20),   # few sites late in the stack
     (SLICED, "f32", 64, 49, 16, 7, 128, 64),       # fp32 at the limits
     (PROJECTED, "bf16", 1, 1, 1, 5, 8, 1),         # one source, one site
+    # above 48 sites the workgroups are persistent and load the next token's
+    # keys during the current token's mix: several tokens per workgroup
+    (SLICED, "bf16", 64, 60, 2, 700, 136, 40),
+    (PROJECTED, "bf16", 57, 55, 3, 530, 256, 16),
 ]
 
 

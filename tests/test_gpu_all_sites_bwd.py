@@ -114,6 +114,7 @@ CASES = [
     (SLICED, 12, 11, 1, 1100, 128, 16),     # several tokens per workgroup
     (PROJECTED, 8, 8, 1, 16, 2048, 32),     # the widest rows (16 slabs)
     (SLICED, 17, 16, 2, 13, 2048, 64),
+    (SLICED, 64, 60, 2, 1100, 136, 40),     # 4 site tiles, several tokens per workgroup
 ]
 
 
