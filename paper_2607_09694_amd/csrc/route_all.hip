@@ -263,9 +263,9 @@ hipError_t launch_all_mt_rp(const AllArgs &a, int dtype, hipStream_t st)
         // Persistent above 48 sites: one workgroup per CU.
         const unsigned grid = MT <= 3 ? (unsigned)a.N : (unsigned)std::min<int64_t>(a.N, kAllFwdGrid);
         hipLaunchKernelGGL((route_all_fwd_bf16<MT, RP>), dim3(grid), dim3(kBlock), 0, st, a);
-    }
-    else
+    } else {
         hipLaunchKernelGGL((route_all_fwd_f32<MT, RP>), dim3((unsigned)a.N), dim3(kBlock), 0, st, a);
+    }
     return hipGetLastError();
 }
 
